@@ -1,0 +1,221 @@
+/*
+ * domino.h — C ABI of the MI355X (gfx950) Domino drafting library.
+ *
+ * The library runs one speculative-decoding draft step of the Domino method
+ * ("Domino: Decoupling Causal Modeling from Autoregressive Drafting in
+ * Speculative Decoding"): a parallel draft backbone over the masked block
+ * (Sec. 4.1.1), the frozen LM head giving base logits (Sec. 4.1.1, base-logit
+ * equation), the Domino head's GRU causal encoder and low-rank logit-space
+ * correction rolled out over the block (Sec. 4.1.2, Fig. 3), construction of
+ * a draft tree from the per-position top-beta tokens, and greedy acceptance of
+ * the longest valid prefix plus a bonus token (Sec. 3.1).
+ *
+ * Conventions for every call:
+ *  - Pointers named as device memory must be device pointers (hipMalloc or a
+ *    torch CUDA tensor); the caller owns all of them.  Host-side arguments are
+ *    the config/weight structs and scalar sizes.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  The draft, tree
+ *    and acceptance calls only enqueue work and return; they never allocate
+ *    and never synchronise.
+ *  - Return codes cover argument validation (done before any HIP call) and
+ *    launch errors.  Conditions only visible on the device (a token id out of
+ *    range, a context length above max_ctx, a malformed tree) are clamped so
+ *    that no access leaves its buffer, and are recorded in an error word at
+ *    the start of the workspace, read with domino_workspace_error().
+ *  - domino_last_error() returns a thread-local message for the last failure.
+ *  - No C++ exception crosses this boundary.  A model handle may be used from
+ *    several streams, but calls that share one workspace must not overlap.
+ *  - Storage type: DOMINO_BF16 stores weights and KV caches as bfloat16,
+ *    DOMINO_F32 as float; all arithmetic is fp32 (bf16 operands are exact in
+ *    fp32; activations feeding bf16 matrix cores are split into a high and a
+ *    low bf16 part so products keep fp32 accuracy).
+ */
+#ifndef DOMINO_H
+#define DOMINO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DOMINO_OK = 0,
+  DOMINO_ERR_INVALID_ARG = -1,  /* a NULL pointer, a size out of range, shapes that disagree */
+  DOMINO_ERR_WORKSPACE = -2,    /* workspace NULL or smaller than the *_workspace_bytes query */
+  DOMINO_ERR_UNSUPPORTED = -3,  /* a shape this build does not handle (message says which) */
+  DOMINO_ERR_HIP = -4,          /* a HIP runtime call failed (message carries hipGetErrorString) */
+  DOMINO_ERR_DEVICE = -5        /* returned by domino_workspace_error when the error word is set */
+} domino_status;
+
+typedef enum { DOMINO_F32 = 0, DOMINO_BF16 = 1 } domino_dtype;
+
+/* Bits of the device error word (domino_workspace_error). */
+enum {
+  DOMINO_DEV_BAD_TOKEN = 1,       /* an anchor / forced / tree token id outside [0, vocab) (clamped) */
+  DOMINO_DEV_BAD_CTX_LEN = 2,     /* ctx_lens[b] outside [n_new, max_ctx] (clamped) */
+  DOMINO_DEV_BAD_TREE = 4,        /* a node_parent entry that is not an earlier node (ignored) */
+  DOMINO_DEV_BARRIER_TIMEOUT = 8  /* a grid barrier in the head loop exceeded its spin bound */
+};
+
+/*
+ * Model shape.  `block` is B = 16 in the paper (anchor + B-1 draft positions,
+ * Sec. 4.1.1 and Sec. 5.1); gru_hidden d_s = 1024 and rank r = 256 (Sec. 4.1.2,
+ * Sec. 5.1).  Layers follow the Qwen3 layout: pre-RMSNorm, per-head q/k
+ * RMSNorm, rotate-half RoPE, grouped-query attention, SwiGLU, no biases.
+ * Limits of this build: head_dim in {64, 128}; hidden, ffn, gru_hidden,
+ * rank and n_q_heads*head_dim multiples of 32; n_q_heads a multiple of
+ * n_kv_heads; block in [2, 64]; mask_token_id in [0, vocab).
+ */
+typedef struct {
+  int32_t hidden, n_layers, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
+  int32_t block, gru_hidden, rank, mask_token_id;
+  float rms_eps, rope_theta;
+  domino_dtype dtype;
+} domino_config;
+
+/*
+ * Weights: device pointers in the config's storage type, row-major [out, in].
+ * Per-layer fields are HOST arrays of n_layers device pointers.
+ *   embed [V, d] (shared frozen target embedding), lm_head [V, d] (shared
+ *   frozen target LM head), final_norm [d];
+ *   per layer: attn_norm [d], wq [nq*dh, d], wk [nkv*dh, d], wv [nkv*dh, d],
+ *   q_norm [dh], k_norm [dh], wo [d, nq*dh], ffn_norm [d],
+ *   w_gate [ffn, d], w_up [ffn, d], w_down [d, ffn];
+ *   GRU (reset-after form, gate order r, z, n): gru_w_ih [3ds, d],
+ *   gru_w_hh [3ds, ds], gru_b_ih [3ds], gru_b_hh [3ds];
+ *   correction: w1 [r, d + ds] with columns [H | S], w2 [V, r].
+ * domino_model_create copies every matrix into its own device memory in a
+ * matrix-core tile order; it keeps borrowing embed, the norm gains and the
+ * GRU biases, which the caller keeps alive until domino_model_destroy.
+ */
+typedef struct {
+  const void *embed, *lm_head, *final_norm;
+  const void *const *attn_norm, *const *wq, *const *wk, *const *wv, *const *q_norm,
+      *const *k_norm, *const *wo, *const *ffn_norm, *const *w_gate, *const *w_up, *const *w_down;
+  const void *gru_w_ih, *gru_w_hh, *gru_b_ih, *gru_b_hh;
+  const void *w1, *w2;
+} domino_weights;
+
+/* Optional per-step debug outputs (device fp32; any field may be NULL).
+ *   hidden       [bs, B-1, d]   post-final-norm H_j (the LM-head input)
+ *   base_logits  [bs, B-1, V]   L_base_j
+ *   final_logits [bs, B-1, V]   L_j = L_base_j + dL_j
+ *   states       [bs, B-1, ds]  S_{j-1}, the GRU state used at position j */
+typedef struct {
+  float *hidden, *base_logits, *final_logits, *states;
+} domino_debug;
+
+typedef struct domino_model *domino_model_t;
+
+/* Validate the config, pack the weights (blocking: runs on the default stream
+ * and synchronises).  On success *out owns device memory freed by destroy. */
+domino_status domino_model_create(const domino_config *cfg, const domino_weights *w,
+                                  domino_model_t *out);
+void domino_model_destroy(domino_model_t m);
+
+/* Bytes of workspace domino_draft_step needs for `batch` rows, caches of
+ * `max_ctx` positions, up to `max_new` projected context rows and top-`branch`
+ * outputs.  Returns 0 for invalid arguments. */
+size_t domino_workspace_bytes(domino_model_t m, int32_t batch, int32_t max_ctx, int32_t max_new,
+                              int32_t branch);
+
+/* Thread-local text of the last error (never NULL). */
+const char *domino_last_error(void);
+
+/*
+ * One draft step (Sec. 4.1.1 block construction, backbone and LM head;
+ * Sec. 4.1.2 causal encoder and correction; Fig. 3 sequential rollout).
+ *  batch           rows, >= 1
+ *  anchor_ids      device int32 [batch]: x_t, the last verified token
+ *  ctx_lens        device int32 [batch]: context length n_b (RoPE positions of
+ *                  the block are n_b .. n_b+B-1), in [n_new, max_ctx]
+ *  ctx_k, ctx_v    device [n_layers][batch][max_ctx][n_kv][d_h] in the storage
+ *                  type; K is post k-norm and RoPE.  Read-only unless n_new > 0.
+ *  ctx_hidden_new  optional device [batch][n_new][d] target hidden states; when
+ *                  given, row i is projected with each layer's W_k (k-norm,
+ *                  RoPE) and W_v and written at position n_b - n_new + i.
+ *  branch          beta in [1, 8]: entries kept per position
+ *  forced_tokens   optional device int32 [batch][B-1]: teacher forcing — the
+ *                  token fed to the causal encoder after position j is
+ *                  forced[b][j-1] instead of the top-1 draft token
+ *  topk_ids        device int32 [batch][B-1][branch], order (value desc, id asc)
+ *  topk_vals       device fp32  [batch][B-1][branch]: final logits L_j
+ *  debug           optional (NULL when timed)
+ *  workspace       device, >= domino_workspace_bytes(m, batch, max_ctx, n_new, branch)
+ */
+domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *anchor_ids,
+                                const int32_t *ctx_lens, void *ctx_k, void *ctx_v, int32_t max_ctx,
+                                const void *ctx_hidden_new, int32_t n_new, int32_t branch,
+                                const int32_t *forced_tokens, int32_t *topk_ids, float *topk_vals,
+                                const domino_debug *debug, void *workspace, size_t workspace_bytes,
+                                void *stream);
+
+/*
+ * Draft tree from the per-position top-beta tokens (spine-and-leaves, BFS
+ * order).  Node 0 is the anchor (parent -1, depth 0, position n_b); node
+ * 1 + (d-1)*branch + rho holds topk_ids[b][d-1][rho] at depth d, position
+ * n_b + d, with parent 0 for d = 1 and 1 + (d-2)*branch (the rank-0 node one
+ * level up) otherwise.  ancestor_mask[b][i][k] = 1 iff k is i or an ancestor
+ * of i.  N + 1 = 1 + depth*branch nodes per row.
+ *  depth in [1, 63], branch in [1, 8]; topk_ids device int32 [batch][depth][branch];
+ *  anchor_ids, ctx_lens device int32 [batch]; node_* device int32 [batch][N+1];
+ *  ancestor_mask device uint8 [batch][N+1][N+1] or NULL.
+ */
+domino_status domino_build_tree(int32_t batch, int32_t depth, int32_t branch,
+                                const int32_t *topk_ids, const int32_t *anchor_ids,
+                                const int32_t *ctx_lens, int32_t *node_token, int32_t *node_parent,
+                                int32_t *node_depth, int32_t *node_pos, uint8_t *ancestor_mask,
+                                void *stream);
+
+/* Workspace bytes for domino_verify_accept. */
+size_t domino_verify_workspace_bytes(int32_t batch, int32_t n_nodes, int32_t vocab);
+
+/*
+ * Greedy acceptance (Sec. 3.1).  R_m = argmax_v target_logits[b][m][v] under
+ * (value desc, id asc), NaN as -inf.  From the root, while some child c of the
+ * current node has node_token[c] == R_cur, accept c and move to it; the bonus
+ * token is R at the last accepted node, so tau = accept_len + 1 in [1, B].
+ * Any tree works (node_parent[c] < c for c > 0, node_parent[0] = -1); only rows
+ * of nodes with children, plus the final node's row, are read.
+ *  n_nodes in [1, 1024]; block B in [2, 64] bounds the walk at B-1 steps;
+ *  target_logits device [batch][n_nodes][vocab] fp32 or bf16;
+ *  accept_len device int32 [batch]; accepted_nodes device int32 [batch][B-1]
+ *  (-1 padded); out_tokens device int32 [batch][B] (accepted tokens then the
+ *  bonus, -1 padded).
+ */
+domino_status domino_verify_accept(int32_t batch, int32_t n_nodes, int32_t vocab, int32_t block,
+                                   const int32_t *node_token, const int32_t *node_parent,
+                                   const void *target_logits, domino_dtype logits_dtype,
+                                   int32_t *accept_len, int32_t *accepted_nodes,
+                                   int32_t *out_tokens, void *workspace, size_t workspace_bytes,
+                                   void *stream);
+
+/* Copy the device error word at the start of a draft or verify workspace to
+ * *out (synchronises `stream`).  Returns DOMINO_ERR_DEVICE when it is set. */
+domino_status domino_workspace_error(const void *workspace, void *stream, int32_t *out);
+
+/* Clear the error word (stream-ordered). */
+domino_status domino_workspace_clear_error(void *workspace, void *stream);
+
+/*
+ * Per-kernel-class timing for benchmarks: while enabled for a class, the
+ * draft step brackets that class's launches with HIP events on its stream.
+ * domino_profile_read synchronises and returns the summed milliseconds and
+ * the number of launches timed since the last reset.
+ */
+enum {
+  DOMINO_KC_EMBED = 0, DOMINO_KC_NORM, DOMINO_KC_QKV, DOMINO_KC_ROPE, DOMINO_KC_ATTN,
+  DOMINO_KC_WO, DOMINO_KC_GATEUP, DOMINO_KC_DOWN, DOMINO_KC_LMHEAD, DOMINO_KC_W1H,
+  DOMINO_KC_HEADLOOP, DOMINO_KC_CTXPROJ, DOMINO_KC_COUNT
+};
+domino_status domino_profile_enable(domino_model_t m, uint32_t class_mask);
+domino_status domino_profile_read(domino_model_t m, int32_t kernel_class, double *total_ms,
+                                  int32_t *launches);
+domino_status domino_profile_reset(domino_model_t m);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DOMINO_H */

@@ -1,0 +1,611 @@
+// Host side of the C ABI declared in include/domino.h: argument validation
+// (always before any HIP call), weight packing at model creation, workspace
+// planning and the launch sequence of one draft step.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/domino.h"
+#include "kernels.h"
+
+using namespace dk;
+
+namespace {
+
+thread_local std::string g_err = "";
+
+domino_status fail(domino_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                           \
+  do {                                                                                          \
+    hipError_t e_ = (expr);                                                                     \
+    if (e_ != hipSuccess) return fail(DOMINO_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+struct Packed {
+  size_t off;
+  int NT, KS;
+};
+
+}  // namespace
+
+struct domino_model {
+  domino_config cfg;
+  Dims D;  // bs filled per call
+  bool bf16;
+  int n_cu;
+  int esz;
+  // borrowed
+  const void *embed, *final_norm, *b_ih, *b_hh;
+  std::vector<const void *> attn_norm, q_norm, k_norm, ffn_norm;
+  // owned
+  void *mem = nullptr;
+  size_t mem_bytes = 0;
+  std::vector<Packed> qkv, wo, gateup, down;
+  Packed lm, w1h, w2;
+  size_t w_ih_off, w_hh_off, w1_off;
+  // profiling
+  uint32_t prof_mask = 0;
+  struct Ev {
+    std::vector<hipEvent_t> a, b;
+    int used = 0;
+  } ev[DOMINO_KC_COUNT];
+
+  const void *at(size_t off) const { return (const char *)mem + off; }
+};
+
+namespace {
+
+int kstep(const domino_model *m) { return m->bf16 ? 32 : 16; }
+
+void prof_begin(domino_model *m, int cls, hipStream_t st) {
+  if (!(m->prof_mask & (1u << cls))) return;
+  auto &e = m->ev[cls];
+  if (e.used >= (int)e.a.size()) return;
+  (void)hipEventRecord(e.a[e.used], st);
+}
+void prof_end(domino_model *m, int cls, hipStream_t st) {
+  if (!(m->prof_mask & (1u << cls))) return;
+  auto &e = m->ev[cls];
+  if (e.used >= (int)e.a.size()) return;
+  (void)hipEventRecord(e.b[e.used], st);
+  e.used++;
+}
+
+domino_status check_config(const domino_config *c) {
+  if (!c) return fail(DOMINO_ERR_INVALID_ARG, "config is NULL");
+  if (c->hidden <= 0 || c->n_layers <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
+      c->ffn <= 0 || c->vocab <= 1 || c->gru_hidden <= 0 || c->rank <= 0)
+    return fail(DOMINO_ERR_INVALID_ARG, "config sizes must be positive");
+  if (c->block < 2 || c->block > 64) return fail(DOMINO_ERR_INVALID_ARG, "block must be in [2, 64]");
+  if (c->mask_token_id < 0 || c->mask_token_id >= c->vocab)
+    return fail(DOMINO_ERR_INVALID_ARG, "mask_token_id must be in [0, vocab)");
+  if (c->dtype != DOMINO_F32 && c->dtype != DOMINO_BF16) return fail(DOMINO_ERR_INVALID_ARG, "bad dtype");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return fail(DOMINO_ERR_INVALID_ARG, "bad eps/theta");
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(DOMINO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c->n_q_heads % c->n_kv_heads) return fail(DOMINO_ERR_UNSUPPORTED, "n_q_heads must be a multiple of n_kv_heads");
+  const int ks = c->dtype == DOMINO_BF16 ? 32 : 16;
+  if (c->hidden % 32 || c->ffn % 32 || c->gru_hidden % 32 || (c->n_q_heads * c->head_dim) % 32)
+    return fail(DOMINO_ERR_UNSUPPORTED, "hidden, ffn, gru_hidden and n_q_heads*head_dim must be multiples of 32");
+  if (c->rank % ks || c->rank > 16 * ks)
+    return fail(DOMINO_ERR_UNSUPPORTED, "rank must be a multiple of %d and at most %d", ks, 16 * ks);
+  const int G = (c->n_q_heads / c->n_kv_heads) * c->block;
+  if (G > 128) return fail(DOMINO_ERR_UNSUPPORTED, "(n_q_heads/n_kv_heads)*block must be at most 128");
+  return DOMINO_OK;
+}
+
+Dims make_dims(const domino_model *m, int bs) {
+  Dims D = m->D;
+  D.bs = bs;
+  return D;
+}
+
+// ---- workspace layout of the draft step
+struct WsLayout {
+  size_t err, bar, tickets, n_tickets, X, A, QKV, Q, Kb, Vb, attn, O, F, H, Lb, P, hbuf, ubuf, pval, pid,
+      ctxkv, part, total;
+  int G;
+  size_t head_lds;
+};
+
+struct Plans {
+  GemmPlan qkv, wo, gateup, down, lm, w1h, ctx;
+};
+
+Plans make_plans(const domino_model *m, int bs, int max_new) {
+  const Dims &D = m->D;
+  const int M = bs * D.B, Mh = bs * (D.B - 1);
+  Plans p;
+  p.qkv = plan_gemm(m->qkv[0].NT, m->qkv[0].KS, M, EPI_STORE, m->n_cu);
+  p.wo = plan_gemm(m->wo[0].NT, m->wo[0].KS, M, EPI_ADD, m->n_cu);
+  p.gateup = plan_gemm(m->gateup[0].NT, m->gateup[0].KS, M, EPI_SWIGLU, m->n_cu);
+  p.down = plan_gemm(m->down[0].NT, m->down[0].KS, M, EPI_ADD, m->n_cu);
+  p.lm = plan_gemm(m->lm.NT, m->lm.KS, Mh, EPI_STORE, m->n_cu);
+  p.w1h = plan_gemm(m->w1h.NT, m->w1h.KS, Mh, EPI_STORE, m->n_cu);
+  const int kvt = 2 * D.nkv * D.dh / 16;
+  p.ctx = plan_gemm(kvt, m->qkv[0].KS, bs * (max_new > 0 ? max_new : 1), EPI_STORE, m->n_cu);
+  return p;
+}
+
+bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, WsLayout &w) {
+  Dims D = make_dims(m, bs);
+  const int M = bs * D.B, Mh = bs * (D.B - 1);
+  Plans p = make_plans(m, bs, max_new);
+  size_t tickets = 0, part = 0;
+  for (const GemmPlan *g : {&p.qkv, &p.wo, &p.gateup, &p.down, &p.lm, &p.w1h, &p.ctx}) {
+    tickets = std::max(tickets, g->tickets);
+    part = std::max(part, g->part_floats);
+  }
+  w.G = head_grid(D, m->n_cu, &w.head_lds);
+  if (w.head_lds > 160 * 1024) return false;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  w.err = take(64);
+  w.bar = take(64);
+  w.n_tickets = tickets;
+  w.tickets = take(tickets * 4);
+  const size_t hdr_end = o;
+  (void)hdr_end;
+  const int qkvw = (D.nq + 2 * D.nkv) * D.dh;
+  w.X = take((size_t)M * D.d * 4);
+  w.A = take((size_t)M * D.d * 4);
+  w.QKV = take((size_t)M * qkvw * 4);
+  w.Q = take((size_t)M * D.nq * D.dh * 4);
+  w.Kb = take((size_t)M * D.nkv * D.dh * 4);
+  w.Vb = take((size_t)M * D.nkv * D.dh * 4);
+  w.attn = take(attn_part_floats(D, max_ctx) * 4);
+  w.O = take((size_t)M * D.nq * D.dh * 4);
+  w.F = take((size_t)M * D.ffn * 4);
+  w.H = take((size_t)Mh * D.d * 4);
+  w.Lb = take((size_t)Mh * D.V * 4);
+  w.P = take((size_t)Mh * D.r * 4);
+  w.hbuf = take((size_t)2 * bs * D.ds * 4);
+  w.ubuf = take((size_t)bs * D.r * 4);
+  w.pval = take((size_t)bs * w.G * beta * 4);
+  w.pid = take((size_t)bs * w.G * beta * 4);
+  w.ctxkv = take((size_t)bs * (max_new > 0 ? max_new : 0) * 2 * D.nkv * D.dh * 4);
+  w.part = take(part * 4);
+  w.total = o;
+  return true;
+}
+
+GemmArgs gemm_args(const void *P, const Packed &pk, int tile0, int ntiles, int N, const float *X, int ldx,
+                   int M, int K, float *Y, int ldy, const GemmPlan &pl, float *part, int *tickets) {
+  GemmArgs a;
+  a.P = P;
+  a.KS = pk.KS;
+  a.tile0 = tile0;
+  a.ntiles = ntiles;
+  a.N = N;
+  a.X = X;
+  a.ldx = ldx;
+  a.M = M;
+  a.K = K;
+  a.Y = Y;
+  a.ldy = ldy;
+  a.ksplit = pl.ksplit;
+  a.part = part;
+  a.tickets = tickets;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *domino_last_error(void) { return g_err.c_str(); }
+
+domino_status domino_model_create(const domino_config *cfg, const domino_weights *w, domino_model_t *out) {
+  if (!out) return fail(DOMINO_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  domino_status s = check_config(cfg);
+  if (s != DOMINO_OK) return s;
+  if (!w) return fail(DOMINO_ERR_INVALID_ARG, "weights is NULL");
+  const int L = cfg->n_layers;
+  if (!w->embed || !w->lm_head || !w->final_norm || !w->gru_w_ih || !w->gru_w_hh || !w->gru_b_ih ||
+      !w->gru_b_hh || !w->w1 || !w->w2)
+    return fail(DOMINO_ERR_INVALID_ARG, "a weight pointer is NULL");
+  const void *const *arrs[] = {w->attn_norm, w->wq, w->wk, w->wv, w->q_norm, w->k_norm,
+                               w->wo, w->ffn_norm, w->w_gate, w->w_up, w->w_down};
+  for (auto a : arrs) {
+    if (!a) return fail(DOMINO_ERR_INVALID_ARG, "a per-layer weight array is NULL");
+    for (int l = 0; l < L; ++l)
+      if (!a[l]) return fail(DOMINO_ERR_INVALID_ARG, "a per-layer weight pointer is NULL (layer %d)", l);
+  }
+
+  domino_model *m = new domino_model();
+  m->cfg = *cfg;
+  m->bf16 = cfg->dtype == DOMINO_BF16;
+  m->esz = m->bf16 ? 2 : 4;
+  Dims &D = m->D;
+  D.bs = 0;
+  D.B = cfg->block;
+  D.d = cfg->hidden;
+  D.nq = cfg->n_q_heads;
+  D.nkv = cfg->n_kv_heads;
+  D.dh = cfg->head_dim;
+  D.ffn = cfg->ffn;
+  D.V = cfg->vocab;
+  D.ds = cfg->gru_hidden;
+  D.r = cfg->rank;
+  D.mask_id = cfg->mask_token_id;
+  D.eps = cfg->rms_eps;
+  D.theta = cfg->rope_theta;
+  D.bf16 = m->bf16;
+  m->embed = w->embed;
+  m->final_norm = w->final_norm;
+  m->b_ih = w->gru_b_ih;
+  m->b_hh = w->gru_b_hh;
+  for (int l = 0; l < L; ++l) {
+    m->attn_norm.push_back(w->attn_norm[l]);
+    m->q_norm.push_back(w->q_norm[l]);
+    m->k_norm.push_back(w->k_norm[l]);
+    m->ffn_norm.push_back(w->ffn_norm[l]);
+  }
+
+  int dev = 0;
+  hipError_t he = hipGetDevice(&dev);
+  if (he == hipSuccess) he = hipDeviceGetAttribute(&m->n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (he != hipSuccess) {
+    delete m;
+    return fail(DOMINO_ERR_HIP, "querying the device: %s", hipGetErrorString(he));
+  }
+
+  // ---- plan packed storage
+  const int KSTEP = kstep(m);
+  auto ks_of = [&](int K) { return (K + KSTEP - 1) / KSTEP; };
+  size_t off = 0;
+  auto add = [&](int N, int K) {
+    Packed p;
+    p.NT = (N + 15) / 16;
+    p.KS = ks_of(K);
+    p.off = off;
+    off = align_up(off + (size_t)p.NT * p.KS * 1024);
+    return p;
+  };
+  const int qd = D.nq * D.dh, kvd = D.nkv * D.dh;
+  for (int l = 0; l < L; ++l) {
+    m->qkv.push_back(add(qd + 2 * kvd, D.d));
+    m->wo.push_back(add(D.d, qd));
+    Packed gu = add(2 * ((D.ffn + 15) / 16) * 16, D.d);
+    m->gateup.push_back(gu);
+    m->down.push_back(add(D.d, D.ffn));
+  }
+  m->lm = add(D.V, D.d);
+  m->w1h = add(D.r, D.d);
+  m->w2 = add(D.V, D.r);
+  m->w_ih_off = off;
+  off = align_up(off + (size_t)3 * D.ds * D.d * m->esz);
+  m->w_hh_off = off;
+  off = align_up(off + (size_t)3 * D.ds * D.ds * m->esz);
+  m->w1_off = off;
+  off = align_up(off + (size_t)D.r * (D.d + D.ds) * m->esz);
+  m->mem_bytes = off;
+
+  he = hipMalloc(&m->mem, m->mem_bytes);
+  if (he != hipSuccess) {
+    delete m;
+    return fail(DOMINO_ERR_HIP, "hipMalloc(%zu): %s", off, hipGetErrorString(he));
+  }
+  hipStream_t st = nullptr;
+  char *base = (char *)m->mem;
+  const bool bf = m->bf16;
+  for (int l = 0; l < L; ++l) {
+    const Packed &p = m->qkv[l];
+    // rows: [wq | wk | wv]; each block starts on a tile boundary (qd, kvd multiples of 16)
+    launch_pack(bf, w->wq[l], qd, D.d, D.d, base + p.off, qd / 16, p.KS, 1, 0, st);
+    launch_pack(bf, w->wk[l], kvd, D.d, D.d, base + p.off + (size_t)(qd / 16) * p.KS * 1024, kvd / 16, p.KS, 1, 0,
+                st);
+    launch_pack(bf, w->wv[l], kvd, D.d, D.d, base + p.off + (size_t)((qd + kvd) / 16) * p.KS * 1024, kvd / 16,
+                p.KS, 1, 0, st);
+    const Packed &o = m->wo[l];
+    launch_pack(bf, w->wo[l], D.d, qd, qd, base + o.off, o.NT, o.KS, 1, 0, st);
+    const Packed &g = m->gateup[l];
+    const int ft = (D.ffn + 15) / 16;
+    launch_pack(bf, w->w_gate[l], D.ffn, D.d, D.d, base + g.off, ft, g.KS, 2, 0, st);
+    launch_pack(bf, w->w_up[l], D.ffn, D.d, D.d, base + g.off, ft, g.KS, 2, 1, st);
+    const Packed &dn = m->down[l];
+    launch_pack(bf, w->w_down[l], D.d, D.ffn, D.ffn, base + dn.off, dn.NT, dn.KS, 1, 0, st);
+  }
+  launch_pack(bf, w->lm_head, D.V, D.d, D.d, base + m->lm.off, m->lm.NT, m->lm.KS, 1, 0, st);
+  launch_pack(bf, w->w1, D.r, D.d, D.d + D.ds, base + m->w1h.off, m->w1h.NT, m->w1h.KS, 1, 0, st);
+  launch_pack(bf, w->w2, D.V, D.r, D.r, base + m->w2.off, m->w2.NT, m->w2.KS, 1, 0, st);
+  he = hipGetLastError();
+  if (he == hipSuccess) he = hipMemcpy(base + m->w_ih_off, w->gru_w_ih, (size_t)3 * D.ds * D.d * m->esz, hipMemcpyDeviceToDevice);
+  if (he == hipSuccess) he = hipMemcpy(base + m->w_hh_off, w->gru_w_hh, (size_t)3 * D.ds * D.ds * m->esz, hipMemcpyDeviceToDevice);
+  if (he == hipSuccess) he = hipMemcpy(base + m->w1_off, w->w1, (size_t)D.r * (D.d + D.ds) * m->esz, hipMemcpyDeviceToDevice);
+  if (he == hipSuccess) he = hipDeviceSynchronize();
+  if (he != hipSuccess) {
+    (void)hipFree(m->mem);
+    delete m;
+    return fail(DOMINO_ERR_HIP, "packing weights: %s", hipGetErrorString(he));
+  }
+  *out = m;
+  return DOMINO_OK;
+}
+
+void domino_model_destroy(domino_model_t m) {
+  if (!m) return;
+  for (auto &e : m->ev) {
+    for (auto x : e.a) (void)hipEventDestroy(x);
+    for (auto x : e.b) (void)hipEventDestroy(x);
+  }
+  if (m->mem) (void)hipFree(m->mem);
+  delete m;
+}
+
+size_t domino_workspace_bytes(domino_model_t m, int32_t batch, int32_t max_ctx, int32_t max_new, int32_t branch) {
+  if (!m || batch < 1 || max_ctx < 0 || max_new < 0 || max_new > max_ctx || branch < 1 || branch > 8) return 0;
+  WsLayout w;
+  if (!layout(m, batch, max_ctx, max_new, branch, w)) return 0;
+  return w.total;
+}
+
+domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
+                                void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new,
+                                int32_t branch, const int32_t *forced_tokens, int32_t *topk_ids, float *topk_vals,
+                                const domino_debug *debug, void *workspace, size_t workspace_bytes, void *stream) {
+  if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
+  if (batch < 1) return fail(DOMINO_ERR_INVALID_ARG, "batch must be >= 1");
+  if (!anchor_ids || !ctx_lens) return fail(DOMINO_ERR_INVALID_ARG, "anchor_ids/ctx_lens is NULL");
+  if (max_ctx < 0) return fail(DOMINO_ERR_INVALID_ARG, "max_ctx must be >= 0");
+  if (max_ctx > 0 && (!ctx_k || !ctx_v)) return fail(DOMINO_ERR_INVALID_ARG, "ctx_k/ctx_v is NULL");
+  if (n_new < 0 || n_new > max_ctx) return fail(DOMINO_ERR_INVALID_ARG, "n_new must be in [0, max_ctx]");
+  if (n_new > 0 && !ctx_hidden_new) return fail(DOMINO_ERR_INVALID_ARG, "ctx_hidden_new is NULL");
+  if (branch < 1 || branch > 8 || branch > m->D.V) return fail(DOMINO_ERR_INVALID_ARG, "branch must be in [1, 8]");
+  if (!topk_ids || !topk_vals) return fail(DOMINO_ERR_INVALID_ARG, "topk_ids/topk_vals is NULL");
+  if (!workspace) return fail(DOMINO_ERR_WORKSPACE, "workspace is NULL");
+  WsLayout w;
+  if (!layout(m, batch, max_ctx, n_new, branch, w))
+    return fail(DOMINO_ERR_UNSUPPORTED, "batch %d needs more LDS than a compute unit has", batch);
+  if (workspace_bytes < w.total)
+    return fail(DOMINO_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, w.total);
+
+  hipStream_t st = (hipStream_t)stream;
+  Dims D = make_dims(m, batch);
+  const Plans p = make_plans(m, batch, n_new);
+  char *ws = (char *)workspace;
+  auto F = [&](size_t off) { return (float *)(ws + off); };
+  int32_t *err = (int32_t *)(ws + w.err);
+  int *tickets = (int *)(ws + w.tickets);
+  float *part = F(w.part);
+  const char *base = (const char *)m->mem;
+  const int M = batch * D.B, Mh = batch * (D.B - 1);
+  const int qd = D.nq * D.dh, kvd = D.nkv * D.dh, qkvw = qd + 2 * kvd;
+  const size_t layer_elems = (size_t)batch * max_ctx * kvd;
+
+  // clear error word, barrier words and split-K tickets
+  launch_fill_u32((uint32_t *)ws, (w.tickets + w.n_tickets * 4) / 4, 0u, st);
+
+  // context rows projected from target hidden states (optional)
+  if (n_new > 0) {
+    for (int l = 0; l < m->cfg.n_layers; ++l) {
+      prof_begin(m, DOMINO_KC_CTXPROJ, st);
+      GemmArgs a = gemm_args(base + m->qkv[l].off, m->qkv[l], qd / 16, 2 * kvd / 16, 2 * kvd,
+                             (const float *)ctx_hidden_new, D.d, batch * n_new, D.d, F(w.ctxkv), 2 * kvd, p.ctx,
+                             part, tickets);
+      launch_gemm(m->bf16, EPI_STORE, a, p.ctx, st);
+      launch_ctx_store(D, F(w.ctxkv), n_new, m->k_norm[l], ctx_lens, max_ctx,
+                       (char *)ctx_k + l * layer_elems * m->esz, (char *)ctx_v + l * layer_elems * m->esz, err, st);
+      prof_end(m, DOMINO_KC_CTXPROJ, st);
+    }
+  }
+
+  prof_begin(m, DOMINO_KC_EMBED, st);
+  launch_embed_block(D, m->embed, anchor_ids, F(w.X), err, st);
+  prof_end(m, DOMINO_KC_EMBED, st);
+
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    const char *ck = (const char *)ctx_k + l * layer_elems * m->esz;
+    const char *cv = (const char *)ctx_v + l * layer_elems * m->esz;
+    prof_begin(m, DOMINO_KC_NORM, st);
+    launch_rmsnorm(D, F(w.X), D.d, m->attn_norm[l], F(w.A), D.d, M, D.d, false, st);
+    prof_end(m, DOMINO_KC_NORM, st);
+
+    prof_begin(m, DOMINO_KC_QKV, st);
+    GemmArgs a = gemm_args(base + m->qkv[l].off, m->qkv[l], 0, m->qkv[l].NT, qkvw, F(w.A), D.d, M, D.d, F(w.QKV),
+                           qkvw, p.qkv, part, tickets);
+    launch_gemm(m->bf16, EPI_STORE, a, p.qkv, st);
+    prof_end(m, DOMINO_KC_QKV, st);
+
+    prof_begin(m, DOMINO_KC_ROPE, st);
+    launch_qk_norm_rope(D, F(w.QKV), m->q_norm[l], m->k_norm[l], ctx_lens, max_ctx, F(w.Q), F(w.Kb), F(w.Vb), st);
+    prof_end(m, DOMINO_KC_ROPE, st);
+
+    prof_begin(m, DOMINO_KC_ATTN, st);
+    launch_attention(D, F(w.Q), F(w.Kb), F(w.Vb), ck, cv, ctx_lens, max_ctx, F(w.attn), F(w.O), err, st);
+    prof_end(m, DOMINO_KC_ATTN, st);
+
+    prof_begin(m, DOMINO_KC_WO, st);
+    a = gemm_args(base + m->wo[l].off, m->wo[l], 0, m->wo[l].NT, D.d, F(w.O), qd, M, qd, F(w.X), D.d, p.wo, part,
+                  tickets);
+    launch_gemm(m->bf16, EPI_ADD, a, p.wo, st);
+    prof_end(m, DOMINO_KC_WO, st);
+
+    prof_begin(m, DOMINO_KC_NORM, st);
+    launch_rmsnorm(D, F(w.X), D.d, m->ffn_norm[l], F(w.A), D.d, M, D.d, false, st);
+    prof_end(m, DOMINO_KC_NORM, st);
+
+    prof_begin(m, DOMINO_KC_GATEUP, st);
+    a = gemm_args(base + m->gateup[l].off, m->gateup[l], 0, m->gateup[l].NT, D.ffn, F(w.A), D.d, M, D.d, F(w.F),
+                  D.ffn, p.gateup, part, tickets);
+    launch_gemm(m->bf16, EPI_SWIGLU, a, p.gateup, st);
+    prof_end(m, DOMINO_KC_GATEUP, st);
+
+    prof_begin(m, DOMINO_KC_DOWN, st);
+    a = gemm_args(base + m->down[l].off, m->down[l], 0, m->down[l].NT, D.d, F(w.F), D.ffn, M, D.ffn, F(w.X), D.d,
+                  p.down, part, tickets);
+    launch_gemm(m->bf16, EPI_ADD, a, p.down, st);
+    prof_end(m, DOMINO_KC_DOWN, st);
+  }
+
+  float *H = (debug && debug->hidden) ? debug->hidden : F(w.H);
+  prof_begin(m, DOMINO_KC_NORM, st);
+  launch_rmsnorm(D, F(w.X), D.d, m->final_norm, H, D.d, Mh, D.d, true, st);
+  prof_end(m, DOMINO_KC_NORM, st);
+
+  float *Lb = (debug && debug->base_logits) ? debug->base_logits : F(w.Lb);
+  prof_begin(m, DOMINO_KC_LMHEAD, st);
+  GemmArgs a = gemm_args(base + m->lm.off, m->lm, 0, m->lm.NT, D.V, H, D.d, Mh, D.d, Lb, D.V, p.lm, part, tickets);
+  launch_gemm(m->bf16, EPI_STORE, a, p.lm, st);
+  prof_end(m, DOMINO_KC_LMHEAD, st);
+
+  prof_begin(m, DOMINO_KC_W1H, st);
+  a = gemm_args(base + m->w1h.off, m->w1h, 0, m->w1h.NT, D.r, H, D.d, Mh, D.d, F(w.P), D.r, p.w1h, part, tickets);
+  launch_gemm(m->bf16, EPI_STORE, a, p.w1h, st);
+  prof_end(m, DOMINO_KC_W1H, st);
+
+  HeadArgs h;
+  h.D = D;
+  h.beta = branch;
+  h.embed = m->embed;
+  h.w_ih = base + m->w_ih_off;
+  h.w_hh = base + m->w_hh_off;
+  h.b_ih = m->b_ih;
+  h.b_hh = m->b_hh;
+  h.w1s_rows = base + m->w1_off;
+  h.w2p = base + m->w2.off;
+  h.P = F(w.P);
+  h.Lbase = Lb;
+  h.anchor = anchor_ids;
+  h.forced = forced_tokens;
+  h.topk_ids = topk_ids;
+  h.topk_vals = topk_vals;
+  h.final_logits = debug ? debug->final_logits : nullptr;
+  h.states = debug ? debug->states : nullptr;
+  h.hbuf = F(w.hbuf);
+  h.ubuf = F(w.ubuf);
+  h.pval = F(w.pval);
+  h.pid = (int32_t *)(ws + w.pid);
+  h.ybuf = nullptr;
+  h.barrier = (unsigned *)(ws + w.bar);
+  h.err = err;
+  h.G = w.G;
+  prof_begin(m, DOMINO_KC_HEADLOOP, st);
+  hipError_t he = launch_head(h, w.head_lds, st);
+  prof_end(m, DOMINO_KC_HEADLOOP, st);
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "head loop launch: %s", hipGetErrorString(he));
+  he = hipGetLastError();
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "draft step launch: %s", hipGetErrorString(he));
+  return DOMINO_OK;
+}
+
+domino_status domino_build_tree(int32_t batch, int32_t depth, int32_t branch, const int32_t *topk_ids,
+                                const int32_t *anchor_ids, const int32_t *ctx_lens, int32_t *node_token,
+                                int32_t *node_parent, int32_t *node_depth, int32_t *node_pos, uint8_t *ancestor_mask,
+                                void *stream) {
+  if (batch < 1) return fail(DOMINO_ERR_INVALID_ARG, "batch must be >= 1");
+  if (depth < 1 || depth > 63) return fail(DOMINO_ERR_INVALID_ARG, "depth must be in [1, 63]");
+  if (branch < 1 || branch > 8) return fail(DOMINO_ERR_INVALID_ARG, "branch must be in [1, 8]");
+  if (!topk_ids || !anchor_ids || !ctx_lens || !node_token || !node_parent || !node_depth || !node_pos)
+    return fail(DOMINO_ERR_INVALID_ARG, "a required pointer is NULL");
+  launch_build_tree(batch, depth, branch, topk_ids, anchor_ids, ctx_lens, node_token, node_parent, node_depth,
+                    node_pos, ancestor_mask, (hipStream_t)stream);
+  hipError_t he = hipGetLastError();
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "build_tree launch: %s", hipGetErrorString(he));
+  return DOMINO_OK;
+}
+
+size_t domino_verify_workspace_bytes(int32_t batch, int32_t n_nodes, int32_t vocab) {
+  if (batch < 1 || n_nodes < 1 || n_nodes > 1024 || vocab < 1) return 0;
+  return accept_ws_bytes(batch, n_nodes, vocab);
+}
+
+domino_status domino_verify_accept(int32_t batch, int32_t n_nodes, int32_t vocab, int32_t block,
+                                   const int32_t *node_token, const int32_t *node_parent, const void *target_logits,
+                                   domino_dtype logits_dtype, int32_t *accept_len, int32_t *accepted_nodes,
+                                   int32_t *out_tokens, void *workspace, size_t workspace_bytes, void *stream) {
+  if (batch < 1) return fail(DOMINO_ERR_INVALID_ARG, "batch must be >= 1");
+  if (n_nodes < 1 || n_nodes > 1024) return fail(DOMINO_ERR_INVALID_ARG, "n_nodes must be in [1, 1024]");
+  if (vocab < 1) return fail(DOMINO_ERR_INVALID_ARG, "vocab must be >= 1");
+  if (block < 2 || block > 64) return fail(DOMINO_ERR_INVALID_ARG, "block must be in [2, 64]");
+  if (logits_dtype != DOMINO_F32 && logits_dtype != DOMINO_BF16) return fail(DOMINO_ERR_INVALID_ARG, "bad logits dtype");
+  if (!node_token || !node_parent || !target_logits || !accept_len || !accepted_nodes || !out_tokens)
+    return fail(DOMINO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (!workspace) return fail(DOMINO_ERR_WORKSPACE, "workspace is NULL");
+  const size_t need = accept_ws_bytes(batch, n_nodes, vocab);
+  if (workspace_bytes < need) return fail(DOMINO_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  hipStream_t st = (hipStream_t)stream;
+  launch_fill_u32((uint32_t *)workspace, 1, 0u, st);
+  launch_accept(batch, n_nodes, vocab, block, node_token, node_parent, target_logits, logits_dtype == DOMINO_BF16,
+                accept_len, accepted_nodes, out_tokens, workspace, st);
+  hipError_t he = hipGetLastError();
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "verify_accept launch: %s", hipGetErrorString(he));
+  return DOMINO_OK;
+}
+
+domino_status domino_workspace_error(const void *workspace, void *stream, int32_t *out) {
+  if (!workspace || !out) return fail(DOMINO_ERR_INVALID_ARG, "workspace/out is NULL");
+  int32_t v = 0;
+  HIP_TRY(hipMemcpyAsync(&v, workspace, 4, hipMemcpyDeviceToHost, (hipStream_t)stream));
+  HIP_TRY(hipStreamSynchronize((hipStream_t)stream));
+  *out = v;
+  if (v) return fail(DOMINO_ERR_DEVICE, "device error word 0x%x", v);
+  return DOMINO_OK;
+}
+
+domino_status domino_workspace_clear_error(void *workspace, void *stream) {
+  if (!workspace) return fail(DOMINO_ERR_INVALID_ARG, "workspace is NULL");
+  launch_fill_u32((uint32_t *)workspace, 1, 0u, (hipStream_t)stream);
+  HIP_TRY(hipGetLastError());
+  return DOMINO_OK;
+}
+
+domino_status domino_profile_enable(domino_model_t m, uint32_t class_mask) {
+  if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
+  for (int c = 0; c < DOMINO_KC_COUNT; ++c) {
+    if (!(class_mask & (1u << c))) continue;
+    auto &e = m->ev[c];
+    while (e.a.size() < 4096) {
+      hipEvent_t x, y;
+      HIP_TRY(hipEventCreate(&x));
+      HIP_TRY(hipEventCreate(&y));
+      e.a.push_back(x);
+      e.b.push_back(y);
+    }
+  }
+  m->prof_mask = class_mask;
+  return DOMINO_OK;
+}
+
+domino_status domino_profile_reset(domino_model_t m) {
+  if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
+  for (auto &e : m->ev) e.used = 0;
+  return DOMINO_OK;
+}
+
+domino_status domino_profile_read(domino_model_t m, int32_t kernel_class, double *total_ms, int32_t *launches) {
+  if (!m || !total_ms || !launches) return fail(DOMINO_ERR_INVALID_ARG, "NULL argument");
+  if (kernel_class < 0 || kernel_class >= DOMINO_KC_COUNT) return fail(DOMINO_ERR_INVALID_ARG, "bad kernel class");
+  auto &e = m->ev[kernel_class];
+  double tot = 0;
+  for (int i = 0; i < e.used; ++i) {
+    HIP_TRY(hipEventSynchronize(e.b[i]));
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, e.a[i], e.b[i]));
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = e.used;
+  return DOMINO_OK;
+}
+
+}  // extern "C"

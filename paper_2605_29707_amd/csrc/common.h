@@ -1,0 +1,89 @@
+// Shared device helpers for the gfx950 kernels: storage types, bf16
+// conversion, matrix-core operand types, wave reductions and the selection
+// order used by every top-k / argmax.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define DEVI __device__ __forceinline__
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// bf16 values are stored as raw 16-bit patterns.
+struct bf16_t {
+  uint16_t v;
+};
+
+DEVI float to_f32(float x) { return x; }
+DEVI float to_f32(bf16_t x) { return __uint_as_float(((uint32_t)x.v) << 16); }
+
+DEVI bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return bf16_t{(uint16_t)((u >> 16) | 0x40)};  // quiet NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return bf16_t{(uint16_t)(u >> 16)};
+}
+DEVI void store_as(float *p, float v) { *p = v; }
+DEVI void store_as(bf16_t *p, float v) { *p = f32_to_bf16(v); }
+
+// Split 8 fp32 values into high and low bf16 parts: x = hi + lo + O(2^-17 |x|).
+// Products of an exact bf16 weight with hi and lo are exact in fp32, so two
+// matrix-core passes reproduce an fp32-accurate dot product.
+DEVI void split8(const float *x, bf16x8 &hi, bf16x8 &lo) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    __bf16 h = (__bf16)x[e];
+    hi[e] = h;
+    lo[e] = (__bf16)(x[e] - (float)h);
+  }
+}
+
+DEVI float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+DEVI float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Selection order: larger value first, then smaller id; NaN counts as -inf.
+DEVI float order_val(float v) { return (v != v) ? -INFINITY : v; }
+DEVI bool better(float va, int ia, float vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+
+// Reduce a (value, id) pair to the wave's best under the selection order.
+DEVI void wave_best(float &v, int &i) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    float ov = __shfl_xor(v, o, 64);
+    int oi = __shfl_xor(i, o, 64);
+    if (better(ov, oi, v, i)) {
+      v = ov;
+      i = oi;
+    }
+  }
+}
+
+// Device error word bits (mirrors include/domino.h).
+enum : int32_t {
+  DEV_BAD_TOKEN = 1,
+  DEV_BAD_CTX_LEN = 2,
+  DEV_BAD_TREE = 4,
+  DEV_BARRIER_TIMEOUT = 8
+};
+
+DEVI void raise_error(int32_t *err, int32_t bit) { atomicOr(err, bit); }
+
+DEVI int clamp_token(int t, int vocab, int32_t *err) {
+  if (t < 0 || t >= vocab) {
+    raise_error(err, DEV_BAD_TOKEN);
+    return t < 0 ? 0 : vocab - 1;
+  }
+  return t;
+}

@@ -1,0 +1,109 @@
+// Launch interfaces between the host C-ABI (api.hip) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dk {
+
+enum { EPI_STORE = 0, EPI_ADD = 1, EPI_SWIGLU = 2 };
+
+struct GemmArgs {
+  const void *P;   // packed weights
+  int KS;          // k-steps per packed tile
+  int tile0;       // first packed tile of this launch
+  int ntiles;      // packed tiles computed by this launch
+  int N;           // valid output columns
+  const float *X;  // activations fp32 [M][ldx]
+  int ldx, M, K;
+  float *Y;        // output fp32 [M][ldy]
+  int ldy;
+  int ksplit;      // workgroups sharing one tile group's K range
+  float *part;     // [ksplit][Mpad][ntiles*16] partial sums (ksplit > 1)
+  int *tickets;    // [mgroups][groups], zero before the first launch
+};
+
+struct GemmPlan {
+  int T, MT, groups, mgroups, ksplit;
+  size_t part_floats, tickets;
+};
+
+GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu);
+void launch_gemm(bool bf16, int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st);
+void launch_pack(bool bf16, const void *W, int N, int K, int ldw, void *P, int NT, int KS,
+                 int tile_mul, int tile_off, hipStream_t st);
+inline int kstep_of(bool bf16) { return bf16 ? 32 : 16; }
+
+// ---- backbone pieces (backbone.hip)
+struct Dims {
+  int bs, B, d, nq, nkv, dh, ffn, V, ds, r, mask_id;
+  float eps, theta;
+  bool bf16;
+};
+
+void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor, float *X,
+                        int32_t *err, hipStream_t st);
+// y[row] = rmsnorm(x[map(row)]) * gain; when skip_anchor, output row i reads
+// input row i + i/(B-1) + 1 (the draft rows of each block).
+void launch_rmsnorm(const Dims &D, const float *x, int ldx, const void *gain, float *y, int ldy,
+                    int rows, int width, bool skip_anchor, hipStream_t st);
+// q/k RMSNorm + RoPE on the QKV projection; writes Q [M][nq][dh], Kb/Vb [M][nkv][dh]
+void launch_qk_norm_rope(const Dims &D, const float *qkv, const void *q_norm, const void *k_norm,
+                         const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb, float *Vb,
+                         hipStream_t st);
+// context K/V from projected hidden rows: kv [bs*n_new][2*nkv*dh] fp32 -> cache
+void launch_ctx_store(const Dims &D, const float *kv, int n_new, const void *k_norm,
+                      const int32_t *ctx_lens, int max_ctx, void *ck, void *cv, int32_t *err,
+                      hipStream_t st);
+int attn_chunk_len();
+int attn_nchunks(int max_ctx, int B);
+void launch_attention(const Dims &D, const float *Q, const float *Kb, const float *Vb,
+                      const void *ck, const void *cv, const int32_t *ctx_lens, int max_ctx,
+                      float *part, float *O, int32_t *err, hipStream_t st);
+size_t attn_part_floats(const Dims &D, int max_ctx);
+
+// ---- Domino head rollout (head.hip)
+struct HeadArgs {
+  Dims D;
+  int beta;
+  const void *embed;     // [V][d]
+  const void *w_ih;      // [3ds][d]
+  const void *w_hh;      // [3ds][ds]
+  const void *b_ih, *b_hh;
+  const void *w1s_rows;  // W1 (full [r][d+ds]); the S half starts at column d
+  const void *w2p;       // W2 packed (tile-major, KS = r / KSTEP)
+  const float *P;        // [bs][B-1][r]: W1[:, :d] H_j
+  const float *Lbase;    // [bs][B-1][V]
+  const int32_t *anchor; // [bs]
+  const int32_t *forced; // [bs][B-1] or null
+  int32_t *topk_ids;     // [bs][B-1][beta]
+  float *topk_vals;
+  float *final_logits;   // optional [bs][B-1][V]
+  float *states;         // optional [bs][B-1][ds]
+  // exchange buffers (workspace)
+  float *hbuf;           // [2][bs][ds]
+  float *ubuf;           // [bs][r]
+  float *pval;           // [bs][G][beta]
+  int32_t *pid;          // [bs][G][beta]
+  int32_t *ybuf;         // [bs]
+  unsigned *barrier;     // zeroed before launch
+  int32_t *err;
+  int G;                 // workgroups (co-resident)
+};
+int head_grid(const Dims &D, int n_cu, size_t *lds_bytes);
+hipError_t launch_head(const HeadArgs &h, size_t lds_bytes, hipStream_t st);
+size_t head_exchange_floats(const Dims &D, int G, int beta);
+
+// ---- tree and acceptance (tree.hip)
+void launch_build_tree(int bs, int depth, int beta, const int32_t *topk, const int32_t *anchor,
+                       const int32_t *ctx_lens, int32_t *tok, int32_t *par, int32_t *dep,
+                       int32_t *pos, uint8_t *mask, hipStream_t st);
+size_t accept_ws_bytes(int bs, int nn, int V);
+void launch_accept(int bs, int nn, int V, int B, const int32_t *tok, const int32_t *par,
+                   const void *logits, bool bf16, int32_t *acc_len, int32_t *acc_nodes,
+                   int32_t *out_tok, void *ws, hipStream_t st);
+
+// misc
+void launch_fill_u32(uint32_t *p, size_t n, uint32_t v, hipStream_t st);
+
+}  // namespace dk

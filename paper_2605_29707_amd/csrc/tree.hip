@@ -1,0 +1,266 @@
+// Draft-tree construction and greedy acceptance (Sec. 3.1: the longest valid
+// prefix plus the target's bonus token).  Integer / compare work only; every
+// argmax uses the total order (value desc, id asc) with NaN as -inf, so the
+// results are exact and independent of reduction order.
+#include "common.h"
+#include "kernels.h"
+
+namespace dk {
+
+// One workgroup per batch row.
+__global__ __launch_bounds__(256) void build_tree_kernel(int depth, int beta,
+                                                         const int32_t *__restrict__ topk,
+                                                         const int32_t *__restrict__ anchor,
+                                                         const int32_t *__restrict__ ctx_lens,
+                                                         int32_t *tok, int32_t *par, int32_t *dep,
+                                                         int32_t *pos, uint8_t *mask) {
+  const int b = blockIdx.x;
+  const int nn = 1 + depth * beta;
+  const int n = ctx_lens[b];
+  for (int i = threadIdx.x; i < nn; i += blockDim.x) {
+    int t, p, d;
+    if (i == 0) {
+      t = anchor[b];
+      p = -1;
+      d = 0;
+    } else {
+      d = (i - 1) / beta + 1;
+      const int rho = (i - 1) % beta;
+      t = topk[((size_t)b * depth + (d - 1)) * beta + rho];
+      p = d == 1 ? 0 : 1 + (d - 2) * beta;
+    }
+    tok[(size_t)b * nn + i] = t;
+    par[(size_t)b * nn + i] = p;
+    dep[(size_t)b * nn + i] = d;
+    pos[(size_t)b * nn + i] = n + d;
+  }
+  if (!mask) return;
+  for (int e = threadIdx.x; e < nn * nn; e += blockDim.x) {
+    const int i = e / nn, k = e % nn;
+    // ancestors of i: i itself, then the spine nodes of depths dep(i)-1 .. 1, then the root
+    uint8_t m = 0;
+    if (k == i || k == 0) {
+      m = 1;
+    } else if (i > 0) {
+      const int di = (i - 1) / beta + 1;
+      const int dk = (k - 1) / beta + 1;
+      const bool spine = ((k - 1) % beta) == 0;
+      m = (spine && dk < di) ? 1 : 0;
+    }
+    mask[((size_t)b * nn + i) * nn + k] = m;
+  }
+}
+
+void launch_build_tree(int bs, int depth, int beta, const int32_t *topk, const int32_t *anchor,
+                       const int32_t *ctx_lens, int32_t *tok, int32_t *par, int32_t *dep,
+                       int32_t *pos, uint8_t *mask, hipStream_t st) {
+  hipLaunchKernelGGL(build_tree_kernel, dim3(bs), dim3(256), 0, st, depth, beta, topk, anchor, ctx_lens,
+                     tok, par, dep, pos, mask);
+}
+
+// ---------------------------------------------------------------------------
+// acceptance
+// workspace: [err:int32][pad to 256 B][flags: uint8 bs*nn (padded)][partials: (float,int) bs*nn*nchunk]
+// ---------------------------------------------------------------------------
+constexpr int ACH = 4096;  // vocabulary elements per argmax chunk
+
+static size_t acc_flags_off() { return 256; }
+static size_t acc_part_off(int bs, int nn) {
+  return (acc_flags_off() + (size_t)bs * nn + 255) & ~(size_t)255;
+}
+size_t accept_ws_bytes(int bs, int nn, int V) {
+  const int nch = (V + ACH - 1) / ACH;
+  return acc_part_off(bs, nn) + (size_t)bs * nn * nch * 8;
+}
+
+template <typename LT>
+DEVI float ld_logit(const LT *p);
+template <>
+DEVI float ld_logit<float>(const float *p) {
+  return *p;
+}
+template <>
+DEVI float ld_logit<bf16_t>(const bf16_t *p) {
+  return to_f32(*p);
+}
+
+// Mark the nodes that have children (their rows are needed by the walk).
+__global__ __launch_bounds__(256) void mark_internal_kernel(int nn, const int32_t *__restrict__ par,
+                                                            uint8_t *flags, int32_t *err) {
+  const int b = blockIdx.x;
+  for (int i = threadIdx.x; i < nn; i += blockDim.x) flags[(size_t)b * nn + i] = 0;
+  __syncthreads();
+  for (int c = threadIdx.x; c < nn; c += blockDim.x) {
+    const int p = par[(size_t)b * nn + c];
+    const bool ok = (c == 0) ? (p == -1) : (p >= 0 && p < c);
+    if (!ok) {
+      raise_error(err, DEV_BAD_TREE);
+      continue;
+    }
+    if (c > 0) flags[(size_t)b * nn + p] = 1;
+  }
+}
+
+// Partial argmax of row (b, m) over one vocabulary chunk, for marked rows.
+template <typename LT>
+__global__ __launch_bounds__(256) void argmax_partial_kernel(int nn, int V, const LT *__restrict__ logits,
+                                                             const uint8_t *__restrict__ flags,
+                                                             float *part_v, int32_t *part_i) {
+  const int ch = blockIdx.x, m = blockIdx.y, b = blockIdx.z;
+  const int nch = gridDim.x;
+  if (!flags[(size_t)b * nn + m]) return;
+  const LT *row = logits + ((size_t)b * nn + m) * V;
+  const int v0 = ch * ACH, v1 = min(V, v0 + ACH);
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  for (int v = v0 + threadIdx.x; v < v1; v += 256) {
+    const float x = order_val(ld_logit<LT>(row + v));
+    if (better(x, v, bv, bi)) {
+      bv = x;
+      bi = v;
+    }
+  }
+  wave_best(bv, bi);
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = bv;
+    si[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w)
+      if (better(sv[w], si[w], bv, bi)) {
+        bv = sv[w];
+        bi = si[w];
+      }
+    const size_t o = ((size_t)b * nn + m) * nch + ch;
+    part_v[o] = bv;
+    part_i[o] = bi;
+  }
+}
+
+// Block-wide argmax of a whole row (for the final node when it is a leaf).
+template <typename LT>
+DEVI int row_argmax(const LT *row, int V, float *sv, int *si) {
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  for (int v = threadIdx.x; v < V; v += blockDim.x) {
+    const float x = order_val(ld_logit<LT>(row + v));
+    if (better(x, v, bv, bi)) {
+      bv = x;
+      bi = v;
+    }
+  }
+  wave_best(bv, bi);
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = bv;
+    si[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  bv = sv[0];
+  bi = si[0];
+  for (int w = 1; w < (int)(blockDim.x >> 6); ++w)
+    if (better(sv[w], si[w], bv, bi)) {
+      bv = sv[w];
+      bi = si[w];
+    }
+  __syncthreads();
+  return bi;
+}
+
+template <typename LT>
+__global__ __launch_bounds__(256) void accept_walk_kernel(int nn, int V, int B, const int32_t *__restrict__ tok,
+                                                          const int32_t *__restrict__ par,
+                                                          const LT *__restrict__ logits,
+                                                          const uint8_t *__restrict__ flags,
+                                                          const float *__restrict__ part_v,
+                                                          const int32_t *__restrict__ part_i,
+                                                          int32_t *acc_len, int32_t *acc_nodes,
+                                                          int32_t *out_tok) {
+  const int b = blockIdx.x;
+  const int nch = (V + ACH - 1) / ACH;
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  __shared__ int s_next;
+  int cur = 0, a = 0;
+  int R = 0;
+  while (true) {
+    // R = argmax of row cur
+    if (flags[(size_t)b * nn + cur]) {
+      float bv = -INFINITY;
+      int bi = INT_MAX;
+      const size_t o = ((size_t)b * nn + cur) * nch;
+      for (int c = threadIdx.x; c < nch; c += blockDim.x)
+        if (better(part_v[o + c], part_i[o + c], bv, bi)) {
+          bv = part_v[o + c];
+          bi = part_i[o + c];
+        }
+      wave_best(bv, bi);
+      if ((threadIdx.x & 63) == 0) {
+        sv[threadIdx.x >> 6] = bv;
+        si[threadIdx.x >> 6] = bi;
+      }
+      __syncthreads();
+      bv = sv[0];
+      bi = si[0];
+      for (int w = 1; w < 4; ++w)
+        if (better(sv[w], si[w], bv, bi)) {
+          bv = sv[w];
+          bi = si[w];
+        }
+      __syncthreads();
+      R = bi;
+    } else {
+      R = row_argmax<LT>(logits + ((size_t)b * nn + cur) * V, V, sv, si);
+    }
+    if (a >= B - 1) break;  // walk bound
+    // the child of cur whose token is R (children have distinct tokens; take the first)
+    if (threadIdx.x == 0) s_next = INT_MAX;
+    __syncthreads();
+    for (int c = threadIdx.x; c < nn; c += blockDim.x)
+      if (c > 0 && par[(size_t)b * nn + c] == cur && tok[(size_t)b * nn + c] == R) atomicMin(&s_next, c);
+    __syncthreads();
+    const int nx = s_next;
+    __syncthreads();
+    if (nx == INT_MAX || nx <= cur) break;
+    if (threadIdx.x == 0) {
+      acc_nodes[(size_t)b * (B - 1) + a] = nx;
+      out_tok[(size_t)b * B + a] = R;
+    }
+    ++a;
+    cur = nx;
+  }
+  if (threadIdx.x == 0) {
+    acc_len[b] = a;
+    out_tok[(size_t)b * B + a] = R;
+  }
+  for (int q = a + 1 + threadIdx.x; q < B; q += blockDim.x) out_tok[(size_t)b * B + q] = -1;
+  for (int q = a + threadIdx.x; q < B - 1; q += blockDim.x) acc_nodes[(size_t)b * (B - 1) + q] = -1;
+}
+
+void launch_accept(int bs, int nn, int V, int B, const int32_t *tok, const int32_t *par,
+                   const void *logits, bool bf16, int32_t *acc_len, int32_t *acc_nodes,
+                   int32_t *out_tok, void *ws, hipStream_t st) {
+  unsigned char *w = (unsigned char *)ws;
+  int32_t *err = (int32_t *)w;
+  uint8_t *flags = w + acc_flags_off();
+  const int nch = (V + ACH - 1) / ACH;
+  float *pv = (float *)(w + acc_part_off(bs, nn));
+  int32_t *pi = (int32_t *)(pv + (size_t)bs * nn * nch);
+  hipLaunchKernelGGL(mark_internal_kernel, dim3(bs), dim3(256), 0, st, nn, par, flags, err);
+  dim3 grid(nch, nn, bs);
+  if (bf16) {
+    hipLaunchKernelGGL(argmax_partial_kernel<bf16_t>, grid, dim3(256), 0, st, nn, V, (const bf16_t *)logits,
+                       flags, pv, pi);
+    hipLaunchKernelGGL(accept_walk_kernel<bf16_t>, dim3(bs), dim3(256), 0, st, nn, V, B, tok, par,
+                       (const bf16_t *)logits, flags, pv, pi, acc_len, acc_nodes, out_tok);
+  } else {
+    hipLaunchKernelGGL(argmax_partial_kernel<float>, grid, dim3(256), 0, st, nn, V, (const float *)logits,
+                       flags, pv, pi);
+    hipLaunchKernelGGL(accept_walk_kernel<float>, dim3(bs), dim3(256), 0, st, nn, V, B, tok, par,
+                       (const float *)logits, flags, pv, pi, acc_len, acc_nodes, out_tok);
+  }
+}
+
+}  // namespace dk

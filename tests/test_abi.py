@@ -1,0 +1,93 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/domino.h declares, and rejects invalid arguments before any HIP call."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2605_29707_amd import binding as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "domino.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(domino_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = bd.load()
+    names = header_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(bd.exported_symbols()) == names
+
+
+def _cfg(**kw):
+    c = dict(hidden=256, n_layers=2, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=1024, vocab=4096,
+             block=16, gru_hidden=1024, rank=256, mask_token_id=4095, rms_eps=1e-6, rope_theta=1e6,
+             dtype=bd.DOMINO_F32)
+    c.update(kw)
+    return bd.domino_config(**c)
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({"hidden": 0}, bd.DOMINO_ERR_INVALID_ARG),
+    ({"block": 1}, bd.DOMINO_ERR_INVALID_ARG),
+    ({"block": 65}, bd.DOMINO_ERR_INVALID_ARG),
+    ({"mask_token_id": 4096}, bd.DOMINO_ERR_INVALID_ARG),
+    ({"dtype": 7}, bd.DOMINO_ERR_INVALID_ARG),
+    ({"head_dim": 96}, bd.DOMINO_ERR_UNSUPPORTED),
+    ({"n_kv_heads": 3}, bd.DOMINO_ERR_UNSUPPORTED),
+    ({"hidden": 250}, bd.DOMINO_ERR_UNSUPPORTED),
+    ({"rank": 1000}, bd.DOMINO_ERR_UNSUPPORTED),
+    ({}, bd.DOMINO_ERR_INVALID_ARG),  # valid config, NULL weights
+])
+def test_model_create_validation(kw, status):
+    lib = bd.load()
+    h = C.c_void_p()
+    cfg = _cfg(**kw)
+    assert lib.domino_model_create(C.byref(cfg), None, C.byref(h)) == status
+    assert h.value is None
+    assert bd.last_error()
+
+
+def test_null_config_and_out():
+    lib = bd.load()
+    h = C.c_void_p()
+    assert lib.domino_model_create(None, None, C.byref(h)) == bd.DOMINO_ERR_INVALID_ARG
+    cfg = _cfg()
+    assert lib.domino_model_create(C.byref(cfg), None, None) == bd.DOMINO_ERR_INVALID_ARG
+
+
+def test_draft_step_validation_without_model():
+    lib = bd.load()
+    st = lib.domino_draft_step(None, 1, None, None, None, None, 0, None, 0, 1, None, None, None, None,
+                               None, 0, None)
+    assert st == bd.DOMINO_ERR_INVALID_ARG
+    assert "model" in bd.last_error()
+    assert lib.domino_workspace_bytes(None, 1, 16, 0, 1) == 0
+
+
+def test_tree_and_accept_validation():
+    lib = bd.load()
+    p = C.c_void_p(16)  # never dereferenced: validation fails first
+    assert lib.domino_build_tree(0, 15, 1, p, p, p, p, p, p, p, None, None) == bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_build_tree(1, 0, 1, p, p, p, p, p, p, p, None, None) == bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_build_tree(1, 15, 9, p, p, p, p, p, p, p, None, None) == bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_build_tree(1, 15, 1, None, p, p, p, p, p, p, None, None) == bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_verify_workspace_bytes(1, 0, 10) == 0
+    assert lib.domino_verify_workspace_bytes(1, 2000, 10) == 0
+    assert lib.domino_verify_workspace_bytes(2, 16, 151936) > 0
+    args = (1, 16, 100, 16, p, p, p, bd.DOMINO_F32, p, p, p)
+    assert lib.domino_verify_accept(*args, None, 10**9, None) == bd.DOMINO_ERR_WORKSPACE
+    assert lib.domino_verify_accept(*args, p, 1, None) == bd.DOMINO_ERR_WORKSPACE
+    assert lib.domino_verify_accept(1, 16, 100, 1, p, p, p, bd.DOMINO_F32, p, p, p, p, 10**9, None) == \
+        bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_verify_accept(1, 16, 100, 16, p, p, p, 5, p, p, p, p, 10**9, None) == \
+        bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_workspace_error(None, None, None) == bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_profile_enable(None, 1) == bd.DOMINO_ERR_INVALID_ARG
