@@ -1,0 +1,229 @@
+"""Benchmark of one Domino draft step on one MI355X.
+
+A step is domino_draft_step + domino_build_tree + domino_verify_accept on
+inputs already resident in HBM (synthetic weights and context of the
+Qwen3-8B shape, bs 1, context 1024, block 16, branch 1 by default).  Prints one
+JSON line.  The CPU-baseline leg times the fp64 CPU oracle on a bounded sample
+(one or more whole steps) on this machine's host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12  # B/s, MI355X HBM3E
+
+
+def algorithmic_bytes(cfg) -> dict:
+    """Bytes a step must move at least: every weight once, the context KV, the
+    target-logit rows the acceptance walk reads, the gathered embedding rows."""
+    d, dh, nq, nkv, F, V = cfg.hidden, cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads, cfg.ffn, cfg.vocab
+    ds, r, bs, B = cfg.gru_hidden, cfg.rank, cfg.batch, cfg.block
+    es = 2 if cfg.dtype == "bf16" else 4
+    layer = d * nq * dh + 2 * d * nkv * dh + nq * dh * d + 3 * d * F
+    head = 3 * ds * d + 3 * ds * ds + r * (d + ds) + V * r
+    parts = {
+        "backbone": es * cfg.n_layers * layer,
+        "lm_head": es * V * d,
+        "domino_head": es * head,
+        "ctx_kv": bs * cfg.n_layers * cfg.ctx * nkv * dh * 2 * es,
+        "target_rows": bs * (B + (1 if cfg.branch > 1 else 0)) * V * 2,
+        "embed_rows": bs * (2 * B - 1) * d * es,
+    }
+    parts["total"] = sum(parts.values())
+    return parts
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="qwen3_8b")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--breakdown", action="store_true", help="extra pass timing every kernel class")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU: this build has no multi-GPU path (asked for {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2605_29707_amd import binding as bd
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    cfg = synth.get_config(args.config)
+    bs, D, beta, V = cfg.batch, cfg.depth, cfg.branch, cfg.vocab
+    t0 = time.time()
+    w = synth.make_weights(cfg, seed=args.seed)
+    inp = synth.make_inputs(cfg, seed=args.seed)
+    print(f"# inputs generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    dw = bd.to_device_weights(w, cfg, dev)
+    model = bd.DominoModel(cfg, dw)
+    kvdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    T = lambda a, dt=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
+    anchor, lens = T(inp["anchor"], torch.int32), T(inp["ctx_lens"], torch.int32)
+    ck, cv = T(inp["ctx_k"], kvdt), T(inp["ctx_v"], kvdt)
+    hid = T(inp["ctx_hidden"]) if inp["ctx_hidden"] is not None else None
+    n_new = 0 if hid is None else hid.shape[1]
+    max_ctx = inp["max_ctx"]
+    ws = torch.empty(model.workspace_bytes(bs, max_ctx, n_new, beta), dtype=torch.uint8, device=dev)
+    ids = torch.empty(bs, D, beta, dtype=torch.int32, device=dev)
+    vals = torch.empty(bs, D, beta, dtype=torch.float32, device=dev)
+    nn = 1 + D * beta
+    tok, par, dep, pos = (torch.empty(bs, nn, dtype=torch.int32, device=dev) for _ in range(4))
+    acc = torch.empty(bs, dtype=torch.int32, device=dev)
+    nodes = torch.empty(bs, D, dtype=torch.int32, device=dev)
+    out = torch.empty(bs, D + 1, dtype=torch.int32, device=dev)
+    vws = torch.empty(bd.domino_verify_workspace_bytes(bs, nn, V), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def draft():
+        bd.domino_draft_step(model, anchor, lens, ck, cv, max_ctx, ids, vals, ws, branch=beta,
+                             ctx_hidden_new=hid, n_new=n_new, stream=stream)
+        bd.domino_build_tree(ids, anchor, lens, tok, par, dep, pos, stream=stream)
+
+    # target logits planted on this step's own tree (the step is deterministic)
+    draft()
+    torch.cuda.synchronize()
+    lg = synth.make_target_logits(cfg, tok.cpu().numpy(), par.cpu().numpy(), seed=args.seed, dtype="bf16")
+    target = T(lg, torch.bfloat16)
+    del lg
+
+    def step():
+        draft()
+        bd.domino_verify_accept(tok, par, target, cfg.block, acc, nodes, out, vws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    assert bd.domino_workspace_error(ws) == 0, "device error word set"
+
+    # timed region: K steps, per-step events, the LM-head launches bracketed by library events
+    dom = "lmhead"
+    bd.domino_profile_enable(model, [dom])
+    bd.domino_profile_reset(model)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(stream)
+    for i in range(args.steps):
+        step()
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    total_ms = evs[0].elapsed_time(evs[-1])
+    per = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    dom_ms, dom_n = bd.domino_profile_read(model, dom)
+    bd.domino_profile_enable(model, [])
+    ms_per_step = total_ms / args.steps
+    tau = float(acc.float().mean().item()) + 1.0
+
+    breakdown = None
+    if args.breakdown:
+        classes = [c for c in bd.KERNEL_CLASSES]
+        bd.domino_profile_enable(model, classes)
+        bd.domino_profile_reset(model)
+        for _ in range(20):
+            step()
+        torch.cuda.synchronize()
+        breakdown = {}
+        for c in classes:
+            ms, n = bd.domino_profile_read(model, c)
+            if n:
+                breakdown[c] = round(ms * 1000.0 / 20, 2)
+        bd.domino_profile_enable(model, [])
+
+    ab = algorithmic_bytes(cfg)
+    step_s = ms_per_step / 1e3
+    dom_launch_s = dom_ms / 1e3 / max(1, dom_n)
+    dom_bytes = ab["lm_head"] + bs * D * cfg.hidden * 4  # weights once + fp32 H rows
+    achieved = dom_bytes / dom_launch_s / 1e9
+
+    res = {
+        "metric": "draft steps/sec + us/step (k=16, Qwen3-8B-shape, bs=1); % HBM roofline",
+        "value": round(1.0 / step_s, 2),
+        "unit": "draft steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "us_per_step_median": round(statistics.median(per) * 1e3, 1),
+        "us_per_step_p10_p90": [round(float(np.percentile(per, 10)) * 1e3, 1),
+                                round(float(np.percentile(per, 90)) * 1e3, 1)],
+        "hbm_roofline_frac_step": round(ab["total"] / step_s / HBM_PEAK, 4),
+        "algorithmic_bytes_per_step": ab["total"],
+        "drafted_tokens_per_s": round(bs * D / step_s, 1),
+        "mean_tau_synthetic": tau,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) context KV, Zipf(1.1) target logits)",
+        "config": {"workload": f"{cfg.name}: draft step + tree + greedy acceptance",
+                   "batch": bs, "ctx": cfg.ctx, "block": cfg.block, "branch": beta,
+                   "hidden": cfg.hidden, "layers": cfg.n_layers, "vocab": V,
+                   "storage": cfg.dtype},
+        "roofline": {"kernel": "lm_head gemm (gemm_kernel<bf16,2,1,STORE>)", "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                     "frac": round(achieved * 1e9 / HBM_PEAK, 4), "traffic": None,
+                     "launch_us": round(dom_launch_s * 1e6, 2), "launches": dom_n,
+                     "algorithmic_bytes_per_launch": dom_bytes},
+    }
+    if breakdown:
+        res["breakdown_us_per_step"] = breakdown
+
+    model.close()
+    del dw, model
+    torch.cuda.empty_cache()
+
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg, w, inp, lg_seed=args.seed, steps=args.cpu_steps)
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(cfg, w, inp, lg_seed, steps):
+    """The fp64 oracle, as it stands, timed on whole steps of the same workload."""
+    import oracle
+    import synth
+    from threadpoolctl import threadpool_info
+
+    w64 = oracle.as_f64_weights(w)
+    cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    beta = cfg.branch
+    times = []
+    for _ in range(steps):
+        t0 = time.time()
+        r = oracle.draft_step(cfg, w64, inp["anchor"], inp["ctx_lens"], inp["ctx_k"], inp["ctx_v"], beta,
+                              ctx_hidden=inp["ctx_hidden"])
+        tree = oracle.build_tree(r["topk_ids"], inp["anchor"], inp["ctx_lens"])
+        t1 = time.time()
+        lg = synth.make_target_logits(cfg, tree["node_token"], tree["node_parent"], seed=lg_seed, dtype="bf16")
+        t2 = time.time()
+        oracle.verify_accept(tree["node_token"], tree["node_parent"], lg, cfg.block)
+        t3 = time.time()
+        times.append((t1 - t0) + (t3 - t2))
+    med = statistics.median(times)
+    return {"value": round(1.0 / med, 4), "unit": "draft steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"{steps} whole steps of the same workload (fp64 numpy oracle; "
+                      f"median {med:.2f} s/step; target-logit generation excluded)"}
+
+
+if __name__ == "__main__":
+    main()

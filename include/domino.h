@@ -64,9 +64,12 @@ enum {
  * Sec. 4.1.1 and Sec. 5.1); gru_hidden d_s = 1024 and rank r = 256 (Sec. 4.1.2,
  * Sec. 5.1).  Layers follow the Qwen3 layout: pre-RMSNorm, per-head q/k
  * RMSNorm, rotate-half RoPE, grouped-query attention, SwiGLU, no biases.
- * Limits of this build: head_dim in {64, 128}; hidden, ffn, gru_hidden,
- * rank and n_q_heads*head_dim multiples of 32; n_q_heads a multiple of
- * n_kv_heads; block in [2, 64]; mask_token_id in [0, vocab).
+ * Limits of this build: head_dim in {64, 128}; hidden, ffn, gru_hidden and
+ * n_q_heads*head_dim multiples of 32; gru_hidden at most 2048 (bf16) or 1024
+ * (f32); rank 256 (bf16) or 128/256 (f32); n_q_heads a multiple of
+ * n_kv_heads with (n_q_heads/n_kv_heads)*block <= 128; block in [2, 64];
+ * mask_token_id in [0, vocab).  domino_model_create also builds the table
+ * G = embed * gru_w_ih^T ([vocab, 3*gru_hidden] fp32) used by the rollout.
  */
 typedef struct {
   int32_t hidden, n_layers, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
@@ -127,7 +130,7 @@ const char *domino_last_error(void);
 /*
  * One draft step (Sec. 4.1.1 block construction, backbone and LM head;
  * Sec. 4.1.2 causal encoder and correction; Fig. 3 sequential rollout).
- *  batch           rows, >= 1
+ *  batch           rows, in [1, 64]
  *  anchor_ids      device int32 [batch]: x_t, the last verified token
  *  ctx_lens        device int32 [batch]: context length n_b (RoPE positions of
  *                  the block are n_b .. n_b+B-1), in [n_new, max_ctx]

@@ -5,6 +5,7 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -57,7 +58,7 @@ struct domino_model {
   size_t mem_bytes = 0;
   std::vector<Packed> qkv, wo, gateup, down;
   Packed lm, w1h, w2;
-  size_t w_ih_off, w_hh_off, w1_off;
+  size_t gtab_off, w_hh_off, w1_off;
   // profiling
   uint32_t prof_mask = 0;
   struct Ev {
@@ -103,8 +104,12 @@ domino_status check_config(const domino_config *c) {
     return fail(DOMINO_ERR_UNSUPPORTED, "hidden, ffn, gru_hidden and n_q_heads*head_dim must be multiples of 32");
   if (c->rank % ks || c->rank > 16 * ks)
     return fail(DOMINO_ERR_UNSUPPORTED, "rank must be a multiple of %d and at most %d", ks, 16 * ks);
-  const int G = (c->n_q_heads / c->n_kv_heads) * c->block;
-  if (G > 128) return fail(DOMINO_ERR_UNSUPPORTED, "(n_q_heads/n_kv_heads)*block must be at most 128");
+  if (!attn_supported(c->n_q_heads, c->n_kv_heads, c->block))
+    return fail(DOMINO_ERR_UNSUPPORTED, "(n_q_heads/n_kv_heads)*block must be 32, 64 or 128");
+  const int epl = c->dtype == DOMINO_BF16 ? 8 : 4;
+  if (c->gru_hidden > 256 * epl) return fail(DOMINO_ERR_UNSUPPORTED, "gru_hidden must be at most %d", 256 * epl);
+  if (c->dtype == DOMINO_BF16 ? c->rank != 256 : (c->rank != 128 && c->rank != 256))
+    return fail(DOMINO_ERR_UNSUPPORTED, "rank must be 256 (bf16) or 128/256 (f32)");
   return DOMINO_OK;
 }
 
@@ -116,79 +121,70 @@ Dims make_dims(const domino_model *m, int bs) {
 
 // ---- workspace layout of the draft step
 struct WsLayout {
-  size_t err, bar, tickets, n_tickets, X, A, QKV, Q, Kb, Vb, attn, O, F, H, Lb, P, hbuf, ubuf, pval, pid,
-      ctxkv, part, total;
-  int G;
-  size_t head_lds;
+  size_t err, X, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, Lb, P, hbuf, ubuf, pval, pid, ctxkv, total;
+  int GC;
 };
 
 struct Plans {
   GemmPlan qkv, wo, gateup, down, lm, w1h, ctx;
 };
 
+constexpr int kMaxSplit = 16;
+
 Plans make_plans(const domino_model *m, int bs, int max_new) {
   const Dims &D = m->D;
   const int M = bs * D.B, Mh = bs * (D.B - 1);
   Plans p;
-  p.qkv = plan_gemm(m->qkv[0].NT, m->qkv[0].KS, M, EPI_STORE, m->n_cu);
-  p.wo = plan_gemm(m->wo[0].NT, m->wo[0].KS, M, EPI_ADD, m->n_cu);
-  p.gateup = plan_gemm(m->gateup[0].NT, m->gateup[0].KS, M, EPI_SWIGLU, m->n_cu);
-  p.down = plan_gemm(m->down[0].NT, m->down[0].KS, M, EPI_ADD, m->n_cu);
-  p.lm = plan_gemm(m->lm.NT, m->lm.KS, Mh, EPI_STORE, m->n_cu);
-  p.w1h = plan_gemm(m->w1h.NT, m->w1h.KS, Mh, EPI_STORE, m->n_cu);
+  // projections whose consumer is elementwise write K-split partial outputs
+  p.qkv = plan_gemm(m->qkv[0].NT, m->qkv[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
+  p.wo = plan_gemm(m->wo[0].NT, m->wo[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
+  p.gateup = plan_gemm(m->gateup[0].NT, m->gateup[0].KS, M, EPI_SWIGLU, m->n_cu, 1);
+  p.down = plan_gemm(m->down[0].NT, m->down[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
+  p.lm = plan_gemm(m->lm.NT, m->lm.KS, Mh, EPI_STORE, m->n_cu, 1);
+  p.w1h = plan_gemm(m->w1h.NT, m->w1h.KS, Mh, EPI_STORE, m->n_cu, 1);
   const int kvt = 2 * D.nkv * D.dh / 16;
-  p.ctx = plan_gemm(kvt, m->qkv[0].KS, bs * (max_new > 0 ? max_new : 1), EPI_STORE, m->n_cu);
+  p.ctx = plan_gemm(kvt, m->qkv[0].KS, bs * (max_new > 0 ? max_new : 1), EPI_STORE, m->n_cu, 1);
   return p;
 }
 
 bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, WsLayout &w) {
   Dims D = make_dims(m, bs);
   const int M = bs * D.B, Mh = bs * (D.B - 1);
-  Plans p = make_plans(m, bs, max_new);
-  size_t tickets = 0, part = 0;
-  for (const GemmPlan *g : {&p.qkv, &p.wo, &p.gateup, &p.down, &p.lm, &p.w1h, &p.ctx}) {
-    tickets = std::max(tickets, g->tickets);
-    part = std::max(part, g->part_floats);
-  }
-  w.G = head_grid(D, m->n_cu, &w.head_lds);
-  if (w.head_lds > 160 * 1024) return false;
+  const Plans p = make_plans(m, bs, max_new);
+  w.GC = head_logits_grid(D);
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t at = o;
     o = align_up(o + bytes);
     return at;
   };
-  w.err = take(64);
-  w.bar = take(64);
-  w.n_tickets = tickets;
-  w.tickets = take(tickets * 4);
-  const size_t hdr_end = o;
-  (void)hdr_end;
+  w.err = take(256);
   const int qkvw = (D.nq + 2 * D.nkv) * D.dh;
   w.X = take((size_t)M * D.d * 4);
   w.A = take((size_t)M * D.d * 4);
-  w.QKV = take((size_t)M * qkvw * 4);
+  w.QKV = take((size_t)p.qkv.ksplit * M * qkvw * 4);
   w.Q = take((size_t)M * D.nq * D.dh * 4);
   w.Kb = take((size_t)M * D.nkv * D.dh * 4);
   w.Vb = take((size_t)M * D.nkv * D.dh * 4);
   w.attn = take(attn_part_floats(D, max_ctx) * 4);
   w.O = take((size_t)M * D.nq * D.dh * 4);
+  w.WOp = take((size_t)p.wo.ksplit * M * D.d * 4);
   w.F = take((size_t)M * D.ffn * 4);
+  w.DNp = take((size_t)p.down.ksplit * M * D.d * 4);
   w.H = take((size_t)Mh * D.d * 4);
   w.Lb = take((size_t)Mh * D.V * 4);
   w.P = take((size_t)Mh * D.r * 4);
   w.hbuf = take((size_t)2 * bs * D.ds * 4);
   w.ubuf = take((size_t)bs * D.r * 4);
-  w.pval = take((size_t)bs * w.G * beta * 4);
-  w.pid = take((size_t)bs * w.G * beta * 4);
+  w.pval = take((size_t)bs * w.GC * beta * 4);
+  w.pid = take((size_t)bs * w.GC * beta * 4);
   w.ctxkv = take((size_t)bs * (max_new > 0 ? max_new : 0) * 2 * D.nkv * D.dh * 4);
-  w.part = take(part * 4);
   w.total = o;
   return true;
 }
 
 GemmArgs gemm_args(const void *P, const Packed &pk, int tile0, int ntiles, int N, const float *X, int ldx,
-                   int M, int K, float *Y, int ldy, const GemmPlan &pl, float *part, int *tickets) {
+                   int M, int K, float *Y, int ldy, const GemmPlan &pl) {
   GemmArgs a;
   a.P = P;
   a.KS = pk.KS;
@@ -202,9 +198,49 @@ GemmArgs gemm_args(const void *P, const Packed &pk, int tile0, int ntiles, int N
   a.Y = Y;
   a.ldy = ldy;
   a.ksplit = pl.ksplit;
-  a.part = part;
-  a.tickets = tickets;
+  a.ysplit = (size_t)M * ldy;
   return a;
+}
+
+}  // namespace
+
+namespace {
+
+// G = E W_ih^T for every vocabulary row (fp32), so the GRU input half of a
+// rollout step is a row gather.  Built with the same matrix-core GEMM as the
+// projections, over the embedding in row chunks.
+hipError_t build_gtab(domino_model *m, const void *w_ih) {
+  const Dims &D = m->D;
+  const int KSTEP = kstep(m);
+  const int N = 3 * D.ds, K = D.d;
+  Packed pk;
+  pk.NT = (N + 15) / 16;
+  pk.KS = (K + KSTEP - 1) / KSTEP;
+  pk.off = 0;
+  const int CH = 8192;
+  void *P = nullptr;
+  float *X = nullptr;
+  hipError_t e = hipMalloc(&P, (size_t)pk.NT * pk.KS * 1024);
+  if (e != hipSuccess) return e;
+  e = hipMalloc(&X, (size_t)CH * K * 4);
+  if (e != hipSuccess) {
+    (void)hipFree(P);
+    return e;
+  }
+  launch_pack(m->bf16, w_ih, N, K, K, P, pk.NT, pk.KS, 1, 0, nullptr);
+  float *G = (float *)((char *)m->mem + m->gtab_off);
+  for (int r0 = 0; r0 < D.V; r0 += CH) {
+    const int rows = std::min(CH, D.V - r0);
+    launch_to_f32((const char *)m->embed + (size_t)r0 * K * m->esz, m->bf16, X, (size_t)rows * K, nullptr);
+    const GemmPlan pl = plan_gemm(pk.NT, pk.KS, rows, EPI_STORE, m->n_cu, 1);
+    const GemmArgs a = gemm_args(P, pk, 0, pk.NT, N, X, K, rows, K, G + (size_t)r0 * N, N, pl);
+    launch_gemm(m->bf16, EPI_STORE, a, pl, nullptr);
+  }
+  e = hipGetLastError();
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  (void)hipFree(P);
+  (void)hipFree(X);
+  return e;
 }
 
 }  // namespace
@@ -292,8 +328,8 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
   m->lm = add(D.V, D.d);
   m->w1h = add(D.r, D.d);
   m->w2 = add(D.V, D.r);
-  m->w_ih_off = off;
-  off = align_up(off + (size_t)3 * D.ds * D.d * m->esz);
+  m->gtab_off = off;
+  off = align_up(off + (size_t)D.V * 3 * D.ds * 4);
   m->w_hh_off = off;
   off = align_up(off + (size_t)3 * D.ds * D.ds * m->esz);
   m->w1_off = off;
@@ -329,7 +365,7 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
   launch_pack(bf, w->w1, D.r, D.d, D.d + D.ds, base + m->w1h.off, m->w1h.NT, m->w1h.KS, 1, 0, st);
   launch_pack(bf, w->w2, D.V, D.r, D.r, base + m->w2.off, m->w2.NT, m->w2.KS, 1, 0, st);
   he = hipGetLastError();
-  if (he == hipSuccess) he = hipMemcpy(base + m->w_ih_off, w->gru_w_ih, (size_t)3 * D.ds * D.d * m->esz, hipMemcpyDeviceToDevice);
+  if (he == hipSuccess) he = build_gtab(m, w->gru_w_ih);
   if (he == hipSuccess) he = hipMemcpy(base + m->w_hh_off, w->gru_w_hh, (size_t)3 * D.ds * D.ds * m->esz, hipMemcpyDeviceToDevice);
   if (he == hipSuccess) he = hipMemcpy(base + m->w1_off, w->w1, (size_t)D.r * (D.d + D.ds) * m->esz, hipMemcpyDeviceToDevice);
   if (he == hipSuccess) he = hipDeviceSynchronize();
@@ -353,9 +389,9 @@ void domino_model_destroy(domino_model_t m) {
 }
 
 size_t domino_workspace_bytes(domino_model_t m, int32_t batch, int32_t max_ctx, int32_t max_new, int32_t branch) {
-  if (!m || batch < 1 || max_ctx < 0 || max_new < 0 || max_new > max_ctx || branch < 1 || branch > 8) return 0;
+  if (!m || batch < 1 || batch > 64 || max_ctx < 0 || max_new < 0 || max_new > max_ctx || branch < 1 || branch > 8) return 0;
   WsLayout w;
-  if (!layout(m, batch, max_ctx, max_new, branch, w)) return 0;
+  layout(m, batch, max_ctx, max_new, branch, w);
   return w.total;
 }
 
@@ -364,7 +400,7 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
                                 int32_t branch, const int32_t *forced_tokens, int32_t *topk_ids, float *topk_vals,
                                 const domino_debug *debug, void *workspace, size_t workspace_bytes, void *stream) {
   if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
-  if (batch < 1) return fail(DOMINO_ERR_INVALID_ARG, "batch must be >= 1");
+  if (batch < 1 || batch > 64) return fail(DOMINO_ERR_INVALID_ARG, "batch must be in [1, 64]");
   if (!anchor_ids || !ctx_lens) return fail(DOMINO_ERR_INVALID_ARG, "anchor_ids/ctx_lens is NULL");
   if (max_ctx < 0) return fail(DOMINO_ERR_INVALID_ARG, "max_ctx must be >= 0");
   if (max_ctx > 0 && (!ctx_k || !ctx_v)) return fail(DOMINO_ERR_INVALID_ARG, "ctx_k/ctx_v is NULL");
@@ -374,8 +410,7 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
   if (!topk_ids || !topk_vals) return fail(DOMINO_ERR_INVALID_ARG, "topk_ids/topk_vals is NULL");
   if (!workspace) return fail(DOMINO_ERR_WORKSPACE, "workspace is NULL");
   WsLayout w;
-  if (!layout(m, batch, max_ctx, n_new, branch, w))
-    return fail(DOMINO_ERR_UNSUPPORTED, "batch %d needs more LDS than a compute unit has", batch);
+  layout(m, batch, max_ctx, n_new, branch, w);
   if (workspace_bytes < w.total)
     return fail(DOMINO_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, w.total);
 
@@ -385,23 +420,20 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
   char *ws = (char *)workspace;
   auto F = [&](size_t off) { return (float *)(ws + off); };
   int32_t *err = (int32_t *)(ws + w.err);
-  int *tickets = (int *)(ws + w.tickets);
-  float *part = F(w.part);
   const char *base = (const char *)m->mem;
   const int M = batch * D.B, Mh = batch * (D.B - 1);
   const int qd = D.nq * D.dh, kvd = D.nkv * D.dh, qkvw = qd + 2 * kvd;
   const size_t layer_elems = (size_t)batch * max_ctx * kvd;
 
-  // clear error word, barrier words and split-K tickets
-  launch_fill_u32((uint32_t *)ws, (w.tickets + w.n_tickets * 4) / 4, 0u, st);
+  // clear the error word
+  launch_fill_u32((uint32_t *)ws, 1, 0u, st);
 
   // context rows projected from target hidden states (optional)
   if (n_new > 0) {
     for (int l = 0; l < m->cfg.n_layers; ++l) {
       prof_begin(m, DOMINO_KC_CTXPROJ, st);
       GemmArgs a = gemm_args(base + m->qkv[l].off, m->qkv[l], qd / 16, 2 * kvd / 16, 2 * kvd,
-                             (const float *)ctx_hidden_new, D.d, batch * n_new, D.d, F(w.ctxkv), 2 * kvd, p.ctx,
-                             part, tickets);
+                             (const float *)ctx_hidden_new, D.d, batch * n_new, D.d, F(w.ctxkv), 2 * kvd, p.ctx);
       launch_gemm(m->bf16, EPI_STORE, a, p.ctx, st);
       launch_ctx_store(D, F(w.ctxkv), n_new, m->k_norm[l], ctx_lens, max_ctx,
                        (char *)ctx_k + l * layer_elems * m->esz, (char *)ctx_v + l * layer_elems * m->esz, err, st);
@@ -413,21 +445,25 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
   launch_embed_block(D, m->embed, anchor_ids, F(w.X), err, st);
   prof_end(m, DOMINO_KC_EMBED, st);
 
+  const size_t rstride = (size_t)M * D.d;  // partial-output stride of the residual projections
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const char *ck = (const char *)ctx_k + l * layer_elems * m->esz;
     const char *cv = (const char *)ctx_v + l * layer_elems * m->esz;
+    // residual += previous layer's down projection, then the attention RMSNorm
     prof_begin(m, DOMINO_KC_NORM, st);
-    launch_rmsnorm(D, F(w.X), D.d, m->attn_norm[l], F(w.A), D.d, M, D.d, false, st);
+    launch_add_norm(D, F(w.X), D.d, F(w.DNp), l > 0 ? p.down.ksplit : 0, rstride, m->attn_norm[l], F(w.A), D.d,
+                    M, D.d, false, st);
     prof_end(m, DOMINO_KC_NORM, st);
 
     prof_begin(m, DOMINO_KC_QKV, st);
     GemmArgs a = gemm_args(base + m->qkv[l].off, m->qkv[l], 0, m->qkv[l].NT, qkvw, F(w.A), D.d, M, D.d, F(w.QKV),
-                           qkvw, p.qkv, part, tickets);
+                           qkvw, p.qkv);
     launch_gemm(m->bf16, EPI_STORE, a, p.qkv, st);
     prof_end(m, DOMINO_KC_QKV, st);
 
     prof_begin(m, DOMINO_KC_ROPE, st);
-    launch_qk_norm_rope(D, F(w.QKV), m->q_norm[l], m->k_norm[l], ctx_lens, max_ctx, F(w.Q), F(w.Kb), F(w.Vb), st);
+    launch_qk_norm_rope(D, F(w.QKV), p.qkv.ksplit, (size_t)M * qkvw, m->q_norm[l], m->k_norm[l], ctx_lens, max_ctx,
+                        F(w.Q), F(w.Kb), F(w.Vb), st);
     prof_end(m, DOMINO_KC_ROPE, st);
 
     prof_begin(m, DOMINO_KC_ATTN, st);
@@ -435,53 +471,54 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
     prof_end(m, DOMINO_KC_ATTN, st);
 
     prof_begin(m, DOMINO_KC_WO, st);
-    a = gemm_args(base + m->wo[l].off, m->wo[l], 0, m->wo[l].NT, D.d, F(w.O), qd, M, qd, F(w.X), D.d, p.wo, part,
-                  tickets);
-    launch_gemm(m->bf16, EPI_ADD, a, p.wo, st);
+    a = gemm_args(base + m->wo[l].off, m->wo[l], 0, m->wo[l].NT, D.d, F(w.O), qd, M, qd, F(w.WOp), D.d, p.wo);
+    launch_gemm(m->bf16, EPI_STORE, a, p.wo, st);
     prof_end(m, DOMINO_KC_WO, st);
 
+    // residual += attention output, then the FFN RMSNorm
     prof_begin(m, DOMINO_KC_NORM, st);
-    launch_rmsnorm(D, F(w.X), D.d, m->ffn_norm[l], F(w.A), D.d, M, D.d, false, st);
+    launch_add_norm(D, F(w.X), D.d, F(w.WOp), p.wo.ksplit, rstride, m->ffn_norm[l], F(w.A), D.d, M, D.d, false,
+                    st);
     prof_end(m, DOMINO_KC_NORM, st);
 
     prof_begin(m, DOMINO_KC_GATEUP, st);
     a = gemm_args(base + m->gateup[l].off, m->gateup[l], 0, m->gateup[l].NT, D.ffn, F(w.A), D.d, M, D.d, F(w.F),
-                  D.ffn, p.gateup, part, tickets);
+                  D.ffn, p.gateup);
     launch_gemm(m->bf16, EPI_SWIGLU, a, p.gateup, st);
     prof_end(m, DOMINO_KC_GATEUP, st);
 
     prof_begin(m, DOMINO_KC_DOWN, st);
-    a = gemm_args(base + m->down[l].off, m->down[l], 0, m->down[l].NT, D.d, F(w.F), D.ffn, M, D.ffn, F(w.X), D.d,
-                  p.down, part, tickets);
-    launch_gemm(m->bf16, EPI_ADD, a, p.down, st);
+    a = gemm_args(base + m->down[l].off, m->down[l], 0, m->down[l].NT, D.d, F(w.F), D.ffn, M, D.ffn, F(w.DNp), D.d,
+                  p.down);
+    launch_gemm(m->bf16, EPI_STORE, a, p.down, st);
     prof_end(m, DOMINO_KC_DOWN, st);
   }
 
+  // residual += last down projection; final RMSNorm of the draft rows -> H
   float *H = (debug && debug->hidden) ? debug->hidden : F(w.H);
   prof_begin(m, DOMINO_KC_NORM, st);
-  launch_rmsnorm(D, F(w.X), D.d, m->final_norm, H, D.d, Mh, D.d, true, st);
+  launch_add_norm(D, F(w.X), D.d, F(w.DNp), p.down.ksplit, rstride, m->final_norm, H, D.d, Mh, D.d, true, st);
   prof_end(m, DOMINO_KC_NORM, st);
 
   float *Lb = (debug && debug->base_logits) ? debug->base_logits : F(w.Lb);
   prof_begin(m, DOMINO_KC_LMHEAD, st);
-  GemmArgs a = gemm_args(base + m->lm.off, m->lm, 0, m->lm.NT, D.V, H, D.d, Mh, D.d, Lb, D.V, p.lm, part, tickets);
+  GemmArgs a = gemm_args(base + m->lm.off, m->lm, 0, m->lm.NT, D.V, H, D.d, Mh, D.d, Lb, D.V, p.lm);
   launch_gemm(m->bf16, EPI_STORE, a, p.lm, st);
   prof_end(m, DOMINO_KC_LMHEAD, st);
 
   prof_begin(m, DOMINO_KC_W1H, st);
-  a = gemm_args(base + m->w1h.off, m->w1h, 0, m->w1h.NT, D.r, H, D.d, Mh, D.d, F(w.P), D.r, p.w1h, part, tickets);
+  a = gemm_args(base + m->w1h.off, m->w1h, 0, m->w1h.NT, D.r, H, D.d, Mh, D.d, F(w.P), D.r, p.w1h);
   launch_gemm(m->bf16, EPI_STORE, a, p.w1h, st);
   prof_end(m, DOMINO_KC_W1H, st);
 
   HeadArgs h;
   h.D = D;
   h.beta = branch;
-  h.embed = m->embed;
-  h.w_ih = base + m->w_ih_off;
+  h.gtab = (const float *)(base + m->gtab_off);
   h.w_hh = base + m->w_hh_off;
   h.b_ih = m->b_ih;
   h.b_hh = m->b_hh;
-  h.w1s_rows = base + m->w1_off;
+  h.w1 = base + m->w1_off;
   h.w2p = base + m->w2.off;
   h.P = F(w.P);
   h.Lbase = Lb;
@@ -495,12 +532,10 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
   h.ubuf = F(w.ubuf);
   h.pval = F(w.pval);
   h.pid = (int32_t *)(ws + w.pid);
-  h.ybuf = nullptr;
-  h.barrier = (unsigned *)(ws + w.bar);
   h.err = err;
-  h.G = w.G;
+  h.GC = w.GC;
   prof_begin(m, DOMINO_KC_HEADLOOP, st);
-  hipError_t he = launch_head(h, w.head_lds, st);
+  hipError_t he = launch_head(h, st);
   prof_end(m, DOMINO_KC_HEADLOOP, st);
   if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "head loop launch: %s", hipGetErrorString(he));
   he = hipGetLastError();

@@ -28,24 +28,53 @@ __global__ __launch_bounds__(256) void embed_block_kernel(const WT *__restrict__
   for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = to_f32(src[c]);
 }
 
+// x[in_row] += sum of the `np` partial outputs (split order), then
+// y[i] = RMSNorm(x[in_row]) * gain.  With skip_anchor, output row i reads
+// input row i + i/(B-1) + 1 (the draft rows of each block) and x is not
+// written back.  One workgroup per output row; each thread owns 8 columns at a
+// time so all its loads are issued together.
 template <typename WT>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float *__restrict__ x, int ldx,
-                                                      const WT *__restrict__ gain, float *__restrict__ y,
-                                                      int ldy, int width, float eps, int skip_anchor,
-                                                      int depth) {
+__global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, int ldx,
+                                                       const float *__restrict__ parts, int np,
+                                                       size_t pstride, const WT *__restrict__ gain,
+                                                       float *__restrict__ y, int ldy, int width, float eps,
+                                                       int skip_anchor, int depth) {
   const int i = blockIdx.x;
   const int in_row = skip_anchor ? i + i / depth + 1 : i;
-  const float *xr = x + (size_t)in_row * ldx;
+  float *xr = x + (size_t)in_row * ldx;
+  const float *pr = parts + (size_t)in_row * ldx;
+  constexpr int PER = 8;
   float ss = 0.f;
-  for (int c = threadIdx.x; c < width; c += blockDim.x) ss = fmaf(xr[c], xr[c], ss);
+  for (int c0 = threadIdx.x * PER; c0 < width; c0 += blockDim.x * PER) {
+    float4 v0 = *(const float4 *)(xr + c0), v1 = *(const float4 *)(xr + c0 + 4);
+    for (int p = 0; p < np; ++p) {
+      const float4 a0 = *(const float4 *)(pr + p * pstride + c0), a1 = *(const float4 *)(pr + p * pstride + c0 + 4);
+      v0.x += a0.x; v0.y += a0.y; v0.z += a0.z; v0.w += a0.w;
+      v1.x += a1.x; v1.y += a1.y; v1.z += a1.z; v1.w += a1.w;
+    }
+    if (np > 0 && !skip_anchor) {
+      *(float4 *)(xr + c0) = v0;
+      *(float4 *)(xr + c0 + 4) = v1;
+    }
+    ss = fmaf(v0.x, v0.x, ss); ss = fmaf(v0.y, v0.y, ss); ss = fmaf(v0.z, v0.z, ss); ss = fmaf(v0.w, v0.w, ss);
+    ss = fmaf(v1.x, v1.x, ss); ss = fmaf(v1.y, v1.y, ss); ss = fmaf(v1.z, v1.z, ss); ss = fmaf(v1.w, v1.w, ss);
+    float *yr = y + (size_t)i * ldy + c0;
+    // stash the summed values in y; scaled below once the norm is known
+    *(float4 *)(yr) = v0;
+    *(float4 *)(yr + 4) = v1;
+  }
   ss = wave_sum(ss);
-  __shared__ float red[4];
+  __shared__ float red[8];
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  float tot = 0.f;
+  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) tot += red[w];
   const float inv = 1.0f / sqrtf(tot / (float)width + eps);
-  float *yr = y + (size_t)i * ldy;
-  for (int c = threadIdx.x; c < width; c += blockDim.x) yr[c] = xr[c] * inv * to_f32(gain[c]);
+  for (int c0 = threadIdx.x * PER; c0 < width; c0 += blockDim.x * PER) {
+    float *yr = y + (size_t)i * ldy + c0;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) yr[e] = yr[e] * inv * to_f32(gain[c0 + e]);
+  }
 }
 
 // One wave per (row, head).  Lane l holds elements l and l+64 (dh = 128) or
@@ -80,8 +109,8 @@ DEVI void norm_rope_head(float (&v)[2], int dh, const WT *__restrict__ gain, flo
 }
 
 template <typename WT>
-__global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restrict__ qkv,
-                                                           const WT *__restrict__ qn,
+__global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restrict__ qkv, int np,
+                                                           size_t pstride, const WT *__restrict__ qn,
                                                            const WT *__restrict__ kn,
                                                            const int32_t *__restrict__ ctx_lens,
                                                            int max_ctx, float *__restrict__ Q,
@@ -100,7 +129,8 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
   const float *src = qkv + (size_t)m * nh * dh + (size_t)hh * dh;
   float v[2] = {0.f, 0.f};
   const int per = dh / 64;
-  for (int q = 0; q < per; ++q) v[q] = src[lane + 64 * q];
+  for (int p = 0; p < np; ++p)  // K-split partial outputs, added in split order
+    for (int q = 0; q < per; ++q) v[q] += src[p * pstride + lane + 64 * q];
   float *dst;
   if (hh < nq) {
     norm_rope_head<WT>(v, dh, qn, eps, pos, theta, true, lane);
@@ -151,111 +181,175 @@ __global__ __launch_bounds__(256) void ctx_store_kernel(const float *__restrict_
 
 // ---------------------------------------------------------------------------
 // block attention: queries = the B block rows of the G query heads sharing one
-// kv head; keys = context[0, n) followed by the B block keys; no mask.
-// Split over key chunks of CH; each chunk writes (max, sum, unnormalised
-// output) per query row and a second kernel merges chunks with log-sum-exp.
+// kv head (R = G*B rows); keys = context[0, n) followed by the B block keys;
+// no mask.  One workgroup per (key chunk of CH, kv head, batch row) writes the
+// chunk's row max, row sum of exp and unnormalised output; a second kernel
+// merges the chunks with log-sum-exp weights.  Q, K, V and P live in LDS as
+// fp32; each thread computes an RPT x 4 block of scores and an RPT x 8 block
+// of outputs, reading 16-byte vectors, so LDS traffic per FMA stays low.
 // ---------------------------------------------------------------------------
-constexpr int CH = 32;
-int attn_chunk_len() { return CH; }
-int attn_nchunks(int max_ctx, int B) { return (max_ctx + B + CH - 1) / CH; }
+constexpr int kAttnThreads = 256;
+
+static int attn_ch(int G) { return G <= 4 ? 64 : 32; }
+int attn_chunk_len() { return 64; }
+int attn_nchunks(int max_ctx, int B) { return (max_ctx + B + 31) / 32; }  // upper bound for any G
 size_t attn_part_floats(const Dims &D, int max_ctx) {
   return (size_t)D.bs * D.nq * D.B * attn_nchunks(max_ctx, D.B) * (D.dh + 2);
 }
 
-template <typename WT>
-__global__ __launch_bounds__(256) void attn_partial_kernel(
+template <typename WT, int RPT, int CH, int DH>
+__global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     const float *__restrict__ Q, const float *__restrict__ Kb, const float *__restrict__ Vb,
     const WT *__restrict__ ck, const WT *__restrict__ cv, const int32_t *__restrict__ ctx_lens,
-    int max_ctx, float *__restrict__ part, int B, int nq, int nkv, int dh, int nch, float scale) {
-  extern __shared__ float smem[];
+    int max_ctx, float *__restrict__ part, int B, int nq, int nkv, int nch, float scale) {
+  constexpr int R = RPT * 16;          // query rows of the group
+  constexpr int DP = DH + 4;           // padded row stride (floats)
+  constexpr int CP = CH + 4;
+  constexpr int KPT = CH / 16;         // keys per thread in the score block
+  constexpr int DPT = DH / 16;         // output dims per thread
+  extern __shared__ __align__(16) float smem[];
+  float *Qs = smem;                    // [R][DP]
+  float *Ks = Qs + R * DP;             // [CH][DP]
+  float *Vs = Ks + CH * DP;            // [CH][DP]
+  float *Ps = Vs + CH * DP;            // [R][CP]
+  float *Ms = Ps + R * CP;             // [R] row max
+
   const int c = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-  const int G = nq / nkv, R = G * B;
+  const int G = nq / nkv;
   int n = ctx_lens[b];
   n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
   const int total = n + B;
   const int c0 = c * CH;
   if (c0 >= total) return;
   const int nk = min(CH, total - c0);
-  const int dp = dh + 1;
-  float *Qs = smem;               // [R][dh]
-  float *Ks = Qs + R * dh;        // [CH][dh+1]
-  float *Vs = Ks + CH * dp;       // [CH][dh]
-  float *S = Vs + CH * dh;        // [R][CH]
   const int tid = threadIdx.x;
 
-  for (int e = tid; e < R * dh; e += 256) {
-    const int qi = e / dh, dd = e % dh;
+  // ---- stage Q rows (R x DH), K and V chunk (CH x DH) as fp32
+  for (int e = tid; e < R * DH / 4; e += kAttnThreads) {
+    const int qi = e / (DH / 4), d4 = e % (DH / 4);
     const int qh = kvh * G + qi / B, j = qi % B;
-    Qs[e] = Q[(((size_t)b * B + j) * nq + qh) * dh + dd];
+    *(float4 *)(Qs + qi * DP + 4 * d4) = *(const float4 *)(Q + (((size_t)b * B + j) * nq + qh) * DH + 4 * d4);
   }
-  for (int e = tid; e < CH * dh; e += 256) {
-    const int t = e / dh, dd = e % dh;
-    float kvk = 0.f, kvv = 0.f;
+  for (int e = tid; e < CH * DH / 4; e += kAttnThreads) {
+    const int t = e / (DH / 4), d4 = e % (DH / 4);
+    float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
     if (t < nk) {
       const int kk = c0 + t;
       if (kk < n) {
-        const size_t off = ((((size_t)b * max_ctx + kk) * nkv) + kvh) * dh + dd;
-        kvk = to_f32(ck[off]);
-        kvv = to_f32(cv[off]);
+        const size_t off = ((((size_t)b * max_ctx + kk) * nkv) + kvh) * DH + 4 * d4;
+        kv = make_float4(to_f32(ck[off]), to_f32(ck[off + 1]), to_f32(ck[off + 2]), to_f32(ck[off + 3]));
+        vv = make_float4(to_f32(cv[off]), to_f32(cv[off + 1]), to_f32(cv[off + 2]), to_f32(cv[off + 3]));
       } else {
-        const size_t off = ((((size_t)b * B + (kk - n)) * nkv) + kvh) * dh + dd;
-        kvk = Kb[off];
-        kvv = Vb[off];
+        const size_t off = ((((size_t)b * B + (kk - n)) * nkv) + kvh) * DH + 4 * d4;
+        kv = *(const float4 *)(Kb + off);
+        vv = *(const float4 *)(Vb + off);
       }
     }
-    Ks[t * dp + dd] = kvk;
-    Vs[t * dh + dd] = kvv;
+    *(float4 *)(Ks + t * DP + 4 * d4) = kv;
+    *(float4 *)(Vs + t * DP + 4 * d4) = vv;
   }
   __syncthreads();
 
-  for (int e = tid; e < R * CH; e += 256) {
-    const int qi = e / CH, t = e % CH;
-    float s = -INFINITY;
-    if (t < nk) {
-      const float *qr = Qs + qi * dh;
-      const float *kr = Ks + t * dp;
-      float a0 = 0.f, a1 = 0.f;
-      for (int dd = 0; dd < dh; dd += 2) {
-        a0 = fmaf(qr[dd], kr[dd], a0);
-        a1 = fmaf(qr[dd + 1], kr[dd + 1], a1);
+  // ---- scores: thread (qb, kb) owns rows qb*RPT.. and keys kb*KPT..
+  const int qb = tid / 16, kb = tid % 16;
+  float s[RPT][KPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i)
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) s[i][k] = 0.f;
+  for (int d = 0; d < DH; d += 4) {
+    float4 kr[KPT];
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) kr[k] = *(const float4 *)(Ks + (kb * KPT + k) * DP + d);
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const float4 q = *(const float4 *)(Qs + (qb * RPT + i) * DP + d);
+#pragma unroll
+      for (int k = 0; k < KPT; ++k) {
+        s[i][k] = fmaf(q.x, kr[k].x, s[i][k]);
+        s[i][k] = fmaf(q.y, kr[k].y, s[i][k]);
+        s[i][k] = fmaf(q.z, kr[k].z, s[i][k]);
+        s[i][k] = fmaf(q.w, kr[k].w, s[i][k]);
       }
-      s = (a0 + a1) * scale;
     }
-    S[e] = s;
   }
-  __syncthreads();
-
-  // per-row max and exp; one wave per row at a time
-  const int wave = tid >> 6, lane = tid & 63;
-  float *rowstat = part;  // written below per row
-  for (int qi = wave; qi < R; qi += 4) {
-    float s = lane < CH ? S[qi * CH + lane] : -INFINITY;
-    const float m = wave_max(s);
-    const float p = (lane < nk) ? expf(s - m) : 0.f;
-    const float l = wave_sum(p);
-    if (lane < CH) S[qi * CH + lane] = p;
-    if (lane == 0) {
+  // row max / exp / row sum over the 16 threads sharing qb (xor over the low 4 lane bits)
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+      s[i][k] = (kb * KPT + k < nk) ? s[i][k] * scale : -INFINITY;
+      m = fmaxf(m, s[i][k]);
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    float l = 0.f;
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+      const float p = (kb * KPT + k < nk) ? expf(s[i][k] - m) : 0.f;
+      Ps[(qb * RPT + i) * CP + kb * KPT + k] = p;
+      l += p;
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) l += __shfl_xor(l, o, 64);
+    if (kb == 0) {
+      const int qi = qb * RPT + i;
       const int qh = kvh * G + qi / B, j = qi % B;
-      float *dst = rowstat + ((((size_t)b * nq + qh) * B + j) * nch + c) * (dh + 2);
-      dst[dh] = m;
-      dst[dh + 1] = l;
+      float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2);
+      dst[DH] = m;
+      dst[DH + 1] = l;
     }
   }
   __syncthreads();
-  for (int e = tid; e < R * dh; e += 256) {
-    const int qi = e / dh, dd = e % dh;
-    const float *pr = S + qi * CH;
-    float acc = 0.f;
-    for (int t = 0; t < nk; ++t) acc = fmaf(pr[t], Vs[t * dh + dd], acc);
+
+  // ---- output: thread (qb, db) owns rows qb*RPT.. and dims db*DPT..
+  const int db = tid % 16;
+  float o[RPT][DPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i)
+#pragma unroll
+    for (int x = 0; x < DPT; ++x) o[i][x] = 0.f;
+  for (int t = 0; t < nk; t += 4) {
+    float4 pr[RPT];
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) pr[i] = *(const float4 *)(Ps + (qb * RPT + i) * CP + t);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      float vr[DPT];
+#pragma unroll
+      for (int x = 0; x < DPT; x += 4) {
+        const float4 v4 = *(const float4 *)(Vs + (t + u) * DP + db * DPT + x);
+        vr[x] = v4.x;
+        vr[x + 1] = v4.y;
+        vr[x + 2] = v4.z;
+        vr[x + 3] = v4.w;
+      }
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) {
+        const float p = u == 0 ? pr[i].x : (u == 1 ? pr[i].y : (u == 2 ? pr[i].z : pr[i].w));
+#pragma unroll
+        for (int x = 0; x < DPT; ++x) o[i][x] = fmaf(p, vr[x], o[i][x]);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int qi = qb * RPT + i;
     const int qh = kvh * G + qi / B, j = qi % B;
-    part[((((size_t)b * nq + qh) * B + j) * nch + c) * (dh + 2) + dd] = acc;
+    float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2) + db * DPT;
+#pragma unroll
+    for (int x = 0; x < DPT; x += 4) *(float4 *)(dst + x) = make_float4(o[i][x], o[i][x + 1], o[i][x + 2], o[i][x + 3]);
   }
 }
 
+// Merge the chunks of one (batch, query head, block row) with log-sum-exp
+// weights; one wave per row, lane c reads chunk c's statistics.
+template <int DH>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float *__restrict__ part,
                                                            const int32_t *__restrict__ ctx_lens,
                                                            int max_ctx, float *__restrict__ O, int bs,
-                                                           int B, int nq, int dh, int nch) {
+                                                           int B, int nq, int nch, int CH) {
   const int lane = threadIdx.x & 63;
   const int item = blockIdx.x * 4 + (threadIdx.x >> 6);  // (b, qh, j)
   if (item >= bs * nq * B) return;
@@ -263,21 +357,42 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float *__restri
   int n = ctx_lens[b];
   n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
   const int nc = (n + B + CH - 1) / CH;
-  const float *base = part + (((size_t)b * nq + qh) * B + j) * nch * (dh + 2);
+  const float *base = part + (((size_t)b * nq + qh) * B + j) * nch * (DH + 2);
   float M = -INFINITY;
-  for (int c = 0; c < nc; ++c) M = fmaxf(M, base[c * (dh + 2) + dh]);
-  float den = 0.f, o0 = 0.f, o1 = 0.f;
-  for (int c = 0; c < nc; ++c) {
-    const float *pc = base + c * (dh + 2);
-    const float w = expf(pc[dh] - M);
-    den = fmaf(w, pc[dh + 1], den);
-    o0 = fmaf(w, pc[lane], o0);
-    if (dh == 128) o1 = fmaf(w, pc[lane + 64], o1);
+  for (int c = lane; c < nc; c += 64) M = fmaxf(M, base[c * (DH + 2) + DH]);
+  M = wave_max(M);
+  float den = 0.f;
+  for (int c = lane; c < nc; c += 64) den += expf(base[c * (DH + 2) + DH] - M) * base[c * (DH + 2) + DH + 1];
+  den = wave_sum(den);
+  constexpr int PER = DH / 64;
+  float acc[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) acc[q] = 0.f;
+  int c = 0;
+  for (; c + 4 <= nc; c += 4) {
+    float w[4], v[4][PER];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      w[u] = base[(c + u) * (DH + 2) + DH];
+#pragma unroll
+      for (int q = 0; q < PER; ++q) v[u][q] = base[(c + u) * (DH + 2) + lane + 64 * q];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float wu = expf(w[u] - M);
+#pragma unroll
+      for (int q = 0; q < PER; ++q) acc[q] = fmaf(wu, v[u][q], acc[q]);
+    }
+  }
+  for (; c < nc; ++c) {
+    const float wu = expf(base[c * (DH + 2) + DH] - M);
+#pragma unroll
+    for (int q = 0; q < PER; ++q) acc[q] = fmaf(wu, base[c * (DH + 2) + lane + 64 * q], acc[q]);
   }
   const float inv = 1.0f / den;
-  float *dst = O + ((size_t)(b * B + j) * nq + qh) * dh;
-  dst[lane] = o0 * inv;
-  if (dh == 128) dst[lane + 64] = o1 * inv;
+  float *dst = O + ((size_t)(b * B + j) * nq + qh) * DH;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) dst[lane + 64 * q] = acc[q] * inv;
 }
 
 // ---------------------------------------------------------------------------
@@ -294,29 +409,29 @@ void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor,
                        D.B, D.d, D.V, D.mask_id, err);
 }
 
-void launch_rmsnorm(const Dims &D, const float *x, int ldx, const void *gain, float *y, int ldy,
-                    int rows, int width, bool skip_anchor, hipStream_t st) {
+void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
+                     const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor, hipStream_t st) {
   if (rows <= 0) return;
   if (D.bf16)
-    hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(rows), dim3(256), 0, st, x, ldx, (const bf16_t *)gain, y,
-                       ldy, width, D.eps, (int)skip_anchor, D.B - 1);
+    hipLaunchKernelGGL(add_norm_kernel<bf16_t>, dim3(rows), dim3(512), 0, st, x, ldx, parts, np, pstride,
+                       (const bf16_t *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(256), 0, st, x, ldx, (const float *)gain, y,
-                       ldy, width, D.eps, (int)skip_anchor, D.B - 1);
+    hipLaunchKernelGGL(add_norm_kernel<float>, dim3(rows), dim3(512), 0, st, x, ldx, parts, np, pstride,
+                       (const float *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1);
 }
 
-void launch_qk_norm_rope(const Dims &D, const float *qkv, const void *q_norm, const void *k_norm,
-                         const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb, float *Vb,
-                         hipStream_t st) {
+void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,
+                         const void *k_norm, const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb,
+                         float *Vb, hipStream_t st) {
   const int M = D.bs * D.B;
   const int items = M * (D.nq + 2 * D.nkv);
   dim3 grid((items + 3) / 4);
   if (D.bf16)
-    hipLaunchKernelGGL(qk_norm_rope_kernel<bf16_t>, grid, dim3(256), 0, st, qkv, (const bf16_t *)q_norm,
+    hipLaunchKernelGGL(qk_norm_rope_kernel<bf16_t>, grid, dim3(256), 0, st, qkv, np, pstride, (const bf16_t *)q_norm,
                        (const bf16_t *)k_norm, ctx_lens, max_ctx, Q, Kb, Vb, M, D.B, D.nq, D.nkv, D.dh,
                        D.eps, D.theta);
   else
-    hipLaunchKernelGGL(qk_norm_rope_kernel<float>, grid, dim3(256), 0, st, qkv, (const float *)q_norm,
+    hipLaunchKernelGGL(qk_norm_rope_kernel<float>, grid, dim3(256), 0, st, qkv, np, pstride, (const float *)q_norm,
                        (const float *)k_norm, ctx_lens, max_ctx, Q, Kb, Vb, M, D.B, D.nq, D.nkv, D.dh,
                        D.eps, D.theta);
 }
@@ -336,9 +451,37 @@ void launch_ctx_store(const Dims &D, const float *kv, int n_new, const void *k_n
                        ctx_lens, max_ctx, (float *)ck, (float *)cv, D.bs, D.nkv, D.dh, D.eps, D.theta, err);
 }
 
-static size_t attn_lds_bytes(const Dims &D) {
+template <typename WT, int RPT, int CH, int DH>
+static void attn_launch_t(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
+                          const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
+                          hipStream_t st) {
+  constexpr int R = RPT * 16, DP = DH + 4, CP = CH + 4;
+  const size_t lds = sizeof(float) * ((size_t)R * DP + 2 * CH * DP + (size_t)R * CP + R);
+  const float scale = 1.0f / sqrtf((float)DH);
+  const int nc = (max_ctx + D.B + CH - 1) / CH;
+  (void)hipFuncSetAttribute((const void *)attn_partial_kernel<WT, RPT, CH, DH>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipLaunchKernelGGL((attn_partial_kernel<WT, RPT, CH, DH>), dim3(nc, D.nkv, D.bs), dim3(kAttnThreads), lds, st,
+                     Q, Kb, Vb, (const WT *)ck, (const WT *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv, nch,
+                     scale);
+}
+
+template <typename WT, int DH>
+static bool attn_dispatch(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
+                          const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
+                          hipStream_t st) {
   const int R = (D.nq / D.nkv) * D.B;
-  return sizeof(float) * ((size_t)R * D.dh + CH * (D.dh + 1) + CH * D.dh + (size_t)R * CH);
+  switch (R) {
+    case 32: attn_launch_t<WT, 2, 64, DH>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st); return true;
+    case 64: attn_launch_t<WT, 4, 64, DH>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st); return true;
+    case 128: attn_launch_t<WT, 8, 32, DH>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st); return true;
+    default: return false;
+  }
+}
+
+bool attn_supported(int nq, int nkv, int B) {
+  const int R = (nq / nkv) * B;
+  return R == 32 || R == 64 || R == 128;
 }
 
 void launch_attention(const Dims &D, const float *Q, const float *Kb, const float *Vb,
@@ -346,24 +489,34 @@ void launch_attention(const Dims &D, const float *Q, const float *Kb, const floa
                       float *part, float *O, int32_t *err, hipStream_t st) {
   (void)err;
   const int nch = attn_nchunks(max_ctx, D.B);
-  const size_t lds = attn_lds_bytes(D);
-  const float scale = 1.0f / sqrtf((float)D.dh);
-  dim3 grid(nch, D.nkv, D.bs);
-  if (D.bf16) {
-    (void)hipFuncSetAttribute((const void *)attn_partial_kernel<bf16_t>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(attn_partial_kernel<bf16_t>, grid, dim3(256), lds, st, Q, Kb, Vb,
-                       (const bf16_t *)ck, (const bf16_t *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv,
-                       D.dh, nch, scale);
+  const int G = D.nq / D.nkv;
+  const int CH = attn_ch(G);
+  if (D.dh == 128) {
+    if (D.bf16) attn_dispatch<bf16_t, 128>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st);
+    else attn_dispatch<float, 128>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st);
   } else {
-    (void)hipFuncSetAttribute((const void *)attn_partial_kernel<float>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(attn_partial_kernel<float>, grid, dim3(256), lds, st, Q, Kb, Vb, (const float *)ck,
-                       (const float *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv, D.dh, nch, scale);
+    if (D.bf16) attn_dispatch<bf16_t, 64>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st);
+    else attn_dispatch<float, 64>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st);
   }
   const int items = D.bs * D.nq * D.B;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3((items + 3) / 4), dim3(256), 0, st, part, ctx_lens, max_ctx,
-                     O, D.bs, D.B, D.nq, D.dh, nch);
+  if (D.dh == 128)
+    hipLaunchKernelGGL(attn_combine_kernel<128>, dim3((items + 3) / 4), dim3(256), 0, st, part, ctx_lens, max_ctx,
+                       O, D.bs, D.B, D.nq, nch, CH);
+  else
+    hipLaunchKernelGGL(attn_combine_kernel<64>, dim3((items + 3) / 4), dim3(256), 0, st, part, ctx_lens, max_ctx,
+                       O, D.bs, D.B, D.nq, nch, CH);
+}
+
+template <typename WT>
+__global__ void to_f32_kernel(const WT *__restrict__ src, float *__restrict__ dst, size_t n) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = to_f32(src[i]);
+}
+void launch_to_f32(const void *src, bool bf16, float *dst, size_t n, hipStream_t st) {
+  if (n == 0) return;
+  const unsigned blocks = (unsigned)((n + 255) / 256);
+  if (bf16) hipLaunchKernelGGL(to_f32_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st, (const bf16_t *)src, dst, n);
+  else hipLaunchKernelGGL(to_f32_kernel<float>, dim3(blocks), dim3(256), 0, st, (const float *)src, dst, n);
 }
 
 __global__ void fill_u32_kernel(uint32_t *p, size_t n, uint32_t v) {

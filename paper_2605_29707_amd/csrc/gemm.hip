@@ -14,23 +14,24 @@
 // bf16 weights meet fp32 activations split into hi + lo bf16 parts (two MFMAs
 // per fragment; products are exact in fp32), so the GEMM keeps fp32 accuracy.
 //
-// Work split: a workgroup of 4 waves owns T consecutive tiles and one of
-// `ksplit` K-ranges; its 4 waves split that range again.  Partial tiles are
-// summed in LDS in wave order, and across workgroups through a workspace in
-// K-range order by whichever workgroup finishes last — the sum order never
-// depends on timing, so results are bitwise reproducible.
+// Work split: a workgroup of 8 waves owns 8/WPT consecutive tiles (WPT waves
+// per tile) and a range of K chunks of KCM k-steps.  The activations of a
+// chunk are staged once per workgroup into LDS, already split into hi/lo
+// fragments, and shared by all its waves; weight fragments of the next chunk
+// are in flight while the current chunk is multiplied.  Loads are issued
+// unconditionally (addresses clamped) and activations before weights, so the
+// in-order vector-memory counter never makes a wave wait for the weights it
+// just prefetched.  When K is split across workgroups (ksplit > 1) each
+// split writes its own partial output and the consuming kernel adds the
+// partials in split order: no workgroup ever waits on another, and the sums
+// are bitwise reproducible.
 #include "common.h"
 #include "kernels.h"
+#include "mfma.h"
+
+#include <algorithm>
 
 namespace dk {
-
-template <typename WT> struct Frag;
-template <> struct Frag<bf16_t> {
-  static constexpr int EPL = 8, KSTEP = 32;
-};
-template <> struct Frag<float> {
-  static constexpr int EPL = 4, KSTEP = 16;
-};
 
 template <typename WT>
 __global__ void pack_kernel(const WT *__restrict__ W, int N, int K, int ldw, WT *__restrict__ P,
@@ -62,225 +63,180 @@ __global__ void pack_kernel(const WT *__restrict__ W, int N, int K, int ldw, WT 
   *(u32x4 *)dst = *(u32x4 *)vals;
 }
 
-// Load this lane's activation fragment (EPL consecutive k of row m), zero
-// outside [0, M) x [0, K).
-template <int EPL>
-DEVI void load_x(const float *__restrict__ X, int ldx, int M, int K, int m, int k0, float *out) {
-  if (m < M && k0 + EPL <= K) {
-    const float4 *p = (const float4 *)(X + (size_t)m * ldx + k0);
-#pragma unroll
-    for (int q = 0; q < EPL / 4; ++q) {
-      float4 v = p[q];
-      out[4 * q + 0] = v.x;
-      out[4 * q + 1] = v.y;
-      out[4 * q + 2] = v.z;
-      out[4 * q + 3] = v.w;
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) out[e] = (m < M && k0 + e < K) ? X[(size_t)m * ldx + k0 + e] : 0.f;
-  }
-}
-
-template <typename WT, int T, int MT>
-struct Mac;
-
-template <int T, int MT>
-struct Mac<bf16_t, T, MT> {
-  DEVI static void step(const u32x4 (&w)[T], const float (&x)[MT][8], floatx4 (&acc)[T][MT]) {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      bf16x8 hi, lo;
-      split8(x[mt], hi, lo);
-#pragma unroll
-      for (int i = 0; i < T; ++i) {
-        bf16x8 a = __builtin_bit_cast(bf16x8, w[i]);
-        acc[i][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, hi, acc[i][mt], 0, 0, 0);
-        acc[i][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, lo, acc[i][mt], 0, 0, 0);
-      }
-    }
-  }
-};
-
-template <int T, int MT>
-struct Mac<float, T, MT> {
-  DEVI static void step(const u32x4 (&w)[T], const float (&x)[MT][4], floatx4 (&acc)[T][MT]) {
-#pragma unroll
-    for (int i = 0; i < T; ++i) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float a = __uint_as_float(w[i][e]);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-          acc[i][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, x[mt][e], acc[i][mt], 0, 0, 0);
-      }
-    }
-  }
-};
 
 DEVI float silu_f(float x) { return x / (1.f + expf(-x)); }
 
-template <typename WT, int T, int MT, int EPI, int U>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
+// X fragment of (k-step s, m-tile mt, lane): EPL consecutive k of row m, zero
+// outside [0, M) x [0, K).  The load itself is always issued at a clamped,
+// valid address (K is a multiple of EPL), so the count of outstanding vector
+// loads stays static.
+template <int EPL>
+DEVI void load_xfrag(const float *__restrict__ X, int ldx, int M, int K, int m, int k0, float4 (&v)[EPL / 4]) {
+  const bool ok = m < M && k0 + EPL <= K;
+  const int mc = m < M ? m : M - 1;
+  const int kc = k0 + EPL <= K ? k0 : K - EPL;
+  const float4 *p = (const float4 *)(X + (size_t)mc * ldx + kc);
+#pragma unroll
+  for (int q = 0; q < EPL / 4; ++q) {
+    const float4 t = p[q];
+    v[q] = ok ? t : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+}
+
+constexpr int kWaves = 8;
+
+template <typename WT, int MT, int WPT, int EPI>
+__global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
   constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int g = lane >> 4, r = lane & 15;
+  constexpr int XF = XStage<WT>::XF;
+  constexpr int KCM = 16 / MT;           // k-steps per chunk
+  constexpr int KW = KCM / WPT;          // k-steps per wave per chunk
+  constexpr int TW = kWaves / WPT;       // tiles per workgroup
+  constexpr int ITEMS = KCM * MT * 64;   // staged fragments per chunk
+  constexpr int IPT = ITEMS / (kWaves * 64);
+  static_assert(ITEMS % (kWaves * 64) == 0, "staging split");
+
+  __shared__ u32x4 xs[2][KCM][MT][64][XF];
+  __shared__ floatx4 xch[kWaves][MT][64];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = blockIdx.x, ky = blockIdx.y, mz = blockIdx.z;
   const int KS = a.KS;
+  const int nch = (KS + KCM - 1) / KCM;
+  const int cpw = (nch + a.ksplit - 1) / a.ksplit;
+  const int c0 = min(nch, ky * cpw), c1 = min(nch, c0 + cpw);
+  const int tile = grp * TW + wave / WPT;
+  const bool tvalid = tile < a.ntiles;
+  const int ksub = (wave % WPT) * KW;    // this wave's first k-step within a chunk
+  const u32x4 *__restrict__ Pv =
+      (const u32x4 *)a.P + ((size_t)(a.tile0 + (tvalid ? tile : 0)) * KS) * 64 + lane;
+  const int mbase = mz * MT * 16;
 
-  const int nw = a.ksplit * 4;
-  const int per = (KS + nw - 1) / nw;
-  const int s0 = (ky * 4 + wave) * per;
-  const int s1 = min(KS, s0 + per);
+  floatx4 acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  floatx4 acc[T][MT];
+  auto load_w = [&](u32x4 (&w)[KW], int c) {
 #pragma unroll
-  for (int i = 0; i < T; ++i)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[i][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  const u32x4 *__restrict__ Pv = (const u32x4 *)a.P;
-  size_t tbase[T];
-  bool tval[T];
-#pragma unroll
-  for (int i = 0; i < T; ++i) {
-    int t = grp * T + i;
-    tval[i] = t < a.ntiles;
-    tbase[i] = ((size_t)(a.tile0 + (tval[i] ? t : 0)) * KS) * 64 + lane;
-  }
-  int mrow[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) mrow[mt] = (mz * MT + mt) * 16 + r;
-
-  int s = s0;
-  for (; s + U <= s1; s += U) {
-    u32x4 w[U][T];
-    float x[U][MT][EPL];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int i = 0; i < T; ++i)
-        w[u][i] = tval[i] ? __builtin_nontemporal_load(&Pv[tbase[i] + (size_t)(s + u) * 64])
-                          : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-        load_x<EPL>(a.X, a.ldx, a.M, a.K, mrow[mt], (s + u) * KSTEP + g * EPL, x[u][mt]);
-#pragma unroll
-    for (int u = 0; u < U; ++u) Mac<WT, T, MT>::step(w[u], x[u], acc);
-  }
-  for (; s < s1; ++s) {
-    u32x4 w[T];
-    float x[MT][EPL];
-#pragma unroll
-    for (int i = 0; i < T; ++i)
-      w[i] = tval[i] ? __builtin_nontemporal_load(&Pv[tbase[i] + (size_t)s * 64]) : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) load_x<EPL>(a.X, a.ldx, a.M, a.K, mrow[mt], s * KSTEP + g * EPL, x[mt]);
-    Mac<WT, T, MT>::step(w, x, acc);
-  }
-
-  // ---- reduce the 4 waves' partial tiles in LDS (fixed wave order)
-  __shared__ floatx4 red[4][T][MT][64];
-  __shared__ int s_last;
-#pragma unroll
-  for (int i = 0; i < T; ++i)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) red[wave][i][mt][lane] = acc[i][mt];
-  __syncthreads();
-
-  constexpr int ITEMS = T * MT * 64;
-  const int Mpad = gridDim.z * MT * 16;
-  const int ncols = a.ntiles * 16;  // columns covered by the launch (partials)
-  for (int it = threadIdx.x; it < ITEMS; it += 256) {
-    const int l = it & 63, mt = (it >> 6) % MT, i = (it >> 6) / MT;
-    floatx4 v = red[0][i][mt][l];
-#pragma unroll
-    for (int wv = 1; wv < 4; ++wv) v += red[wv][i][mt][l];
-    red[0][i][mt][l] = v;
-    if (a.ksplit > 1) {
-      const int m = (mz * MT + mt) * 16 + (l & 15);
-      const int n = (grp * T + i) * 16 + 4 * (l >> 4);
-      if (grp * T + i < a.ntiles)
-        *(floatx4 *)(a.part + ((size_t)ky * Mpad + m) * ncols + n) = v;
+    for (int u = 0; u < KW; ++u) {
+      const int s = min(c * KCM + ksub + u, KS - 1);
+      w[u] = __builtin_nontemporal_load(Pv + (size_t)s * 64);
     }
-  }
-  if (a.ksplit > 1) {
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      int *tk = a.tickets + (size_t)blockIdx.z * gridDim.x + grp;
-      int prev = atomicAdd(tk, 1);
-      s_last = (prev == a.ksplit - 1);
-      if (s_last) atomicExch(tk, 0);  // ready for the next launch
+  };
+  auto load_x = [&](float4 (&v)[IPT][EPL / 4], int c) {
+#pragma unroll
+    for (int q = 0; q < IPT; ++q) {
+      const int it = tid + q * kWaves * 64;
+      const int l = it & 63, mt = (it >> 6) % MT, s = (it >> 6) / MT;
+      const int m = mbase + mt * 16 + (l & 15);
+      const int k0 = (c * KCM + s) * KSTEP + (l >> 4) * EPL;
+      load_xfrag<EPL>(a.X, a.ldx, a.M, a.K, m, k0, v[q]);
     }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-  } else {
-    __syncthreads();
-  }
-
-  // ---- epilogue
-  if (EPI == EPI_SWIGLU) {
-    // tiles come in (gate, up) pairs; output column = 16*pair + 4g + e
-    constexpr int PAIRS = T / 2;
-    for (int it = threadIdx.x; it < PAIRS * MT * 64; it += 256) {
-      const int l = it & 63, mt = (it >> 6) % MT, q = (it >> 6) / MT;
-      const int m = (mz * MT + mt) * 16 + (l & 15);
-      const int tg = grp * T + 2 * q;
-      if (m >= a.M || tg + 1 >= a.ntiles) continue;
-      floatx4 gv, uv;
-      if (a.ksplit > 1) {
-        gv = floatx4{0.f, 0.f, 0.f, 0.f};
-        uv = gv;
-        const int n = tg * 16 + 4 * (l >> 4);
-        for (int kz = 0; kz < a.ksplit; ++kz) {
-          const float *row = a.part + ((size_t)kz * Mpad + m) * ncols;
-          gv += *(const floatx4 *)(row + n);
-          uv += *(const floatx4 *)(row + n + 16);
-        }
-      } else {
-        gv = red[0][2 * q][mt][l];
-        uv = red[0][2 * q + 1][mt][l];
+  };
+  auto store_x = [&](const float4 (&v)[IPT][EPL / 4], int buf) {
+#pragma unroll
+    for (int q = 0; q < IPT; ++q) {
+      const int it = tid + q * kWaves * 64;
+      const int l = it & 63, mt = (it >> 6) % MT, s = (it >> 6) / MT;
+      XStage<WT>::put(&xs[buf][s][mt][l][0], v[q]);
+    }
+  };
+  auto compute = [&](const u32x4 (&w)[KW], int c, int buf) {
+#pragma unroll
+    for (int u = 0; u < KW; ++u) {
+      if (c * KCM + ksub + u < KS) {
+        u32x4 xf[MT * XF];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int f = 0; f < XF; ++f) xf[mt * XF + f] = xs[buf][ksub + u][mt][lane][f];
+        Mac2<WT, MT>::step(w[u], xf, acc);
       }
-      const int col = (tg / 2) * 16 + 4 * (l >> 4);
-      float *y = a.Y + (size_t)m * a.ldy + col;
+    }
+  };
+
+  if (c0 < c1) {
+    u32x4 wa[KW], wb[KW];
+    float4 xr[IPT][EPL / 4];
+    load_x(xr, c0);
+    load_w(wa, c0);
+    store_x(xr, 0);
+    __syncthreads();
+    for (int c = c0; c < c1; c += 2) {
+      // chunk c in (wa, buf 0); prefetch c+1 into (xr, wb)
+      const bool n1 = c + 1 < c1;
+      if (n1) {
+        load_x(xr, c + 1);
+        load_w(wb, c + 1);
+      }
+      compute(wa, c, 0);
+      if (n1) store_x(xr, 1);
+      __syncthreads();
+      if (!n1) break;
+      const bool n2 = c + 2 < c1;
+      if (n2) {
+        load_x(xr, c + 2);
+        load_w(wa, c + 2);
+      }
+      compute(wb, c + 1, 1);
+      if (n2) store_x(xr, 0);
+      __syncthreads();
+    }
+  }
+
+  // waves sharing a tile: fold into the first one
+  if (WPT > 1) {
+    if (wave % WPT) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) xch[wave][mt][lane] = acc[mt];
+    }
+    __syncthreads();
+    if (wave % WPT == 0) {
+#pragma unroll
+      for (int q = 1; q < WPT; ++q)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[mt] += xch[wave + q][mt][lane];
+    }
+  }
+
+  float *Y = a.Y + (size_t)ky * a.ysplit;
+  if (EPI == EPI_SWIGLU) {
+    // tiles come in (gate, up) pairs held by owner waves w and w + WPT
+    __syncthreads();
+    const bool owner = wave % WPT == 0;
+    const bool up = ((wave / WPT) & 1) == 1;
+    if (owner && up) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) xch[wave][mt][lane] = acc[mt];
+    }
+    __syncthreads();
+    if (!owner || up || tile + 1 >= a.ntiles) return;
+    const int col = (tile / 2) * 16 + 4 * (lane >> 4);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = mbase + mt * 16 + (lane & 15);
+      if (m >= a.M) continue;
+      const floatx4 uv = xch[wave + WPT][mt][lane];
+      float *y = Y + (size_t)m * a.ldy + col;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (col + e < a.N) y[e] = silu_f(gv[e]) * uv[e];
+        if (col + e < a.N) y[e] = silu_f(acc[mt][e]) * uv[e];
     }
     return;
   }
-  for (int it = threadIdx.x; it < ITEMS; it += 256) {
-    const int l = it & 63, mt = (it >> 6) % MT, i = (it >> 6) / MT;
-    const int m = (mz * MT + mt) * 16 + (l & 15);
-    const int t = grp * T + i;
-    if (m >= a.M || t >= a.ntiles) continue;
-    const int n = t * 16 + 4 * (l >> 4);
-    floatx4 v;
-    if (a.ksplit > 1) {
-      v = floatx4{0.f, 0.f, 0.f, 0.f};
-      for (int kz = 0; kz < a.ksplit; ++kz) v += *(const floatx4 *)(a.part + ((size_t)kz * Mpad + m) * ncols + n);
-    } else {
-      v = red[0][i][mt][l];
-    }
-    float *y = a.Y + (size_t)m * a.ldy + n;
+  if (wave % WPT || !tvalid) return;
+  const int n = tile * 16 + 4 * (lane >> 4);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = mbase + mt * 16 + (lane & 15);
+    if (m >= a.M) continue;
+    float *y = Y + (size_t)m * a.ldy + n;
     if (n + 4 <= a.N && ((a.ldy & 3) == 0)) {
-      if (EPI == EPI_ADD) {
-        floatx4 o = *(floatx4 *)y;
-        *(floatx4 *)y = o + v;
-      } else {
-        *(floatx4 *)y = v;
-      }
+      *(floatx4 *)y = acc[mt];
     } else {
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (n + e < a.N) {
-          if (EPI == EPI_ADD) y[e] += v[e];
-          else y[e] = v[e];
-        }
+        if (n + e < a.N) y[e] = acc[mt][e];
     }
   }
 }
@@ -288,46 +244,47 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu) {
+GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu, int max_split) {
   GemmPlan p;
   p.MT = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-  p.T = (epi == EPI_SWIGLU) ? 2 : (ntiles >= 2 ? 2 : 1);
-  p.groups = (ntiles + p.T - 1) / p.T;
+  const int kcm = 16 / p.MT;
+  const int nch = (KS + kcm - 1) / kcm;
   p.mgroups = (M + 16 * p.MT - 1) / (16 * p.MT);
-  const int target = 2 * n_cu;  // workgroups wanted in flight
-  int ks = 1;
-  const int base = p.groups * p.mgroups;
-  while (base * ks < target && KS / ((ks + 1) * 4) >= 8) ++ks;
-  p.ksplit = ks;
-  p.part_floats = ks > 1 ? (size_t)ks * p.mgroups * p.MT * 16 * ntiles * 16 : 0;
-  p.tickets = ks > 1 ? (size_t)p.groups * p.mgroups : 0;
+  p.WPT = 1;
+  if ((ntiles + 7) / 8 * p.mgroups < n_cu && kcm >= 2) p.WPT = 2;
+  if (max_split > 1) p.WPT = 1;
+  const int tw = 8 / p.WPT;
+  p.groups = (ntiles + tw - 1) / tw;
+  p.ksplit = 1;
+  // split K (largest divisor of the chunk count) until about 1.5 workgroups per CU
+  for (int s = 2; s <= std::min(nch, max_split); ++s)
+    if (nch % s == 0 && p.groups * p.mgroups * s <= (3 * n_cu) / 2) p.ksplit = s;
+  (void)epi;
   return p;
 }
 
-template <typename WT, int T, int MT, int EPI>
+template <typename WT, int MT, int WPT, int EPI>
 static void launch_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
   dim3 grid(p.groups, p.ksplit, p.mgroups);
-  hipLaunchKernelGGL((gemm_kernel<WT, T, MT, EPI, 4>), grid, dim3(256), 0, st, a);
+  hipLaunchKernelGGL((gemm_kernel<WT, MT, WPT, EPI>), grid, dim3(kWaves * 64), 0, st, a);
 }
 
-template <typename WT, int T, int MT>
-static void launch_epi(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
-  if (epi == EPI_STORE) launch_t<WT, T, MT, EPI_STORE>(a, p, st);
-  else if (epi == EPI_ADD) launch_t<WT, T, MT, EPI_ADD>(a, p, st);
-  else launch_t<WT, 2, MT, EPI_SWIGLU>(a, p, st);
+template <typename WT, int MT>
+static void launch_m(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
+  if (p.WPT == 1) {
+    if (epi == EPI_SWIGLU) launch_t<WT, MT, 1, EPI_SWIGLU>(a, p, st);
+    else launch_t<WT, MT, 1, EPI_STORE>(a, p, st);
+  } else {
+    if (epi == EPI_SWIGLU) launch_t<WT, MT, 2, EPI_SWIGLU>(a, p, st);
+    else launch_t<WT, MT, 2, EPI_STORE>(a, p, st);
+  }
 }
 
 template <typename WT>
 static void launch_w(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
-  if (p.T == 1) {
-    if (p.MT == 1) launch_epi<WT, 1, 1>(epi, a, p, st);
-    else if (p.MT == 2) launch_epi<WT, 1, 2>(epi, a, p, st);
-    else launch_epi<WT, 1, 4>(epi, a, p, st);
-  } else {
-    if (p.MT == 1) launch_epi<WT, 2, 1>(epi, a, p, st);
-    else if (p.MT == 2) launch_epi<WT, 2, 2>(epi, a, p, st);
-    else launch_epi<WT, 2, 4>(epi, a, p, st);
-  }
+  if (p.MT == 1) launch_m<WT, 1>(epi, a, p, st);
+  else if (p.MT == 2) launch_m<WT, 2>(epi, a, p, st);
+  else launch_m<WT, 4>(epi, a, p, st);
 }
 
 void launch_gemm(bool bf16, int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {

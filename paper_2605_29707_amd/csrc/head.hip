@@ -1,94 +1,25 @@
 // Domino-head rollout (Sec. 4.1.2 causal encoder and low-rank correction,
-// Fig. 3 sequential rollout) as one persistent, cooperatively launched kernel.
+// Fig. 3 sequential rollout), as three short kernels per draft position j:
 //
-// For draft position j = 1 .. B-1 (all batch rows together):
-//   A  S_{j-1} = GRU(E[y_{j-1}], S_{j-2})      each workgroup owns a slice of
-//      the d_s state indices (its W_ih / W_hh rows stay in LDS for the whole
-//      rollout when they fit)
-//   B  u = SiLU(W1[:, :d] H_j + W1[:, d:] S_{j-1})  (the H half is precomputed
-//      for all j by a GEMM before the loop); each workgroup owns a slice of r
-//   C  L_j = L_base_j + W2 u over the workgroup's vocabulary slice, then the
-//      slice's top-beta under (value desc, id asc)
-//   D  every workgroup merges all slices' top-beta lists (redundantly, so no
-//      further barrier is needed) and takes y_j = top-1 (or the forced token)
-// Grid barriers separate A|B, B|C and C|D.  Each barrier's spin is bounded; on
-// timeout the kernel records DEV_BARRIER_TIMEOUT and every workgroup exits.
+//   gru    y_{j-1} = top-1 of position j-1 (merged from the logits kernel's
+//          per-workgroup lists; the anchor for j = 1; a forced token when
+//          teacher forcing), then S_{j-1} = GRU(E[y_{j-1}], S_{j-2}) for a
+//          slice of the d_s state indices per workgroup.  The input half of
+//          the gates, E[y] W_ih^T, is a row of the table G = E W_ih^T built at
+//          model creation, so a step gathers 3*d_s values instead of streaming
+//          W_ih.
+//   u      u = SiLU(W1[:, :d] H_j + W1[:, d:] S_{j-1}), the H half precomputed
+//          for all j by a GEMM before the loop.
+//   logits L_j = L_base_j + W2 u over a vocabulary slice per workgroup, and the
+//          slice's top-beta under (value desc, id asc).
+// A kernel boundary is the cheapest grid-wide handshake on this device (about
+// 1.6 us against about 4 us for a 256-workgroup spin barrier), so the
+// rollout is 3(B-1)+1 launches rather than one persistent kernel.
 #include "common.h"
 #include "kernels.h"
+#include "mfma.h"
 
 namespace dk {
-
-constexpr unsigned kSpinLimit = 1u << 22;
-
-struct Lds {
-  int ipw, upw, tpw_max, rows_max;
-  bool gru_lds;
-  size_t gru_off, lv_off, u_off, ys_off, abort_off, total;
-};
-
-static Lds plan_lds(const Dims &D, int G, bool bf16) {
-  Lds L;
-  const int esz = bf16 ? 2 : 4;
-  const int NT = (D.V + 15) / 16;
-  L.ipw = (D.ds + G - 1) / G;
-  L.upw = (D.r + G - 1) / G;
-  L.tpw_max = (NT + G - 1) / G;
-  L.rows_max = L.tpw_max * 16;
-  size_t off = 0;
-  L.lv_off = off;
-  off += (size_t)D.bs * L.rows_max * 4;
-  L.u_off = off;
-  off += (size_t)D.bs * D.r * 4;
-  L.ys_off = off;
-  off += (size_t)D.bs * 4;
-  L.abort_off = off;
-  off += 16;
-  off = (off + 15) & ~(size_t)15;
-  const size_t gru = (size_t)L.ipw * 3 * (D.d + D.ds) * esz;
-  const size_t budget = 150 * 1024;
-  L.gru_lds = off + gru <= budget;
-  L.gru_off = off;
-  if (L.gru_lds) off += gru;
-  L.total = off;
-  return L;
-}
-
-template <typename WT>
-struct HeadKernelArgs {
-  HeadArgs h;
-  Lds L;
-};
-
-// Bounded grid barrier.  Returns false if this or another workgroup gave up.
-DEVI bool grid_sync(unsigned *bar, unsigned *abort_flag, unsigned target, int32_t *err,
-                    volatile int *s_ok) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int ok = 1;
-    atomicAdd(bar, 1u);
-    unsigned spins = 0;
-    while (true) {
-      const unsigned v = __hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (v >= target) break;
-      if (__hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-        ok = 0;
-        break;
-      }
-      if (++spins > kSpinLimit) {
-        raise_error(err, DEV_BARRIER_TIMEOUT);
-        atomicExch(abort_flag, 1u);
-        ok = 0;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-    *s_ok = ok;
-  }
-  __syncthreads();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  return *s_ok != 0;
-}
 
 // Insert (v, id) into a sorted 8-entry list (best first) by bubbling.
 DEVI void list_insert(float (&lv)[8], int (&li)[8], float v, int id) {
@@ -105,8 +36,8 @@ DEVI void list_insert(float (&lv)[8], int (&li)[8], float v, int id) {
   }
 }
 
-// Wave-level top-beta of `cnt` candidates; candidate c is produced by get(c).
-// Lane 0 ends with the result in ov/oi (first beta entries valid).
+// Wave-level top-beta of `cnt` candidates produced by get(c); every lane ends
+// with the same result in ov/oi (first beta entries valid).
 template <typename Get>
 DEVI void wave_select(Get get, int cnt, int beta, float (&ov)[8], int (&oi)[8]) {
   const int lane = threadIdx.x & 63;
@@ -142,182 +73,93 @@ DEVI void wave_select(Get get, int cnt, int beta, float (&ov)[8], int (&oi)[8]) 
   }
 }
 
-template <typename WT>
-DEVI float2 ld2(const WT *p);
-template <>
-DEVI float2 ld2<float>(const float *p) {
-  return *(const float2 *)p;
-}
-template <>
-DEVI float2 ld2<bf16_t>(const bf16_t *p) {
-  const uint32_t u = *(const uint32_t *)p;
-  return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+// wave_select over candidates in global memory: each lane loads its
+// candidates 8 at a time, all loads of a batch in flight together.
+DEVI void wave_select_mem(const float *__restrict__ pv, const int32_t *__restrict__ pi, int cnt, int beta,
+                          float (&ov)[8], int (&oi)[8]) {
+  const int lane = threadIdx.x & 63;
+  float lv[8];
+  int li[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    lv[q] = -INFINITY;
+    li[q] = INT_MAX;
+  }
+  for (int c0 = 0; c0 < cnt; c0 += 8 * 64) {
+    float v[8];
+    int id[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int c = c0 + u * 64 + lane;
+      const int cc = c < cnt ? c : cnt - 1;
+      v[u] = pv[cc];
+      id[u] = c < cnt ? pi[cc] : INT_MAX;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (id[u] != INT_MAX) list_insert(lv, li, order_val(v[u]), id[u]);
+  }
+  for (int k = 0; k < beta; ++k) {
+    float bv = lv[0];
+    int bi = li[0];
+    wave_best(bv, bi);
+    ov[k] = bv;
+    oi[k] = bi;
+    if (li[0] == bi && bi != INT_MAX) {
+#pragma unroll
+      for (int q = 0; q < 7; ++q) {
+        lv[q] = lv[q + 1];
+        li[q] = li[q + 1];
+      }
+      lv[7] = -INFINITY;
+      li[7] = INT_MAX;
+    }
+  }
 }
 
 DEVI float sigm(float x) { return 1.f / (1.f + expf(-x)); }
 
 template <typename WT>
-__global__ __launch_bounds__(256) void head_kernel(HeadKernelArgs<WT> ka) {
-  const HeadArgs &h = ka.h;
-  const Lds &L = ka.L;
-  const Dims &D = h.D;
-  extern __shared__ __align__(16) unsigned char smem[];
-  float *lv = (float *)(smem + L.lv_off);
-  float *us = (float *)(smem + L.u_off);
-  int *ys = (int *)(smem + L.ys_off);
-  volatile int *s_ok = (volatile int *)(smem + L.abort_off);
-  WT *gw = (WT *)(smem + L.gru_off);
-
-  const int G = h.G, g = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int bs = D.bs, d = D.d, ds = D.ds, r = D.r, V = D.V, depth = D.B - 1;
-  const int beta = h.beta;
-  const int kw = d + ds;
-  const int i0 = min(ds, g * L.ipw), i1 = min(ds, i0 + L.ipw);
-  const int k0 = min(r, g * L.upw), k1 = min(r, k0 + L.upw);
-  const int NT = (V + 15) / 16;
-  const int t0 = (int)((long long)g * NT / G), t1 = (int)((long long)(g + 1) * NT / G);
-  const int row0 = t0 * 16, nrows = min(V, t1 * 16) - row0;
-  unsigned *bar = h.barrier, *abort_flag = h.barrier + 1;
-  unsigned nbar = 0;
-
-  // GRU rows of this workgroup into LDS: local row (li*3 + q) = [W_ih | W_hh] of gate q, index i0+li
-  const WT *w_ih = (const WT *)h.w_ih, *w_hh = (const WT *)h.w_hh;
-  if (L.gru_lds) {
-    const int nr = (i1 - i0) * 3;
-    for (int e = tid; e < nr * kw; e += 256) {
-      const int lr = e / kw, c = e % kw;
-      const int i = i0 + lr / 3, q = lr % 3;
-      gw[e] = c < d ? w_ih[(size_t)(q * ds + i) * d + c] : w_hh[(size_t)(q * ds + i) * ds + (c - d)];
-    }
+DEVI void unpack16(const u32x4 &w, float *f);
+template <>
+DEVI void unpack16<bf16_t>(const u32x4 &w, float *f) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    f[2 * q] = __uint_as_float(w[q] << 16);
+    f[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
   }
-  for (int b = tid; b < bs; b += 256) ys[b] = clamp_token(h.anchor[b], V, h.err);
-  __syncthreads();
+}
+template <>
+DEVI void unpack16<float>(const u32x4 &w, float *f) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) f[q] = __uint_as_float(w[q]);
+}
 
-  const WT *embed = (const WT *)h.embed;
-  const WT *b_ih = (const WT *)h.b_ih, *b_hh = (const WT *)h.b_hh;
-  const WT *w1 = (const WT *)h.w1s_rows;
-  constexpr int EPL = sizeof(WT) == 2 ? 8 : 4, KSTEP = 4 * EPL;
-  const int KS = r / KSTEP;
-  const u32x4 *w2p = (const u32x4 *)h.w2p;
+// ---------------------------------------------------------------------------
+// gru: merge position j-1's lists (j >= 2), choose y_{j-1}, advance the state
+// slice.  With j == B (merge_only) it only writes the last position's top-beta.
+// ---------------------------------------------------------------------------
+template <typename WT>
+__global__ __launch_bounds__(256) void head_gru_kernel(HeadArgs h, int j, int merge_only) {
+  constexpr int EPL = 16 / sizeof(WT);
+  const Dims &D = h.D;
+  const int bs = D.bs, ds = D.ds, depth = D.B - 1, beta = h.beta, V = D.V;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ int ys[64];
 
-  for (int j = 1; j <= depth; ++j) {
-    const float *hprev = h.hbuf + (size_t)((j - 1) & 1) * bs * ds;
-    float *hnext = h.hbuf + (size_t)(j & 1) * bs * ds;
-    const bool first = (j == 1);
-
-    // ---------------- A: GRU state slice
-    for (int item = wave; item < (i1 - i0) * bs; item += 4) {
-      const int li = item % (i1 - i0), b = item / (i1 - i0);
-      const int i = i0 + li;
-      const WT *e = embed + (size_t)ys[b] * d;
-      const float *hp = hprev + (size_t)b * ds;
-      float acc[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      for (int c = 2 * lane; c < d; c += 128) {
-        const float2 ev = ld2<WT>(e + c);
-#pragma unroll
-        for (int q = 0; q < 3; ++q) {
-          const float2 wv = L.gru_lds ? ld2<WT>(gw + (size_t)(li * 3 + q) * kw + c)
-                                      : ld2<WT>(w_ih + (size_t)(q * ds + i) * d + c);
-          acc[q] = fmaf(wv.x, ev.x, fmaf(wv.y, ev.y, acc[q]));
-        }
-      }
-      if (!first) {
-        for (int c = 2 * lane; c < ds; c += 128) {
-          const float2 hv = *(const float2 *)(hp + c);
-#pragma unroll
-          for (int q = 0; q < 3; ++q) {
-            const float2 wv = L.gru_lds ? ld2<WT>(gw + (size_t)(li * 3 + q) * kw + d + c)
-                                        : ld2<WT>(w_hh + (size_t)(q * ds + i) * ds + c);
-            acc[3 + q] = fmaf(wv.x, hv.x, fmaf(wv.y, hv.y, acc[3 + q]));
-          }
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < 6; ++q) acc[q] = wave_sum(acc[q]);
-      if (lane == 0) {
-        const float gir = acc[0] + to_f32(b_ih[i]), giz = acc[1] + to_f32(b_ih[ds + i]),
-                    gin = acc[2] + to_f32(b_ih[2 * ds + i]);
-        const float ghr = acc[3] + to_f32(b_hh[i]), ghz = acc[4] + to_f32(b_hh[ds + i]),
-                    ghn = acc[5] + to_f32(b_hh[2 * ds + i]);
-        const float rg = sigm(gir + ghr), zg = sigm(giz + ghz);
-        const float ng = tanhf(gin + rg * ghn);
-        const float hold = first ? 0.f : hp[i];
-        const float hn = (1.f - zg) * ng + zg * hold;
-        hnext[(size_t)b * ds + i] = hn;
-        if (h.states) h.states[((size_t)b * depth + (j - 1)) * ds + i] = hn;
-      }
-    }
-    if (!grid_sync(bar, abort_flag, (++nbar) * G, h.err, s_ok)) return;
-
-    // ---------------- B: u slice
-    for (int item = wave; item < (k1 - k0) * bs; item += 4) {
-      const int lk = item % (k1 - k0), b = item / (k1 - k0);
-      const int k = k0 + lk;
-      const float *hn = hnext + (size_t)b * ds;
-      const WT *wr = w1 + (size_t)k * (d + ds) + d;
-      float acc = 0.f;
-      for (int c = 2 * lane; c < ds; c += 128) {
-        const float2 wv = ld2<WT>(wr + c);
-        const float2 hv = *(const float2 *)(hn + c);
-        acc = fmaf(wv.x, hv.x, fmaf(wv.y, hv.y, acc));
-      }
-      acc = wave_sum(acc);
-      if (lane == 0) {
-        const float x = h.P[((size_t)b * depth + (j - 1)) * r + k] + acc;
-        h.ubuf[(size_t)b * r + k] = x / (1.f + expf(-x));
-      }
-    }
-    if (!grid_sync(bar, abort_flag, (++nbar) * G, h.err, s_ok)) return;
-
-    // ---------------- C: corrected logits of this slice
-    for (int e = tid; e < bs * r; e += 256) us[e] = h.ubuf[e];
-    __syncthreads();
-    {
-      const int gq = lane >> 4, rr = lane & 15;
-      for (int t = t0 + wave; t < t1; t += 4) {
-        u32x4 wf[16];
-#pragma unroll
-        for (int s = 0; s < 16; ++s)
-          if (s < KS) wf[s] = w2p[((size_t)t * KS + s) * 64 + lane];
-        const int n = t * 16 + rr;
-        for (int b = 0; b < bs; ++b) {
-          const float *ub = us + (size_t)b * r;
-          float acc = 0.f;
-#pragma unroll
-          for (int s = 0; s < 16; ++s) {
-            if (s < KS) {
-              const float *uu = ub + s * KSTEP + gq * EPL;
-              if (EPL == 8) {
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                  const uint32_t wv = wf[s][q];
-                  acc = fmaf(__uint_as_float(wv << 16), uu[2 * q], acc);
-                  acc = fmaf(__uint_as_float(wv & 0xffff0000u), uu[2 * q + 1], acc);
-                }
-              } else {
-#pragma unroll
-                for (int q = 0; q < 4; ++q) acc = fmaf(__uint_as_float(wf[s][q]), uu[q], acc);
-              }
-            }
-          }
-          acc += __shfl_xor(acc, 16, 64);
-          acc += __shfl_xor(acc, 32, 64);
-          if (gq == 0 && n < V) {
-            const float val = h.Lbase[((size_t)b * depth + (j - 1)) * V + n] + acc;
-            lv[(size_t)b * L.rows_max + (n - row0)] = val;
-            if (h.final_logits) h.final_logits[((size_t)b * depth + (j - 1)) * V + n] = val;
-          }
-        }
-      }
-    }
-    __syncthreads();
-    for (int b = wave; b < bs; b += 4) {
+  // ---- y_{j-1}
+  for (int b = wave; b < bs; b += 4) {
+    int y;
+    if (j == 1) {
+      y = clamp_token(h.anchor[b], V, h.err);
+    } else {
       float ov[8];
       int oi[8];
-      const float *lb = lv + (size_t)b * L.rows_max;
-      wave_select([&](int c, float &v, int &id) { v = lb[c]; id = row0 + c; }, nrows, beta, ov, oi);
-      if (lane < beta) {
+      const float *pv = h.pval + (size_t)b * h.GC * beta;
+      const int32_t *pi = h.pid + (size_t)b * h.GC * beta;
+      wave_select_mem(pv, pi, h.GC * beta, beta, ov, oi);
+      y = oi[0] < 0 ? 0 : (oi[0] >= V ? V - 1 : oi[0]);  // always a valid row of G
+      if (blockIdx.x == 0 && lane < beta) {
         float v = ov[0];
         int id = oi[0];
 #pragma unroll
@@ -326,64 +168,281 @@ __global__ __launch_bounds__(256) void head_kernel(HeadKernelArgs<WT> ka) {
             v = ov[q];
             id = oi[q];
           }
-        h.pval[((size_t)b * G + g) * beta + lane] = v;
-        h.pid[((size_t)b * G + g) * beta + lane] = id;
+        h.topk_ids[((size_t)b * depth + (j - 2)) * beta + lane] = id;
+        h.topk_vals[((size_t)b * depth + (j - 2)) * beta + lane] = v;
       }
+      if (h.forced) y = clamp_token(h.forced[(size_t)b * depth + (j - 2)], V, h.err);
     }
-    if (!grid_sync(bar, abort_flag, (++nbar) * G, h.err, s_ok)) return;
+    if (lane == 0) ys[b] = y;
+  }
+  if (merge_only) return;
+  __syncthreads();
 
-    // ---------------- D: merge all slices, choose y_j
-    for (int b = wave; b < bs; b += 4) {
-      float ov[8];
-      int oi[8];
-      const float *pv = h.pval + (size_t)b * G * beta;
-      const int32_t *pi = h.pid + (size_t)b * G * beta;
-      wave_select([&](int c, float &v, int &id) { v = pv[c]; id = pi[c]; }, G * beta, beta, ov, oi);
-      if (lane == 0) {
-        int y = oi[0];
-        if (h.forced) y = clamp_token(h.forced[(size_t)b * depth + (j - 1)], V, h.err);
-        ys[b] = y;
-        if (g == 0) {
-          for (int q = 0; q < beta; ++q) {
-            h.topk_ids[((size_t)b * depth + (j - 1)) * beta + q] = oi[q];
-            h.topk_vals[((size_t)b * depth + (j - 1)) * beta + q] = ov[q];
+  // ---- state slice: one wave per state index; lanes stride over d_s
+  const float *hprev = h.hbuf + (size_t)((j - 1) & 1) * bs * ds;
+  float *hnext = h.hbuf + (size_t)(j & 1) * bs * ds;
+  const WT *whh = (const WT *)h.w_hh;
+  const WT *bih = (const WT *)h.b_ih, *bhh = (const WT *)h.b_hh;
+  const int nchunk = ds / EPL;  // EPL-element chunks per row
+  for (int i = blockIdx.x * 4 + wave; i < ds; i += gridDim.x * 4) {
+    // W_hh rows (r, z, n) of index i stay in registers across the batch loop
+    u32x4 w[3][4];
+#pragma unroll
+    for (int q = 0; q < 3; ++q)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int ch = lane + 64 * c;
+        w[q][c] = (ch < nchunk && j > 1) ? *(const u32x4 *)(whh + ((size_t)(q * ds + i)) * ds + (size_t)ch * EPL)
+                                         : u32x4{0u, 0u, 0u, 0u};
+      }
+    for (int b = 0; b < bs; ++b) {
+      float acc[3] = {0.f, 0.f, 0.f};
+      if (j > 1) {
+        const float *hp = hprev + (size_t)b * ds;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int ch = lane + 64 * c;
+          if (ch < nchunk) {
+            float hv[EPL];
+#pragma unroll
+            for (int e = 0; e < EPL; e += 4) {
+              const float4 t = *(const float4 *)(hp + (size_t)ch * EPL + e);
+              hv[e] = t.x;
+              hv[e + 1] = t.y;
+              hv[e + 2] = t.z;
+              hv[e + 3] = t.w;
+            }
+#pragma unroll
+            for (int q = 0; q < 3; ++q) {
+              float wf[EPL];
+              unpack16<WT>(w[q][c], wf);
+#pragma unroll
+              for (int e = 0; e < EPL; ++e) acc[q] = fmaf(wf[e], hv[e], acc[q]);
+            }
           }
         }
+#pragma unroll
+        for (int q = 0; q < 3; ++q) acc[q] = wave_sum(acc[q]);
+      }
+      if (lane == 0) {
+        const float *gy = h.gtab + (size_t)ys[b] * 3 * ds;
+        const float gir = gy[i] + to_f32(bih[i]), giz = gy[ds + i] + to_f32(bih[ds + i]),
+                    gin = gy[2 * ds + i] + to_f32(bih[2 * ds + i]);
+        const float ghr = acc[0] + to_f32(bhh[i]), ghz = acc[1] + to_f32(bhh[ds + i]),
+                    ghn = acc[2] + to_f32(bhh[2 * ds + i]);
+        const float rg = sigm(gir + ghr), zg = sigm(giz + ghz);
+        const float ng = tanhf(gin + rg * ghn);
+        const float hold = j > 1 ? hprev[(size_t)b * ds + i] : 0.f;
+        const float hn = (1.f - zg) * ng + zg * hold;
+        hnext[(size_t)b * ds + i] = hn;
+        if (h.states) h.states[((size_t)b * depth + (j - 1)) * ds + i] = hn;
       }
     }
-    __syncthreads();
   }
 }
 
-int head_grid(const Dims &D, int n_cu, size_t *lds_bytes) {
-  const int G = n_cu;
-  Lds L = plan_lds(D, G, D.bf16);
-  *lds_bytes = L.total;
-  return G;
-}
-
-size_t head_exchange_floats(const Dims &D, int G, int beta) {
-  // hbuf [2][bs][ds] + ubuf [bs][r] + pval/pid [bs][G][beta]
-  return (size_t)2 * D.bs * D.ds + (size_t)D.bs * D.r + (size_t)2 * D.bs * G * beta;
-}
-
+// ---------------------------------------------------------------------------
+// u: one wave per (k) output, all batch rows
+// ---------------------------------------------------------------------------
 template <typename WT>
-static hipError_t launch_t(const HeadArgs &h, size_t lds_bytes, hipStream_t st) {
-  HeadKernelArgs<WT> ka;
-  ka.h = h;
-  ka.L = plan_lds(h.D, h.G, h.D.bf16);
-  if (ka.L.total != lds_bytes) return hipErrorInvalidValue;
-  hipError_t e = hipFuncSetAttribute((const void *)head_kernel<WT>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)lds_bytes);
-  if (e != hipSuccess) return e;
-  void *args[] = {&ka};
-  return hipLaunchCooperativeKernel((const void *)head_kernel<WT>, dim3(h.G), dim3(256), args,
-                                    (unsigned)lds_bytes, st);
+__global__ __launch_bounds__(256) void head_u_kernel(HeadArgs h, int j) {
+  constexpr int EPL = 16 / sizeof(WT);
+  const Dims &D = h.D;
+  const int bs = D.bs, d = D.d, ds = D.ds, r = D.r, depth = D.B - 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int k = blockIdx.x * 4 + wave;
+  if (k >= r) return;
+  const float *hn = h.hbuf + (size_t)(j & 1) * bs * ds;
+  const WT *wr = (const WT *)h.w1 + (size_t)k * (d + ds) + d;
+  const int nchunk = ds / EPL;
+  u32x4 w[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int ch = lane + 64 * c;
+    w[c] = ch < nchunk ? *(const u32x4 *)(wr + (size_t)ch * EPL) : u32x4{0u, 0u, 0u, 0u};
+  }
+  for (int b = 0; b < bs; ++b) {
+    const float *hb = hn + (size_t)b * ds;
+    float acc = 0.f;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int ch = lane + 64 * c;
+      if (ch < nchunk) {
+        float wf[EPL];
+        unpack16<WT>(w[c], wf);
+#pragma unroll
+        for (int e = 0; e < EPL; e += 4) {
+          const float4 t = *(const float4 *)(hb + (size_t)ch * EPL + e);
+          acc = fmaf(wf[e], t.x, acc);
+          acc = fmaf(wf[e + 1], t.y, acc);
+          acc = fmaf(wf[e + 2], t.z, acc);
+          acc = fmaf(wf[e + 3], t.w, acc);
+        }
+      }
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) {
+      const float x = h.P[((size_t)b * depth + (j - 1)) * r + k] + acc;
+      h.ubuf[(size_t)b * r + k] = x / (1.f + expf(-x));
+    }
+  }
 }
 
-hipError_t launch_head(const HeadArgs &h, size_t lds_bytes, hipStream_t st) {
-  if (h.D.bf16) return launch_t<bf16_t>(h, lds_bytes, st);
-  return launch_t<float>(h, lds_bytes, st);
+// ---------------------------------------------------------------------------
+// logits: matrix-core W2 tiles times the staged u (batch rows as the 16
+// columns of the B operand, hi/lo split for bf16), plus L_base, then each
+// workgroup's top-beta per batch row.  A workgroup covers ROWS vocabulary
+// rows (8 waves x kTPW tiles of 16).
+// ---------------------------------------------------------------------------
+constexpr int kLogitWaves = 8, kTPW = 2;
+constexpr int kLogitRows = kLogitWaves * kTPW * 16;
+
+template <typename WT, int KS, int MT>
+__global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs h, int j) {
+  constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP, XF = XStage<WT>::XF;
+  const Dims &D = h.D;
+  const int bs = D.bs, r = D.r, V = D.V, depth = D.B - 1, beta = h.beta;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, cc = lane & 15;
+  const int NT = (V + 15) / 16;
+  const int row0 = blockIdx.x * kLogitRows;
+  extern __shared__ __align__(16) unsigned char smem[];
+  u32x4 *us = (u32x4 *)smem;                                      // [KS][MT][64][XF]
+  float *lv = (float *)(smem + sizeof(u32x4) * KS * MT * 64 * XF);  // [bs][kLogitRows]
+
+  // W2 fragments of this wave's tiles, then the L_base values it will add
+  const u32x4 *w2p = (const u32x4 *)h.w2p;
+  u32x4 wf[kTPW][KS];
+  int tiles[kTPW];
+#pragma unroll
+  for (int q = 0; q < kTPW; ++q) {
+    tiles[q] = (blockIdx.x * kLogitWaves + wave) * kTPW + q;
+    const int t = tiles[q] < NT ? tiles[q] : NT - 1;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) wf[q][s] = w2p[((size_t)t * KS + s) * 64 + lane];
+  }
+  float lb[kTPW][MT][4];
+#pragma unroll
+  for (int q = 0; q < kTPW; ++q)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int bb = mt * 16 + cc;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int n = tiles[q] * 16 + 4 * g + e;
+        lb[q][mt][e] = (bb < bs && n < V) ? h.Lbase[((size_t)bb * depth + (j - 1)) * V + n] : 0.f;
+      }
+    }
+  // stage u as matrix-core B fragments
+  for (int it = tid; it < KS * MT * 64; it += kLogitWaves * 64) {
+    const int l = it & 63, mt = (it >> 6) % MT, s = (it >> 6) / MT;
+    const int bb = mt * 16 + (l & 15);
+    const int k0 = s * KSTEP + (l >> 4) * EPL;
+    float4 v[EPL / 4];
+#pragma unroll
+    for (int q = 0; q < EPL / 4; ++q)
+      v[q] = bb < bs ? *(const float4 *)(h.ubuf + (size_t)bb * r + k0 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+    XStage<WT>::put(us + (size_t)it * XF, v);
+  }
+  __syncthreads();
+
+  floatx4 acc[kTPW][MT];
+#pragma unroll
+  for (int q = 0; q < kTPW; ++q)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    u32x4 xf[MT * XF];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int f = 0; f < XF; ++f) xf[mt * XF + f] = us[((size_t)(s * MT + mt) * 64 + lane) * XF + f];
+#pragma unroll
+    for (int q = 0; q < kTPW; ++q) Mac2<WT, MT>::step(wf[q][s], xf, acc[q]);
+  }
+
+  // corrected logits of this workgroup's rows
+#pragma unroll
+  for (int q = 0; q < kTPW; ++q)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int bb = mt * 16 + cc;
+      if (bb >= bs) continue;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int n = tiles[q] * 16 + 4 * g + e;
+        const float val = lb[q][mt][e] + acc[q][mt][e];
+        lv[(size_t)bb * kLogitRows + (n - row0)] = n < V ? val : -INFINITY;
+        if (n < V && h.final_logits) h.final_logits[((size_t)bb * depth + (j - 1)) * V + n] = val;
+      }
+    }
+  __syncthreads();
+  const int nrows = min(kLogitRows, V - row0);
+  for (int bb = wave; bb < bs; bb += kLogitWaves) {
+    float ov[8];
+    int oi[8];
+    const float *lr = lv + (size_t)bb * kLogitRows;
+    wave_select([&](int c, float &v, int &id) { v = lr[c]; id = row0 + c; }, nrows, beta, ov, oi);
+    if (lane < beta) {
+      float v = ov[0];
+      int id = oi[0];
+#pragma unroll
+      for (int q = 1; q < 8; ++q)
+        if (lane == q) {
+          v = ov[q];
+          id = oi[q];
+        }
+      h.pval[((size_t)bb * h.GC + blockIdx.x) * beta + lane] = v;
+      h.pid[((size_t)bb * h.GC + blockIdx.x) * beta + lane] = id;
+    }
+  }
+}
+
+int head_logits_grid(const Dims &D) { return (D.V + kLogitRows - 1) / kLogitRows; }
+
+size_t head_exchange_floats(const Dims &D, int GC, int beta) {
+  // hbuf [2][bs][ds] + ubuf [bs][r] + pval/pid [bs][GC][beta]
+  return (size_t)2 * D.bs * D.ds + (size_t)D.bs * D.r + (size_t)2 * D.bs * GC * beta;
+}
+
+template <typename WT, int KS, int MT>
+static void launch_loop(const HeadArgs &h, hipStream_t st) {
+  const Dims &D = h.D;
+  const int depth = D.B - 1;
+  const int ga = min((D.ds + 3) / 4, 256);
+  const int gb = (D.r + 3) / 4;
+  constexpr int XF = XStage<WT>::XF;
+  const size_t lds = sizeof(u32x4) * KS * MT * 64 * XF + sizeof(float) * (size_t)D.bs * kLogitRows;
+  (void)hipFuncSetAttribute((const void *)head_logits_kernel<WT, KS, MT>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  for (int j = 1; j <= depth; ++j) {
+    hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(ga), dim3(256), 0, st, h, j, 0);
+    hipLaunchKernelGGL(head_u_kernel<WT>, dim3(gb), dim3(256), 0, st, h, j);
+    hipLaunchKernelGGL((head_logits_kernel<WT, KS, MT>), dim3(h.GC), dim3(kLogitWaves * 64), lds, st, h, j);
+  }
+  hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(1), dim3(256), 0, st, h, depth + 1, 1);
+}
+
+template <typename WT, int KS>
+static void launch_mt(const HeadArgs &h, hipStream_t st) {
+  if (h.D.bs <= 16) launch_loop<WT, KS, 1>(h, st);
+  else if (h.D.bs <= 32) launch_loop<WT, KS, 2>(h, st);
+  else launch_loop<WT, KS, 4>(h, st);
+}
+
+hipError_t launch_head(const HeadArgs &h, hipStream_t st) {
+  const bool bf = h.D.bf16;
+  const int KS = h.D.r / (bf ? 32 : 16);
+  if (bf) {
+    if (KS == 8) launch_mt<bf16_t, 8>(h, st);
+    else return hipErrorInvalidValue;
+  } else {
+    if (KS == 16) launch_mt<float, 16>(h, st);
+    else if (KS == 8) launch_mt<float, 8>(h, st);
+    else return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace dk

@@ -6,7 +6,7 @@
 
 namespace dk {
 
-enum { EPI_STORE = 0, EPI_ADD = 1, EPI_SWIGLU = 2 };
+enum { EPI_STORE = 0, EPI_SWIGLU = 2 };
 
 struct GemmArgs {
   const void *P;   // packed weights
@@ -16,19 +16,19 @@ struct GemmArgs {
   int N;           // valid output columns
   const float *X;  // activations fp32 [M][ldx]
   int ldx, M, K;
-  float *Y;        // output fp32 [M][ldy]
+  float *Y;        // output fp32 [M][ldy]; K-split ky writes Y + ky*ysplit
   int ldy;
-  int ksplit;      // workgroups sharing one tile group's K range
-  float *part;     // [ksplit][Mpad][ntiles*16] partial sums (ksplit > 1)
-  int *tickets;    // [mgroups][groups], zero before the first launch
+  size_t ysplit;
+  int ksplit;
 };
 
 struct GemmPlan {
-  int T, MT, groups, mgroups, ksplit;
-  size_t part_floats, tickets;
+  int MT, WPT, groups, mgroups, ksplit;
 };
 
-GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu);
+// max_split = 1: one workgroup covers all of K (direct output); otherwise K
+// may be split up to max_split ways into partial outputs.
+GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu, int max_split);
 void launch_gemm(bool bf16, int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st);
 void launch_pack(bool bf16, const void *W, int N, int K, int ldw, void *P, int NT, int KS,
                  int tile_mul, int tile_off, hipStream_t st);
@@ -43,14 +43,16 @@ struct Dims {
 
 void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor, float *X,
                         int32_t *err, hipStream_t st);
-// y[row] = rmsnorm(x[map(row)]) * gain; when skip_anchor, output row i reads
-// input row i + i/(B-1) + 1 (the draft rows of each block).
-void launch_rmsnorm(const Dims &D, const float *x, int ldx, const void *gain, float *y, int ldy,
-                    int rows, int width, bool skip_anchor, hipStream_t st);
-// q/k RMSNorm + RoPE on the QKV projection; writes Q [M][nq][dh], Kb/Vb [M][nkv][dh]
-void launch_qk_norm_rope(const Dims &D, const float *qkv, const void *q_norm, const void *k_norm,
-                         const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb, float *Vb,
-                         hipStream_t st);
+// x[map(row)] += sum of np partials (pstride floats apart), then
+// y[row] = rmsnorm(x[map(row)]) * gain; with skip_anchor, output row i reads
+// input row i + i/(B-1) + 1 (the draft rows of each block) and x is left as is.
+void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
+                     const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor, hipStream_t st);
+// q/k RMSNorm + RoPE on the QKV projection (sum of np partials); writes
+// Q [M][nq][dh], Kb/Vb [M][nkv][dh]
+void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,
+                         const void *k_norm, const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb,
+                         float *Vb, hipStream_t st);
 // context K/V from projected hidden rows: kv [bs*n_new][2*nkv*dh] fp32 -> cache
 void launch_ctx_store(const Dims &D, const float *kv, int n_new, const void *k_norm,
                       const int32_t *ctx_lens, int max_ctx, void *ck, void *cv, int32_t *err,
@@ -61,16 +63,16 @@ void launch_attention(const Dims &D, const float *Q, const float *Kb, const floa
                       const void *ck, const void *cv, const int32_t *ctx_lens, int max_ctx,
                       float *part, float *O, int32_t *err, hipStream_t st);
 size_t attn_part_floats(const Dims &D, int max_ctx);
+bool attn_supported(int nq, int nkv, int B);
 
 // ---- Domino head rollout (head.hip)
 struct HeadArgs {
   Dims D;
   int beta;
-  const void *embed;     // [V][d]
-  const void *w_ih;      // [3ds][d]
+  const float *gtab;     // [V][3ds] = E W_ih^T (built at model creation)
   const void *w_hh;      // [3ds][ds]
   const void *b_ih, *b_hh;
-  const void *w1s_rows;  // W1 (full [r][d+ds]); the S half starts at column d
+  const void *w1;        // [r][d+ds]; the S half starts at column d
   const void *w2p;       // W2 packed (tile-major, KS = r / KSTEP)
   const float *P;        // [bs][B-1][r]: W1[:, :d] H_j
   const float *Lbase;    // [bs][B-1][V]
@@ -80,19 +82,16 @@ struct HeadArgs {
   float *topk_vals;
   float *final_logits;   // optional [bs][B-1][V]
   float *states;         // optional [bs][B-1][ds]
-  // exchange buffers (workspace)
   float *hbuf;           // [2][bs][ds]
   float *ubuf;           // [bs][r]
-  float *pval;           // [bs][G][beta]
-  int32_t *pid;          // [bs][G][beta]
-  int32_t *ybuf;         // [bs]
-  unsigned *barrier;     // zeroed before launch
+  float *pval;           // [bs][GC][beta]
+  int32_t *pid;          // [bs][GC][beta]
   int32_t *err;
-  int G;                 // workgroups (co-resident)
+  int GC;                // workgroups of the logits kernel
 };
-int head_grid(const Dims &D, int n_cu, size_t *lds_bytes);
-hipError_t launch_head(const HeadArgs &h, size_t lds_bytes, hipStream_t st);
-size_t head_exchange_floats(const Dims &D, int G, int beta);
+int head_logits_grid(const Dims &D);
+size_t head_exchange_floats(const Dims &D, int GC, int beta);
+hipError_t launch_head(const HeadArgs &h, hipStream_t st);
 
 // ---- tree and acceptance (tree.hip)
 void launch_build_tree(int bs, int depth, int beta, const int32_t *topk, const int32_t *anchor,
@@ -104,6 +103,7 @@ void launch_accept(int bs, int nn, int V, int B, const int32_t *tok, const int32
                    int32_t *out_tok, void *ws, hipStream_t st);
 
 // misc
+void launch_to_f32(const void *src, bool bf16, float *dst, size_t n, hipStream_t st);
 void launch_fill_u32(uint32_t *p, size_t n, uint32_t v, hipStream_t st);
 
 }  // namespace dk

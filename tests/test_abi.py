@@ -44,6 +44,8 @@ def _cfg(**kw):
     ({"n_kv_heads": 3}, bd.DOMINO_ERR_UNSUPPORTED),
     ({"hidden": 250}, bd.DOMINO_ERR_UNSUPPORTED),
     ({"rank": 1000}, bd.DOMINO_ERR_UNSUPPORTED),
+    ({"rank": 64}, bd.DOMINO_ERR_UNSUPPORTED),
+    ({"gru_hidden": 2048}, bd.DOMINO_ERR_UNSUPPORTED),
     ({}, bd.DOMINO_ERR_INVALID_ARG),  # valid config, NULL weights
 ])
 def test_model_create_validation(kw, status):
