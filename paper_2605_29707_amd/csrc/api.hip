@@ -57,7 +57,7 @@ struct domino_model {
   void *mem = nullptr;
   size_t mem_bytes = 0;
   std::vector<Packed> qkv, wo, gateup, down;
-  Packed lm, w1h, w2;
+  Packed lm, w2;
   size_t gtab_off, w_hh_off, w1_off;
   // profiling
   uint32_t prof_mask = 0;
@@ -104,6 +104,7 @@ domino_status check_config(const domino_config *c) {
     return fail(DOMINO_ERR_UNSUPPORTED, "hidden, ffn, gru_hidden and n_q_heads*head_dim must be multiples of 32");
   if (c->rank % ks || c->rank > 16 * ks)
     return fail(DOMINO_ERR_UNSUPPORTED, "rank must be a multiple of %d and at most %d", ks, 16 * ks);
+  if (c->hidden > 8192) return fail(DOMINO_ERR_UNSUPPORTED, "hidden must be at most 8192");
   if (!attn_supported(c->n_q_heads, c->n_kv_heads, c->block))
     return fail(DOMINO_ERR_UNSUPPORTED, "(n_q_heads/n_kv_heads)*block must be 32, 64 or 128");
   const int epl = c->dtype == DOMINO_BF16 ? 8 : 4;
@@ -121,12 +122,13 @@ Dims make_dims(const domino_model *m, int bs) {
 
 // ---- workspace layout of the draft step
 struct WsLayout {
-  size_t err, X, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, Lb, P, hbuf, ubuf, pval, pid, ctxkv, total;
-  int GC;
+  size_t err, best, hdr_words, X, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ubuf, pval, pid, ctxkv,
+      total;
+  int GC, ldl;
 };
 
 struct Plans {
-  GemmPlan qkv, wo, gateup, down, lm, w1h, ctx;
+  GemmPlan qkv, wo, gateup, down, lm, ctx;
 };
 
 constexpr int kMaxSplit = 16;
@@ -141,7 +143,6 @@ Plans make_plans(const domino_model *m, int bs, int max_new) {
   p.gateup = plan_gemm(m->gateup[0].NT, m->gateup[0].KS, M, EPI_SWIGLU, m->n_cu, 1);
   p.down = plan_gemm(m->down[0].NT, m->down[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
   p.lm = plan_gemm(m->lm.NT, m->lm.KS, Mh, EPI_STORE, m->n_cu, 1);
-  p.w1h = plan_gemm(m->w1h.NT, m->w1h.KS, Mh, EPI_STORE, m->n_cu, 1);
   const int kvt = 2 * D.nkv * D.dh / 16;
   p.ctx = plan_gemm(kvt, m->qkv[0].KS, bs * (max_new > 0 ? max_new : 1), EPI_STORE, m->n_cu, 1);
   return p;
@@ -159,6 +160,8 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
     return at;
   };
   w.err = take(256);
+  w.best = take((size_t)(D.B - 1) * bs * head_best_slots() * 8);
+  w.hdr_words = o / 4;  // error word and best keys: cleared at every step
   const int qkvw = (D.nq + 2 * D.nkv) * D.dh;
   w.X = take((size_t)M * D.d * 4);
   w.A = take((size_t)M * D.d * 4);
@@ -172,12 +175,12 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.F = take((size_t)M * D.ffn * 4);
   w.DNp = take((size_t)p.down.ksplit * M * D.d * 4);
   w.H = take((size_t)Mh * D.d * 4);
-  w.Lb = take((size_t)Mh * D.V * 4);
-  w.P = take((size_t)Mh * D.r * 4);
+  w.ldl = m->lm.NT * 16;
+  w.LP = take((size_t)Mh * w.ldl * 4);  // [L_base | pad | P] per draft row
   w.hbuf = take((size_t)2 * bs * D.ds * 4);
   w.ubuf = take((size_t)bs * D.r * 4);
-  w.pval = take((size_t)bs * w.GC * beta * 4);
-  w.pid = take((size_t)bs * w.GC * beta * 4);
+  w.pval = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
+  w.pid = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
   w.ctxkv = take((size_t)bs * (max_new > 0 ? max_new : 0) * 2 * D.nkv * D.dh * 4);
   w.total = o;
   return true;
@@ -325,8 +328,8 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
     m->gateup.push_back(gu);
     m->down.push_back(add(D.d, D.ffn));
   }
-  m->lm = add(D.V, D.d);
-  m->w1h = add(D.r, D.d);
+  // LM head and W1's H half share the input H: one packed matrix, W1 tiles after the vocabulary tiles
+  m->lm = add(((D.V + 15) / 16) * 16 + D.r, D.d);
   m->w2 = add(D.V, D.r);
   m->gtab_off = off;
   off = align_up(off + (size_t)D.V * 3 * D.ds * 4);
@@ -361,8 +364,10 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
     const Packed &dn = m->down[l];
     launch_pack(bf, w->w_down[l], D.d, D.ffn, D.ffn, base + dn.off, dn.NT, dn.KS, 1, 0, st);
   }
-  launch_pack(bf, w->lm_head, D.V, D.d, D.d, base + m->lm.off, m->lm.NT, m->lm.KS, 1, 0, st);
-  launch_pack(bf, w->w1, D.r, D.d, D.d + D.ds, base + m->w1h.off, m->w1h.NT, m->w1h.KS, 1, 0, st);
+  const int vt = (D.V + 15) / 16;
+  launch_pack(bf, w->lm_head, D.V, D.d, D.d, base + m->lm.off, vt, m->lm.KS, 1, 0, st);
+  launch_pack(bf, w->w1, D.r, D.d, D.d + D.ds, base + m->lm.off + (size_t)vt * m->lm.KS * 1024, D.r / 16, m->lm.KS,
+              1, 0, st);
   launch_pack(bf, w->w2, D.V, D.r, D.r, base + m->w2.off, m->w2.NT, m->w2.KS, 1, 0, st);
   he = hipGetLastError();
   if (he == hipSuccess) he = build_gtab(m, w->gru_w_ih);
@@ -425,8 +430,8 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
   const int qd = D.nq * D.dh, kvd = D.nkv * D.dh, qkvw = qd + 2 * kvd;
   const size_t layer_elems = (size_t)batch * max_ctx * kvd;
 
-  // clear the error word
-  launch_fill_u32((uint32_t *)ws, 1, 0u, st);
+  // clear the error word and the rollout's best keys
+  launch_fill_u32((uint32_t *)ws, w.hdr_words, 0u, st);
 
   // context rows projected from target hidden states (optional)
   if (n_new > 0) {
@@ -441,18 +446,15 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
     }
   }
 
-  prof_begin(m, DOMINO_KC_EMBED, st);
-  launch_embed_block(D, m->embed, anchor_ids, F(w.X), err, st);
-  prof_end(m, DOMINO_KC_EMBED, st);
-
   const size_t rstride = (size_t)M * D.d;  // partial-output stride of the residual projections
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const char *ck = (const char *)ctx_k + l * layer_elems * m->esz;
     const char *cv = (const char *)ctx_v + l * layer_elems * m->esz;
     // residual += previous layer's down projection, then the attention RMSNorm
     prof_begin(m, DOMINO_KC_NORM, st);
+    // (layer 0: the residual starts as the embedding of [anchor, MASK, ...])
     launch_add_norm(D, F(w.X), D.d, F(w.DNp), l > 0 ? p.down.ksplit : 0, rstride, m->attn_norm[l], F(w.A), D.d,
-                    M, D.d, false, st);
+                    M, D.d, false, l == 0 ? m->embed : nullptr, anchor_ids, err, st);
     prof_end(m, DOMINO_KC_NORM, st);
 
     prof_begin(m, DOMINO_KC_QKV, st);
@@ -478,7 +480,7 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
     // residual += attention output, then the FFN RMSNorm
     prof_begin(m, DOMINO_KC_NORM, st);
     launch_add_norm(D, F(w.X), D.d, F(w.WOp), p.wo.ksplit, rstride, m->ffn_norm[l], F(w.A), D.d, M, D.d, false,
-                    st);
+                    nullptr, nullptr, err, st);
     prof_end(m, DOMINO_KC_NORM, st);
 
     prof_begin(m, DOMINO_KC_GATEUP, st);
@@ -497,19 +499,21 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
   // residual += last down projection; final RMSNorm of the draft rows -> H
   float *H = (debug && debug->hidden) ? debug->hidden : F(w.H);
   prof_begin(m, DOMINO_KC_NORM, st);
-  launch_add_norm(D, F(w.X), D.d, F(w.DNp), p.down.ksplit, rstride, m->final_norm, H, D.d, Mh, D.d, true, st);
+  launch_add_norm(D, F(w.X), D.d, F(w.DNp), p.down.ksplit, rstride, m->final_norm, H, D.d, Mh, D.d, true,
+                  nullptr, nullptr, err, st);
   prof_end(m, DOMINO_KC_NORM, st);
 
-  float *Lb = (debug && debug->base_logits) ? debug->base_logits : F(w.Lb);
+  // LM head and W1's H half in one pass over H: columns [0, V) are L_base, [ldl - r, ldl) are P
+  float *LP = F(w.LP);
   prof_begin(m, DOMINO_KC_LMHEAD, st);
-  GemmArgs a = gemm_args(base + m->lm.off, m->lm, 0, m->lm.NT, D.V, H, D.d, Mh, D.d, Lb, D.V, p.lm);
+  GemmArgs a = gemm_args(base + m->lm.off, m->lm, 0, m->lm.NT, w.ldl, H, D.d, Mh, D.d, LP, w.ldl, p.lm);
   launch_gemm(m->bf16, EPI_STORE, a, p.lm, st);
   prof_end(m, DOMINO_KC_LMHEAD, st);
-
-  prof_begin(m, DOMINO_KC_W1H, st);
-  a = gemm_args(base + m->w1h.off, m->w1h, 0, m->w1h.NT, D.r, H, D.d, Mh, D.d, F(w.P), D.r, p.w1h);
-  launch_gemm(m->bf16, EPI_STORE, a, p.w1h, st);
-  prof_end(m, DOMINO_KC_W1H, st);
+  if (debug && debug->base_logits) {
+    hipError_t ce = hipMemcpy2DAsync(debug->base_logits, (size_t)D.V * 4, LP, (size_t)w.ldl * 4, (size_t)D.V * 4, Mh,
+                                     hipMemcpyDeviceToDevice, st);
+    if (ce != hipSuccess) return fail(DOMINO_ERR_HIP, "copying base logits: %s", hipGetErrorString(ce));
+  }
 
   HeadArgs h;
   h.D = D;
@@ -520,8 +524,11 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
   h.b_hh = m->b_hh;
   h.w1 = base + m->w1_off;
   h.w2p = base + m->w2.off;
-  h.P = F(w.P);
-  h.Lbase = Lb;
+  h.P = LP + (w.ldl - D.r);
+  h.ldp = w.ldl;
+  h.Lbase = LP;
+  h.ldl = w.ldl;
+  h.best = (unsigned long long *)(ws + w.best);
   h.anchor = anchor_ids;
   h.forced = forced_tokens;
   h.topk_ids = topk_ids;

@@ -28,40 +28,72 @@ __global__ __launch_bounds__(256) void embed_block_kernel(const WT *__restrict__
   for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = to_f32(src[c]);
 }
 
-// x[in_row] += sum of the `np` partial outputs (split order), then
+// x[in_row] += sum of the `np` (<= 16) partial outputs (split order), then
 // y[i] = RMSNorm(x[in_row]) * gain.  With skip_anchor, output row i reads
 // input row i + i/(B-1) + 1 (the draft rows of each block) and x is not
-// written back.  One workgroup per output row; each thread owns 8 columns at a
-// time so all its loads are issued together.
+// written back.  With `tok` given, the row is first replaced by the embedding
+// row of its token (the anchor for block position 0, MASK otherwise).  One
+// workgroup per output row; a thread keeps its 16 columns in registers and
+// issues all of its loads together.
 template <typename WT>
 __global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, int ldx,
                                                        const float *__restrict__ parts, int np,
                                                        size_t pstride, const WT *__restrict__ gain,
                                                        float *__restrict__ y, int ldy, int width, float eps,
-                                                       int skip_anchor, int depth) {
+                                                       int skip_anchor, int depth, const WT *__restrict__ embed,
+                                                       const int32_t *__restrict__ anchor, int mask_id, int V,
+                                                       int32_t *err) {
   const int i = blockIdx.x;
   const int in_row = skip_anchor ? i + i / depth + 1 : i;
   float *xr = x + (size_t)in_row * ldx;
   const float *pr = parts + (size_t)in_row * ldx;
-  constexpr int PER = 8;
+  constexpr int PER = 8, IT = 2;
+  const WT *er = nullptr;
+  if (embed) {
+    const int B = depth + 1;
+    int tok = mask_id;
+    if (in_row % B == 0) {
+      tok = anchor[in_row / B];
+      if (tok < 0 || tok >= V) {
+        if (threadIdx.x == 0) raise_error(err, DEV_BAD_TOKEN);
+        tok = tok < 0 ? 0 : V - 1;
+      }
+    }
+    er = embed + (size_t)tok * width;
+  }
+  float v[IT][PER];
   float ss = 0.f;
-  for (int c0 = threadIdx.x * PER; c0 < width; c0 += blockDim.x * PER) {
-    float4 v0 = *(const float4 *)(xr + c0), v1 = *(const float4 *)(xr + c0 + 4);
-    for (int p = 0; p < np; ++p) {
-      const float4 a0 = *(const float4 *)(pr + p * pstride + c0), a1 = *(const float4 *)(pr + p * pstride + c0 + 4);
-      v0.x += a0.x; v0.y += a0.y; v0.z += a0.z; v0.w += a0.w;
-      v1.x += a1.x; v1.y += a1.y; v1.z += a1.z; v1.w += a1.w;
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int c0 = (threadIdx.x + it * blockDim.x) * PER;
+    if (c0 >= width) continue;
+    if (er) {
+#pragma unroll
+      for (int e = 0; e < PER; ++e) v[it][e] = to_f32(er[c0 + e]);
+    } else {
+      const float4 a = *(const float4 *)(xr + c0), c = *(const float4 *)(xr + c0 + 4);
+      v[it][0] = a.x; v[it][1] = a.y; v[it][2] = a.z; v[it][3] = a.w;
+      v[it][4] = c.x; v[it][5] = c.y; v[it][6] = c.z; v[it][7] = c.w;
     }
-    if (np > 0 && !skip_anchor) {
-      *(float4 *)(xr + c0) = v0;
-      *(float4 *)(xr + c0 + 4) = v1;
+    float4 pa[16], pc[16];
+#pragma unroll
+    for (int p = 0; p < 16; ++p)
+      if (p < np) {
+        pa[p] = *(const float4 *)(pr + p * pstride + c0);
+        pc[p] = *(const float4 *)(pr + p * pstride + c0 + 4);
+      }
+#pragma unroll
+    for (int p = 0; p < 16; ++p)
+      if (p < np) {
+        v[it][0] += pa[p].x; v[it][1] += pa[p].y; v[it][2] += pa[p].z; v[it][3] += pa[p].w;
+        v[it][4] += pc[p].x; v[it][5] += pc[p].y; v[it][6] += pc[p].z; v[it][7] += pc[p].w;
+      }
+    if ((np > 0 || er) && !skip_anchor) {
+      *(float4 *)(xr + c0) = make_float4(v[it][0], v[it][1], v[it][2], v[it][3]);
+      *(float4 *)(xr + c0 + 4) = make_float4(v[it][4], v[it][5], v[it][6], v[it][7]);
     }
-    ss = fmaf(v0.x, v0.x, ss); ss = fmaf(v0.y, v0.y, ss); ss = fmaf(v0.z, v0.z, ss); ss = fmaf(v0.w, v0.w, ss);
-    ss = fmaf(v1.x, v1.x, ss); ss = fmaf(v1.y, v1.y, ss); ss = fmaf(v1.z, v1.z, ss); ss = fmaf(v1.w, v1.w, ss);
-    float *yr = y + (size_t)i * ldy + c0;
-    // stash the summed values in y; scaled below once the norm is known
-    *(float4 *)(yr) = v0;
-    *(float4 *)(yr + 4) = v1;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) ss = fmaf(v[it][e], v[it][e], ss);
   }
   ss = wave_sum(ss);
   __shared__ float red[8];
@@ -70,10 +102,16 @@ __global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, in
   float tot = 0.f;
   for (int w = 0; w < (int)(blockDim.x >> 6); ++w) tot += red[w];
   const float inv = 1.0f / sqrtf(tot / (float)width + eps);
-  for (int c0 = threadIdx.x * PER; c0 < width; c0 += blockDim.x * PER) {
-    float *yr = y + (size_t)i * ldy + c0;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) yr[e] = yr[e] * inv * to_f32(gain[c0 + e]);
+  for (int it = 0; it < IT; ++it) {
+    const int c0 = (threadIdx.x + it * blockDim.x) * PER;
+    if (c0 >= width) continue;
+    float o[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) o[e] = v[it][e] * inv * to_f32(gain[c0 + e]);
+    float *yr = y + (size_t)i * ldy + c0;
+    *(float4 *)(yr) = make_float4(o[0], o[1], o[2], o[3]);
+    *(float4 *)(yr + 4) = make_float4(o[4], o[5], o[6], o[7]);
   }
 }
 
@@ -129,8 +167,18 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
   const float *src = qkv + (size_t)m * nh * dh + (size_t)hh * dh;
   float v[2] = {0.f, 0.f};
   const int per = dh / 64;
-  for (int p = 0; p < np; ++p)  // K-split partial outputs, added in split order
-    for (int q = 0; q < per; ++q) v[q] += src[p * pstride + lane + 64 * q];
+  {
+    // K-split partial outputs, added in split order; all loads issued together
+    float t[16][2];
+#pragma unroll
+    for (int p = 0; p < 16; ++p)
+      if (p < np)
+        for (int q = 0; q < per; ++q) t[p][q] = src[p * pstride + lane + 64 * q];
+#pragma unroll
+    for (int p = 0; p < 16; ++p)
+      if (p < np)
+        for (int q = 0; q < per; ++q) v[q] += t[p][q];
+  }
   float *dst;
   if (hh < nq) {
     norm_rope_head<WT>(v, dh, qn, eps, pos, theta, true, lane);
@@ -190,6 +238,13 @@ __global__ __launch_bounds__(256) void ctx_store_kernel(const float *__restrict_
 // ---------------------------------------------------------------------------
 constexpr int kAttnThreads = 256;
 
+DEVI float4 ld4_f32(const float *p) { return *(const float4 *)p; }
+DEVI float4 ld4_f32(const bf16_t *p) {
+  const uint2 u = *(const uint2 *)p;
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                     __uint_as_float(u.y & 0xffff0000u));
+}
+
 static int attn_ch(int G) { return G <= 4 ? 64 : 32; }
 int attn_chunk_len() { return 64; }
 int attn_nchunks(int max_ctx, int B) { return (max_ctx + B + 31) / 32; }  // upper bound for any G
@@ -225,32 +280,43 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   const int tid = threadIdx.x;
 
   // ---- stage Q rows (R x DH), K and V chunk (CH x DH) as fp32
+#pragma unroll
   for (int e = tid; e < R * DH / 4; e += kAttnThreads) {
     const int qi = e / (DH / 4), d4 = e % (DH / 4);
     const int qh = kvh * G + qi / B, j = qi % B;
     *(float4 *)(Qs + qi * DP + 4 * d4) = *(const float4 *)(Q + (((size_t)b * B + j) * nq + qh) * DH + 4 * d4);
   }
-  for (int e = tid; e < CH * DH / 4; e += kAttnThreads) {
-    const int t = e / (DH / 4), d4 = e % (DH / 4);
-    float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
-    if (t < nk) {
-      const int kk = c0 + t;
+  {
+    constexpr int NE = CH * DH / 4 / kAttnThreads;  // float4 groups per thread
+    float4 kv[NE], vv[NE];
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      const int e = tid + q * kAttnThreads;
+      const int t = e / (DH / 4), d4 = e % (DH / 4);
+      const int kk = min(c0 + t, total - 1);
       if (kk < n) {
         const size_t off = ((((size_t)b * max_ctx + kk) * nkv) + kvh) * DH + 4 * d4;
-        kv = make_float4(to_f32(ck[off]), to_f32(ck[off + 1]), to_f32(ck[off + 2]), to_f32(ck[off + 3]));
-        vv = make_float4(to_f32(cv[off]), to_f32(cv[off + 1]), to_f32(cv[off + 2]), to_f32(cv[off + 3]));
+        kv[q] = ld4_f32(ck + off);
+        vv[q] = ld4_f32(cv + off);
       } else {
         const size_t off = ((((size_t)b * B + (kk - n)) * nkv) + kvh) * DH + 4 * d4;
-        kv = *(const float4 *)(Kb + off);
-        vv = *(const float4 *)(Vb + off);
+        kv[q] = *(const float4 *)(Kb + off);
+        vv[q] = *(const float4 *)(Vb + off);
       }
     }
-    *(float4 *)(Ks + t * DP + 4 * d4) = kv;
-    *(float4 *)(Vs + t * DP + 4 * d4) = vv;
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      const int e = tid + q * kAttnThreads;
+      const int t = e / (DH / 4), d4 = e % (DH / 4);
+      const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+      *(float4 *)(Ks + t * DP + 4 * d4) = t < nk ? kv[q] : z;
+      *(float4 *)(Vs + t * DP + 4 * d4) = t < nk ? vv[q] : z;
+    }
   }
   __syncthreads();
 
-  // ---- scores: thread (qb, kb) owns rows qb*RPT.. and keys kb*KPT..
+  // ---- scores: thread (qb, kb) owns rows qb*RPT.. and keys kb, kb+16, ...
+  // (consecutive threads read consecutive K rows: conflict-free LDS banks)
   const int qb = tid / 16, kb = tid % 16;
   float s[RPT][KPT];
 #pragma unroll
@@ -260,7 +326,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   for (int d = 0; d < DH; d += 4) {
     float4 kr[KPT];
 #pragma unroll
-    for (int k = 0; k < KPT; ++k) kr[k] = *(const float4 *)(Ks + (kb * KPT + k) * DP + d);
+    for (int k = 0; k < KPT; ++k) kr[k] = *(const float4 *)(Ks + (kb + 16 * k) * DP + d);
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
       const float4 q = *(const float4 *)(Qs + (qb * RPT + i) * DP + d);
@@ -279,7 +345,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     float m = -INFINITY;
 #pragma unroll
     for (int k = 0; k < KPT; ++k) {
-      s[i][k] = (kb * KPT + k < nk) ? s[i][k] * scale : -INFINITY;
+      s[i][k] = (kb + 16 * k < nk) ? s[i][k] * scale : -INFINITY;
       m = fmaxf(m, s[i][k]);
     }
 #pragma unroll
@@ -287,8 +353,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     float l = 0.f;
 #pragma unroll
     for (int k = 0; k < KPT; ++k) {
-      const float p = (kb * KPT + k < nk) ? expf(s[i][k] - m) : 0.f;
-      Ps[(qb * RPT + i) * CP + kb * KPT + k] = p;
+      const float p = (kb + 16 * k < nk) ? expf(s[i][k] - m) : 0.f;
+      Ps[(qb * RPT + i) * CP + kb + 16 * k] = p;
       l += p;
     }
 #pragma unroll
@@ -410,14 +476,17 @@ void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor,
 }
 
 void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
-                     const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor, hipStream_t st) {
+                     const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
+                     const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st) {
   if (rows <= 0) return;
   if (D.bf16)
     hipLaunchKernelGGL(add_norm_kernel<bf16_t>, dim3(rows), dim3(512), 0, st, x, ldx, parts, np, pstride,
-                       (const bf16_t *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1);
+                       (const bf16_t *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1,
+                       (const bf16_t *)embed, anchor, D.mask_id, D.V, err);
   else
     hipLaunchKernelGGL(add_norm_kernel<float>, dim3(rows), dim3(512), 0, st, x, ldx, parts, np, pstride,
-                       (const float *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1);
+                       (const float *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1, (const float *)embed,
+                       anchor, D.mask_id, D.V, err);
 }
 
 void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,

@@ -8,13 +8,16 @@
 //          the gates, E[y] W_ih^T, is a row of the table G = E W_ih^T built at
 //          model creation, so a step gathers 3*d_s values instead of streaming
 //          W_ih.
-//   u      u = SiLU(W1[:, :d] H_j + W1[:, d:] S_{j-1}), the H half precomputed
-//          for all j by a GEMM before the loop.
-//   logits L_j = L_base_j + W2 u over a vocabulary slice per workgroup, and the
-//          slice's top-beta under (value desc, id asc).
+//   u      u = SiLU(W1[:, :d] H_j + W1[:, d:] S_{j-1}) (the H half comes from
+//          the LM-head GEMM).
+//   logits L_j = L_base_j + W2 u over a vocabulary slice per workgroup, the
+//          slice's top-beta under (value desc, id asc), and an atomic max of
+//          its top-1 into the position's key.
 // A kernel boundary is the cheapest grid-wide handshake on this device (about
 // 1.6 us against about 4 us for a 256-workgroup spin barrier), so the
-// rollout is 3(B-1)+1 launches rather than one persistent kernel.
+// rollout is 3(B-1)+1 launches rather than one persistent kernel; the top-1
+// of each position is a 64-bit atomic max, so no launch merges lists inside
+// the loop (the full top-beta lists are merged once at the end).
 #include "common.h"
 #include "kernels.h"
 #include "mfma.h"
@@ -119,6 +122,21 @@ DEVI void wave_select_mem(const float *__restrict__ pv, const int32_t *__restric
 
 DEVI float sigm(float x) { return 1.f / (1.f + expf(-x)); }
 
+constexpr int kBestSlots = 8;  // atomic targets per (position, row), spread to cut contention
+
+// 64-bit key whose unsigned order is the selection order: the float mapped
+// to an order-preserving unsigned value (NaN as -inf) in the high half, the
+// complement of the id in the low half (smaller id wins a tie).
+DEVI unsigned long long encode_best(float v, int id) {
+  uint32_t u = __float_as_uint(order_val(v));
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((unsigned long long)u << 32) | (unsigned long long)(0xffffffffu - (uint32_t)id);
+}
+DEVI int decode_best_id(unsigned long long key, int V) {
+  const int id = (int)(0xffffffffu - (uint32_t)(key & 0xffffffffu));
+  return id < 0 ? 0 : (id >= V ? V - 1 : id);  // an unset key never reaches here
+}
+
 template <typename WT>
 DEVI void unpack16(const u32x4 &w, float *f);
 template <>
@@ -136,55 +154,41 @@ DEVI void unpack16<float>(const u32x4 &w, float *f) {
 }
 
 // ---------------------------------------------------------------------------
-// gru: merge position j-1's lists (j >= 2), choose y_{j-1}, advance the state
-// slice.  With j == B (merge_only) it only writes the last position's top-beta.
+// gru: choose y_{j-1} and advance this workgroup's slice of the state.
 // ---------------------------------------------------------------------------
 template <typename WT>
-__global__ __launch_bounds__(256) void head_gru_kernel(HeadArgs h, int j, int merge_only) {
+__global__ __launch_bounds__(256) void head_gru_kernel(HeadArgs h, int j) {
   constexpr int EPL = 16 / sizeof(WT);
   const Dims &D = h.D;
   const int bs = D.bs, ds = D.ds, depth = D.B - 1, beta = h.beta, V = D.V;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __shared__ int ys[64];
 
-  // ---- y_{j-1}
-  for (int b = wave; b < bs; b += 4) {
+  // ---- y_{j-1}: the anchor, a forced token, or the decoded best key of position j-1
+  for (int b = threadIdx.x; b < bs; b += blockDim.x) {
     int y;
-    if (j == 1) {
-      y = clamp_token(h.anchor[b], V, h.err);
-    } else {
-      float ov[8];
-      int oi[8];
-      const float *pv = h.pval + (size_t)b * h.GC * beta;
-      const int32_t *pi = h.pid + (size_t)b * h.GC * beta;
-      wave_select_mem(pv, pi, h.GC * beta, beta, ov, oi);
-      y = oi[0] < 0 ? 0 : (oi[0] >= V ? V - 1 : oi[0]);  // always a valid row of G
-      if (blockIdx.x == 0 && lane < beta) {
-        float v = ov[0];
-        int id = oi[0];
+    if (j == 1) y = clamp_token(h.anchor[b], V, h.err);
+    else if (h.forced) y = clamp_token(h.forced[(size_t)b * depth + (j - 2)], V, h.err);
+    else {
+      const unsigned long long *bk = h.best + ((size_t)(j - 2) * bs + b) * kBestSlots;
+      unsigned long long key = bk[0];
 #pragma unroll
-        for (int q = 1; q < 8; ++q)
-          if (lane == q) {
-            v = ov[q];
-            id = oi[q];
-          }
-        h.topk_ids[((size_t)b * depth + (j - 2)) * beta + lane] = id;
-        h.topk_vals[((size_t)b * depth + (j - 2)) * beta + lane] = v;
-      }
-      if (h.forced) y = clamp_token(h.forced[(size_t)b * depth + (j - 2)], V, h.err);
+      for (int q = 1; q < kBestSlots; ++q) key = bk[q] > key ? bk[q] : key;
+      y = decode_best_id(key, V);
     }
-    if (lane == 0) ys[b] = y;
+    ys[b] = y;
   }
-  if (merge_only) return;
   __syncthreads();
 
-  // ---- state slice: one wave per state index; lanes stride over d_s
+  // ---- state slice: one wave per state index (4 per round); lanes stride over d_s
   const float *hprev = h.hbuf + (size_t)((j - 1) & 1) * bs * ds;
   float *hnext = h.hbuf + (size_t)(j & 1) * bs * ds;
   const WT *whh = (const WT *)h.w_hh;
   const WT *bih = (const WT *)h.b_ih, *bhh = (const WT *)h.b_hh;
   const int nchunk = ds / EPL;  // EPL-element chunks per row
-  for (int i = blockIdx.x * 4 + wave; i < ds; i += gridDim.x * 4) {
+  for (int i0 = blockIdx.x * 4; i0 < ds; i0 += gridDim.x * 4) {
+    const int i = i0 + wave;
+    const bool live = i < ds;
     // W_hh rows (r, z, n) of index i stay in registers across the batch loop
     u32x4 w[3][4];
 #pragma unroll
@@ -192,12 +196,13 @@ __global__ __launch_bounds__(256) void head_gru_kernel(HeadArgs h, int j, int me
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const int ch = lane + 64 * c;
-        w[q][c] = (ch < nchunk && j > 1) ? *(const u32x4 *)(whh + ((size_t)(q * ds + i)) * ds + (size_t)ch * EPL)
-                                         : u32x4{0u, 0u, 0u, 0u};
+        w[q][c] = (live && ch < nchunk && j > 1)
+                      ? *(const u32x4 *)(whh + ((size_t)(q * ds + i)) * ds + (size_t)ch * EPL)
+                      : u32x4{0u, 0u, 0u, 0u};
       }
     for (int b = 0; b < bs; ++b) {
       float acc[3] = {0.f, 0.f, 0.f};
-      if (j > 1) {
+      if (j > 1 && live) {
         const float *hp = hprev + (size_t)b * ds;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
@@ -225,17 +230,20 @@ __global__ __launch_bounds__(256) void head_gru_kernel(HeadArgs h, int j, int me
         for (int q = 0; q < 3; ++q) acc[q] = wave_sum(acc[q]);
       }
       if (lane == 0) {
-        const float *gy = h.gtab + (size_t)ys[b] * 3 * ds;
-        const float gir = gy[i] + to_f32(bih[i]), giz = gy[ds + i] + to_f32(bih[ds + i]),
-                    gin = gy[2 * ds + i] + to_f32(bih[2 * ds + i]);
-        const float ghr = acc[0] + to_f32(bhh[i]), ghz = acc[1] + to_f32(bhh[ds + i]),
-                    ghn = acc[2] + to_f32(bhh[2 * ds + i]);
-        const float rg = sigm(gir + ghr), zg = sigm(giz + ghz);
-        const float ng = tanhf(gin + rg * ghn);
-        const float hold = j > 1 ? hprev[(size_t)b * ds + i] : 0.f;
-        const float hn = (1.f - zg) * ng + zg * hold;
-        hnext[(size_t)b * ds + i] = hn;
-        if (h.states) h.states[((size_t)b * depth + (j - 1)) * ds + i] = hn;
+        float hn = 0.f;
+        if (live) {
+          const float *gy = h.gtab + (size_t)ys[b] * 3 * ds;
+          const float gir = gy[i] + to_f32(bih[i]), giz = gy[ds + i] + to_f32(bih[ds + i]),
+                      gin = gy[2 * ds + i] + to_f32(bih[2 * ds + i]);
+          const float ghr = acc[0] + to_f32(bhh[i]), ghz = acc[1] + to_f32(bhh[ds + i]),
+                      ghn = acc[2] + to_f32(bhh[2 * ds + i]);
+          const float rg = sigm(gir + ghr), zg = sigm(giz + ghz);
+          const float ng = tanhf(gin + rg * ghn);
+          const float hold = j > 1 ? hprev[(size_t)b * ds + i] : 0.f;
+          hn = (1.f - zg) * ng + zg * hold;
+          hnext[(size_t)b * ds + i] = hn;
+          if (h.states) h.states[((size_t)b * depth + (j - 1)) * ds + i] = hn;
+        }
       }
     }
   }
@@ -282,7 +290,7 @@ __global__ __launch_bounds__(256) void head_u_kernel(HeadArgs h, int j) {
     }
     acc = wave_sum(acc);
     if (lane == 0) {
-      const float x = h.P[((size_t)b * depth + (j - 1)) * r + k] + acc;
+      const float x = h.P[((size_t)b * depth + (j - 1)) * h.ldp + k] + acc;
       h.ubuf[(size_t)b * r + k] = x / (1.f + expf(-x));
     }
   }
@@ -294,12 +302,17 @@ __global__ __launch_bounds__(256) void head_u_kernel(HeadArgs h, int j) {
 // workgroup's top-beta per batch row.  A workgroup covers ROWS vocabulary
 // rows (8 waves x kTPW tiles of 16).
 // ---------------------------------------------------------------------------
-constexpr int kLogitWaves = 8, kTPW = 2;
-constexpr int kLogitRows = kLogitWaves * kTPW * 16;
+constexpr int kLogitWaves = 8;
+// W2 tiles per wave: as many as fit the registers (all of a wave's loads are
+// issued at once, and the grid then fits the GPU in one round)
+constexpr int kTpwSmall = 5;
+constexpr int logit_tpw(int KS, int MT) { return KS * MT <= 8 ? kTpwSmall : (KS * MT <= 16 ? 2 : 1); }
 
 template <typename WT, int KS, int MT>
 __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs h, int j) {
   constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP, XF = XStage<WT>::XF;
+  constexpr int kTPW = logit_tpw(KS, MT);
+  constexpr int kLogitRows = kLogitWaves * kTPW * 16;
   const Dims &D = h.D;
   const int bs = D.bs, r = D.r, V = D.V, depth = D.B - 1, beta = h.beta;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -330,10 +343,10 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int n = tiles[q] * 16 + 4 * g + e;
-        lb[q][mt][e] = (bb < bs && n < V) ? h.Lbase[((size_t)bb * depth + (j - 1)) * V + n] : 0.f;
+        lb[q][mt][e] = (bb < bs && n < V) ? h.Lbase[((size_t)bb * depth + (j - 1)) * h.ldl + n] : 0.f;
       }
     }
-  // stage u as matrix-core B fragments
+  // u staged as matrix-core B fragments
   for (int it = tid; it < KS * MT * 64; it += kLogitWaves * 64) {
     const int l = it & 63, mt = (it >> 6) % MT, s = (it >> 6) / MT;
     const int bb = mt * 16 + (l & 15);
@@ -393,35 +406,65 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
           v = ov[q];
           id = oi[q];
         }
-      h.pval[((size_t)bb * h.GC + blockIdx.x) * beta + lane] = v;
-      h.pid[((size_t)bb * h.GC + blockIdx.x) * beta + lane] = id;
+      const size_t o = (((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x) * beta + lane;
+      h.pval[o] = v;
+      h.pid[o] = id;
     }
+    // top-1 of this workgroup into the position's best key (order-independent max)
+    if (lane == 0 && oi[0] != INT_MAX)
+      atomicMax(&h.best[((size_t)(j - 1) * bs + bb) * kBestSlots + (blockIdx.x % kBestSlots)], encode_best(ov[0], oi[0]));
   }
 }
 
-int head_logits_grid(const Dims &D) { return (D.V + kLogitRows - 1) / kLogitRows; }
-
-size_t head_exchange_floats(const Dims &D, int GC, int beta) {
-  // hbuf [2][bs][ds] + ubuf [bs][r] + pval/pid [bs][GC][beta]
-  return (size_t)2 * D.bs * D.ds + (size_t)D.bs * D.r + (size_t)2 * D.bs * GC * beta;
+// Merge every workgroup's top-beta list of one (position, batch row) after the
+// rollout; one wave per (j, b).
+__global__ __launch_bounds__(64) void head_merge_kernel(HeadArgs h) {
+  const int j = blockIdx.x, b = blockIdx.y;
+  const int bs = h.D.bs, depth = h.D.B - 1, beta = h.beta;
+  const int lane = threadIdx.x;
+  const size_t base = ((size_t)j * bs + b) * h.GC * beta;
+  float ov[8];
+  int oi[8];
+  wave_select_mem(h.pval + base, h.pid + base, h.GC * beta, beta, ov, oi);
+  if (lane < beta) {
+    float v = ov[0];
+    int id = oi[0];
+#pragma unroll
+    for (int q = 1; q < 8; ++q)
+      if (lane == q) {
+        v = ov[q];
+        id = oi[q];
+      }
+    h.topk_ids[((size_t)b * depth + j) * beta + lane] = id;
+    h.topk_vals[((size_t)b * depth + j) * beta + lane] = v;
+  }
 }
+
+static int logit_rows(const Dims &D) {
+  const int KS = D.r / (D.bf16 ? 32 : 16);
+  const int MT = D.bs <= 16 ? 1 : (D.bs <= 32 ? 2 : 4);
+  return kLogitWaves * logit_tpw(KS, MT) * 16;
+}
+int head_logits_grid(const Dims &D) { return (D.V + logit_rows(D) - 1) / logit_rows(D); }
+
+
 
 template <typename WT, int KS, int MT>
 static void launch_loop(const HeadArgs &h, hipStream_t st) {
   const Dims &D = h.D;
   const int depth = D.B - 1;
   const int ga = min((D.ds + 3) / 4, 256);
-  const int gb = (D.r + 3) / 4;
   constexpr int XF = XStage<WT>::XF;
-  const size_t lds = sizeof(u32x4) * KS * MT * 64 * XF + sizeof(float) * (size_t)D.bs * kLogitRows;
+  const size_t lds = sizeof(u32x4) * KS * MT * 64 * XF + sizeof(float) * (size_t)D.bs * logit_rows(D);
   (void)hipFuncSetAttribute((const void *)head_logits_kernel<WT, KS, MT>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  const int gb = (D.r + 3) / 4;
   for (int j = 1; j <= depth; ++j) {
-    hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(ga), dim3(256), 0, st, h, j, 0);
+    hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(ga), dim3(256), 0, st, h, j);
     hipLaunchKernelGGL(head_u_kernel<WT>, dim3(gb), dim3(256), 0, st, h, j);
     hipLaunchKernelGGL((head_logits_kernel<WT, KS, MT>), dim3(h.GC), dim3(kLogitWaves * 64), lds, st, h, j);
   }
-  hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(1), dim3(256), 0, st, h, depth + 1, 1);
+  hipLaunchKernelGGL(head_merge_kernel, dim3(depth, D.bs), dim3(64), 0, st, h);
 }
 
 template <typename WT, int KS>
@@ -445,4 +488,8 @@ hipError_t launch_head(const HeadArgs &h, hipStream_t st) {
   return hipGetLastError();
 }
 
+}  // namespace dk
+
+namespace dk {
+int head_best_slots() { return kBestSlots; }
 }  // namespace dk

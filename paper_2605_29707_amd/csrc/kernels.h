@@ -46,8 +46,11 @@ void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor,
 // x[map(row)] += sum of np partials (pstride floats apart), then
 // y[row] = rmsnorm(x[map(row)]) * gain; with skip_anchor, output row i reads
 // input row i + i/(B-1) + 1 (the draft rows of each block) and x is left as is.
+// With `embed` given, x rows are first set to the embedding rows of the masked
+// block ([anchor, MASK, ...]) before the (empty) partial sum.
 void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
-                     const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor, hipStream_t st);
+                     const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
+                     const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st);
 // q/k RMSNorm + RoPE on the QKV projection (sum of np partials); writes
 // Q [M][nq][dh], Kb/Vb [M][nkv][dh]
 void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,
@@ -74,8 +77,10 @@ struct HeadArgs {
   const void *b_ih, *b_hh;
   const void *w1;        // [r][d+ds]; the S half starts at column d
   const void *w2p;       // W2 packed (tile-major, KS = r / KSTEP)
-  const float *P;        // [bs][B-1][r]: W1[:, :d] H_j
-  const float *Lbase;    // [bs][B-1][V]
+  const float *P;        // [bs][B-1] rows of stride ldp: W1[:, :d] H_j
+  int ldp;
+  const float *Lbase;    // [bs][B-1] rows of stride ldl: L_base_j
+  int ldl;
   const int32_t *anchor; // [bs]
   const int32_t *forced; // [bs][B-1] or null
   int32_t *topk_ids;     // [bs][B-1][beta]
@@ -84,13 +89,14 @@ struct HeadArgs {
   float *states;         // optional [bs][B-1][ds]
   float *hbuf;           // [2][bs][ds]
   float *ubuf;           // [bs][r]
-  float *pval;           // [bs][GC][beta]
-  int32_t *pid;          // [bs][GC][beta]
+  float *pval;           // [B-1][bs][GC][beta] per-workgroup top-beta lists
+  int32_t *pid;
+  unsigned long long *best;  // [B-1][bs][8] best (value, id) keys per position, zeroed per step
   int32_t *err;
   int GC;                // workgroups of the logits kernel
 };
 int head_logits_grid(const Dims &D);
-size_t head_exchange_floats(const Dims &D, int GC, int beta);
+int head_best_slots();
 hipError_t launch_head(const HeadArgs &h, hipStream_t st);
 
 // ---- tree and acceptance (tree.hip)

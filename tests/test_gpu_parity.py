@@ -43,9 +43,11 @@ def test_tiny_parity_context_from_hidden_states():
     run.close()
 
 
-@pytest.mark.parametrize("beta,lens", [(3, [128, 37, 0]), (8, [5, 128, 64])])
+@pytest.mark.parametrize("beta,lens", [(3, [128, 37, 0]), (8, [5, 128, 64]),
+                                       (2, [128 - 3 * i for i in range(20)]),
+                                       (1, [(37 * i) % 129 for i in range(40)])])
 def test_tiny_ragged_batch_branches(beta, lens):
-    cfg = synth.get_config("tiny").with_(batch=3, branch=beta, ctx_from_hidden=False)
+    cfg = synth.get_config("tiny").with_(batch=len(lens), branch=beta, ctx_from_hidden=False)
     w = synth.make_weights(cfg, seed=2, gain_std=0.1)
     lens = np.array(lens, np.int32)
     inp = synth.make_inputs(cfg, seed=2, ctx_lens=lens, max_ctx=128)
