@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -58,7 +59,7 @@ struct domino_model {
   size_t mem_bytes = 0;
   std::vector<Packed> qkv, wo, gateup, down;
   Packed lm, w2;
-  size_t gtab_off, w_hh_off, w1_off;
+  size_t gtab_off, w_hh_off, w1_off, freq_off;
   // profiling
   uint32_t prof_mask = 0;
   struct Ev {
@@ -289,6 +290,7 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
   D.eps = cfg->rms_eps;
   D.theta = cfg->rope_theta;
   D.bf16 = m->bf16;
+  D.inv_freq = nullptr;  // set once the model memory exists
   m->embed = w->embed;
   m->final_norm = w->final_norm;
   m->b_ih = w->gru_b_ih;
@@ -337,6 +339,8 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
   off = align_up(off + (size_t)3 * D.ds * D.ds * m->esz);
   m->w1_off = off;
   off = align_up(off + (size_t)D.r * (D.d + D.ds) * m->esz);
+  m->freq_off = off;
+  off = align_up(off + (size_t)(D.dh / 2) * sizeof(double));
   m->mem_bytes = off;
 
   he = hipMalloc(&m->mem, m->mem_bytes);
@@ -346,6 +350,7 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
   }
   hipStream_t st = nullptr;
   char *base = (char *)m->mem;
+  D.inv_freq = (const double *)(base + m->freq_off);
   const bool bf = m->bf16;
   for (int l = 0; l < L; ++l) {
     const Packed &p = m->qkv[l];
@@ -371,6 +376,12 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
   launch_pack(bf, w->w2, D.V, D.r, D.r, base + m->w2.off, m->w2.NT, m->w2.KS, 1, 0, st);
   he = hipGetLastError();
   if (he == hipSuccess) he = build_gtab(m, w->gru_w_ih);
+  if (he == hipSuccess) {
+    // RoPE inverse frequencies theta^(-2i/dh), exact in fp64 on the host
+    std::vector<double> f(D.dh / 2);
+    for (int i = 0; i < D.dh / 2; ++i) f[i] = std::pow((double)cfg->rope_theta, -2.0 * i / (double)D.dh);
+    he = hipMemcpy(base + m->freq_off, f.data(), f.size() * sizeof(double), hipMemcpyHostToDevice);
+  }
   if (he == hipSuccess) he = hipMemcpy(base + m->w_hh_off, w->gru_w_hh, (size_t)3 * D.ds * D.ds * m->esz, hipMemcpyDeviceToDevice);
   if (he == hipSuccess) he = hipMemcpy(base + m->w1_off, w->w1, (size_t)D.r * (D.d + D.ds) * m->esz, hipMemcpyDeviceToDevice);
   if (he == hipSuccess) he = hipDeviceSynchronize();

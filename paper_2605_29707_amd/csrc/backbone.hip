@@ -1,8 +1,8 @@
 // Draft-backbone kernels other than the projections (Sec. 4.1.1): block
 // embedding, RMSNorm, per-head q/k RMSNorm + rotate-half RoPE, projection of
 // context hidden states into the KV cache, and split-KV block attention.
-// All arithmetic is fp32; RoPE angles are formed in fp64 so that positions in
-// the thousands keep full fp32 accuracy in the rotated values.
+// All arithmetic is fp32; RoPE angles are formed and range-reduced in fp64 so
+// that positions in the thousands keep full fp32 accuracy in the rotated values.
 #include "common.h"
 #include "kernels.h"
 
@@ -119,7 +119,7 @@ __global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, in
 // l (dh = 64); RoPE pairs element i with i + dh/2.
 template <typename WT>
 DEVI void norm_rope_head(float (&v)[2], int dh, const WT *__restrict__ gain, float eps, int pos,
-                         float theta, bool rotate, int lane) {
+                         const double *__restrict__ inv_freq, bool rotate, int lane) {
   const int per = dh / 64;
   float ss = 0.f;
   for (int q = 0; q < per; ++q) ss = fmaf(v[q], v[q], ss);
@@ -127,20 +127,19 @@ DEVI void norm_rope_head(float (&v)[2], int dh, const WT *__restrict__ gain, flo
   const float inv = 1.0f / sqrtf(ss / (float)dh + eps);
   for (int q = 0; q < per; ++q) v[q] = v[q] * inv * to_f32(gain[lane + 64 * q]);
   if (!rotate) return;
+  // angle pos * theta^(-2i/dh): formed and reduced modulo 2*pi in fp64, then an
+  // fp32 sine/cosine of the reduced angle (|error| ~ 1e-7 at positions of 10^4)
+  const int i = dh == 128 ? lane : (lane & 31);
+  const double ang = (double)pos * inv_freq[i];
+  const double k = rint(ang * 0.15915494309189535);
+  const double red = fma(-k, 6.283185307179586, ang) - k * 2.4492935982947064e-16;
+  float s, c;
+  sincosf((float)red, &s, &c);
   if (dh == 128) {
-    const double w = pow((double)theta, -2.0 * (double)lane / 128.0);
-    double sd, cd;
-    sincos((double)pos * w, &sd, &cd);
-    const float c = (float)cd, s = (float)sd;
     const float x1 = v[0], x2 = v[1];
     v[0] = x1 * c - x2 * s;
     v[1] = x2 * c + x1 * s;
   } else {  // dh == 64: partner lives 32 lanes away
-    const int i = lane & 31;
-    const double w = pow((double)theta, -2.0 * (double)i / 64.0);
-    double sd, cd;
-    sincos((double)pos * w, &sd, &cd);
-    const float c = (float)cd, s = (float)sd;
     const float p = __shfl_xor(v[0], 32, 64);
     v[0] = (lane < 32) ? (v[0] * c - p * s) : (v[0] * c + p * s);
   }
@@ -154,7 +153,8 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
                                                            int max_ctx, float *__restrict__ Q,
                                                            float *__restrict__ Kb,
                                                            float *__restrict__ Vb, int M, int B, int nq,
-                                                           int nkv, int dh, float eps, float theta) {
+                                                           int nkv, int dh, float eps,
+                                                           const double *__restrict__ inv_freq) {
   const int lane = threadIdx.x & 63;
   const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int nh = nq + 2 * nkv;
@@ -181,10 +181,10 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
   }
   float *dst;
   if (hh < nq) {
-    norm_rope_head<WT>(v, dh, qn, eps, pos, theta, true, lane);
+    norm_rope_head<WT>(v, dh, qn, eps, pos, inv_freq, true, lane);
     dst = Q + ((size_t)m * nq + hh) * dh;
   } else if (hh < nq + nkv) {
-    norm_rope_head<WT>(v, dh, kn, eps, pos, theta, true, lane);
+    norm_rope_head<WT>(v, dh, kn, eps, pos, inv_freq, true, lane);
     dst = Kb + ((size_t)m * nkv + (hh - nq)) * dh;
   } else {
     dst = Vb + ((size_t)m * nkv + (hh - nq - nkv)) * dh;
@@ -199,7 +199,8 @@ __global__ __launch_bounds__(256) void ctx_store_kernel(const float *__restrict_
                                                         const int32_t *__restrict__ ctx_lens,
                                                         int max_ctx, WT *__restrict__ ck,
                                                         WT *__restrict__ cv, int bs, int nkv, int dh,
-                                                        float eps, float theta, int32_t *err) {
+                                                        float eps, const double *__restrict__ inv_freq,
+                                                        int32_t *err) {
   const int lane = threadIdx.x & 63;
   const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (item >= bs * n_new * 2 * nkv) return;
@@ -219,7 +220,7 @@ __global__ __launch_bounds__(256) void ctx_store_kernel(const float *__restrict_
   WT *dst;
   const size_t off = (((size_t)b * max_ctx + pos) * nkv) * dh;
   if (hh < nkv) {
-    norm_rope_head<WT>(v, dh, kn, eps, pos, theta, true, lane);
+    norm_rope_head<WT>(v, dh, kn, eps, pos, inv_freq, true, lane);
     dst = ck + off + (size_t)hh * dh;
   } else {
     dst = cv + off + (size_t)(hh - nkv) * dh;
@@ -232,13 +233,16 @@ __global__ __launch_bounds__(256) void ctx_store_kernel(const float *__restrict_
 // kv head (R = G*B rows); keys = context[0, n) followed by the B block keys;
 // no mask.  One workgroup per (key chunk of CH, kv head, batch row) writes the
 // chunk's row max, row sum of exp and unnormalised output; a second kernel
-// merges the chunks with log-sum-exp weights.  Q, K, V and P live in LDS as
-// fp32; each thread computes an RPT x 4 block of scores and an RPT x 8 block
-// of outputs, reading 16-byte vectors, so LDS traffic per FMA stays low.
+// merges the chunks with log-sum-exp weights.  Both products run on the
+// matrix cores (see attn_partial_kernel).
 // ---------------------------------------------------------------------------
 constexpr int kAttnThreads = 256;
 
 DEVI float4 ld4_f32(const float *p) { return *(const float4 *)p; }
+// component-wise select (a whole-vector select can be lowered through scratch memory)
+DEVI float4 keep4(bool ok, const float4 &v) {
+  return make_float4(ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f);
+}
 DEVI float4 ld4_f32(const bf16_t *p) {
   const uint2 u = *(const uint2 *)p;
   return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
@@ -252,22 +256,44 @@ size_t attn_part_floats(const Dims &D, int max_ctx) {
   return (size_t)D.bs * D.nq * D.B * attn_nchunks(max_ctx, D.B) * (D.dh + 2);
 }
 
-template <typename WT, int RPT, int CH, int DH>
+// Split 8 consecutive fp32 values (two 16-byte LDS vectors) into hi/lo bf16
+// matrix-core fragments.
+DEVI void frag_split(const float *p, bf16x8 &hi, bf16x8 &lo) {
+  const float4 a = *(const float4 *)p, c = *(const float4 *)(p + 4);
+  const float f[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
+  split8(f, hi, lo);
+}
+DEVI floatx4 mfma3(const bf16x8 &ah, const bf16x8 &al, const bf16x8 &bh, const bf16x8 &bl, floatx4 acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, acc, 0, 0, 0);
+  return acc;
+}
+
+// Matrix-core attention partial for one (key chunk, kv head, batch row):
+//   S^T = K Q^T  (16-key x 16-query tiles), softmax statistics per query row,
+//   O   = P V    (16-query x 16-dim tiles), with every fp32 operand split into
+//   hi + lo bf16 parts (three passes, the lo*lo term dropped: ~2^-16 relative).
+// Q, K, P live in LDS row-major; V is staged transposed so a B fragment (8
+// consecutive keys of one dim) is one contiguous read.
+template <typename WT, int QT, int CH, int DH>
 __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     const float *__restrict__ Q, const float *__restrict__ Kb, const float *__restrict__ Vb,
     const WT *__restrict__ ck, const WT *__restrict__ cv, const int32_t *__restrict__ ctx_lens,
     int max_ctx, float *__restrict__ part, int B, int nq, int nkv, int nch, float scale) {
-  constexpr int R = RPT * 16;          // query rows of the group
-  constexpr int DP = DH + 4;           // padded row stride (floats)
-  constexpr int CP = CH + 4;
-  constexpr int KPT = CH / 16;         // keys per thread in the score block
-  constexpr int DPT = DH / 16;         // output dims per thread
+  constexpr int R = QT * 16;      // query rows of the group
+  constexpr int KT = CH / 16;     // key tiles
+  constexpr int DT = DH / 16;     // output dim tiles
+  constexpr int QTW = QT * KT / 4;  // query tiles per wave in the score phase
+  constexpr int DTW = DT / 4;     // dim tiles per wave in the output phase
+  constexpr int DP = DH + 4, CP = CH + 4;
   extern __shared__ __align__(16) float smem[];
-  float *Qs = smem;                    // [R][DP]
-  float *Ks = Qs + R * DP;             // [CH][DP]
-  float *Vs = Ks + CH * DP;            // [CH][DP]
-  float *Ps = Vs + CH * DP;            // [R][CP]
-  float *Ms = Ps + R * CP;             // [R] row max
+  float *Qs = smem;               // [R][DP]
+  float *Ks = Qs + R * DP;        // [CH][DP]
+  float *Vt = Ks + CH * DP;       // [DH][CP]  (transposed)
+  float *Ps = Vt + DH * CP;       // [R][CP]
+  float *Rm = Ps + R * CP;        // [KT][R] partial row max
+  float *Rl = Rm + KT * R;        // [KT][R] partial row sum
 
   const int c = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int G = nq / nkv;
@@ -277,136 +303,147 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   const int c0 = c * CH;
   if (c0 >= total) return;
   const int nk = min(CH, total - c0);
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, cc = lane & 15;
 
-  // ---- stage Q rows (R x DH), K and V chunk (CH x DH) as fp32
-#pragma unroll
-  for (int e = tid; e < R * DH / 4; e += kAttnThreads) {
-    const int qi = e / (DH / 4), d4 = e % (DH / 4);
-    const int qh = kvh * G + qi / B, j = qi % B;
-    *(float4 *)(Qs + qi * DP + 4 * d4) = *(const float4 *)(Q + (((size_t)b * B + j) * nq + qh) * DH + 4 * d4);
-  }
+  // ---- stage Q rows, K chunk (row-major) and V chunk (transposed), fp32
   {
-    constexpr int NE = CH * DH / 4 / kAttnThreads;  // float4 groups per thread
+    constexpr int NQ = R * DH / 4 / kAttnThreads;
+    float4 qv[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int e = tid + q * kAttnThreads;
+      const int qi = e / (DH / 4), d4 = e % (DH / 4);
+      const int qh = kvh * G + qi / B, j = qi % B;
+      qv[q] = *(const float4 *)(Q + (((size_t)b * B + j) * nq + qh) * DH + 4 * d4);
+    }
+    constexpr int NE = CH * DH / 4 / kAttnThreads;
     float4 kv[NE], vv[NE];
 #pragma unroll
     for (int q = 0; q < NE; ++q) {
       const int e = tid + q * kAttnThreads;
       const int t = e / (DH / 4), d4 = e % (DH / 4);
       const int kk = min(c0 + t, total - 1);
-      if (kk < n) {
-        const size_t off = ((((size_t)b * max_ctx + kk) * nkv) + kvh) * DH + 4 * d4;
-        kv[q] = ld4_f32(ck + off);
-        vv[q] = ld4_f32(cv + off);
-      } else {
-        const size_t off = ((((size_t)b * B + (kk - n)) * nkv) + kvh) * DH + 4 * d4;
-        kv[q] = *(const float4 *)(Kb + off);
-        vv[q] = *(const float4 *)(Vb + off);
-      }
+      if (kk < n) kv[q] = ld4_f32(ck + ((((size_t)b * max_ctx + kk) * nkv) + kvh) * DH + 4 * d4);
+      else kv[q] = *(const float4 *)(Kb + ((((size_t)b * B + (kk - n)) * nkv) + kvh) * DH + 4 * d4);
+      const int tv = e % CH, dv = e / CH;                   // V: consecutive lanes, consecutive keys
+      const int kv2 = min(c0 + tv, total - 1);
+      if (kv2 < n) vv[q] = ld4_f32(cv + ((((size_t)b * max_ctx + kv2) * nkv) + kvh) * DH + 4 * dv);
+      else vv[q] = *(const float4 *)(Vb + ((((size_t)b * B + (kv2 - n)) * nkv) + kvh) * DH + 4 * dv);
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int e = tid + q * kAttnThreads;
+      const int qi = e / (DH / 4), d4 = e % (DH / 4);
+      *(float4 *)(Qs + qi * DP + 4 * d4) = qv[q];
     }
 #pragma unroll
     for (int q = 0; q < NE; ++q) {
       const int e = tid + q * kAttnThreads;
       const int t = e / (DH / 4), d4 = e % (DH / 4);
-      const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-      *(float4 *)(Ks + t * DP + 4 * d4) = t < nk ? kv[q] : z;
-      *(float4 *)(Vs + t * DP + 4 * d4) = t < nk ? vv[q] : z;
+      *(float4 *)(Ks + t * DP + 4 * d4) = keep4(t < nk, kv[q]);
+      const int tv = e % CH, dv = e / CH;
+      const float4 v = keep4(tv < nk, vv[q]);
+      Vt[(4 * dv + 0) * CP + tv] = v.x;
+      Vt[(4 * dv + 1) * CP + tv] = v.y;
+      Vt[(4 * dv + 2) * CP + tv] = v.z;
+      Vt[(4 * dv + 3) * CP + tv] = v.w;
     }
   }
   __syncthreads();
 
-  // ---- scores: thread (qb, kb) owns rows qb*RPT.. and keys kb, kb+16, ...
-  // (consecutive threads read consecutive K rows: conflict-free LDS banks)
-  const int qb = tid / 16, kb = tid % 16;
-  float s[RPT][KPT];
+  // ---- scores: wave w owns key tile kt = w % KT and QTW query tiles
+  const int kt = wave % KT, qt0 = (wave / KT) * QTW;
+  floatx4 sacc[QTW];
 #pragma unroll
-  for (int i = 0; i < RPT; ++i)
+  for (int i = 0; i < QTW; ++i) sacc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k = 0; k < KPT; ++k) s[i][k] = 0.f;
-  for (int d = 0; d < DH; d += 4) {
-    float4 kr[KPT];
+  for (int s = 0; s < DH / 32; ++s) {
+    bf16x8 kh, kl;
+    frag_split(Ks + (16 * kt + cc) * DP + 32 * s + 8 * g, kh, kl);
 #pragma unroll
-    for (int k = 0; k < KPT; ++k) kr[k] = *(const float4 *)(Ks + (kb + 16 * k) * DP + d);
-#pragma unroll
-    for (int i = 0; i < RPT; ++i) {
-      const float4 q = *(const float4 *)(Qs + (qb * RPT + i) * DP + d);
-#pragma unroll
-      for (int k = 0; k < KPT; ++k) {
-        s[i][k] = fmaf(q.x, kr[k].x, s[i][k]);
-        s[i][k] = fmaf(q.y, kr[k].y, s[i][k]);
-        s[i][k] = fmaf(q.z, kr[k].z, s[i][k]);
-        s[i][k] = fmaf(q.w, kr[k].w, s[i][k]);
-      }
+    for (int i = 0; i < QTW; ++i) {
+      bf16x8 qh, ql;
+      frag_split(Qs + (16 * (qt0 + i) + cc) * DP + 32 * s + 8 * g, qh, ql);
+      sacc[i] = mfma3(kh, kl, qh, ql, sacc[i]);
     }
   }
-  // row max / exp / row sum over the 16 threads sharing qb (xor over the low 4 lane bits)
+  // lane (g, cc) holds S[q = 16*qt + cc][key = 16*kt + 4g + e]
 #pragma unroll
-  for (int i = 0; i < RPT; ++i) {
+  for (int i = 0; i < QTW; ++i) {
     float m = -INFINITY;
 #pragma unroll
-    for (int k = 0; k < KPT; ++k) {
-      s[i][k] = (kb + 16 * k < nk) ? s[i][k] * scale : -INFINITY;
-      m = fmaxf(m, s[i][k]);
+    for (int e = 0; e < 4; ++e) {
+      const int key = 16 * kt + 4 * g + e;
+      sacc[i][e] = key < nk ? sacc[i][e] * scale : -INFINITY;
+      m = fmaxf(m, sacc[i][e]);
     }
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-    float l = 0.f;
-#pragma unroll
-    for (int k = 0; k < KPT; ++k) {
-      const float p = (kb + 16 * k < nk) ? expf(s[i][k] - m) : 0.f;
-      Ps[(qb * RPT + i) * CP + kb + 16 * k] = p;
-      l += p;
-    }
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) l += __shfl_xor(l, o, 64);
-    if (kb == 0) {
-      const int qi = qb * RPT + i;
-      const int qh = kvh * G + qi / B, j = qi % B;
-      float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2);
-      dst[DH] = m;
-      dst[DH + 1] = l;
-    }
+    m = fmaxf(m, __shfl_xor(m, 16, 64));
+    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    if (g == 0) Rm[kt * R + 16 * (qt0 + i) + cc] = m;
   }
   __syncthreads();
+#pragma unroll
+  for (int i = 0; i < QTW; ++i) {
+    const int q = 16 * (qt0 + i) + cc;
+    float m = Rm[q];
+#pragma unroll
+    for (int k2 = 1; k2 < KT; ++k2) m = fmaxf(m, Rm[k2 * R + q]);
+    float p[4], l = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int key = 16 * kt + 4 * g + e;
+      p[e] = key < nk ? expf(sacc[i][e] - m) : 0.f;
+      l += p[e];
+    }
+    *(float4 *)(Ps + q * CP + 16 * kt + 4 * g) = make_float4(p[0], p[1], p[2], p[3]);
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    if (g == 0) Rl[kt * R + q] = l;
+  }
+  __syncthreads();
+  // softmax statistics of the chunk per query row
+  for (int q = tid; q < R; q += kAttnThreads) {
+    float m = Rm[q], l = 0.f;
+    for (int k2 = 1; k2 < KT; ++k2) m = fmaxf(m, Rm[k2 * R + q]);
+    for (int k2 = 0; k2 < KT; ++k2) l += Rl[k2 * R + q];
+    const int qh = kvh * G + q / B, j = q % B;
+    float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2);
+    dst[DH] = m;
+    dst[DH + 1] = l;
+  }
 
-  // ---- output: thread (qb, db) owns rows qb*RPT.. and dims db*DPT..
-  const int db = tid % 16;
-  float o[RPT][DPT];
+  // ---- output: wave w owns DTW dim tiles, all query tiles
+  floatx4 oacc[QT][DTW];
 #pragma unroll
-  for (int i = 0; i < RPT; ++i)
+  for (int i = 0; i < QT; ++i)
 #pragma unroll
-    for (int x = 0; x < DPT; ++x) o[i][x] = 0.f;
-  for (int t = 0; t < nk; t += 4) {
-    float4 pr[RPT];
+    for (int x = 0; x < DTW; ++x) oacc[i][x] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < RPT; ++i) pr[i] = *(const float4 *)(Ps + (qb * RPT + i) * CP + t);
+  for (int s = 0; s < CH / 32; ++s) {
+    bf16x8 vh[DTW], vl[DTW];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      float vr[DPT];
+    for (int x = 0; x < DTW; ++x)
+      frag_split(Vt + (16 * (wave * DTW + x) + cc) * CP + 32 * s + 8 * g, vh[x], vl[x]);
 #pragma unroll
-      for (int x = 0; x < DPT; x += 4) {
-        const float4 v4 = *(const float4 *)(Vs + (t + u) * DP + db * DPT + x);
-        vr[x] = v4.x;
-        vr[x + 1] = v4.y;
-        vr[x + 2] = v4.z;
-        vr[x + 3] = v4.w;
-      }
+    for (int i = 0; i < QT; ++i) {
+      bf16x8 ph, pl;
+      frag_split(Ps + (16 * i + cc) * CP + 32 * s + 8 * g, ph, pl);
 #pragma unroll
-      for (int i = 0; i < RPT; ++i) {
-        const float p = u == 0 ? pr[i].x : (u == 1 ? pr[i].y : (u == 2 ? pr[i].z : pr[i].w));
-#pragma unroll
-        for (int x = 0; x < DPT; ++x) o[i][x] = fmaf(p, vr[x], o[i][x]);
-      }
+      for (int x = 0; x < DTW; ++x) oacc[i][x] = mfma3(ph, pl, vh[x], vl[x], oacc[i][x]);
     }
   }
+  // lane (g, cc) holds O[q = 16*i + 4g + e][dim = 16*dt + cc]
 #pragma unroll
-  for (int i = 0; i < RPT; ++i) {
-    const int qi = qb * RPT + i;
-    const int qh = kvh * G + qi / B, j = qi % B;
-    float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2) + db * DPT;
+  for (int i = 0; i < QT; ++i)
 #pragma unroll
-    for (int x = 0; x < DPT; x += 4) *(float4 *)(dst + x) = make_float4(o[i][x], o[i][x + 1], o[i][x + 2], o[i][x + 3]);
-  }
+    for (int e = 0; e < 4; ++e) {
+      const int q = 16 * i + 4 * g + e;
+      const int qh = kvh * G + q / B, j = q % B;
+      float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2);
+#pragma unroll
+      for (int x = 0; x < DTW; ++x) dst[16 * (wave * DTW + x) + cc] = oacc[i][x][e];
+    }
 }
 
 // Merge the chunks of one (batch, query head, block row) with log-sum-exp
@@ -424,36 +461,32 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float *__restri
   n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
   const int nc = (n + B + CH - 1) / CH;
   const float *base = part + (((size_t)b * nq + qh) * B + j) * nch * (DH + 2);
+  // chunk statistics: lane c holds chunk c (and c + 64, ...)
   float M = -INFINITY;
   for (int c = lane; c < nc; c += 64) M = fmaxf(M, base[c * (DH + 2) + DH]);
   M = wave_max(M);
   float den = 0.f;
   for (int c = lane; c < nc; c += 64) den += expf(base[c * (DH + 2) + DH] - M) * base[c * (DH + 2) + DH + 1];
   den = wave_sum(den);
-  constexpr int PER = DH / 64;
+  constexpr int PER = DH / 64, CB = 16;
   float acc[PER];
 #pragma unroll
   for (int q = 0; q < PER; ++q) acc[q] = 0.f;
-  int c = 0;
-  for (; c + 4 <= nc; c += 4) {
-    float w[4], v[4][PER];
+  for (int c0 = 0; c0 < nc; c0 += CB) {
+    float w[CB], v[CB][PER];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      w[u] = base[(c + u) * (DH + 2) + DH];
+    for (int u = 0; u < CB; ++u) {  // all loads of the batch in flight together
+      const int cu = min(c0 + u, nc - 1);
+      w[u] = base[cu * (DH + 2) + DH];
 #pragma unroll
-      for (int q = 0; q < PER; ++q) v[u][q] = base[(c + u) * (DH + 2) + lane + 64 * q];
+      for (int q = 0; q < PER; ++q) v[u][q] = base[cu * (DH + 2) + lane + 64 * q];
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float wu = expf(w[u] - M);
+    for (int u = 0; u < CB; ++u) {
+      const float wu = c0 + u < nc ? expf(w[u] - M) : 0.f;
 #pragma unroll
       for (int q = 0; q < PER; ++q) acc[q] = fmaf(wu, v[u][q], acc[q]);
     }
-  }
-  for (; c < nc; ++c) {
-    const float wu = expf(base[c * (DH + 2) + DH] - M);
-#pragma unroll
-    for (int q = 0; q < PER; ++q) acc[q] = fmaf(wu, base[c * (DH + 2) + lane + 64 * q], acc[q]);
   }
   const float inv = 1.0f / den;
   float *dst = O + ((size_t)(b * B + j) * nq + qh) * DH;
@@ -498,11 +531,11 @@ void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride
   if (D.bf16)
     hipLaunchKernelGGL(qk_norm_rope_kernel<bf16_t>, grid, dim3(256), 0, st, qkv, np, pstride, (const bf16_t *)q_norm,
                        (const bf16_t *)k_norm, ctx_lens, max_ctx, Q, Kb, Vb, M, D.B, D.nq, D.nkv, D.dh,
-                       D.eps, D.theta);
+                       D.eps, D.inv_freq);
   else
     hipLaunchKernelGGL(qk_norm_rope_kernel<float>, grid, dim3(256), 0, st, qkv, np, pstride, (const float *)q_norm,
                        (const float *)k_norm, ctx_lens, max_ctx, Q, Kb, Vb, M, D.B, D.nq, D.nkv, D.dh,
-                       D.eps, D.theta);
+                       D.eps, D.inv_freq);
 }
 
 void launch_ctx_store(const Dims &D, const float *kv, int n_new, const void *k_norm,
@@ -513,19 +546,21 @@ void launch_ctx_store(const Dims &D, const float *kv, int n_new, const void *k_n
   dim3 grid((items + 3) / 4);
   if (D.bf16)
     hipLaunchKernelGGL(ctx_store_kernel<bf16_t>, grid, dim3(256), 0, st, kv, n_new, (const bf16_t *)k_norm,
-                       ctx_lens, max_ctx, (bf16_t *)ck, (bf16_t *)cv, D.bs, D.nkv, D.dh, D.eps, D.theta,
+                       ctx_lens, max_ctx, (bf16_t *)ck, (bf16_t *)cv, D.bs, D.nkv, D.dh, D.eps, D.inv_freq,
                        err);
   else
     hipLaunchKernelGGL(ctx_store_kernel<float>, grid, dim3(256), 0, st, kv, n_new, (const float *)k_norm,
-                       ctx_lens, max_ctx, (float *)ck, (float *)cv, D.bs, D.nkv, D.dh, D.eps, D.theta, err);
+                       ctx_lens, max_ctx, (float *)ck, (float *)cv, D.bs, D.nkv, D.dh, D.eps, D.inv_freq,
+                       err);
 }
 
 template <typename WT, int RPT, int CH, int DH>
 static void attn_launch_t(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
                           const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
                           hipStream_t st) {
-  constexpr int R = RPT * 16, DP = DH + 4, CP = CH + 4;
-  const size_t lds = sizeof(float) * ((size_t)R * DP + 2 * CH * DP + (size_t)R * CP + R);
+  constexpr int R = RPT * 16, DP = DH + 4, CP = CH + 4, KT = CH / 16;
+  const size_t lds =
+      sizeof(float) * ((size_t)R * DP + (size_t)CH * DP + (size_t)DH * CP + (size_t)R * CP + 2 * KT * R);
   const float scale = 1.0f / sqrtf((float)DH);
   const int nc = (max_ctx + D.B + CH - 1) / CH;
   (void)hipFuncSetAttribute((const void *)attn_partial_kernel<WT, RPT, CH, DH>,

@@ -39,6 +39,7 @@ struct Dims {
   int bs, B, d, nq, nkv, dh, ffn, V, ds, r, mask_id;
   float eps, theta;
   bool bf16;
+  const double *inv_freq;  // device [dh/2]: theta^(-2i/dh), fp64
 };
 
 void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor, float *X,
