@@ -123,8 +123,8 @@ Dims make_dims(const domino_model *m, int bs) {
 
 // ---- workspace layout of the draft step
 struct WsLayout {
-  size_t err, best, hdr_words, X, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ubuf, pval, pid, ctxkv,
-      total;
+  size_t err, best, hdr_words, X, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
+      ctxkv, total;
   int GC, ldl;
 };
 
@@ -179,6 +179,7 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.ldl = m->lm.NT * 16;
   w.LP = take((size_t)Mh * w.ldl * 4);  // [L_base | pad | P] per draft row
   w.hbuf = take((size_t)2 * bs * D.ds * 4);
+  w.ghbuf = take((size_t)2 * bs * 3 * D.ds * 4);
   w.ubuf = take((size_t)bs * D.r * 4);
   w.pval = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
   w.pid = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
@@ -547,6 +548,7 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
   h.final_logits = debug ? debug->final_logits : nullptr;
   h.states = debug ? debug->states : nullptr;
   h.hbuf = F(w.hbuf);
+  h.ghbuf = F(w.ghbuf);
   h.ubuf = F(w.ubuf);
   h.pval = F(w.pval);
   h.pid = (int32_t *)(ws + w.pid);

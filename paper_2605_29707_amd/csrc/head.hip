@@ -39,31 +39,20 @@ DEVI void list_insert(float (&lv)[8], int (&li)[8], float v, int id) {
   }
 }
 
-// Wave-level top-beta of `cnt` candidates produced by get(c); every lane ends
-// with the same result in ov/oi (first beta entries valid).
-template <typename Get>
-DEVI void wave_select(Get get, int cnt, int beta, float (&ov)[8], int (&oi)[8]) {
+// Extract the wave's top-beta from per-lane sorted lists: lane k (< beta)
+// receives the k-th best in (mv, mi); other lanes get (-inf, INT_MAX).
+DEVI void wave_extract(float (&lv)[8], int (&li)[8], int beta, float &mv, int &mi) {
   const int lane = threadIdx.x & 63;
-  float lv[8];
-  int li[8];
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    lv[q] = -INFINITY;
-    li[q] = INT_MAX;
-  }
-  for (int c = lane; c < cnt; c += 64) {
-    float v;
-    int id;
-    get(c, v, id);
-    if (id == INT_MAX) continue;
-    list_insert(lv, li, order_val(v), id);
-  }
+  mv = -INFINITY;
+  mi = INT_MAX;
   for (int k = 0; k < beta; ++k) {
     float bv = lv[0];
     int bi = li[0];
     wave_best(bv, bi);
-    ov[k] = bv;
-    oi[k] = bi;
+    if (lane == k) {
+      mv = bv;
+      mi = bi;
+    }
     if (li[0] == bi && bi != INT_MAX) {  // ids are unique: exactly one owner advances
 #pragma unroll
       for (int q = 0; q < 7; ++q) {
@@ -76,10 +65,50 @@ DEVI void wave_select(Get get, int cnt, int beta, float (&ov)[8], int (&oi)[8]) 
   }
 }
 
+// Wave-level top-beta of the candidates c in [c0, c1) produced by get(c);
+// lane k (< beta) ends with the k-th best in (mv, mi).
+template <typename Get>
+DEVI void wave_select(Get get, int c0, int c1, int beta, float &mv, int &mi) {
+  const int lane = threadIdx.x & 63;
+  if (beta == 1) {  // a running best is enough
+    float bv = -INFINITY;
+    int bi = INT_MAX;
+    for (int c = c0 + lane; c < c1; c += 64) {
+      float v;
+      int id;
+      get(c, v, id);
+      v = order_val(v);
+      if (id != INT_MAX && better(v, id, bv, bi)) {
+        bv = v;
+        bi = id;
+      }
+    }
+    wave_best(bv, bi);
+    mv = lane == 0 ? bv : -INFINITY;
+    mi = lane == 0 ? bi : INT_MAX;
+    return;
+  }
+  float lv[8];
+  int li[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    lv[q] = -INFINITY;
+    li[q] = INT_MAX;
+  }
+  for (int c = c0 + lane; c < c1; c += 64) {
+    float v;
+    int id;
+    get(c, v, id);
+    if (id == INT_MAX) continue;
+    list_insert(lv, li, order_val(v), id);
+  }
+  wave_extract(lv, li, beta, mv, mi);
+}
+
 // wave_select over candidates in global memory: each lane loads its
 // candidates 8 at a time, all loads of a batch in flight together.
 DEVI void wave_select_mem(const float *__restrict__ pv, const int32_t *__restrict__ pi, int cnt, int beta,
-                          float (&ov)[8], int (&oi)[8]) {
+                          float &mv, int &mi) {
   const int lane = threadIdx.x & 63;
   float lv[8];
   int li[8];
@@ -102,22 +131,7 @@ DEVI void wave_select_mem(const float *__restrict__ pv, const int32_t *__restric
     for (int u = 0; u < 8; ++u)
       if (id[u] != INT_MAX) list_insert(lv, li, order_val(v[u]), id[u]);
   }
-  for (int k = 0; k < beta; ++k) {
-    float bv = lv[0];
-    int bi = li[0];
-    wave_best(bv, bi);
-    ov[k] = bv;
-    oi[k] = bi;
-    if (li[0] == bi && bi != INT_MAX) {
-#pragma unroll
-      for (int q = 0; q < 7; ++q) {
-        lv[q] = lv[q + 1];
-        li[q] = li[q + 1];
-      }
-      lv[7] = -INFINITY;
-      li[7] = INT_MAX;
-    }
-  }
+  wave_extract(lv, li, beta, mv, mi);
 }
 
 DEVI float sigm(float x) { return 1.f / (1.f + expf(-x)); }
@@ -297,6 +311,147 @@ __global__ __launch_bounds__(256) void head_u_kernel(HeadArgs h, int j) {
 }
 
 // ---------------------------------------------------------------------------
+// state (batches up to kFusedBatch; replaces gru + u): every workgroup forms
+// the whole S_{j-1} itself from the gathered input gates G[y_{j-1}], the
+// hidden gates W_hh S_{j-2} that the previous position left in ghbuf, and
+// S_{j-2}; its waves then take rows of the stacked matrix [W1[:, d:]; W_hh]
+// against S_{j-1}.  The first r rows give u_j = SiLU(P_j + W1[:, d:] S_{j-1}),
+// the other 3 d_s rows the hidden gates of position j+1, so the elementwise
+// update is the only step repeated per workgroup and no launch sits between
+// the state and u.  Weight rows are loaded before the state is formed.
+// ---------------------------------------------------------------------------
+constexpr int kFusedBatch = 8;
+constexpr int kStateWaves = 8;
+constexpr int kStateMaxGrid = 256;
+
+template <typename WT>
+__global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h, int j) {
+  constexpr int EPL = 16 / sizeof(WT);
+  const Dims &D = h.D;
+  const int bs = D.bs, ds = D.ds, r = D.r, d = D.d, depth = D.B - 1, V = D.V;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  extern __shared__ __align__(16) float sl[];  // S_{j-1} [bs][ds]
+  __shared__ int ys[kFusedBatch];
+  const int nchunk = ds / EPL;  // <= 256
+  const int nrows = r + (j < depth ? 3 * ds : 0);
+  const int nw = gridDim.x * kStateWaves;
+  const int w0 = blockIdx.x * kStateWaves + wave;
+  const WT *w1 = (const WT *)h.w1, *whh = (const WT *)h.w_hh;
+
+  // ---- two rows per wave per round (rows w0 + k*nw); the first round's loads go out now
+  u32x4 w[2][4];
+  auto load_rows = [&](int base) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int row = min(base + q * nw, nrows - 1);
+      const WT *p = row < r ? w1 + (size_t)row * (d + ds) + d : whh + (size_t)(row - r) * ds;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int ch = min(lane + 64 * c, nchunk - 1);
+        w[q][c] = *(const u32x4 *)(p + (size_t)ch * EPL);
+      }
+    }
+  };
+  load_rows(w0);
+
+  // ---- y_{j-1}: the anchor, a forced token, or the decoded best key of position j-1
+  if (tid < bs) {
+    const int b = tid;
+    int y;
+    if (j == 1) y = clamp_token(h.anchor[b], V, h.err);
+    else if (h.forced) y = clamp_token(h.forced[(size_t)b * depth + (j - 2)], V, h.err);
+    else {
+      const unsigned long long *bk = h.best + ((size_t)(j - 2) * bs + b) * kBestSlots;
+      unsigned long long key = bk[0];
+#pragma unroll
+      for (int q = 1; q < kBestSlots; ++q) key = bk[q] > key ? bk[q] : key;
+      y = decode_best_id(key, V);
+    }
+    ys[b] = y;
+  }
+  __syncthreads();
+
+  // ---- S_{j-1} = GRU(x = E[y_{j-1}], S_{j-2}), four state indices per item
+  const WT *bih = (const WT *)h.b_ih, *bhh = (const WT *)h.b_hh;
+  const float *ghp = h.ghbuf + (size_t)((j - 1) & 1) * bs * 3 * ds;  // W_hh S_{j-2}
+  const float *sprev = h.hbuf + (size_t)(j & 1) * bs * ds;            // S_{j-2}
+  float *scur = h.hbuf + (size_t)((j - 1) & 1) * bs * ds;             // S_{j-1}
+  for (int it = tid; it < bs * ds / 4; it += kStateWaves * 64) {
+    const int b = it / (ds / 4), i = (it % (ds / 4)) * 4;
+    const float *gy = h.gtab + (size_t)ys[b] * 3 * ds;
+    float gi[3][4], gh[3][4], hold[4];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      const float4 a = *(const float4 *)(gy + q * ds + i);
+      const float4 c = j > 1 ? *(const float4 *)(ghp + (size_t)b * 3 * ds + q * ds + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+      gi[q][0] = a.x; gi[q][1] = a.y; gi[q][2] = a.z; gi[q][3] = a.w;
+      gh[q][0] = c.x; gh[q][1] = c.y; gh[q][2] = c.z; gh[q][3] = c.w;
+    }
+    {
+      const float4 c = j > 1 ? *(const float4 *)(sprev + (size_t)b * ds + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+      hold[0] = c.x; hold[1] = c.y; hold[2] = c.z; hold[3] = c.w;
+    }
+    float out[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int ii = i + e;
+      const float rg = sigm(gi[0][e] + to_f32(bih[ii]) + gh[0][e] + to_f32(bhh[ii]));
+      const float zg = sigm(gi[1][e] + to_f32(bih[ds + ii]) + gh[1][e] + to_f32(bhh[ds + ii]));
+      const float ng = tanhf(gi[2][e] + to_f32(bih[2 * ds + ii]) + rg * (gh[2][e] + to_f32(bhh[2 * ds + ii])));
+      out[e] = (1.f - zg) * ng + zg * hold[e];
+    }
+    const float4 o = make_float4(out[0], out[1], out[2], out[3]);
+    *(float4 *)(sl + (size_t)b * ds + i) = o;
+    if (blockIdx.x == 0) {
+      *(float4 *)(scur + (size_t)b * ds + i) = o;
+      if (h.states) *(float4 *)(h.states + ((size_t)b * depth + (j - 1)) * ds + i) = o;
+    }
+  }
+  __syncthreads();
+
+  // ---- rows of [W1[:, d:]; W_hh] against S_{j-1}
+  float *ghn = h.ghbuf + (size_t)(j & 1) * bs * 3 * ds;  // W_hh S_{j-1}
+  for (int base = w0; base < nrows; base += 2 * nw) {
+    if (base != w0) load_rows(base);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int row = base + q * nw;
+      if (row >= nrows) continue;  // wave-uniform
+      float wf[4][EPL];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) unpack16<WT>(w[q][c], wf[c]);
+      for (int b = 0; b < bs; ++b) {
+        const float *sb = sl + (size_t)b * ds;
+        float acc = 0.f;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int ch = lane + 64 * c;
+          if (ch < nchunk) {
+#pragma unroll
+            for (int e = 0; e < EPL; e += 4) {
+              const float4 t = *(const float4 *)(sb + (size_t)ch * EPL + e);
+              acc = fmaf(wf[c][e], t.x, acc);
+              acc = fmaf(wf[c][e + 1], t.y, acc);
+              acc = fmaf(wf[c][e + 2], t.z, acc);
+              acc = fmaf(wf[c][e + 3], t.w, acc);
+            }
+          }
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) {
+          if (row < r) {
+            const float x = h.P[((size_t)b * depth + (j - 1)) * h.ldp + row] + acc;
+            h.ubuf[(size_t)b * r + row] = x / (1.f + expf(-x));
+          } else {
+            ghn[(size_t)b * 3 * ds + (row - r)] = acc;
+          }
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // logits: matrix-core W2 tiles times the staged u (batch rows as the 16
 // columns of the B operand, hi/lo split for bf16), plus L_base, then each
 // workgroup's top-beta per batch row.  A workgroup covers ROWS vocabulary
@@ -323,6 +478,20 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
   u32x4 *us = (u32x4 *)smem;                                      // [KS][MT][64][XF]
   float *lv = (float *)(smem + sizeof(u32x4) * KS * MT * 64 * XF);  // [bs][kLogitRows]
 
+  // u_j first (a few L2-resident values), so the matrix-core work can follow
+  // the W2 stream as its fragments arrive
+  constexpr int kUIt = (KS * MT * 64 + kLogitWaves * 64 - 1) / (kLogitWaves * 64);
+  float4 uv[kUIt][EPL / 4];
+#pragma unroll
+  for (int q = 0; q < kUIt; ++q) {
+    const int it = min(tid + q * kLogitWaves * 64, KS * MT * 64 - 1);
+    const int l = it & 63, mt = (it >> 6) % MT, s = (it >> 6) / MT;
+    const int bb = mt * 16 + (l & 15);
+    const int k0 = s * KSTEP + (l >> 4) * EPL;
+#pragma unroll
+    for (int e = 0; e < EPL / 4; ++e)
+      uv[q][e] = bb < bs ? *(const float4 *)(h.ubuf + (size_t)bb * r + k0 + 4 * e) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   // W2 fragments of this wave's tiles, then the L_base values it will add
   const u32x4 *w2p = (const u32x4 *)h.w2p;
   u32x4 wf[kTPW][KS];
@@ -334,28 +503,23 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
 #pragma unroll
     for (int s = 0; s < KS; ++s) wf[q][s] = w2p[((size_t)t * KS + s) * 64 + lane];
   }
-  float lb[kTPW][MT][4];
+  // L_base rows are padded to whole tiles (ldl >= 16 * NT), so a tile's four
+  // values load as one float4; entries past V are masked below
+  float4 lb[kTPW][MT];
 #pragma unroll
   for (int q = 0; q < kTPW; ++q)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int bb = mt * 16 + cc;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int n = tiles[q] * 16 + 4 * g + e;
-        lb[q][mt][e] = (bb < bs && n < V) ? h.Lbase[((size_t)bb * depth + (j - 1)) * h.ldl + n] : 0.f;
-      }
+      const int t = tiles[q] < NT ? tiles[q] : NT - 1;
+      lb[q][mt] = bb < bs ? *(const float4 *)(h.Lbase + ((size_t)bb * depth + (j - 1)) * h.ldl + t * 16 + 4 * g)
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   // u staged as matrix-core B fragments
-  for (int it = tid; it < KS * MT * 64; it += kLogitWaves * 64) {
-    const int l = it & 63, mt = (it >> 6) % MT, s = (it >> 6) / MT;
-    const int bb = mt * 16 + (l & 15);
-    const int k0 = s * KSTEP + (l >> 4) * EPL;
-    float4 v[EPL / 4];
 #pragma unroll
-    for (int q = 0; q < EPL / 4; ++q)
-      v[q] = bb < bs ? *(const float4 *)(h.ubuf + (size_t)bb * r + k0 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
-    XStage<WT>::put(us + (size_t)it * XF, v);
+  for (int q = 0; q < kUIt; ++q) {
+    const int it = tid + q * kLogitWaves * 64;
+    if (it < KS * MT * 64) XStage<WT>::put(us + (size_t)it * XF, uv[q]);
   }
   __syncthreads();
 
@@ -385,34 +549,53 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int n = tiles[q] * 16 + 4 * g + e;
-        const float val = lb[q][mt][e] + acc[q][mt][e];
+        const float lbe = e == 0 ? lb[q][mt].x : (e == 1 ? lb[q][mt].y : (e == 2 ? lb[q][mt].z : lb[q][mt].w));
+        const float val = lbe + acc[q][mt][e];
         lv[(size_t)bb * kLogitRows + (n - row0)] = n < V ? val : -INFINITY;
         if (n < V && h.final_logits) h.final_logits[((size_t)bb * depth + (j - 1)) * V + n] = val;
       }
     }
   __syncthreads();
   const int nrows = min(kLogitRows, V - row0);
-  for (int bb = wave; bb < bs; bb += kLogitWaves) {
-    float ov[8];
-    int oi[8];
-    const float *lr = lv + (size_t)bb * kLogitRows;
-    wave_select([&](int c, float &v, int &id) { v = lr[c]; id = row0 + c; }, nrows, beta, ov, oi);
+  // this workgroup's top-beta per batch row; with fewer rows than waves, each
+  // row's candidates are split over P waves and the P lists merged after
+  const int P = bs >= kLogitWaves ? 1 : kLogitWaves / bs;
+  __shared__ float cand_v[kLogitWaves][8];
+  __shared__ int cand_i[kLogitWaves][8];
+  auto emit = [&](int bb, float mv, int mi) __attribute__((always_inline)) {
     if (lane < beta) {
-      float v = ov[0];
-      int id = oi[0];
-#pragma unroll
-      for (int q = 1; q < 8; ++q)
-        if (lane == q) {
-          v = ov[q];
-          id = oi[q];
-        }
       const size_t o = (((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x) * beta + lane;
-      h.pval[o] = v;
-      h.pid[o] = id;
+      h.pval[o] = mv;
+      h.pid[o] = mi;
     }
     // top-1 of this workgroup into the position's best key (order-independent max)
-    if (lane == 0 && oi[0] != INT_MAX)
-      atomicMax(&h.best[((size_t)(j - 1) * bs + bb) * kBestSlots + (blockIdx.x % kBestSlots)], encode_best(ov[0], oi[0]));
+    if (lane == 0 && mi != INT_MAX)
+      atomicMax(&h.best[((size_t)(j - 1) * bs + bb) * kBestSlots + (blockIdx.x % kBestSlots)], encode_best(mv, mi));
+  };
+  for (int t = wave; t < bs * P; t += kLogitWaves) {
+    const int bb = t / P, part = t % P;
+    float mv;
+    int mi;
+    const float *lr = lv + (size_t)bb * kLogitRows;
+    wave_select([&](int c, float &v, int &id) { v = lr[c]; id = row0 + c; }, part * nrows / P,
+                (part + 1) * nrows / P, beta, mv, mi);
+    if (P == 1) {
+      emit(bb, mv, mi);
+    } else if (lane < 8) {
+      cand_v[t][lane] = mv;
+      cand_i[t][lane] = mi;
+    }
+  }
+  if (P > 1) {
+    __syncthreads();
+    if (wave < bs) {
+      float mv;
+      int mi;
+      const int t0 = wave * P;
+      wave_select([&](int c, float &v, int &id) { v = cand_v[t0 + c / beta][c % beta]; id = cand_i[t0 + c / beta][c % beta]; },
+                  0, P * beta, beta, mv, mi);
+      emit(wave, mv, mi);
+    }
   }
 }
 
@@ -423,20 +606,12 @@ __global__ __launch_bounds__(64) void head_merge_kernel(HeadArgs h) {
   const int bs = h.D.bs, depth = h.D.B - 1, beta = h.beta;
   const int lane = threadIdx.x;
   const size_t base = ((size_t)j * bs + b) * h.GC * beta;
-  float ov[8];
-  int oi[8];
-  wave_select_mem(h.pval + base, h.pid + base, h.GC * beta, beta, ov, oi);
+  float mv;
+  int mi;
+  wave_select_mem(h.pval + base, h.pid + base, h.GC * beta, beta, mv, mi);
   if (lane < beta) {
-    float v = ov[0];
-    int id = oi[0];
-#pragma unroll
-    for (int q = 1; q < 8; ++q)
-      if (lane == q) {
-        v = ov[q];
-        id = oi[q];
-      }
-    h.topk_ids[((size_t)b * depth + j) * beta + lane] = id;
-    h.topk_vals[((size_t)b * depth + j) * beta + lane] = v;
+    h.topk_ids[((size_t)b * depth + j) * beta + lane] = mi;
+    h.topk_vals[((size_t)b * depth + j) * beta + lane] = mv;
   }
 }
 
@@ -459,9 +634,19 @@ static void launch_loop(const HeadArgs &h, hipStream_t st) {
   (void)hipFuncSetAttribute((const void *)head_logits_kernel<WT, KS, MT>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   const int gb = (D.r + 3) / 4;
+  const bool fused = D.bs <= kFusedBatch;
+  const size_t slds = sizeof(float) * (size_t)D.bs * D.ds;
+  const int gs = min((D.r + 3 * D.ds + 2 * kStateWaves - 1) / (2 * kStateWaves), kStateMaxGrid);
+  if (fused)
+    (void)hipFuncSetAttribute((const void *)head_state_kernel<WT>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)slds);
   for (int j = 1; j <= depth; ++j) {
-    hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(ga), dim3(256), 0, st, h, j);
-    hipLaunchKernelGGL(head_u_kernel<WT>, dim3(gb), dim3(256), 0, st, h, j);
+    if (fused) {
+      hipLaunchKernelGGL(head_state_kernel<WT>, dim3(gs), dim3(kStateWaves * 64), slds, st, h, j);
+    } else {
+      hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(ga), dim3(256), 0, st, h, j);
+      hipLaunchKernelGGL(head_u_kernel<WT>, dim3(gb), dim3(256), 0, st, h, j);
+    }
     hipLaunchKernelGGL((head_logits_kernel<WT, KS, MT>), dim3(h.GC), dim3(kLogitWaves * 64), lds, st, h, j);
   }
   hipLaunchKernelGGL(head_merge_kernel, dim3(depth, D.bs), dim3(64), 0, st, h);

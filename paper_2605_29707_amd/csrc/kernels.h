@@ -88,7 +88,8 @@ struct HeadArgs {
   float *topk_vals;
   float *final_logits;   // optional [bs][B-1][V]
   float *states;         // optional [bs][B-1][ds]
-  float *hbuf;           // [2][bs][ds]
+  float *hbuf;           // [2][bs][ds] states by parity of the position
+  float *ghbuf;          // [2][bs][3ds] W_hh S by parity (fused small-batch path)
   float *ubuf;           // [bs][r]
   float *pval;           // [B-1][bs][GC][beta] per-workgroup top-beta lists
   int32_t *pid;

@@ -60,6 +60,23 @@ def test_tiny_ragged_batch_branches(beta, lens):
     run.close()
 
 
+@pytest.mark.parametrize("batch,beta", [(1, 1), (5, 4), (8, 8), (12, 2)])
+def test_tiny_bf16_batches(batch, beta):
+    """bf16 storage on the small shape, on both sides of the small-batch rollout
+    path (up to 8 rows: one fused state kernel per position; above: the
+    three-kernel rollout), with the per-workgroup selection split over waves."""
+    cfg = synth.get_config("tiny").with_(dtype="bf16", batch=batch, branch=beta, ctx_from_hidden=False)
+    w = synth.make_weights(cfg, seed=11, gain_std=0.1)
+    inp = synth.make_inputs(cfg, seed=11)
+    log(f"tiny bf16 batch={batch} beta={beta}")
+    run = GpuRun(cfg, w, inp["max_ctx"], beta=beta)
+    gpu = run.step(inp)
+    assert gpu["err"] == 0
+    ref = oracle_for(cfg, oracle.as_f64_weights(w), inp, gpu, beta)
+    check_against_oracle(cfg, gpu, ref, 2e-2, beta)
+    run.close()
+
+
 def test_teacher_forcing_and_perturbation_causality():
     cfg = synth.get_config("tiny").with_(ctx_from_hidden=False, batch=2)
     w = synth.make_weights(cfg, seed=3)
