@@ -338,7 +338,17 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
   const int w0 = blockIdx.x * kStateWaves + wave;
   const WT *w1 = (const WT *)h.w1, *whh = (const WT *)h.w_hh;
 
-  // ---- two rows per wave per round (rows w0 + k*nw); the first round's loads go out now
+  // ---- the sources of y_{j-1} first (every thread, clamped batch row, so no
+  // branch holds the later loads back), then this wave's weight rows
+  const int bq = min(tid, bs - 1);
+  const int anc = h.anchor[bq];
+  unsigned long long keys[kBestSlots];
+  {
+    const unsigned long long *bk = h.best + ((size_t)(j > 1 ? j - 2 : 0) * bs + bq) * kBestSlots;
+#pragma unroll
+    for (int q = 0; q < kBestSlots; ++q) keys[q] = bk[q];
+  }
+  // two rows per wave per round (rows w0 + k*nw); the first round's loads go out now
   u32x4 w[2][4];
   auto load_rows = [&](int base) {
 #pragma unroll
@@ -356,18 +366,16 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
 
   // ---- y_{j-1}: the anchor, a forced token, or the decoded best key of position j-1
   if (tid < bs) {
-    const int b = tid;
     int y;
-    if (j == 1) y = clamp_token(h.anchor[b], V, h.err);
-    else if (h.forced) y = clamp_token(h.forced[(size_t)b * depth + (j - 2)], V, h.err);
+    if (j == 1) y = clamp_token(anc, V, h.err);
+    else if (h.forced) y = clamp_token(h.forced[(size_t)tid * depth + (j - 2)], V, h.err);  // teacher forcing
     else {
-      const unsigned long long *bk = h.best + ((size_t)(j - 2) * bs + b) * kBestSlots;
-      unsigned long long key = bk[0];
+      unsigned long long key = keys[0];
 #pragma unroll
-      for (int q = 1; q < kBestSlots; ++q) key = bk[q] > key ? bk[q] : key;
+      for (int q = 1; q < kBestSlots; ++q) key = keys[q] > key ? keys[q] : key;
       y = decode_best_id(key, V);
     }
-    ys[b] = y;
+    ys[tid] = y;
   }
   __syncthreads();
 
@@ -488,23 +496,20 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
     const int l = it & 63, mt = (it >> 6) % MT, s = (it >> 6) / MT;
     const int bb = mt * 16 + (l & 15);
     const int k0 = s * KSTEP + (l >> 4) * EPL;
+    // unconditional loads at a clamped row: a guarded load becomes a branch
+    // whose join drains every outstanding load, holding back the W2 stream
+    // issued below.  Columns of padding rows (bb >= bs) only reach output
+    // columns that are never read, so their values do not matter.
+    const float *src = h.ubuf + (size_t)min(bb, bs - 1) * r + k0;
 #pragma unroll
-    for (int e = 0; e < EPL / 4; ++e)
-      uv[q][e] = bb < bs ? *(const float4 *)(h.ubuf + (size_t)bb * r + k0 + 4 * e) : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int e = 0; e < EPL / 4; ++e) uv[q][e] = *(const float4 *)(src + 4 * e);
   }
-  // W2 fragments of this wave's tiles, then the L_base values it will add
-  const u32x4 *w2p = (const u32x4 *)h.w2p;
-  u32x4 wf[kTPW][KS];
+  // then the L_base values this wave will add (rows are padded to whole tiles,
+  // ldl >= 16 * NT, so a tile's four values load as one float4; entries past V
+  // are masked below), then the W2 fragments of its tiles
   int tiles[kTPW];
 #pragma unroll
-  for (int q = 0; q < kTPW; ++q) {
-    tiles[q] = (blockIdx.x * kLogitWaves + wave) * kTPW + q;
-    const int t = tiles[q] < NT ? tiles[q] : NT - 1;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) wf[q][s] = w2p[((size_t)t * KS + s) * 64 + lane];
-  }
-  // L_base rows are padded to whole tiles (ldl >= 16 * NT), so a tile's four
-  // values load as one float4; entries past V are masked below
+  for (int q = 0; q < kTPW; ++q) tiles[q] = (blockIdx.x * kLogitWaves + wave) * kTPW + q;
   float4 lb[kTPW][MT];
 #pragma unroll
   for (int q = 0; q < kTPW; ++q)
@@ -512,9 +517,17 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
     for (int mt = 0; mt < MT; ++mt) {
       const int bb = mt * 16 + cc;
       const int t = tiles[q] < NT ? tiles[q] : NT - 1;
-      lb[q][mt] = bb < bs ? *(const float4 *)(h.Lbase + ((size_t)bb * depth + (j - 1)) * h.ldl + t * 16 + 4 * g)
-                          : make_float4(0.f, 0.f, 0.f, 0.f);
+      // clamped row, unconditional (lanes of padding rows are never read)
+      lb[q][mt] = *(const float4 *)(h.Lbase + ((size_t)min(bb, bs - 1) * depth + (j - 1)) * h.ldl + t * 16 + 4 * g);
     }
+  const u32x4 *w2p = (const u32x4 *)h.w2p;
+  u32x4 wf[kTPW][KS];
+#pragma unroll
+  for (int q = 0; q < kTPW; ++q) {
+    const int t = tiles[q] < NT ? tiles[q] : NT - 1;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) wf[q][s] = w2p[((size_t)t * KS + s) * 64 + lane];
+  }
   // u staged as matrix-core B fragments
 #pragma unroll
   for (int q = 0; q < kUIt; ++q) {
@@ -528,18 +541,80 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
   for (int q = 0; q < kTPW; ++q)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // tile-major, in the order the fragments were requested: tile q's products
+  // start as soon as its fragments arrive, overlapping the rest of the stream
 #pragma unroll
-  for (int s = 0; s < KS; ++s) {
-    u32x4 xf[MT * XF];
+  for (int q = 0; q < kTPW; ++q)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int s = 0; s < KS; ++s) {
+      u32x4 xf[MT * XF];
 #pragma unroll
-      for (int f = 0; f < XF; ++f) xf[mt * XF + f] = us[((size_t)(s * MT + mt) * 64 + lane) * XF + f];
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int q = 0; q < kTPW; ++q) Mac2<WT, MT>::step(wf[q][s], xf, acc[q]);
-  }
+        for (int f = 0; f < XF; ++f) xf[mt * XF + f] = us[((size_t)(s * MT + mt) * 64 + lane) * XF + f];
+      Mac2<WT, MT>::step(wf[q][s], xf, acc[q]);
+    }
 
-  // corrected logits of this workgroup's rows
+  // corrected logits of this workgroup's rows: lane (g, cc) holds rows
+  // 16 t + 4 g + e of batch row mt * 16 + cc
+  if (beta == 1) {
+    // top-1 without staging: a running best per batch row in registers, the
+    // four lanes of a row combined by shuffles, then one entry per (wave, row)
+    __shared__ float best_v[kLogitWaves][64];
+    __shared__ int best_i[kLogitWaves][64];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int bb = mt * 16 + cc;
+      float bv = -INFINITY;
+      int bi = INT_MAX;
+#pragma unroll
+      for (int q = 0; q < kTPW; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int n = tiles[q] * 16 + 4 * g + e;
+          const float lbe = e == 0 ? lb[q][mt].x : (e == 1 ? lb[q][mt].y : (e == 2 ? lb[q][mt].z : lb[q][mt].w));
+          const float val = lbe + acc[q][mt][e];
+          if (bb < bs && n < V) {
+            if (h.final_logits) h.final_logits[((size_t)bb * depth + (j - 1)) * V + n] = val;
+            const float ov = order_val(val);
+            if (better(ov, n, bv, bi)) {
+              bv = ov;
+              bi = n;
+            }
+          }
+        }
+#pragma unroll
+      for (int o = 16; o <= 32; o <<= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (better(ov, oi, bv, bi)) {
+          bv = ov;
+          bi = oi;
+        }
+      }
+      if (g == 0) {
+        best_v[wave][bb] = bv;
+        best_i[wave][bb] = bi;
+      }
+    }
+    __syncthreads();
+    for (int bb = tid; bb < bs; bb += kLogitWaves * 64) {
+      float v = best_v[0][bb];
+      int id = best_i[0][bb];
+#pragma unroll
+      for (int w = 1; w < kLogitWaves; ++w)
+        if (better(best_v[w][bb], best_i[w][bb], v, id)) {
+          v = best_v[w][bb];
+          id = best_i[w][bb];
+        }
+      const size_t o = ((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x;
+      h.pval[o] = v;
+      h.pid[o] = id;
+      if (id != INT_MAX)
+        atomicMax(&h.best[((size_t)(j - 1) * bs + bb) * kBestSlots + (blockIdx.x % kBestSlots)], encode_best(v, id));
+    }
+    return;
+  }
 #pragma unroll
   for (int q = 0; q < kTPW; ++q)
 #pragma unroll
