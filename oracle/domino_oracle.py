@@ -159,7 +159,7 @@ def draft_backbone(cfg, w, anchor, ctx_k, ctx_v, ctx_len):
     ctx_k/ctx_v: [L, max_ctx, nkv, d_h] for this batch row.  Returns [B-1, d].
     """
     n = int(ctx_len)
-    x = np.asarray(w["embed"], F64)[masked_block(cfg, anchor)]
+    x = np.asarray(np.asarray(w["embed"])[masked_block(cfg, anchor)], F64)  # rows first, then exact upcast
     pos = np.arange(n, n + cfg.block, dtype=F64)
     for l, lw in enumerate(w["layers"]):
         x = backbone_layer(cfg, lw, x, pos, ctx_k[l, :n], ctx_v[l, :n])
@@ -353,12 +353,17 @@ def verify_accept(node_token, node_parent, target_logits, block=16):
     return {"accept_len": acc_len, "accepted_nodes": acc_nodes, "out_tokens": out_tok}
 
 
-def as_f64_weights(w):
-    """Copy a weight dict to float64 once, so repeated oracle calls do not convert."""
+def as_f64_weights(w, keep=()):
+    """Copy a weight dict to float64 once, so repeated oracle calls do not convert.
+
+    Entries named in `keep` stay as they are (e.g. the embedding table, of which
+    only a few rows are ever read; the rows are upcast exactly where used)."""
     out = {}
     for k, v in w.items():
         if k == "layers":
             out[k] = [{kk: np.asarray(vv, F64) for kk, vv in lw.items()} for lw in v]
+        elif k in keep:
+            out[k] = v
         else:
             out[k] = np.asarray(v, F64)
     return out

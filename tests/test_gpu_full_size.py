@@ -1,0 +1,100 @@
+"""Full-size GPU parity for the larger drafting workloads, on sampled batch rows.
+
+Each test runs the whole batch through the C-ABI at the workload's real shape
+(the launch configuration the benchmark uses: debug outputs off, then again
+with them on, which must give identical top-beta), and checks a few batch rows
+against the fp64 oracle run on those rows alone (batch rows are independent,
+so the oracle computes them one by one).  The oracle is teacher-forced on the
+GPU's drafted tokens so both sides roll out the same prefixes; tolerances are
+the bf16 bar (2e-2 absolute) and top-1 / top-beta agreement away from
+oracle near-ties.
+
+The 8B batch-32 workload additionally builds its 61-node trees and runs greedy
+acceptance over the full [32, 61, 151936] bf16 target logits, bit-exact
+against the oracle.
+"""
+import gc
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_helpers import GpuRun, check_against_oracle, log
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+
+def _tree_and_accept(gpu_topk, inp, cfg, seed):
+    from paper_2605_29707_amd import binding as bd
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    bs, depth, beta = gpu_topk.shape
+    nn = 1 + depth * beta
+    outs = [torch.empty(bs, nn, dtype=torch.int32, device=dev) for _ in range(4)]
+    mask = torch.empty(bs, nn, nn, dtype=torch.uint8, device=dev)
+    bd.domino_build_tree(t(gpu_topk), t(inp["anchor"]), t(inp["ctx_lens"]), *outs, ancestor_mask=mask)
+    torch.cuda.synchronize()
+    keys = ("node_token", "node_parent", "node_depth", "node_pos")
+    got = {k: o.cpu().numpy() for k, o in zip(keys, outs)}
+    got["ancestor_mask"] = mask.cpu().numpy()
+    want = oracle.build_tree(gpu_topk, inp["anchor"], inp["ctx_lens"])
+    for k in want:
+        np.testing.assert_array_equal(got[k], want[k], err_msg=k)
+    log(f"tree bit-exact: {bs} rows x {nn} nodes")
+
+    lg = synth.make_target_logits(cfg, want["node_token"], want["node_parent"], seed=seed, dtype="bf16")
+    lt = torch.from_numpy(lg).to(dev).to(torch.bfloat16)
+    del lg
+    acc = torch.empty(bs, dtype=torch.int32, device=dev)
+    nodes = torch.empty(bs, cfg.block - 1, dtype=torch.int32, device=dev)
+    toks = torch.empty(bs, cfg.block, dtype=torch.int32, device=dev)
+    ws = torch.empty(bd.domino_verify_workspace_bytes(bs, nn, cfg.vocab), dtype=torch.uint8, device=dev)
+    bd.domino_verify_accept(outs[0], outs[1], lt, cfg.block, acc, nodes, toks, ws)
+    torch.cuda.synchronize()
+    assert bd.domino_workspace_error(ws) == 0
+    res = oracle.verify_accept(want["node_token"], want["node_parent"], lt.float().cpu().numpy(), cfg.block)
+    np.testing.assert_array_equal(acc.cpu().numpy(), res["accept_len"])
+    np.testing.assert_array_equal(nodes.cpu().numpy(), res["accepted_nodes"])
+    np.testing.assert_array_equal(toks.cpu().numpy(), res["out_tokens"])
+    log(f"acceptance bit-exact; accept lengths {res['accept_len'].tolist()}")
+
+
+@pytest.mark.parametrize("name,rows", [("qwen3_8b_bs32", [0, 13, 31]),
+                                       ("qwen3_4b_ctx8k", [0, 3]),
+                                       ("qwen3_32b", [0, 15])])
+def test_full_size_sampled_rows(name, rows):
+    cfg = synth.get_config(name)
+    beta = cfg.branch
+    log(f"{name}: {cfg}")
+    w = synth.make_weights(cfg, seed=3)
+    inp = synth.make_inputs(cfg, seed=3)
+    log("weights and inputs generated; uploading + packing")
+    run = GpuRun(cfg, w, inp["max_ctx"], beta=beta)
+    plain = run.step(inp, debug=False)
+    gpu = run.step(inp, debug=True)
+    assert gpu["err"] == 0
+    np.testing.assert_array_equal(plain["topk_ids"], gpu["topk_ids"])
+    np.testing.assert_array_equal(plain["topk_vals"], gpu["topk_vals"])
+    log("gpu steps done")
+    run.close()
+    del run, plain
+    torch.cuda.empty_cache()
+    if beta > 1:
+        _tree_and_accept(gpu["topk_ids"], inp, cfg, seed=3)
+
+    rows = np.array(rows)
+    log(f"oracle (fp64) on rows {rows.tolist()}")
+    w64 = oracle.as_f64_weights(w, keep=("embed",))  # embedding rows are upcast where read
+    del w
+    gc.collect()
+    ref = oracle.draft_step(cfg, w64, inp["anchor"][rows], inp["ctx_lens"][rows], inp["ctx_k"][:, rows],
+                            inp["ctx_v"][:, rows], beta, forced=gpu["topk_ids"][rows, :, 0])
+    sub = {k: gpu[k][rows] for k in ("topk_ids", "topk_vals", "hidden", "base_logits", "final_logits", "states")}
+    n = check_against_oracle(cfg, sub, ref, 2e-2, beta)
+    log(f"top-beta entries checked: {n}")
+    assert n >= len(rows) * 10
