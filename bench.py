@@ -63,8 +63,11 @@ def algorithmic_bytes(cfg) -> dict:
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--flush-steps", type=int, default=50,
+                    help="extra steps, each after a 512 MiB scratch write that evicts on-chip caches; "
+                         "reported per step (the write itself is not timed)")
     ap.add_argument("--config", default="qwen3_8b")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -168,6 +171,26 @@ def main():
         taus += (acc.cpu().numpy() + 1).tolist()
     tau = float(np.mean(taus))
 
+    flushed = None
+    if args.flush_steps > 0:
+        scratch = torch.empty(512 * (1 << 20) // 4, dtype=torch.float32, device=dev)
+        fe = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.flush_steps)]
+        torch.cuda.synchronize()
+        for i in range(args.flush_steps):
+            scratch.fill_(float(i))  # a fill kernel, not a memset
+            fe[i][0].record(stream)
+            step()
+            fe[i][1].record(stream)
+        torch.cuda.synchronize()
+        fper = [a.elapsed_time(b) for a, b in fe]
+        flushed = {"steps": args.flush_steps,
+                   "us_per_step_median": round(statistics.median(fper) * 1e3, 1),
+                   "us_per_step_p10_p90": [round(float(np.percentile(fper, 10)) * 1e3, 1),
+                                           round(float(np.percentile(fper, 90)) * 1e3, 1)]}
+        del scratch
+        torch.cuda.empty_cache()
+
     breakdown = None
     if args.breakdown:
         classes = [c for c in bd.KERNEL_CLASSES]
@@ -221,6 +244,8 @@ def main():
                      "launch_us": round(dom_launch_s * 1e6, 2), "launches": dom_n,
                      "algorithmic_bytes_per_launch": dom_bytes},
     }
+    if flushed:
+        res["after_cache_flush"] = flushed
     if breakdown:
         res["breakdown_us_per_step"] = breakdown
 
