@@ -44,6 +44,8 @@ import numpy as np
 
 F64 = np.float64
 
+from .sampling_oracle import sample_draft  # noqa: E402  (sampled drafting, Fig. 3)
+
 
 # ----------------------------------------------------------------------------
 # elementary operations
@@ -219,11 +221,16 @@ def argmax_total(vals):
     return int(np.flatnonzero(v == m)[0])
 
 
-def domino_head(cfg, w, h, lbase, anchor, beta, forced=None):
+def domino_head(cfg, w, h, lbase, anchor, beta, forced=None, sampling=None, gaps_out=None):
     """Sequential rollout over the B-1 draft positions for one batch row.
 
     Returns (topk_ids [B-1, beta], topk_vals [B-1, beta], final logits
     [B-1, V], causal states [B-1, d_s], drafted tokens [B-1]).
+
+    sampling = (temperature, seed, row): each position's token is drawn from
+    softmax(final / T) (sampling_oracle.sample_draft; beta must be 1) and
+    topk_vals holds its final logit; the draw's key gap is appended to gaps_out.
+    Teacher forcing (forced) still decides the fed-back tokens.
     """
     depth = cfg.block - 1
     s = np.zeros(cfg.gru_hidden, F64)
@@ -238,7 +245,15 @@ def domino_head(cfg, w, h, lbase, anchor, beta, forced=None):
         s = gru_cell(w, np.asarray(embed[y], F64), s)          # S_{j-1} sees y_0..y_{j-1}
         states[j] = s
         final[j] = np.asarray(lbase[j], F64) + correction(w, h[j], s)
-        ids[j], vals[j] = top_beta(final[j], beta)
+        if sampling is None:
+            ids[j], vals[j] = top_beta(final[j], beta)
+        else:
+            assert beta == 1, "sampled drafting is defined for one token per position"
+            temperature, seed, row = sampling
+            tok, gap = sample_draft(final[j], temperature, seed, row, j + 1)
+            ids[j, 0], vals[j, 0] = tok, final[j][tok]
+            if gaps_out is not None:
+                gaps_out.append(gap)
         y = int(forced[j]) if forced is not None else int(ids[j, 0])
         drafted[j] = y
     return ids, vals, final, states, drafted
@@ -248,13 +263,16 @@ def domino_head(cfg, w, h, lbase, anchor, beta, forced=None):
 # one draft step for a batch
 # ----------------------------------------------------------------------------
 def draft_step(cfg, w, anchor, ctx_lens, ctx_k, ctx_v, beta, forced=None,
-               ctx_hidden=None):
+               ctx_hidden=None, sampling=None, rows=None):
     """Full draft step.
 
     anchor, ctx_lens: [bs]; ctx_k/ctx_v: [L, bs, max_ctx, nkv, d_h]; forced:
     optional [bs, B-1]; ctx_hidden: optional [bs, n_new, d] projected into
     positions [ctx_len - n_new, ctx_len) of every layer before drafting.
-    Returns a dict of arrays with a leading batch axis.
+    sampling: optional (temperature, seed) for sampled drafting; `rows` gives
+    the batch-row index each row's random streams use (default 0..bs-1).
+    Returns a dict of arrays with a leading batch axis ("sample_gap" [bs, B-1]
+    when sampling).
     """
     bs = len(anchor)
     ctx_k = np.array(ctx_k, dtype=F64, copy=True)
@@ -272,10 +290,14 @@ def draft_step(cfg, w, anchor, ctx_lens, ctx_k, ctx_v, beta, forced=None,
                 ctx_v[l, b, n - n_new:n] = v
         h = draft_backbone(cfg, w, anchor[b], ctx_k[:, b], ctx_v[:, b], n)
         lb = base_logits(w, h)
+        gaps = []
+        smp = None if sampling is None else (sampling[0], sampling[1], b if rows is None else int(rows[b]))
         ids, vals, final, states, drafted = domino_head(
-            cfg, w, h, lb, anchor[b], beta, None if forced is None else forced[b])
+            cfg, w, h, lb, anchor[b], beta, None if forced is None else forced[b], smp, gaps)
         for k, v in zip(out, (ids, vals, lb, final, h, states, drafted)):
             out[k].append(v)
+        if sampling is not None:
+            out.setdefault("sample_gap", []).append(np.array(gaps))
     res = {k: np.stack(v) for k, v in out.items()}
     res["ctx_k"], res["ctx_v"] = ctx_k, ctx_v
     return res
