@@ -156,6 +156,32 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
                                 void *stream);
 
 /*
+ * One draft step with temperature sampling (Fig. 3: each draft token is drawn
+ * from the final logits l_i + c_i; here from softmax((l_i + c_i) / T)), branch 1.
+ * Same arguments as domino_draft_step except:
+ *  temperature     T > 0 (finite)
+ *  seed            64-bit key of the Philox-4x32-10 draws (Salmon et al., SC
+ *                  2011): the token at depth j of row b is
+ *                  argmax_v (L_j[v] / T + g), g = -log(-log u) of the word
+ *                  (seed; counter v/4, j, b, stream 0; word v%4), u = (floor(
+ *                  word / 2^9) + 1/2) / 2^23 — a draw from softmax(L_j / T);
+ *                  the same step with the same seed draws the same tokens
+ *  topk_ids        device int32 [batch][B-1][1]: the drawn tokens (fed back to
+ *                  the causal encoder unless forced_tokens is given)
+ *  topk_vals       device fp32 [batch][B-1][1]: the drawn tokens' final logits
+ *  final_logits    device fp32 [batch][B-1][vocab], required: L_j, which
+ *                  domino_verify_sample needs as the draft distributions
+ *  debug           optional; its final_logits field is ignored
+ *  workspace       >= domino_workspace_bytes(m, batch, max_ctx, n_new, 1)
+ */
+domino_status domino_draft_step_sampled(domino_model_t m, int32_t batch, const int32_t *anchor_ids,
+                                        const int32_t *ctx_lens, void *ctx_k, void *ctx_v, int32_t max_ctx,
+                                        const void *ctx_hidden_new, int32_t n_new, float temperature,
+                                        uint64_t seed, const int32_t *forced_tokens, int32_t *topk_ids,
+                                        float *topk_vals, float *final_logits, const domino_debug *debug,
+                                        void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Draft tree from the per-position top-beta tokens (spine-and-leaves, BFS
  * order).  Node 0 is the anchor (parent -1, depth 0, position n_b); node
  * 1 + (d-1)*branch + rho holds topk_ids[b][d-1][rho] at depth d, position
@@ -195,7 +221,44 @@ domino_status domino_verify_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                                    int32_t *out_tokens, void *workspace, size_t workspace_bytes,
                                    void *stream);
 
-/* Copy the device error word at the start of a draft or verify workspace to
+/* Workspace bytes for domino_verify_sample. */
+size_t domino_verify_sample_workspace_bytes(int32_t batch, int32_t block, int32_t vocab);
+
+/*
+ * Speculative-sampling verification of a drafted chain at temperature T
+ * (Sec. 3.1, the standard speculative verification rule), branch 1.
+ * For depth j = 1..B-1, p_j = softmax(target_logits[b][j-1] / T) (row m is the
+ * target's distribution after node m) and q_j = softmax(draft_logits[b][j-1] /
+ * T).  Draft token x_j = node_token[b][j] is accepted iff u_j q_j(x_j) <
+ * p_j(x_j), i.e. with probability min(1, p_j(x_j) / q_j(x_j)), u_j the uniform
+ * of (seed; counter 0, j, b, stream 1; word 0).  At the first rejection j the
+ * bonus token is a draw from max(0, p_j - q_j) (normalised); if all B-1 are
+ * accepted, from p_B; draws are argmax_v (log w_v + g_v) over w_v > 0 with g
+ * from (seed; counter v/4, j, b, stream 2; word v%4).  NaN logits count as
+ * -inf.  tau = accept_len + 1 in [1, B].
+ *  block B in [2, 64]; node_token device int32 [batch][B] (node 0 the anchor,
+ *  node j the draft token at depth j); target_logits device [batch][B][vocab]
+ *  fp32 or bf16; draft_logits device fp32 [batch][B-1][vocab] (the
+ *  final_logits of domino_draft_step_sampled); accept_len device int32
+ *  [batch]; accepted_nodes device int32 [batch][B-1] (node indices, -1
+ *  padded); out_tokens device int32 [batch][B] (accepted tokens then the
+ *  bonus, -1 padded).  An out-of-range draft token sets DOMINO_DEV_BAD_TOKEN
+ *  and counts as rejected.
+ */
+domino_status domino_verify_sample(int32_t batch, int32_t block, int32_t vocab, const int32_t *node_token,
+                                   const void *target_logits, domino_dtype logits_dtype,
+                                   const float *draft_logits, float temperature, uint64_t seed,
+                                   int32_t *accept_len, int32_t *accepted_nodes, int32_t *out_tokens,
+                                   void *workspace, size_t workspace_bytes, void *stream);
+
+/* Philox-4x32-10 (Salmon et al., SC 2011) of n explicit counters: counters
+ * device uint32 [n][4], key = (key lo, key hi) 32-bit words, out device uint32
+ * [n][4].  The generator behind the sampled calls, for callers and tests that
+ * need the same draws. */
+domino_status domino_philox4x32_10(const uint32_t *counters, uint64_t key, uint32_t *out, int32_t n,
+                                   void *stream);
+
+/* Copy the device error word at the start of a draft or verify workspace to/* Copy the device error word at the start of a draft or verify workspace to
  * *out (synchronises `stream`).  Returns DOMINO_ERR_DEVICE when it is set. */
 domino_status domino_workspace_error(const void *workspace, void *stream, int32_t *out);
 

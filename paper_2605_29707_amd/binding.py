@@ -84,6 +84,12 @@ def load() -> C.CDLL:
         "domino_profile_enable": (i32, [P, u32]),
         "domino_profile_read": (i32, [P, i32, C.POINTER(C.c_double), C.POINTER(i32)]),
         "domino_profile_reset": (i32, [P]),
+        "domino_draft_step_sampled": (i32, [P, i32, P, P, P, P, i32, P, i32, C.c_float, C.c_uint64, P, P, P, P,
+                                            C.POINTER(domino_debug), P, sz, P]),
+        "domino_verify_sample_workspace_bytes": (sz, [i32, i32, i32]),
+        "domino_verify_sample": (i32, [i32, i32, i32, P, P, C.c_int, P, C.c_float, C.c_uint64, P, P, P, P, sz,
+                                       P]),
+        "domino_philox4x32_10": (i32, [P, C.c_uint64, P, i32, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -97,7 +103,9 @@ def exported_symbols():
     return ["domino_model_create", "domino_model_destroy", "domino_workspace_bytes", "domino_last_error",
             "domino_draft_step", "domino_build_tree", "domino_verify_workspace_bytes",
             "domino_verify_accept", "domino_workspace_error", "domino_workspace_clear_error",
-            "domino_profile_enable", "domino_profile_read", "domino_profile_reset"]
+            "domino_profile_enable", "domino_profile_read", "domino_profile_reset",
+            "domino_draft_step_sampled", "domino_verify_sample_workspace_bytes", "domino_verify_sample",
+            "domino_philox4x32_10"]
 
 
 def last_error() -> str:
@@ -193,6 +201,41 @@ def domino_draft_step(model: DominoModel, anchor, ctx_lens, ctx_k, ctx_v, max_ct
         int(max_ctx), _ptr(ctx_hidden_new), int(n_new), int(branch), _ptr(forced), _ptr(topk_ids),
         _ptr(topk_vals), C.byref(dbg) if dbg is not None else None, _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def domino_draft_step_sampled(model: DominoModel, anchor, ctx_lens, ctx_k, ctx_v, max_ctx, topk_ids, topk_vals,
+                              final_logits, workspace, temperature, seed, ctx_hidden_new=None, n_new=0,
+                              forced=None, debug=None, stream=None):
+    dbg = None
+    if debug:
+        dbg = domino_debug(**{k: (debug[k].data_ptr() if debug.get(k) is not None else None)
+                              for k in ("hidden", "base_logits", "final_logits", "states")})
+    _check(load().domino_draft_step_sampled(
+        model.handle, int(anchor.shape[0]), _ptr(anchor), _ptr(ctx_lens), _ptr(ctx_k), _ptr(ctx_v),
+        int(max_ctx), _ptr(ctx_hidden_new), int(n_new), float(temperature), int(seed) & (2**64 - 1),
+        _ptr(forced), _ptr(topk_ids), _ptr(topk_vals), _ptr(final_logits),
+        C.byref(dbg) if dbg is not None else None, _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def domino_verify_sample_workspace_bytes(batch, block, vocab) -> int:
+    return int(load().domino_verify_sample_workspace_bytes(batch, block, vocab))
+
+
+def domino_verify_sample(node_token, target_logits, draft_logits, temperature, seed, accept_len, accepted_nodes,
+                         out_tokens, workspace, stream=None):
+    import torch
+    bs, B, V = target_logits.shape
+    dt = DOMINO_BF16 if target_logits.dtype == torch.bfloat16 else DOMINO_F32
+    _check(load().domino_verify_sample(bs, B, V, _ptr(node_token), _ptr(target_logits), dt, _ptr(draft_logits),
+                                       float(temperature), int(seed) & (2**64 - 1), _ptr(accept_len),
+                                       _ptr(accepted_nodes), _ptr(out_tokens), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def domino_philox4x32_10(counters, key, out, stream=None):
+    _check(load().domino_philox4x32_10(_ptr(counters), int(key) & (2**64 - 1), _ptr(out),
+                                       int(counters.shape[0]), _stream(stream)))
 
 
 def domino_build_tree(topk_ids, anchor, ctx_lens, node_token, node_parent, node_depth, node_pos,

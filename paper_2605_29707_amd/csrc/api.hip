@@ -124,7 +124,7 @@ Dims make_dims(const domino_model *m, int bs) {
 // ---- workspace layout of the draft step
 struct WsLayout {
   size_t err, best, hdr_words, X, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
-      ctxkv, total;
+      praw, ctxkv, total;
   int GC, ldl;
 };
 
@@ -183,6 +183,7 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.ubuf = take((size_t)bs * D.r * 4);
   w.pval = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
   w.pid = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
+  w.praw = take((size_t)(D.B - 1) * bs * w.GC * 4);
   w.ctxkv = take((size_t)bs * (max_new > 0 ? max_new : 0) * 2 * D.nkv * D.dh * 4);
   w.total = o;
   return true;
@@ -412,10 +413,17 @@ size_t domino_workspace_bytes(domino_model_t m, int32_t batch, int32_t max_ctx, 
   return w.total;
 }
 
-domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
-                                void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new,
-                                int32_t branch, const int32_t *forced_tokens, int32_t *topk_ids, float *topk_vals,
-                                const domino_debug *debug, void *workspace, size_t workspace_bytes, void *stream) {
+namespace {
+struct SampleOpt {
+  float temperature;
+  uint64_t seed;
+};
+
+domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
+                              void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new,
+                              int32_t branch, const int32_t *forced_tokens, int32_t *topk_ids, float *topk_vals,
+                              const domino_debug *debug, void *workspace, size_t workspace_bytes, void *stream,
+                              const SampleOpt *smp) {
   if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
   if (batch < 1 || batch > 64) return fail(DOMINO_ERR_INVALID_ARG, "batch must be in [1, 64]");
   if (!anchor_ids || !ctx_lens) return fail(DOMINO_ERR_INVALID_ARG, "anchor_ids/ctx_lens is NULL");
@@ -554,6 +562,11 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
   h.pid = (int32_t *)(ws + w.pid);
   h.err = err;
   h.GC = w.GC;
+  h.sample = smp ? 1 : 0;
+  h.inv_temp = smp ? 1.0f / smp->temperature : 1.0f;
+  h.seed_lo = smp ? (uint32_t)smp->seed : 0u;
+  h.seed_hi = smp ? (uint32_t)(smp->seed >> 32) : 0u;
+  h.praw = F(w.praw);
   prof_begin(m, DOMINO_KC_HEADLOOP, st);
   hipError_t he = launch_head(h, st);
   prof_end(m, DOMINO_KC_HEADLOOP, st);
@@ -561,6 +574,33 @@ domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *
   he = hipGetLastError();
   if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "draft step launch: %s", hipGetErrorString(he));
   return DOMINO_OK;
+}
+
+}  // namespace
+
+domino_status domino_draft_step(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
+                                void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new,
+                                int32_t branch, const int32_t *forced_tokens, int32_t *topk_ids, float *topk_vals,
+                                const domino_debug *debug, void *workspace, size_t workspace_bytes, void *stream) {
+  return draft_step_impl(m, batch, anchor_ids, ctx_lens, ctx_k, ctx_v, max_ctx, ctx_hidden_new, n_new, branch,
+                         forced_tokens, topk_ids, topk_vals, debug, workspace, workspace_bytes, stream, nullptr);
+}
+
+domino_status domino_draft_step_sampled(domino_model_t m, int32_t batch, const int32_t *anchor_ids,
+                                        const int32_t *ctx_lens, void *ctx_k, void *ctx_v, int32_t max_ctx,
+                                        const void *ctx_hidden_new, int32_t n_new, float temperature, uint64_t seed,
+                                        const int32_t *forced_tokens, int32_t *topk_ids, float *topk_vals,
+                                        float *final_logits, const domino_debug *debug, void *workspace,
+                                        size_t workspace_bytes, void *stream) {
+  if (!(temperature > 0.f) || !std::isfinite(temperature) || 1.0f / temperature > 1e30f)
+    return fail(DOMINO_ERR_INVALID_ARG, "temperature must be positive and finite");
+  if (!final_logits) return fail(DOMINO_ERR_INVALID_ARG, "final_logits is NULL (the verifier needs them)");
+  domino_debug dbg = {};
+  if (debug) dbg = *debug;
+  dbg.final_logits = final_logits;
+  const SampleOpt smp = {temperature, seed};
+  return draft_step_impl(m, batch, anchor_ids, ctx_lens, ctx_k, ctx_v, max_ctx, ctx_hidden_new, n_new, 1,
+                         forced_tokens, topk_ids, topk_vals, &dbg, workspace, workspace_bytes, stream, &smp);
 }
 
 domino_status domino_build_tree(int32_t batch, int32_t depth, int32_t branch, const int32_t *topk_ids,
@@ -604,6 +644,44 @@ domino_status domino_verify_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                 accept_len, accepted_nodes, out_tokens, workspace, st);
   hipError_t he = hipGetLastError();
   if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "verify_accept launch: %s", hipGetErrorString(he));
+  return DOMINO_OK;
+}
+
+size_t domino_verify_sample_workspace_bytes(int32_t batch, int32_t block, int32_t vocab) {
+  if (batch < 1 || block < 2 || block > 64 || vocab < 1) return 0;
+  return vs_ws_bytes(batch, block, vocab);
+}
+
+domino_status domino_verify_sample(int32_t batch, int32_t block, int32_t vocab, const int32_t *node_token,
+                                   const void *target_logits, domino_dtype logits_dtype, const float *draft_logits,
+                                   float temperature, uint64_t seed, int32_t *accept_len, int32_t *accepted_nodes,
+                                   int32_t *out_tokens, void *workspace, size_t workspace_bytes, void *stream) {
+  if (batch < 1) return fail(DOMINO_ERR_INVALID_ARG, "batch must be >= 1");
+  if (block < 2 || block > 64) return fail(DOMINO_ERR_INVALID_ARG, "block must be in [2, 64]");
+  if (vocab < 1) return fail(DOMINO_ERR_INVALID_ARG, "vocab must be >= 1");
+  if (logits_dtype != DOMINO_F32 && logits_dtype != DOMINO_BF16) return fail(DOMINO_ERR_INVALID_ARG, "bad logits dtype");
+  if (!(temperature > 0.f) || !std::isfinite(temperature) || 1.0f / temperature > 1e30f)
+    return fail(DOMINO_ERR_INVALID_ARG, "temperature must be positive and finite");
+  if (!node_token || !target_logits || !draft_logits || !accept_len || !accepted_nodes || !out_tokens)
+    return fail(DOMINO_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (!workspace) return fail(DOMINO_ERR_WORKSPACE, "workspace is NULL");
+  const size_t need = vs_ws_bytes(batch, block, vocab);
+  if (workspace_bytes < need) return fail(DOMINO_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  hipStream_t st = (hipStream_t)stream;
+  launch_fill_u32((uint32_t *)workspace, 1, 0u, st);
+  launch_verify_sample(batch, block, vocab, node_token, target_logits, logits_dtype == DOMINO_BF16, draft_logits,
+                       temperature, seed, accept_len, accepted_nodes, out_tokens, workspace, st);
+  hipError_t he = hipGetLastError();
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "verify_sample launch: %s", hipGetErrorString(he));
+  return DOMINO_OK;
+}
+
+domino_status domino_philox4x32_10(const uint32_t *counters, uint64_t key, uint32_t *out, int32_t n, void *stream) {
+  if (n < 0) return fail(DOMINO_ERR_INVALID_ARG, "n must be >= 0");
+  if (n > 0 && (!counters || !out)) return fail(DOMINO_ERR_INVALID_ARG, "counters/out is NULL");
+  launch_philox_words(counters, key, out, n, (hipStream_t)stream);
+  hipError_t he = hipGetLastError();
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "philox launch: %s", hipGetErrorString(he));
   return DOMINO_OK;
 }
 

@@ -57,6 +57,19 @@ DEVI bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
+// 64-bit key whose unsigned order is the selection order: the float mapped
+// to an order-preserving unsigned value (NaN as -inf) in the high half, the
+// complement of the id in the low half (smaller id wins a tie).
+DEVI unsigned long long encode_best(float v, int id) {
+  uint32_t u = __float_as_uint(order_val(v));
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((unsigned long long)u << 32) | (unsigned long long)(0xffffffffu - (uint32_t)id);
+}
+DEVI int decode_best_id(unsigned long long key, int V) {
+  const int id = (int)(0xffffffffu - (uint32_t)(key & 0xffffffffu));
+  return id < 0 ? 0 : (id >= V ? V - 1 : id);  // an unset key never reaches here
+}
+
 // Reduce a (value, id) pair to the wave's best under the selection order.
 DEVI void wave_best(float &v, int &i) {
 #pragma unroll

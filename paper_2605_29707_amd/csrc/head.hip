@@ -21,6 +21,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "mfma.h"
+#include "philox.h"
 
 namespace dk {
 
@@ -137,19 +138,6 @@ DEVI void wave_select_mem(const float *__restrict__ pv, const int32_t *__restric
 DEVI float sigm(float x) { return 1.f / (1.f + expf(-x)); }
 
 constexpr int kBestSlots = 8;  // atomic targets per (position, row), spread to cut contention
-
-// 64-bit key whose unsigned order is the selection order: the float mapped
-// to an order-preserving unsigned value (NaN as -inf) in the high half, the
-// complement of the id in the low half (smaller id wins a tie).
-DEVI unsigned long long encode_best(float v, int id) {
-  uint32_t u = __float_as_uint(order_val(v));
-  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return ((unsigned long long)u << 32) | (unsigned long long)(0xffffffffu - (uint32_t)id);
-}
-DEVI int decode_best_id(unsigned long long key, int V) {
-  const int id = (int)(0xffffffffu - (uint32_t)(key & 0xffffffffu));
-  return id < 0 ? 0 : (id >= V ? V - 1 : id);  // an unset key never reaches here
-}
 
 template <typename WT>
 DEVI void unpack16(const u32x4 &w, float *f);
@@ -560,15 +548,19 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
   if (beta == 1) {
     // top-1 without staging: a running best per batch row in registers, the
     // four lanes of a row combined by shuffles, then one entry per (wave, row)
-    __shared__ float best_v[kLogitWaves][64];
+    // With sampling the key is L / T + Gumbel noise of (row, position, id): the
+    // maximum is a draw from softmax(L / T); raw carries the chosen L.
+    __shared__ float best_v[kLogitWaves][64], best_r[kLogitWaves][64];
     __shared__ int best_i[kLogitWaves][64];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int bb = mt * 16 + cc;
-      float bv = -INFINITY;
+      float bv = -INFINITY, br = 0.f;
       int bi = INT_MAX;
 #pragma unroll
-      for (int q = 0; q < kTPW; ++q)
+      for (int q = 0; q < kTPW; ++q) {
+        Philox4 noise = {{0u, 0u, 0u, 0u}};
+        if (h.sample && bb < bs) noise = rng_block(h.seed_lo, h.seed_hi, RNG_DRAFT, bb, j, tiles[q] * 4 + g);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int n = tiles[q] * 16 + 4 * g + e;
@@ -576,40 +568,48 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
           const float val = lbe + acc[q][mt][e];
           if (bb < bs && n < V) {
             if (h.final_logits) h.final_logits[((size_t)bb * depth + (j - 1)) * V + n] = val;
-            const float ov = order_val(val);
+            const float key = h.sample ? val * h.inv_temp + rng_gumbel(noise.x[e]) : val;
+            const float ov = order_val(key);
             if (better(ov, n, bv, bi)) {
               bv = ov;
               bi = n;
+              br = val;
             }
           }
         }
+      }
 #pragma unroll
       for (int o = 16; o <= 32; o <<= 1) {
         const float ov = __shfl_xor(bv, o, 64);
         const int oi = __shfl_xor(bi, o, 64);
+        const float orw = __shfl_xor(br, o, 64);
         if (better(ov, oi, bv, bi)) {
           bv = ov;
           bi = oi;
+          br = orw;
         }
       }
       if (g == 0) {
         best_v[wave][bb] = bv;
         best_i[wave][bb] = bi;
+        best_r[wave][bb] = br;
       }
     }
     __syncthreads();
     for (int bb = tid; bb < bs; bb += kLogitWaves * 64) {
-      float v = best_v[0][bb];
+      float v = best_v[0][bb], raw = best_r[0][bb];
       int id = best_i[0][bb];
 #pragma unroll
       for (int w = 1; w < kLogitWaves; ++w)
         if (better(best_v[w][bb], best_i[w][bb], v, id)) {
           v = best_v[w][bb];
           id = best_i[w][bb];
+          raw = best_r[w][bb];
         }
       const size_t o = ((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x;
       h.pval[o] = v;
       h.pid[o] = id;
+      if (h.sample) h.praw[o] = raw;
       if (id != INT_MAX)
         atomicMax(&h.best[((size_t)(j - 1) * bs + bb) * kBestSlots + (blockIdx.x % kBestSlots)], encode_best(v, id));
     }
@@ -681,6 +681,36 @@ __global__ __launch_bounds__(64) void head_merge_kernel(HeadArgs h) {
   const int bs = h.D.bs, depth = h.D.B - 1, beta = h.beta;
   const int lane = threadIdx.x;
   const size_t base = ((size_t)j * bs + b) * h.GC * beta;
+  if (h.sample) {  // branch 1: the largest key wins; its raw logit is the reported value
+    float bv = -INFINITY, br = 0.f;
+    int bi = INT_MAX;
+    for (int c = lane; c < h.GC; c += 64) {
+      const float v = order_val(h.pval[base + c]);
+      const int id = h.pid[base + c];
+      const float raw = h.praw[base + c];
+      if (id != INT_MAX && better(v, id, bv, bi)) {
+        bv = v;
+        bi = id;
+        br = raw;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      const float orw = __shfl_xor(br, o, 64);
+      if (better(ov, oi, bv, bi)) {
+        bv = ov;
+        bi = oi;
+        br = orw;
+      }
+    }
+    if (lane == 0) {
+      h.topk_ids[(size_t)b * depth + j] = bi;
+      h.topk_vals[(size_t)b * depth + j] = br;
+    }
+    return;
+  }
   float mv;
   int mi;
   wave_select_mem(h.pval + base, h.pid + base, h.GC * beta, beta, mv, mi);

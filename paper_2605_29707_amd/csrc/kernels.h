@@ -94,6 +94,13 @@ struct HeadArgs {
   float *pval;           // [B-1][bs][GC][beta] per-workgroup top-beta lists
   int32_t *pid;
   unsigned long long *best;  // [B-1][bs][8] best (value, id) keys per position, zeroed per step
+  // temperature sampling (branch 1): the selection key is L / T + Gumbel noise
+  // (Philox stream RNG_DRAFT); praw [B-1][bs][GC] keeps each workgroup's chosen
+  // token's raw final logit for topk_vals
+  int sample;
+  float inv_temp;
+  uint32_t seed_lo, seed_hi;
+  float *praw;
   int32_t *err;
   int GC;                // workgroups of the logits kernel
 };
@@ -109,6 +116,13 @@ size_t accept_ws_bytes(int bs, int nn, int V);
 void launch_accept(int bs, int nn, int V, int B, const int32_t *tok, const int32_t *par,
                    const void *logits, bool bf16, int32_t *acc_len, int32_t *acc_nodes,
                    int32_t *out_tok, void *ws, hipStream_t st);
+
+// ---- temperature sampling: speculative-sampling verification (sample.hip)
+size_t vs_ws_bytes(int bs, int B, int V);
+void launch_verify_sample(int bs, int B, int V, const int32_t *node_token, const void *target, bool bf16,
+                          const float *draft, float temperature, uint64_t seed, int32_t *accept_len,
+                          int32_t *accepted_nodes, int32_t *out_tokens, void *ws, hipStream_t st);
+void launch_philox_words(const uint32_t *ctr, uint64_t key, uint32_t *out, int n, hipStream_t st);
 
 // misc
 void launch_to_f32(const void *src, bool bf16, float *dst, size_t n, hipStream_t st);

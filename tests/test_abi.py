@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def header_functions():
     src = open(os.path.join(ROOT, "include", "domino.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(domino_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(domino_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_library_exports_every_declared_function():
@@ -93,3 +93,34 @@ def test_tree_and_accept_validation():
         bd.DOMINO_ERR_INVALID_ARG
     assert lib.domino_workspace_error(None, None, None) == bd.DOMINO_ERR_INVALID_ARG
     assert lib.domino_profile_enable(None, 1) == bd.DOMINO_ERR_INVALID_ARG
+
+
+def test_sampling_entry_points_validation():
+    lib = bd.load()
+    p = C.c_void_p(16)  # never dereferenced: validation fails first
+    # sampled drafting: model, temperature and the required final_logits are checked first
+    st = lib.domino_draft_step_sampled(None, 1, p, p, p, p, 16, None, 0, 1.0, 7, None, p, p, p, None, p, 10**9,
+                                       None)
+    assert st == bd.DOMINO_ERR_INVALID_ARG
+    for t in (0.0, -1.0, float("inf"), float("nan")):
+        st = lib.domino_draft_step_sampled(None, 1, p, p, p, p, 16, None, 0, t, 7, None, p, p, p, None, p, 10**9,
+                                           None)
+        assert st == bd.DOMINO_ERR_INVALID_ARG and "temperature" in bd.last_error()
+    st = lib.domino_draft_step_sampled(None, 1, p, p, p, p, 16, None, 0, 1.0, 7, None, p, p, None, None, p,
+                                       10**9, None)
+    assert st == bd.DOMINO_ERR_INVALID_ARG and "final_logits" in bd.last_error()
+    # sampled verification
+    assert lib.domino_verify_sample_workspace_bytes(1, 1, 100) == 0
+    assert lib.domino_verify_sample_workspace_bytes(1, 16, 0) == 0
+    assert lib.domino_verify_sample_workspace_bytes(2, 16, 151936) > 0
+    ok = (1, 16, 100, p, p, bd.DOMINO_BF16, p)
+    assert lib.domino_verify_sample(*ok, 0.0, 1, p, p, p, p, 10**9, None) == bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_verify_sample(1, 1, 100, p, p, bd.DOMINO_F32, p, 1.0, 1, p, p, p, p, 10**9, None) == \
+        bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_verify_sample(1, 16, 100, p, p, 9, p, 1.0, 1, p, p, p, p, 10**9, None) == \
+        bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_verify_sample(*ok, 1.0, 1, p, p, None, p, 10**9, None) == bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_verify_sample(*ok, 1.0, 1, p, p, p, None, 10**9, None) == bd.DOMINO_ERR_WORKSPACE
+    assert lib.domino_verify_sample(*ok, 1.0, 1, p, p, p, p, 8, None) == bd.DOMINO_ERR_WORKSPACE
+    assert lib.domino_philox4x32_10(None, 0, None, 4, None) == bd.DOMINO_ERR_INVALID_ARG
+    assert lib.domino_philox4x32_10(None, 0, None, -1, None) == bd.DOMINO_ERR_INVALID_ARG

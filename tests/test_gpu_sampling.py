@@ -1,0 +1,190 @@
+"""GPU parity of temperature sampling (drafting and speculative-sampling
+verification) through the C-ABI, against the sampling oracle.
+
+Random draws are Philox-4x32-10 words on both sides (each side implements the
+generator from its published definition), so the GPU and the oracle draw the
+same noise; the sampled token and the accept/reject decisions are then
+decisions on floating-point values that differ by rounding (fp32 on the GPU,
+fp64 in the oracle).  They must agree wherever the oracle's decision is not
+within rounding of flipping: the drawn token where the oracle's two best keys
+are at least 1e-3 apart, each accept decision where |u - p/q| >= 1e-4, the
+bonus token where its two best keys are at least 0.05 apart (the residual
+max(0, p - q) loses relative accuracy where p and q nearly cancel).  Logits
+keep the drafting tolerances (1e-4 fp32, 2e-2 bf16).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_helpers import GpuRun, log
+
+so = oracle.sampling_oracle
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2605_29707_amd import binding as bd  # noqa: E402
+
+DEV = torch.device("cuda:0")
+GAP_DRAFT, MARGIN_ACCEPT, GAP_BONUS = 1e-3, 1e-4, 0.05
+
+
+def _t(a, dt=None):
+    t = torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    return t if dt is None else t.to(dt)
+
+
+def test_philox_device_matches_known_answers_and_oracle():
+    import json
+    import os
+    kat = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "philox4x32_10_kat.json")))
+    for v in kat["vectors"]:
+        ctr = _t(np.array([[int(x, 16) for x in v["counter"]]], np.uint32).view(np.int32))
+        k0, k1 = (int(x, 16) for x in v["key"])
+        out = torch.empty(1, 4, dtype=torch.int32, device=DEV)
+        bd.domino_philox4x32_10(ctr, k0 | (k1 << 32), out)
+        torch.cuda.synchronize()
+        assert [int(x) for x in out.cpu().numpy().view(np.uint32)[0]] == [int(x, 16) for x in v["out"]]
+    rng = np.random.default_rng(0)
+    ctr = rng.integers(0, 2**32, size=(4096, 4), dtype=np.uint64).astype(np.uint32)
+    key = int(rng.integers(0, 2**63))
+    out = torch.empty(4096, 4, dtype=torch.int32, device=DEV)
+    bd.domino_philox4x32_10(_t(ctr.view(np.int32)), key, out)
+    torch.cuda.synchronize()
+    want = so.philox4x32_10(ctr, so.seed_key(key))
+    np.testing.assert_array_equal(out.cpu().numpy().view(np.uint32), want)
+
+
+def _sampled_step(run, inp, T, seed, forced=None):
+    cfg = run.cfg
+    bs, D, V = cfg.batch, cfg.depth, cfg.vocab
+    final = torch.empty(bs, D, V, dtype=torch.float32, device=DEV)
+    states = torch.empty(bs, D, cfg.gru_hidden, dtype=torch.float32, device=DEV)
+    kvdt = run.kv_dtype()
+    bd.domino_draft_step_sampled(run.model, _t(inp["anchor"], torch.int32), _t(inp["ctx_lens"], torch.int32),
+                                 _t(inp["ctx_k"], kvdt), _t(inp["ctx_v"], kvdt), inp["max_ctx"], run.ids, run.vals,
+                                 final, run.ws, T, seed, forced=None if forced is None else _t(forced, torch.int32),
+                                 debug={"states": states})
+    torch.cuda.synchronize()
+    return {"topk_ids": run.ids.cpu().numpy().copy(), "topk_vals": run.vals.cpu().numpy().copy(),
+            "final_logits": final.cpu().numpy(), "states": states.cpu().numpy(),
+            "err": bd.domino_workspace_error(run.ws)}
+
+
+def _check_sampled(cfg, gpu, inp, w64, T, seed, tol):
+    drafted = gpu["topk_ids"][:, :, 0]
+    ref = oracle.draft_step(cfg, w64, inp["anchor"], inp["ctx_lens"], inp["ctx_k"], inp["ctx_v"], 1,
+                            forced=drafted, sampling=(T, seed))
+    err = float(np.abs(gpu["final_logits"] - ref["final_logits"]).max())
+    serr = float(np.abs(gpu["states"] - ref["states"]).max())
+    log(f"T={T}: max |gpu - oracle| final_logits={err:.2e} states={serr:.2e}")
+    assert err < tol and serr < tol
+    # the reported value is the drawn token's final logit
+    np.testing.assert_allclose(gpu["topk_vals"][:, :, 0], np.take_along_axis(
+        ref["final_logits"], drafted[:, :, None].astype(np.int64), axis=2)[:, :, 0], atol=tol, rtol=0)
+    mask = ref["sample_gap"] >= GAP_DRAFT
+    assert np.array_equal(drafted[mask], ref["topk_ids"][:, :, 0][mask])
+    log(f"drawn tokens compared: {int(mask.sum())} of {mask.size}")
+    return int(mask.sum()), mask.size
+
+
+@pytest.mark.parametrize("dtype,batch,T", [("f32", 3, 1.0), ("f32", 1, 0.6), ("bf16", 5, 1.0), ("bf16", 12, 1.3)])
+def test_sampled_drafting_tiny(dtype, batch, T):
+    cfg = synth.get_config("tiny").with_(dtype=dtype, batch=batch, branch=1, ctx_from_hidden=False)
+    w = synth.make_weights(cfg, seed=21, gain_std=0.1)
+    inp = synth.make_inputs(cfg, seed=21)
+    run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
+    seed = 0x1234_5678_9ABC + batch
+    gpu = _sampled_step(run, inp, T, seed)
+    assert gpu["err"] == 0
+    again = _sampled_step(run, inp, T, seed)                 # a draw is a pure function of the seed
+    np.testing.assert_array_equal(again["topk_ids"], gpu["topk_ids"])
+    other = _sampled_step(run, inp, T, seed + 1)
+    assert not np.array_equal(other["topk_ids"], gpu["topk_ids"])
+    run.close()
+    n, tot = _check_sampled(cfg, gpu, inp, oracle.as_f64_weights(w), T, seed, 1e-4 if dtype == "f32" else 2e-2)
+    assert n >= 0.9 * tot
+
+
+def test_sampled_drafting_qwen3_8b_full_size():
+    cfg = synth.get_config("qwen3_8b")
+    w = synth.make_weights(cfg, seed=0)
+    inp = synth.make_inputs(cfg, seed=0)
+    run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
+    gpu = _sampled_step(run, inp, 1.0, seed=42)
+    assert gpu["err"] == 0
+    run.close()
+    del run
+    torch.cuda.empty_cache()
+    n, tot = _check_sampled(cfg, gpu, inp, oracle.as_f64_weights(w, keep=("embed",)), 1.0, 42, 2e-2)
+    assert n >= 12
+
+
+def _verify_gpu(tok, target, draft, T, seed):
+    bs, B, V = target.shape
+    acc = torch.empty(bs, dtype=torch.int32, device=DEV)
+    nodes = torch.empty(bs, B - 1, dtype=torch.int32, device=DEV)
+    out = torch.empty(bs, B, dtype=torch.int32, device=DEV)
+    ws = torch.empty(bd.domino_verify_sample_workspace_bytes(bs, B, V), dtype=torch.uint8, device=DEV)
+    bd.domino_verify_sample(_t(tok), target, _t(draft), T, seed, acc, nodes, out, ws)
+    torch.cuda.synchronize()
+    assert bd.domino_workspace_error(ws) == 0
+    return {"accept_len": acc.cpu().numpy(), "accepted_nodes": nodes.cpu().numpy(), "out_tokens": out.cpu().numpy()}
+
+
+def _compare_verify(got, ref):
+    """Rows whose every decision is clear of rounding must agree exactly."""
+    bs = got["accept_len"].shape[0]
+    clear = np.array([min(ref["accept_margins"][b], default=1.0) >= MARGIN_ACCEPT and ref["bonus_gap"][b] >= GAP_BONUS
+                      for b in range(bs)])
+    for k in ("accept_len", "accepted_nodes", "out_tokens"):
+        np.testing.assert_array_equal(got[k][clear], ref[k][clear], err_msg=k)
+    return int(clear.sum())
+
+
+@pytest.mark.parametrize("V,dtype,T,spread", [(151936, "bf16", 1.0, 0.5), (50000, "f32", 1.0, 1.5),
+                                              (4096, "f32", 0.7, 0.2), (151936, "bf16", 1.0, 0.0)])
+def test_verify_sample_bit_exact_where_clear(V, dtype, T, spread):
+    bs, B = 24, 16
+    rng = np.random.default_rng(V + int(10 * spread))
+    draft = (rng.normal(size=(bs, B - 1, V)) * 2.0).astype(np.float32)
+    target = np.concatenate([draft, rng.normal(size=(bs, 1, V)).astype(np.float32) * 2.0], axis=1)
+    target = target + (rng.normal(size=target.shape) * spread).astype(np.float32)   # spread 0: p == q up to rounding
+    if dtype == "bf16":
+        target = synth.bf16_round(target)
+    seed = 777 + V
+    tok = np.zeros((bs, B), np.int32)
+    tok[:, 0] = rng.integers(0, V, size=bs)
+    for b in range(bs):
+        for j in range(1, B):
+            tok[b, j], _ = so.sample_draft(draft[b, j - 1], T, seed, b, j)
+    tt = _t(target, torch.bfloat16 if dtype == "bf16" else torch.float32)
+    got = _verify_gpu(tok, tt, draft, T, seed)
+    ref = so.verify_sample(tok, target.astype(np.float64), draft, T, seed)
+    n = _compare_verify(got, ref)
+    log(f"V={V} {dtype} T={T} spread={spread}: rows compared {n}/{bs}; accept lengths {ref['accept_len'].tolist()}")
+    assert n >= bs * 3 // 4
+    assert np.all((got["accept_len"] >= 0) & (got["accept_len"] <= B - 1))
+
+
+def test_sampled_pipeline_tiny():
+    """Sampled draft -> chain -> sampled verification, against the oracle."""
+    cfg = synth.get_config("tiny").with_(batch=4, branch=1, ctx_from_hidden=False)
+    w = synth.make_weights(cfg, seed=5, gain_std=0.1)
+    inp = synth.make_inputs(cfg, seed=5)
+    run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
+    T, seed = 1.0, 99
+    gpu = _sampled_step(run, inp, T, seed)
+    run.close()
+    tree = oracle.build_tree(gpu["topk_ids"], inp["anchor"], inp["ctx_lens"])
+    rng = np.random.default_rng(5)
+    target = (gpu["final_logits"][:, :, :] + rng.normal(size=gpu["final_logits"].shape) * 0.3).astype(np.float32)
+    target = np.concatenate([target, rng.normal(size=(cfg.batch, 1, cfg.vocab)).astype(np.float32)], axis=1)
+    got = _verify_gpu(tree["node_token"], _t(target), gpu["final_logits"], T, seed)
+    ref = so.verify_sample(tree["node_token"], target.astype(np.float64), gpu["final_logits"], T, seed)
+    n = _compare_verify(got, ref)
+    log(f"pipeline rows compared {n}/{cfg.batch}; accept lengths {ref['accept_len'].tolist()}")
+    assert n >= cfg.batch - 1
