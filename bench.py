@@ -65,6 +65,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--sample-steps", type=int, default=100,
+                    help="extra steps at temperature 1: sampled drafting + tree + speculative-sampling "
+                         "verification (reported per step; 0 skips)")
     ap.add_argument("--flush-steps", type=int, default=50,
                     help="extra steps, each after a 512 MiB scratch write that evicts on-chip caches; "
                          "reported per step (the write itself is not timed)")
@@ -171,6 +174,37 @@ def main():
         taus += (acc.cpu().numpy() + 1).tolist()
     tau = float(np.mean(taus))
 
+    sampled = None
+    if args.sample_steps > 0 and beta == 1:
+        final = torch.empty(bs, D, V, dtype=torch.float32, device=dev)
+        sws = torch.empty(bd.domino_verify_sample_workspace_bytes(bs, cfg.block, V), dtype=torch.uint8, device=dev)
+
+        def step_sampled(i):
+            bd.domino_draft_step_sampled(model, anchor, lens, ck, cv, max_ctx, ids, vals, final, ws, 1.0,
+                                         seed=1000 + i, ctx_hidden_new=hid, n_new=n_new, stream=stream)
+            bd.domino_build_tree(ids, anchor, lens, tok, par, dep, pos, stream=stream)
+            bd.domino_verify_sample(tok, targets[i % len(targets)], final, 1.0, 1000 + i, acc, nodes, out, sws,
+                                    stream=stream)
+
+        for i in range(5):
+            step_sampled(i)
+        se = [torch.cuda.Event(enable_timing=True) for _ in range(args.sample_steps + 1)]
+        stau = torch.zeros(args.sample_steps, bs, dtype=torch.int32, device=dev)
+        torch.cuda.synchronize()
+        se[0].record(stream)
+        for i in range(args.sample_steps):
+            step_sampled(i)
+            se[i + 1].record(stream)
+            stau[i].copy_(acc)
+        torch.cuda.synchronize()
+        assert bd.domino_workspace_error(ws) == 0 and bd.domino_workspace_error(sws) == 0
+        sper = [se[i].elapsed_time(se[i + 1]) for i in range(args.sample_steps)]
+        sampled = {"temperature": 1.0, "steps": args.sample_steps,
+                   "ms_per_step": round(se[0].elapsed_time(se[-1]) / args.sample_steps, 4),
+                   "us_per_step_median": round(statistics.median(sper) * 1e3, 1),
+                   "mean_tau_synthetic": round(float(stau.float().mean().item()) + 1.0, 3)}
+        del final, sws
+
     flushed = None
     if args.flush_steps > 0:
         scratch = torch.empty(512 * (1 << 20) // 4, dtype=torch.float32, device=dev)
@@ -244,6 +278,8 @@ def main():
                      "launch_us": round(dom_launch_s * 1e6, 2), "launches": dom_n,
                      "algorithmic_bytes_per_launch": dom_bytes},
     }
+    if sampled:
+        res["sampling_t1"] = sampled
     if flushed:
         res["after_cache_flush"] = flushed
     if breakdown:
