@@ -68,6 +68,9 @@ def main():
     ap.add_argument("--sample-steps", type=int, default=100,
                     help="extra steps at temperature 1: sampled drafting + tree + speculative-sampling "
                          "verification (reported per step; 0 skips)")
+    ap.add_argument("--append-rows", type=int, default=4,
+                    help="extra pass whose steps first append this many target hidden states to the context "
+                         "KV cache of every layer (about tau of the previous cycle; 0 skips)")
     ap.add_argument("--flush-steps", type=int, default=50,
                     help="extra steps, each after a 512 MiB scratch write that evicts on-chip caches; "
                          "reported per step (the write itself is not timed)")
@@ -225,6 +228,33 @@ def main():
         del scratch
         torch.cuda.empty_cache()
 
+    appended = None
+    if args.append_rows > 0 and hid is None:
+        na = args.append_rows
+        ah = T(synth.make_append_hidden(cfg, na, seed=args.seed))
+        aws = torch.empty(model.workspace_bytes(bs, max_ctx, na, beta), dtype=torch.uint8, device=dev)
+
+        def step_append():
+            bd.domino_draft_step(model, anchor, lens, ck, cv, max_ctx, ids, vals, aws, branch=beta,
+                                 ctx_hidden_new=ah, n_new=na, stream=stream)
+            bd.domino_build_tree(ids, anchor, lens, tok, par, dep, pos, stream=stream)
+            bd.domino_verify_accept(tok, par, targets[0], cfg.block, acc, nodes, out, vws, stream=stream)
+
+        for _ in range(5):
+            step_append()
+        ae = [torch.cuda.Event(enable_timing=True) for _ in range(51)]
+        torch.cuda.synchronize()
+        ae[0].record(stream)
+        for i in range(50):
+            step_append()
+            ae[i + 1].record(stream)
+        torch.cuda.synchronize()
+        assert bd.domino_workspace_error(aws) == 0
+        aper = [ae[i].elapsed_time(ae[i + 1]) for i in range(50)]
+        appended = {"rows": na, "steps": 50, "ms_per_step": round(ae[0].elapsed_time(ae[-1]) / 50, 4),
+                    "us_per_step_median": round(statistics.median(aper) * 1e3, 1)}
+        del aws
+
     breakdown = None
     if args.breakdown:
         classes = [c for c in bd.KERNEL_CLASSES]
@@ -282,6 +312,8 @@ def main():
         res["sampling_t1"] = sampled
     if flushed:
         res["after_cache_flush"] = flushed
+    if appended:
+        res["with_context_append"] = appended
     if breakdown:
         res["breakdown_us_per_step"] = breakdown
 

@@ -13,6 +13,7 @@ from .inputs import (  # noqa: F401
     make_target_logits,
     make_random_topk,
     make_forced_tokens,
+    make_append_hidden,
     weight_shapes,
     head_param_count,
 )

@@ -35,7 +35,7 @@ _LAYER_BASE = 100
 _LAYER_KEYS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down",
                "attn_norm", "ffn_norm", "q_norm", "k_norm")
 _T_ANCHOR, _T_CTX_K, _T_CTX_V, _T_CTX_H, _T_CTX_IDS, _T_TARGET = 1000, 1001, 1002, 1003, 1004, 1005
-_T_TOPK, _T_FORCED, _T_CTXLEN = 1006, 1007, 1008
+_T_TOPK, _T_FORCED, _T_CTXLEN, _T_APPEND_H = 1006, 1007, 1008, 1009
 
 
 def _threads() -> int:
@@ -178,6 +178,12 @@ def make_inputs(cfg: DominoConfig, seed: int = 0, ctx_lens=None, max_ctx: int | 
         out["ctx_v"] = _normal(seed, _T_CTX_V, shape, 1.0, bf)
         out["ctx_hidden"] = None
     return out
+
+
+def make_append_hidden(cfg: DominoConfig, n_new: int, seed: int = 0) -> np.ndarray:
+    """Target hidden states of the tokens accepted last cycle, [bs, n_new, d] N(0, 1)
+    (storage-type values), to be appended to a KV-cache context."""
+    return _normal(seed, _T_APPEND_H, (cfg.batch, n_new, cfg.hidden), 1.0, cfg.dtype == "bf16")
 
 
 def make_forced_tokens(cfg: DominoConfig, seed: int = 0) -> np.ndarray:

@@ -66,6 +66,7 @@ class GpuRun:
         if debug:
             out.update({k: v.cpu().numpy() for k, v in dbg.items()})
         out["ctx_k"] = ck.float().cpu().numpy()
+        out["ctx_v"] = cv.float().cpu().numpy()
         return out
 
     def close(self):

@@ -98,3 +98,39 @@ def test_full_size_sampled_rows(name, rows):
     n = check_against_oracle(cfg, sub, ref, 2e-2, beta)
     log(f"top-beta entries checked: {n}")
     assert n >= len(rows) * 10
+
+
+def test_context_append_qwen3_8b():
+    """Context-KV append at full size: the hidden states of tau = 4 accepted
+    tokens are projected by every layer's W_k (k-norm, RoPE) and W_v into a bf16
+    cache of 1024 positions, then the block is drafted over the updated cache."""
+    cfg = synth.get_config("qwen3_8b")
+    n_new = 4
+    w = synth.make_weights(cfg, seed=0)
+    inp = synth.make_inputs(cfg, seed=0)
+    inp["ctx_hidden"] = synth.make_append_hidden(cfg, n_new, seed=0)
+    run = GpuRun(cfg, w, inp["max_ctx"], beta=1, n_new=n_new)
+    gpu = run.step(inp, debug=True)
+    assert gpu["err"] == 0
+    run.close()
+    del run
+    torch.cuda.empty_cache()
+    w64 = oracle.as_f64_weights(w, keep=("embed",))
+    del w
+    n = int(inp["ctx_lens"][0])
+    pos = np.arange(n - n_new, n, dtype=np.float64)
+    worst = 0.0
+    for l, lw in enumerate(w64["layers"]):
+        k, v = oracle.project_context_kv(cfg, lw, inp["ctx_hidden"][0], pos)
+        for got, want in ((gpu["ctx_k"][l, 0, n - n_new:n], k), (gpu["ctx_v"][l, 0, n - n_new:n], v)):
+            # stored in bf16: round-to-nearest error at most 2^-9 relative, plus the fp32 arithmetic
+            assert np.all(np.abs(got - want) <= np.abs(want) * 2.0 ** -8 + 1e-4)
+            worst = max(worst, float(np.max(np.abs(got - want) / (np.abs(want) + 1e-3))))
+        # rows before the append are untouched
+        np.testing.assert_array_equal(gpu["ctx_k"][l, 0, :n - n_new], inp["ctx_k"][l, 0, :n - n_new])
+        np.testing.assert_array_equal(gpu["ctx_v"][l, 0, :n - n_new], inp["ctx_v"][l, 0, :n - n_new])
+    log(f"appended K/V rows within bf16 rounding (worst relative {worst:.2e})")
+    ref = oracle.draft_step(cfg, w64, inp["anchor"], inp["ctx_lens"], gpu["ctx_k"], gpu["ctx_v"], 1,
+                            forced=gpu["topk_ids"][:, :, 0])
+    checked = check_against_oracle(cfg, gpu, ref, 2e-2, 1)
+    assert checked >= 12
