@@ -269,7 +269,10 @@ domino_status domino_workspace_clear_error(void *workspace, void *stream);
  * Per-kernel-class timing for benchmarks: while enabled for a class, the
  * draft step brackets that class's launches with HIP events on its stream.
  * domino_profile_read synchronises and returns the summed milliseconds and
- * the number of launches timed since the last reset.
+ * the number of launches timed since the last reset.  Classes that currently
+ * have no launches of their own (EMBED: the embedding gather is part of the
+ * first NORM launch; W1H: W1's H half shares the LMHEAD launch; CTXPROJ: the
+ * appended context rows ride in the QKV launches) read back zero launches.
  */
 enum {
   DOMINO_KC_EMBED = 0, DOMINO_KC_NORM, DOMINO_KC_QKV, DOMINO_KC_ROPE, DOMINO_KC_ATTN,

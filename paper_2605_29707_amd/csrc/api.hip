@@ -124,12 +124,12 @@ Dims make_dims(const domino_model *m, int bs) {
 // ---- workspace layout of the draft step
 struct WsLayout {
   size_t err, best, hdr_words, X, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
-      praw, ctxkv, total;
+      praw, total;
   int GC, ldl;
 };
 
 struct Plans {
-  GemmPlan qkv, wo, gateup, down, lm, ctx;
+  GemmPlan qkv, wo, gateup, down, lm;
 };
 
 constexpr int kMaxSplit = 16;
@@ -139,13 +139,12 @@ Plans make_plans(const domino_model *m, int bs, int max_new) {
   const int M = bs * D.B, Mh = bs * (D.B - 1);
   Plans p;
   // projections whose consumer is elementwise write K-split partial outputs
-  p.qkv = plan_gemm(m->qkv[0].NT, m->qkv[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
+  // QKV also projects the appended context rows (rows M .. M + bs*max_new - 1)
+  p.qkv = plan_gemm(m->qkv[0].NT, m->qkv[0].KS, M + bs * max_new, EPI_STORE, m->n_cu, kMaxSplit);
   p.wo = plan_gemm(m->wo[0].NT, m->wo[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
   p.gateup = plan_gemm(m->gateup[0].NT, m->gateup[0].KS, M, EPI_SWIGLU, m->n_cu, 1);
   p.down = plan_gemm(m->down[0].NT, m->down[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
   p.lm = plan_gemm(m->lm.NT, m->lm.KS, Mh, EPI_STORE, m->n_cu, 1);
-  const int kvt = 2 * D.nkv * D.dh / 16;
-  p.ctx = plan_gemm(kvt, m->qkv[0].KS, bs * (max_new > 0 ? max_new : 1), EPI_STORE, m->n_cu, 1);
   return p;
 }
 
@@ -165,8 +164,9 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.hdr_words = o / 4;  // error word and best keys: cleared at every step
   const int qkvw = (D.nq + 2 * D.nkv) * D.dh;
   w.X = take((size_t)M * D.d * 4);
-  w.A = take((size_t)M * D.d * 4);
-  w.QKV = take((size_t)p.qkv.ksplit * M * qkvw * 4);
+  const int Ma = M + bs * max_new;  // block rows, then the appended context rows
+  w.A = take((size_t)Ma * D.d * 4);
+  w.QKV = take((size_t)p.qkv.ksplit * Ma * qkvw * 4);
   w.Q = take((size_t)M * D.nq * D.dh * 4);
   w.Kb = take((size_t)M * D.nkv * D.dh * 4);
   w.Vb = take((size_t)M * D.nkv * D.dh * 4);
@@ -184,7 +184,6 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.pval = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
   w.pid = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
   w.praw = take((size_t)(D.B - 1) * bs * w.GC * 4);
-  w.ctxkv = take((size_t)bs * (max_new > 0 ? max_new : 0) * 2 * D.nkv * D.dh * 4);
   w.total = o;
   return true;
 }
@@ -453,17 +452,14 @@ domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *an
   // clear the error word and the rollout's best keys
   launch_fill_u32((uint32_t *)ws, w.hdr_words, 0u, st);
 
-  // context rows projected from target hidden states (optional)
+  // appended context rows (target hidden states) ride along in the QKV
+  // projection: they sit after the block rows of its input, and the RMSNorms
+  // only ever rewrite the block rows
+  const int Ma = M + batch * n_new;
   if (n_new > 0) {
-    for (int l = 0; l < m->cfg.n_layers; ++l) {
-      prof_begin(m, DOMINO_KC_CTXPROJ, st);
-      GemmArgs a = gemm_args(base + m->qkv[l].off, m->qkv[l], qd / 16, 2 * kvd / 16, 2 * kvd,
-                             (const float *)ctx_hidden_new, D.d, batch * n_new, D.d, F(w.ctxkv), 2 * kvd, p.ctx);
-      launch_gemm(m->bf16, EPI_STORE, a, p.ctx, st);
-      launch_ctx_store(D, F(w.ctxkv), n_new, m->k_norm[l], ctx_lens, max_ctx,
-                       (char *)ctx_k + l * layer_elems * m->esz, (char *)ctx_v + l * layer_elems * m->esz, err, st);
-      prof_end(m, DOMINO_KC_CTXPROJ, st);
-    }
+    hipError_t ce = hipMemcpyAsync(F(w.A) + (size_t)M * D.d, ctx_hidden_new, (size_t)batch * n_new * D.d * 4,
+                                   hipMemcpyDeviceToDevice, st);
+    if (ce != hipSuccess) return fail(DOMINO_ERR_HIP, "staging ctx_hidden_new: %s", hipGetErrorString(ce));
   }
 
   const size_t rstride = (size_t)M * D.d;  // partial-output stride of the residual projections
@@ -478,14 +474,14 @@ domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *an
     prof_end(m, DOMINO_KC_NORM, st);
 
     prof_begin(m, DOMINO_KC_QKV, st);
-    GemmArgs a = gemm_args(base + m->qkv[l].off, m->qkv[l], 0, m->qkv[l].NT, qkvw, F(w.A), D.d, M, D.d, F(w.QKV),
+    GemmArgs a = gemm_args(base + m->qkv[l].off, m->qkv[l], 0, m->qkv[l].NT, qkvw, F(w.A), D.d, Ma, D.d, F(w.QKV),
                            qkvw, p.qkv);
     launch_gemm(m->bf16, EPI_STORE, a, p.qkv, st);
     prof_end(m, DOMINO_KC_QKV, st);
 
     prof_begin(m, DOMINO_KC_ROPE, st);
-    launch_qk_norm_rope(D, F(w.QKV), p.qkv.ksplit, (size_t)M * qkvw, m->q_norm[l], m->k_norm[l], ctx_lens, max_ctx,
-                        F(w.Q), F(w.Kb), F(w.Vb), st);
+    launch_qk_norm_rope(D, F(w.QKV), p.qkv.ksplit, (size_t)Ma * qkvw, m->q_norm[l], m->k_norm[l], ctx_lens, max_ctx,
+                        F(w.Q), F(w.Kb), F(w.Vb), n_new, (void *)ck, (void *)cv, err, st);
     prof_end(m, DOMINO_KC_ROPE, st);
 
     prof_begin(m, DOMINO_KC_ATTN, st);

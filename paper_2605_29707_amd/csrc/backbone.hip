@@ -145,6 +145,11 @@ DEVI void norm_rope_head(float (&v)[2], int dh, const WT *__restrict__ gain, flo
   }
 }
 
+// Block rows m < M: Q and K heads get their RMSNorm and RoPE (position n_b + j),
+// V heads are copied; Q, Kb, Vb are [M][heads][dh].  Rows M + b*n_new + i are
+// context rows appended from target hidden states (the same GEMM projected
+// them): their K heads get the k-norm and RoPE at position n_b - n_new + i and
+// are stored, with their V heads, into the cache in the storage type.
 template <typename WT>
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restrict__ qkv, int np,
                                                            size_t pstride, const WT *__restrict__ qn,
@@ -154,16 +159,23 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
                                                            float *__restrict__ Kb,
                                                            float *__restrict__ Vb, int M, int B, int nq,
                                                            int nkv, int dh, float eps,
-                                                           const double *__restrict__ inv_freq) {
+                                                           const double *__restrict__ inv_freq, int n_new,
+                                                           WT *__restrict__ ck, WT *__restrict__ cv,
+                                                           int32_t *err) {
   const int lane = threadIdx.x & 63;
   const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int nh = nq + 2 * nkv;
-  if (item >= M * nh) return;
-  const int m = item / nh, hh = item % nh;
-  const int b = m / B, j = m % B;
-  int n = ctx_lens[b];
-  n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
-  const int pos = n + j;
+  int m, hh;
+  if (item < M * nh) {
+    m = item / nh;
+    hh = item % nh;
+  } else {  // appended context rows: K and V heads only
+    const int a = item - M * nh;
+    const int bs = M / B;
+    if (a >= bs * n_new * 2 * nkv) return;
+    m = M + a / (2 * nkv);
+    hh = nq + a % (2 * nkv);
+  }
   const float *src = qkv + (size_t)m * nh * dh + (size_t)hh * dh;
   float v[2] = {0.f, 0.f};
   const int per = dh / 64;
@@ -179,6 +191,29 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
       if (p < np)
         for (int q = 0; q < per; ++q) v[q] += t[p][q];
   }
+  if (m >= M) {
+    const int r = m - M, b = r / n_new, i = r % n_new;
+    int n = ctx_lens[b];
+    if (n < n_new || n > max_ctx) {
+      if (lane == 0 && i == 0 && hh == nq) raise_error(err, DEV_BAD_CTX_LEN);
+      n = n < n_new ? n_new : max_ctx;
+    }
+    const int pos = n - n_new + i;
+    const size_t off = (((size_t)b * max_ctx + pos) * nkv) * dh;
+    WT *dst;
+    if (hh < nq + nkv) {
+      norm_rope_head<WT>(v, dh, kn, eps, pos, inv_freq, true, lane);
+      dst = ck + off + (size_t)(hh - nq) * dh;
+    } else {
+      dst = cv + off + (size_t)(hh - nq - nkv) * dh;
+    }
+    for (int q = 0; q < per; ++q) store_as(dst + lane + 64 * q, v[q]);
+    return;
+  }
+  const int b = m / B, j = m % B;
+  int n = ctx_lens[b];
+  n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
+  const int pos = n + j;
   float *dst;
   if (hh < nq) {
     norm_rope_head<WT>(v, dh, qn, eps, pos, inv_freq, true, lane);
@@ -190,42 +225,6 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
     dst = Vb + ((size_t)m * nkv + (hh - nq - nkv)) * dh;
   }
   for (int q = 0; q < per; ++q) dst[lane + 64 * q] = v[q];
-}
-
-// kv: [bs*n_new][2*nkv*dh] = [K heads | V heads] of the projected hidden rows.
-template <typename WT>
-__global__ __launch_bounds__(256) void ctx_store_kernel(const float *__restrict__ kv, int n_new,
-                                                        const WT *__restrict__ kn,
-                                                        const int32_t *__restrict__ ctx_lens,
-                                                        int max_ctx, WT *__restrict__ ck,
-                                                        WT *__restrict__ cv, int bs, int nkv, int dh,
-                                                        float eps, const double *__restrict__ inv_freq,
-                                                        int32_t *err) {
-  const int lane = threadIdx.x & 63;
-  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (item >= bs * n_new * 2 * nkv) return;
-  const int row = item / (2 * nkv), hh = item % (2 * nkv);
-  const int b = row / n_new, i = row % n_new;
-  int n = ctx_lens[b];
-  if (n < n_new || n > max_ctx) {
-    if (lane == 0 && i == 0 && hh == 0) raise_error(err, DEV_BAD_CTX_LEN);
-    n = n < n_new ? n_new : max_ctx;
-  }
-  const int pos = n - n_new + i;
-  if (pos < 0 || pos >= max_ctx) return;
-  const float *src = kv + (size_t)row * 2 * nkv * dh + (size_t)hh * dh;
-  float v[2] = {0.f, 0.f};
-  const int per = dh / 64;
-  for (int q = 0; q < per; ++q) v[q] = src[lane + 64 * q];
-  WT *dst;
-  const size_t off = (((size_t)b * max_ctx + pos) * nkv) * dh;
-  if (hh < nkv) {
-    norm_rope_head<WT>(v, dh, kn, eps, pos, inv_freq, true, lane);
-    dst = ck + off + (size_t)hh * dh;
-  } else {
-    dst = cv + off + (size_t)(hh - nkv) * dh;
-  }
-  for (int q = 0; q < per; ++q) store_as(dst + lane + 64 * q, v[q]);
 }
 
 // ---------------------------------------------------------------------------
@@ -524,34 +523,18 @@ void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int n
 
 void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,
                          const void *k_norm, const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb,
-                         float *Vb, hipStream_t st) {
+                         float *Vb, int n_new, void *ck, void *cv, int32_t *err, hipStream_t st) {
   const int M = D.bs * D.B;
-  const int items = M * (D.nq + 2 * D.nkv);
+  const int items = M * (D.nq + 2 * D.nkv) + D.bs * n_new * 2 * D.nkv;
   dim3 grid((items + 3) / 4);
   if (D.bf16)
     hipLaunchKernelGGL(qk_norm_rope_kernel<bf16_t>, grid, dim3(256), 0, st, qkv, np, pstride, (const bf16_t *)q_norm,
                        (const bf16_t *)k_norm, ctx_lens, max_ctx, Q, Kb, Vb, M, D.B, D.nq, D.nkv, D.dh,
-                       D.eps, D.inv_freq);
+                       D.eps, D.inv_freq, n_new, (bf16_t *)ck, (bf16_t *)cv, err);
   else
     hipLaunchKernelGGL(qk_norm_rope_kernel<float>, grid, dim3(256), 0, st, qkv, np, pstride, (const float *)q_norm,
                        (const float *)k_norm, ctx_lens, max_ctx, Q, Kb, Vb, M, D.B, D.nq, D.nkv, D.dh,
-                       D.eps, D.inv_freq);
-}
-
-void launch_ctx_store(const Dims &D, const float *kv, int n_new, const void *k_norm,
-                      const int32_t *ctx_lens, int max_ctx, void *ck, void *cv, int32_t *err,
-                      hipStream_t st) {
-  const int items = D.bs * n_new * 2 * D.nkv;
-  if (items <= 0) return;
-  dim3 grid((items + 3) / 4);
-  if (D.bf16)
-    hipLaunchKernelGGL(ctx_store_kernel<bf16_t>, grid, dim3(256), 0, st, kv, n_new, (const bf16_t *)k_norm,
-                       ctx_lens, max_ctx, (bf16_t *)ck, (bf16_t *)cv, D.bs, D.nkv, D.dh, D.eps, D.inv_freq,
-                       err);
-  else
-    hipLaunchKernelGGL(ctx_store_kernel<float>, grid, dim3(256), 0, st, kv, n_new, (const float *)k_norm,
-                       ctx_lens, max_ctx, (float *)ck, (float *)cv, D.bs, D.nkv, D.dh, D.eps, D.inv_freq,
-                       err);
+                       D.eps, D.inv_freq, n_new, (float *)ck, (float *)cv, err);
 }
 
 template <typename WT, int RPT, int CH, int DH>

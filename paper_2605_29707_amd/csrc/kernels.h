@@ -53,14 +53,12 @@ void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int n
                      const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
                      const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st);
 // q/k RMSNorm + RoPE on the QKV projection (sum of np partials); writes
-// Q [M][nq][dh], Kb/Vb [M][nkv][dh]
+// Q [M][nq][dh], Kb/Vb [M][nkv][dh].  The projection's rows M + b*n_new + i
+// (n_new appended context rows per batch row) have their K (k-norm, RoPE at
+// n_b - n_new + i) and V stored into this layer's cache ck/cv.
 void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,
                          const void *k_norm, const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb,
-                         float *Vb, hipStream_t st);
-// context K/V from projected hidden rows: kv [bs*n_new][2*nkv*dh] fp32 -> cache
-void launch_ctx_store(const Dims &D, const float *kv, int n_new, const void *k_norm,
-                      const int32_t *ctx_lens, int max_ctx, void *ck, void *cv, int32_t *err,
-                      hipStream_t st);
+                         float *Vb, int n_new, void *ck, void *cv, int32_t *err, hipStream_t st);
 int attn_chunk_len();
 int attn_nchunks(int max_ctx, int B);
 void launch_attention(const Dims &D, const float *Q, const float *Kb, const float *Vb,
