@@ -35,7 +35,7 @@ __global__ __launch_bounds__(256) void embed_block_kernel(const WT *__restrict__
 // row of its token (the anchor for block position 0, MASK otherwise).  One
 // workgroup per output row; a thread keeps its 16 columns in registers and
 // issues all of its loads together.
-template <typename WT>
+template <typename WT, int MAXP>
 __global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, int ldx,
                                                        const float *__restrict__ parts, int np,
                                                        size_t pstride, const WT *__restrict__ gain,
@@ -75,15 +75,18 @@ __global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, in
       v[it][0] = a.x; v[it][1] = a.y; v[it][2] = a.z; v[it][3] = a.w;
       v[it][4] = c.x; v[it][5] = c.y; v[it][6] = c.z; v[it][7] = c.w;
     }
-    float4 pa[16], pc[16];
+    // MAXP slots loaded unconditionally (slot index clamped to a valid
+    // partial) and added only below np: a guarded load would end in a branch
+    // join that drains every outstanding load, serialising the partials
+    float4 pa[MAXP], pc[MAXP];
 #pragma unroll
-    for (int p = 0; p < 16; ++p)
-      if (p < np) {
-        pa[p] = *(const float4 *)(pr + p * pstride + c0);
-        pc[p] = *(const float4 *)(pr + p * pstride + c0 + 4);
-      }
+    for (int p = 0; p < MAXP; ++p) {
+      const int pp = min(p, max(np, 1) - 1);
+      pa[p] = *(const float4 *)(pr + pp * pstride + c0);
+      pc[p] = *(const float4 *)(pr + pp * pstride + c0 + 4);
+    }
 #pragma unroll
-    for (int p = 0; p < 16; ++p)
+    for (int p = 0; p < MAXP; ++p)
       if (p < np) {
         v[it][0] += pa[p].x; v[it][1] += pa[p].y; v[it][2] += pa[p].z; v[it][3] += pa[p].w;
         v[it][4] += pc[p].x; v[it][5] += pc[p].y; v[it][6] += pc[p].z; v[it][7] += pc[p].w;
@@ -150,7 +153,7 @@ DEVI void norm_rope_head(float (&v)[2], int dh, const WT *__restrict__ gain, flo
 // context rows appended from target hidden states (the same GEMM projected
 // them): their K heads get the k-norm and RoPE at position n_b - n_new + i and
 // are stored, with their V heads, into the cache in the storage type.
-template <typename WT>
+template <typename WT, int MAXP>
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restrict__ qkv, int np,
                                                            size_t pstride, const WT *__restrict__ qn,
                                                            const WT *__restrict__ kn,
@@ -181,15 +184,19 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
   const int per = dh / 64;
   {
     // K-split partial outputs, added in split order; all loads issued together
-    float t[16][2];
+    // (MAXP slots, clamped to a valid partial, added only below np)
+    float t[MAXP][2];
 #pragma unroll
-    for (int p = 0; p < 16; ++p)
-      if (p < np)
-        for (int q = 0; q < per; ++q) t[p][q] = src[p * pstride + lane + 64 * q];
+    for (int p = 0; p < MAXP; ++p) {
+      const int pp = min(p, max(np, 1) - 1);
 #pragma unroll
-    for (int p = 0; p < 16; ++p)
+      for (int q = 0; q < 2; ++q) t[p][q] = src[pp * pstride + lane + 64 * min(q, per - 1)];
+    }
+#pragma unroll
+    for (int p = 0; p < MAXP; ++p)
       if (p < np)
-        for (int q = 0; q < per; ++q) v[q] += t[p][q];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) v[q] += q < per ? t[p][q] : 0.f;
   }
   if (m >= M) {
     const int r = m - M, b = r / n_new, i = r % n_new;
@@ -316,19 +323,38 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
       const int qh = kvh * G + qi / B, j = qi % B;
       qv[q] = *(const float4 *)(Q + (((size_t)b * B + j) * nq + qh) * DH + 4 * d4);
     }
+    // Each key comes from the cache (index < n) or the block (index >= n).
+    // Both candidates are loaded unconditionally at clamped, valid addresses
+    // and selected per lane: a per-lane guarded load would become a branch
+    // whose join drains every outstanding load, serialising the staging into
+    // one memory round trip per load.  Without a context the cache candidate
+    // reads the block buffer instead (discarded: no index is < 0).
     constexpr int NE = CH * DH / 4 / kAttnThreads;
-    float4 kv[NE], vv[NE];
+    const WT *ckb = n > 0 ? ck : (const WT *)Kb, *cvb = n > 0 ? cv : (const WT *)Vb;
+    const int nl = n > 0 ? n - 1 : 0;
+    float4 kc[NE], kbk[NE], vc[NE], vbk[NE];
 #pragma unroll
     for (int q = 0; q < NE; ++q) {
       const int e = tid + q * kAttnThreads;
       const int t = e / (DH / 4), d4 = e % (DH / 4);
       const int kk = min(c0 + t, total - 1);
-      if (kk < n) kv[q] = ld4_f32(ck + ((((size_t)b * max_ctx + kk) * nkv) + kvh) * DH + 4 * d4);
-      else kv[q] = *(const float4 *)(Kb + ((((size_t)b * B + (kk - n)) * nkv) + kvh) * DH + 4 * d4);
+      const size_t crow = n > 0 ? (((size_t)b * max_ctx + min(kk, nl)) * nkv + kvh) * DH : (size_t)kvh * DH;
+      kc[q] = ld4_f32(ckb + crow + 4 * d4);
+      kbk[q] = *(const float4 *)(Kb + ((((size_t)b * B + min(max(kk - n, 0), B - 1)) * nkv) + kvh) * DH + 4 * d4);
       const int tv = e % CH, dv = e / CH;                   // V: consecutive lanes, consecutive keys
       const int kv2 = min(c0 + tv, total - 1);
-      if (kv2 < n) vv[q] = ld4_f32(cv + ((((size_t)b * max_ctx + kv2) * nkv) + kvh) * DH + 4 * dv);
-      else vv[q] = *(const float4 *)(Vb + ((((size_t)b * B + (kv2 - n)) * nkv) + kvh) * DH + 4 * dv);
+      const size_t vrow = n > 0 ? (((size_t)b * max_ctx + min(kv2, nl)) * nkv + kvh) * DH : (size_t)kvh * DH;
+      vc[q] = ld4_f32(cvb + vrow + 4 * dv);
+      vbk[q] = *(const float4 *)(Vb + ((((size_t)b * B + min(max(kv2 - n, 0), B - 1)) * nkv) + kvh) * DH + 4 * dv);
+    }
+    float4 kv[NE], vv[NE];
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      const int e = tid + q * kAttnThreads;
+      const int kk = min(c0 + e / (DH / 4), total - 1);
+      const int kv2 = min(c0 + e % CH, total - 1);
+      kv[q] = kk < n ? kc[q] : kbk[q];
+      vv[q] = kv2 < n ? vc[q] : vbk[q];
     }
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
@@ -507,34 +533,51 @@ void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor,
                        D.B, D.d, D.V, D.mask_id, err);
 }
 
+template <typename WT, int MAXP>
+static void add_norm_t(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
+                       const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
+                       const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st) {
+  hipLaunchKernelGGL((add_norm_kernel<WT, MAXP>), dim3(rows), dim3(512), 0, st, x, ldx, parts, np, pstride,
+                     (const WT *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1, (const WT *)embed, anchor,
+                     D.mask_id, D.V, err);
+}
+
 void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
                      const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
                      const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st) {
   if (rows <= 0) return;
-  if (D.bf16)
-    hipLaunchKernelGGL(add_norm_kernel<bf16_t>, dim3(rows), dim3(512), 0, st, x, ldx, parts, np, pstride,
-                       (const bf16_t *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1,
-                       (const bf16_t *)embed, anchor, D.mask_id, D.V, err);
-  else
-    hipLaunchKernelGGL(add_norm_kernel<float>, dim3(rows), dim3(512), 0, st, x, ldx, parts, np, pstride,
-                       (const float *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1, (const float *)embed,
-                       anchor, D.mask_id, D.V, err);
+  if (np < 0 || np > 16) return;  // partial counts come from the GEMM planner (<= 16)
+  if (D.bf16) {
+    if (np <= 8) add_norm_t<bf16_t, 8>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st);
+    else add_norm_t<bf16_t, 16>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st);
+  } else {
+    if (np <= 8) add_norm_t<float, 8>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st);
+    else add_norm_t<float, 16>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st);
+  }
+}
+
+template <typename WT, int MAXP>
+static void qk_norm_rope_t(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,
+                           const void *k_norm, const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb, float *Vb,
+                           int n_new, void *ck, void *cv, int32_t *err, hipStream_t st) {
+  const int M = D.bs * D.B;
+  const int items = M * (D.nq + 2 * D.nkv) + D.bs * n_new * 2 * D.nkv;
+  hipLaunchKernelGGL((qk_norm_rope_kernel<WT, MAXP>), dim3((items + 3) / 4), dim3(256), 0, st, qkv, np, pstride,
+                     (const WT *)q_norm, (const WT *)k_norm, ctx_lens, max_ctx, Q, Kb, Vb, M, D.B, D.nq, D.nkv, D.dh,
+                     D.eps, D.inv_freq, n_new, (WT *)ck, (WT *)cv, err);
 }
 
 void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,
                          const void *k_norm, const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb,
                          float *Vb, int n_new, void *ck, void *cv, int32_t *err, hipStream_t st) {
-  const int M = D.bs * D.B;
-  const int items = M * (D.nq + 2 * D.nkv) + D.bs * n_new * 2 * D.nkv;
-  dim3 grid((items + 3) / 4);
-  if (D.bf16)
-    hipLaunchKernelGGL(qk_norm_rope_kernel<bf16_t>, grid, dim3(256), 0, st, qkv, np, pstride, (const bf16_t *)q_norm,
-                       (const bf16_t *)k_norm, ctx_lens, max_ctx, Q, Kb, Vb, M, D.B, D.nq, D.nkv, D.dh,
-                       D.eps, D.inv_freq, n_new, (bf16_t *)ck, (bf16_t *)cv, err);
-  else
-    hipLaunchKernelGGL(qk_norm_rope_kernel<float>, grid, dim3(256), 0, st, qkv, np, pstride, (const float *)q_norm,
-                       (const float *)k_norm, ctx_lens, max_ctx, Q, Kb, Vb, M, D.B, D.nq, D.nkv, D.dh,
-                       D.eps, D.inv_freq, n_new, (float *)ck, (float *)cv, err);
+  if (np < 1 || np > 16) return;  // partial counts come from the GEMM planner (1..16)
+  if (D.bf16) {
+    if (np <= 8) qk_norm_rope_t<bf16_t, 8>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st);
+    else qk_norm_rope_t<bf16_t, 16>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st);
+  } else {
+    if (np <= 8) qk_norm_rope_t<float, 8>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st);
+    else qk_norm_rope_t<float, 16>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st);
+  }
 }
 
 template <typename WT, int RPT, int CH, int DH>

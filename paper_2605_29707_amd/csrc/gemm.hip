@@ -251,7 +251,9 @@ GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu, int max_split) 
   const int nch = (KS + kcm - 1) / kcm;
   p.mgroups = (M + 16 * p.MT - 1) / (16 * p.MT);
   p.WPT = 1;
-  if ((ntiles + 7) / 8 * p.mgroups < n_cu && kcm >= 2) p.WPT = 2;
+  // Two waves per tile (more workgroups for grids that leave CUs idle) was
+  // measured slower: it doubles the activation staging per weight byte.
+  (void)kcm;
   if (max_split > 1) p.WPT = 1;
   const int tw = 8 / p.WPT;
   p.groups = (ntiles + tw - 1) / tw;

@@ -72,9 +72,10 @@ __global__ __launch_bounds__(kVsThreads) void vs_lse_partial_kernel(const LT *__
   float z[kVsPer];
   float m = -INFINITY;
 #pragma unroll
-  for (int q = 0; q < kVsPer; ++q) {
+  for (int q = 0; q < kVsPer; ++q) {  // unconditional loads at clamped ids, masked afterwards
     const int v = c * kVsChunk + q * kVsThreads + threadIdx.x;
-    const float x = v < V ? order_val(row_logit<LT>(target, draft, b, r, B, V, v) * inv_t) : -INFINITY;
+    const float raw = row_logit<LT>(target, draft, b, r, B, V, min(v, V - 1));
+    const float x = v < V ? order_val(raw * inv_t) : -INFINITY;
     z[q] = x;
     m = fmaxf(m, x);
   }
@@ -123,18 +124,25 @@ __global__ __launch_bounds__(kVsThreads) void vs_bonus_partial_kernel(
   const float lt = lse[0], ld = lse[1];
   float bv = -INFINITY;
   int bi = INT_MAX;
+  // all loads first, at clamped ids (masked afterwards), so none waits on another
+  float tl[kVsPer], dl[kVsPer];
+  const int jd = j < B ? j - 1 : B - 2;  // the last depth has no draft row (its q is 0)
+#pragma unroll
+  for (int q = 0; q < kVsPer; ++q) {
+    const int v = min(c * kVsChunk + ((q / 4) * kVsThreads + threadIdx.x) * 4 + (q % 4), V - 1);
+    tl[q] = row_logit<LT>(target, draft, b, j - 1, B, V, v);
+    dl[q] = draft[((size_t)b * (B - 1) + jd) * V + v];
+  }
 #pragma unroll
   for (int grp = 0; grp < kVsPer / 4; ++grp) {
     const int v0 = c * kVsChunk + (grp * kVsThreads + threadIdx.x) * 4;  // four consecutive ids
-    if (v0 >= V) continue;
     const Philox4 noise = rng_block(seed_lo, seed_hi, RNG_BONUS, b, j, v0 / 4);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int v = v0 + e;
-      if (v >= V) break;
-      const float p = expf(order_val(row_logit<LT>(target, draft, b, j - 1, B, V, v) * inv_t) - lt);
-      const float q = j < B ? expf(order_val(draft[((size_t)b * (B - 1) + (j - 1)) * V + v] * inv_t) - ld) : 0.f;
-      const float w = fmaxf(p - q, 0.f);
+      const float p = expf(order_val(tl[grp * 4 + e] * inv_t) - lt);
+      const float q = j < B ? expf(order_val(dl[grp * 4 + e] * inv_t) - ld) : 0.f;
+      const float w = v < V ? fmaxf(p - q, 0.f) : 0.f;
       if (w > 0.f) {
         const float key = logf(w) + rng_gumbel(noise.x[e]);
         if (better(key, v, bv, bi)) {
