@@ -74,6 +74,8 @@ def main():
     ap.add_argument("--flush-steps", type=int, default=50,
                     help="extra steps, each after a 512 MiB scratch write that evicts on-chip caches; "
                          "reported per step (the write itself is not timed)")
+    ap.add_argument("--train-steps", type=int, default=50,
+                    help="extra pass timing the teacher-forced training forward + curriculum loss (0: skip)")
     ap.add_argument("--config", default="qwen3_8b")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -255,6 +257,47 @@ def main():
                     "us_per_step_median": round(statistics.median(aper) * 1e3, 1)}
         del aws
 
+    trained = None
+    if args.train_steps > 0:
+        import synth as _s
+        labels = T(_s.make_forced_tokens(cfg, seed=args.seed), torch.int32)
+        tws = torch.empty(bd.domino_train_workspace_bytes(model, bs, max_ctx, n_new), dtype=torch.uint8,
+                          device=dev)
+        tloss = torch.empty(3, dtype=torch.float32, device=dev)
+
+        def step_train():
+            bd.domino_train_forward(model, anchor, lens, ck, cv, max_ctx, labels, 0.5, float(D), tloss, tws,
+                                    ctx_hidden_new=hid, n_new=n_new, stream=stream)
+
+        for _ in range(5):
+            step_train()
+        nt = args.train_steps
+        te = [torch.cuda.Event(enable_timing=True) for _ in range(nt + 1)]
+        bd.domino_profile_enable(model, ["trainloss", "headloop"])
+        bd.domino_profile_reset(model)
+        torch.cuda.synchronize()
+        te[0].record(stream)
+        for i in range(nt):
+            step_train()
+            te[i + 1].record(stream)
+        torch.cuda.synchronize()
+        assert bd.domino_workspace_error(tws) == 0
+        lms, ln = bd.domino_profile_read(model, "trainloss")
+        hms, hn = bd.domino_profile_read(model, "headloop")
+        bd.domino_profile_enable(model, [])
+        tper = [te[i].elapsed_time(te[i + 1]) for i in range(nt)]
+        t_s = te[0].elapsed_time(te[-1]) / nt / 1e3
+        tbytes = algorithmic_bytes(cfg)
+        tb = tbytes["total"] - tbytes["target_rows"]
+        trained = {"steps": nt, "lambda": 0.5, "gamma": float(D), "ms_per_pass": round(t_s * 1e3, 4),
+                   "us_per_pass_median": round(statistics.median(tper) * 1e3, 1),
+                   "positions_per_s": round(bs * D / t_s, 1),
+                   "hbm_roofline_frac": round(tb / t_s / HBM_PEAK, 4), "algorithmic_bytes": tb,
+                   "state_recurrence_us": round(hms * 1e3 / max(1, hn), 1),
+                   "w2_ce_loss_us": round(lms * 1e3 / max(1, ln), 1),
+                   "loss": [round(float(x), 5) for x in tloss.cpu().tolist()]}
+        del tws
+
     breakdown = None
     if args.breakdown:
         classes = [c for c in bd.KERNEL_CLASSES]
@@ -314,6 +357,8 @@ def main():
         res["after_cache_flush"] = flushed
     if appended:
         res["with_context_append"] = appended
+    if trained:
+        res["training_forward"] = trained
     if breakdown:
         res["breakdown_us_per_step"] = breakdown
 

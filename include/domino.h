@@ -181,6 +181,40 @@ domino_status domino_draft_step_sampled(domino_model_t m, int32_t batch, const i
                                         float *topk_vals, float *final_logits, const domino_debug *debug,
                                         void *workspace, size_t workspace_bytes, void *stream);
 
+/* Bytes of workspace domino_train_forward needs (0 for invalid arguments). */
+size_t domino_train_workspace_bytes(domino_model_t m, int32_t batch, int32_t max_ctx, int32_t max_new);
+
+/*
+ * Teacher-forced training forward and the base-anchored curriculum loss
+ * (Sec. 4.2).  The block goes through the backbone and LM head as in
+ * domino_draft_step; the causal encoder is fed the ground-truth tokens (the
+ * anchor, then labels[b][0 .. B-3]), and for every draft position k = 0..B-2
+ *   CE_base[b][k]  = -log softmax(L_base)[labels[b][k]]
+ *   CE_final[b][k] = -log softmax(L_base + W2 u)[labels[b][k]]
+ * (NaN logits count as -inf).  With w_k = exp(-k / gamma):
+ *   L_base  = sum_{b,k} w_k CE_base  / (batch * sum_k w_k), likewise L_final,
+ *   loss    = (1 - lambda) L_final + lambda L_base.
+ * The corrected logits are reduced on chip; they reach memory only through
+ * debug->final_logits.  Deterministic: no floating-point atomics.
+ * Same arguments as domino_draft_step except:
+ *  labels          device int32 [batch][B-1]: ground-truth tokens of the draft
+ *                  positions; a label outside [0, vocab) sets DOMINO_DEV_BAD_TOKEN
+ *                  and gives NaN CEs
+ *  lambda          curriculum weight in [0, 1] (annealed 1 -> 0 by the caller)
+ *  gamma           position decay, positive and finite
+ *  loss            device fp32 [3]: total, L_base, L_final
+ *  ce              optional device fp32 [2][batch][B-1]: CE_base, then CE_final
+ *  debug           optional; hidden, base_logits, final_logits (L_base + W2 u)
+ *                  and states as in domino_draft_step
+ *  workspace       >= domino_train_workspace_bytes(m, batch, max_ctx, n_new)
+ */
+domino_status domino_train_forward(domino_model_t m, int32_t batch, const int32_t *anchor_ids,
+                                   const int32_t *ctx_lens, void *ctx_k, void *ctx_v, int32_t max_ctx,
+                                   const void *ctx_hidden_new, int32_t n_new, const int32_t *labels,
+                                   float lambda, float gamma, float *loss, float *ce,
+                                   const domino_debug *debug, void *workspace, size_t workspace_bytes,
+                                   void *stream);
+
 /*
  * Draft tree from the per-position top-beta tokens (spine-and-leaves, BFS
  * order).  Node 0 is the anchor (parent -1, depth 0, position n_b); node
@@ -277,7 +311,7 @@ domino_status domino_workspace_clear_error(void *workspace, void *stream);
 enum {
   DOMINO_KC_EMBED = 0, DOMINO_KC_NORM, DOMINO_KC_QKV, DOMINO_KC_ROPE, DOMINO_KC_ATTN,
   DOMINO_KC_WO, DOMINO_KC_GATEUP, DOMINO_KC_DOWN, DOMINO_KC_LMHEAD, DOMINO_KC_W1H,
-  DOMINO_KC_HEADLOOP, DOMINO_KC_CTXPROJ, DOMINO_KC_COUNT
+  DOMINO_KC_HEADLOOP, DOMINO_KC_CTXPROJ, DOMINO_KC_TRAINLOSS, DOMINO_KC_COUNT
 };
 domino_status domino_profile_enable(domino_model_t m, uint32_t class_mask);
 domino_status domino_profile_read(domino_model_t m, int32_t kernel_class, double *total_ms,

@@ -25,7 +25,7 @@ DOMINO_F32, DOMINO_BF16 = 0, 1
 DEV_BAD_TOKEN, DEV_BAD_CTX_LEN, DEV_BAD_TREE, DEV_BARRIER_TIMEOUT = 1, 2, 4, 8
 
 KERNEL_CLASSES = ["embed", "norm", "qkv", "rope", "attn", "wo", "gateup", "down", "lmhead", "w1h",
-                  "headloop", "ctxproj"]
+                  "headloop", "ctxproj", "trainloss"]
 
 
 class domino_config(C.Structure):
@@ -90,6 +90,9 @@ def load() -> C.CDLL:
         "domino_verify_sample": (i32, [i32, i32, i32, P, P, C.c_int, P, C.c_float, C.c_uint64, P, P, P, P, sz,
                                        P]),
         "domino_philox4x32_10": (i32, [P, C.c_uint64, P, i32, P]),
+        "domino_train_workspace_bytes": (sz, [P, i32, i32, i32]),
+        "domino_train_forward": (i32, [P, i32, P, P, P, P, i32, P, i32, P, C.c_float, C.c_float, P, P,
+                                       C.POINTER(domino_debug), P, sz, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -105,7 +108,7 @@ def exported_symbols():
             "domino_verify_accept", "domino_workspace_error", "domino_workspace_clear_error",
             "domino_profile_enable", "domino_profile_read", "domino_profile_reset",
             "domino_draft_step_sampled", "domino_verify_sample_workspace_bytes", "domino_verify_sample",
-            "domino_philox4x32_10"]
+            "domino_philox4x32_10", "domino_train_workspace_bytes", "domino_train_forward"]
 
 
 def last_error() -> str:
@@ -215,6 +218,26 @@ def domino_draft_step_sampled(model: DominoModel, anchor, ctx_lens, ctx_k, ctx_v
         int(max_ctx), _ptr(ctx_hidden_new), int(n_new), float(temperature), int(seed) & (2**64 - 1),
         _ptr(forced), _ptr(topk_ids), _ptr(topk_vals), _ptr(final_logits),
         C.byref(dbg) if dbg is not None else None, _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def domino_train_workspace_bytes(model: DominoModel, batch, max_ctx, max_new=0) -> int:
+    n = load().domino_train_workspace_bytes(model.handle, batch, max_ctx, max_new)
+    if n == 0:
+        raise DominoError(DOMINO_ERR_INVALID_ARG, "domino_train_workspace_bytes returned 0: " + last_error())
+    return int(n)
+
+
+def domino_train_forward(model: DominoModel, anchor, ctx_lens, ctx_k, ctx_v, max_ctx, labels, lam, gamma, loss,
+                         workspace, ce=None, ctx_hidden_new=None, n_new=0, debug=None, stream=None):
+    dbg = None
+    if debug:
+        dbg = domino_debug(**{k: (debug[k].data_ptr() if debug.get(k) is not None else None)
+                              for k in ("hidden", "base_logits", "final_logits", "states")})
+    _check(load().domino_train_forward(
+        model.handle, int(anchor.shape[0]), _ptr(anchor), _ptr(ctx_lens), _ptr(ctx_k), _ptr(ctx_v),
+        int(max_ctx), _ptr(ctx_hidden_new), int(n_new), _ptr(labels), float(lam), float(gamma), _ptr(loss),
+        _ptr(ce), C.byref(dbg) if dbg is not None else None, _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
 
 

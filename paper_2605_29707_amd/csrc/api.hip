@@ -58,7 +58,10 @@ struct domino_model {
   void *mem = nullptr;
   size_t mem_bytes = 0;
   std::vector<Packed> qkv, wo, gateup, down;
-  Packed lm, w2;
+  Packed lm, w2, w1s;
+  // training forward: the state recurrence runs on a second stream beside the backbone
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   size_t gtab_off, w_hh_off, w1_off, freq_off;
   // profiling
   uint32_t prof_mask = 0;
@@ -334,6 +337,7 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
   // LM head and W1's H half share the input H: one packed matrix, W1 tiles after the vocabulary tiles
   m->lm = add(((D.V + 15) / 16) * 16 + D.r, D.d);
   m->w2 = add(D.V, D.r);
+  m->w1s = add(D.r, D.ds);  // W1's S half on its own, for the batched u of the training forward
   m->gtab_off = off;
   off = align_up(off + (size_t)D.V * 3 * D.ds * 4);
   m->w_hh_off = off;
@@ -375,6 +379,8 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
   launch_pack(bf, w->w1, D.r, D.d, D.d + D.ds, base + m->lm.off + (size_t)vt * m->lm.KS * 1024, D.r / 16, m->lm.KS,
               1, 0, st);
   launch_pack(bf, w->w2, D.V, D.r, D.r, base + m->w2.off, m->w2.NT, m->w2.KS, 1, 0, st);
+  launch_pack(bf, (const char *)w->w1 + (size_t)D.d * m->esz, D.r, D.ds, D.d + D.ds, base + m->w1s.off, m->w1s.NT,
+              m->w1s.KS, 1, 0, st);
   he = hipGetLastError();
   if (he == hipSuccess) he = build_gtab(m, w->gru_w_ih);
   if (he == hipSuccess) {
@@ -401,6 +407,9 @@ void domino_model_destroy(domino_model_t m) {
     for (auto x : e.a) (void)hipEventDestroy(x);
     for (auto x : e.b) (void)hipEventDestroy(x);
   }
+  if (m->fork) (void)hipEventDestroy(m->fork);
+  if (m->join) (void)hipEventDestroy(m->join);
+  if (m->side) (void)hipStreamDestroy(m->side);
   if (m->mem) (void)hipFree(m->mem);
   delete m;
 }
@@ -418,11 +427,8 @@ struct SampleOpt {
   uint64_t seed;
 };
 
-domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
-                              void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new,
-                              int32_t branch, const int32_t *forced_tokens, int32_t *topk_ids, float *topk_vals,
-                              const domino_debug *debug, void *workspace, size_t workspace_bytes, void *stream,
-                              const SampleOpt *smp) {
+domino_status check_step_args(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
+                              void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new) {
   if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
   if (batch < 1 || batch > 64) return fail(DOMINO_ERR_INVALID_ARG, "batch must be in [1, 64]");
   if (!anchor_ids || !ctx_lens) return fail(DOMINO_ERR_INVALID_ARG, "anchor_ids/ctx_lens is NULL");
@@ -430,18 +436,17 @@ domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *an
   if (max_ctx > 0 && (!ctx_k || !ctx_v)) return fail(DOMINO_ERR_INVALID_ARG, "ctx_k/ctx_v is NULL");
   if (n_new < 0 || n_new > max_ctx) return fail(DOMINO_ERR_INVALID_ARG, "n_new must be in [0, max_ctx]");
   if (n_new > 0 && !ctx_hidden_new) return fail(DOMINO_ERR_INVALID_ARG, "ctx_hidden_new is NULL");
-  if (branch < 1 || branch > 8 || branch > m->D.V) return fail(DOMINO_ERR_INVALID_ARG, "branch must be in [1, 8]");
-  if (!topk_ids || !topk_vals) return fail(DOMINO_ERR_INVALID_ARG, "topk_ids/topk_vals is NULL");
-  if (!workspace) return fail(DOMINO_ERR_WORKSPACE, "workspace is NULL");
-  WsLayout w;
-  layout(m, batch, max_ctx, n_new, branch, w);
-  if (workspace_bytes < w.total)
-    return fail(DOMINO_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, w.total);
+  return DOMINO_OK;
+}
 
-  hipStream_t st = (hipStream_t)stream;
+// The masked block through the draft backbone, the final norm and the LM head
+// (with W1's H half): leaves [L_base | pad | P] in the workspace's LP.
+domino_status run_backbone(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
+                           void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new,
+                           const domino_debug *debug, char *ws, const WsLayout &w, hipStream_t st,
+                           bool clear_header = true) {
   Dims D = make_dims(m, batch);
   const Plans p = make_plans(m, batch, n_new);
-  char *ws = (char *)workspace;
   auto F = [&](size_t off) { return (float *)(ws + off); };
   int32_t *err = (int32_t *)(ws + w.err);
   const char *base = (const char *)m->mem;
@@ -450,8 +455,7 @@ domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *an
   const size_t layer_elems = (size_t)batch * max_ctx * kvd;
 
   // clear the error word and the rollout's best keys
-  launch_fill_u32((uint32_t *)ws, w.hdr_words, 0u, st);
-
+  if (clear_header) launch_fill_u32((uint32_t *)ws, w.hdr_words, 0u, st);
   // appended context rows (target hidden states) ride along in the QKV
   // projection: they sit after the block rows of its input, and the RMSNorms
   // only ever rewrite the block rows
@@ -531,6 +535,15 @@ domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *an
     if (ce != hipSuccess) return fail(DOMINO_ERR_HIP, "copying base logits: %s", hipGetErrorString(ce));
   }
 
+  return DOMINO_OK;
+}
+
+HeadArgs head_args(domino_model_t m, int32_t batch, int32_t branch, char *ws, const WsLayout &w,
+                   const int32_t *anchor_ids, const int32_t *forced_tokens, const domino_debug *debug) {
+  const Dims D = make_dims(m, batch);
+  const char *base = (const char *)m->mem;
+  auto F = [&](size_t off) { return (float *)(ws + off); };
+  float *LP = F(w.LP);
   HeadArgs h;
   h.D = D;
   h.beta = branch;
@@ -547,22 +560,55 @@ domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *an
   h.best = (unsigned long long *)(ws + w.best);
   h.anchor = anchor_ids;
   h.forced = forced_tokens;
-  h.topk_ids = topk_ids;
-  h.topk_vals = topk_vals;
+  h.topk_ids = nullptr;
+  h.topk_vals = nullptr;
   h.final_logits = debug ? debug->final_logits : nullptr;
   h.states = debug ? debug->states : nullptr;
   h.hbuf = F(w.hbuf);
   h.ghbuf = F(w.ghbuf);
   h.ubuf = F(w.ubuf);
+  h.u_ld = D.r;
+  h.u_pos = 0;
+  h.skip_u = 0;
   h.pval = F(w.pval);
   h.pid = (int32_t *)(ws + w.pid);
-  h.err = err;
+  h.err = (int32_t *)(ws + w.err);
   h.GC = w.GC;
+  h.sample = 0;
+  h.inv_temp = 1.0f;
+  h.seed_lo = 0u;
+  h.seed_hi = 0u;
+  h.praw = F(w.praw);
+  return h;
+}
+
+domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
+                              void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new,
+                              int32_t branch, const int32_t *forced_tokens, int32_t *topk_ids, float *topk_vals,
+                              const domino_debug *debug, void *workspace, size_t workspace_bytes, void *stream,
+                              const SampleOpt *smp) {
+  domino_status s = check_step_args(m, batch, anchor_ids, ctx_lens, ctx_k, ctx_v, max_ctx, ctx_hidden_new, n_new);
+  if (s != DOMINO_OK) return s;
+  if (branch < 1 || branch > 8 || branch > m->D.V) return fail(DOMINO_ERR_INVALID_ARG, "branch must be in [1, 8]");
+  if (!topk_ids || !topk_vals) return fail(DOMINO_ERR_INVALID_ARG, "topk_ids/topk_vals is NULL");
+  if (!workspace) return fail(DOMINO_ERR_WORKSPACE, "workspace is NULL");
+  WsLayout w;
+  layout(m, batch, max_ctx, n_new, branch, w);
+  if (workspace_bytes < w.total)
+    return fail(DOMINO_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, w.total);
+
+  hipStream_t st = (hipStream_t)stream;
+  char *ws = (char *)workspace;
+  s = run_backbone(m, batch, anchor_ids, ctx_lens, ctx_k, ctx_v, max_ctx, ctx_hidden_new, n_new, debug, ws, w, st);
+  if (s != DOMINO_OK) return s;
+
+  HeadArgs h = head_args(m, batch, branch, ws, w, anchor_ids, forced_tokens, debug);
+  h.topk_ids = topk_ids;
+  h.topk_vals = topk_vals;
   h.sample = smp ? 1 : 0;
   h.inv_temp = smp ? 1.0f / smp->temperature : 1.0f;
   h.seed_lo = smp ? (uint32_t)smp->seed : 0u;
   h.seed_hi = smp ? (uint32_t)(smp->seed >> 32) : 0u;
-  h.praw = F(w.praw);
   prof_begin(m, DOMINO_KC_HEADLOOP, st);
   hipError_t he = launch_head(h, st);
   prof_end(m, DOMINO_KC_HEADLOOP, st);
@@ -597,6 +643,126 @@ domino_status domino_draft_step_sampled(domino_model_t m, int32_t batch, const i
   const SampleOpt smp = {temperature, seed};
   return draft_step_impl(m, batch, anchor_ids, ctx_lens, ctx_k, ctx_v, max_ctx, ctx_hidden_new, n_new, 1,
                          forced_tokens, topk_ids, topk_vals, &dbg, workspace, workspace_bytes, stream, &smp);
+}
+
+namespace {
+// training forward: the draft-step layout (branch 1) plus every position's u,
+// the per-workgroup log-sum-exp pairs, the label logits and the per-row CEs
+struct TrainLayout {
+  WsLayout w;
+  size_t S, Y, part, lab, ce, total;
+  int GCt;
+};
+void train_layout(const domino_model *m, int bs, int max_ctx, int max_new, TrainLayout &t) {
+  layout(m, bs, max_ctx, max_new, 1, t.w);
+  const Dims &D = m->D;
+  const size_t Mr = (size_t)bs * (D.B - 1);
+  t.GCt = train_ce_grid(D.V, D.r, m->bf16);
+  size_t o = t.w.total;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  t.S = take(Mr * D.ds * 4);
+  t.Y = take(Mr * D.r * 4);
+  t.part = take(Mr * t.GCt * 16);
+  t.lab = take(2 * Mr * 4);
+  t.ce = take(2 * Mr * 4);
+  t.total = o;
+}
+}  // namespace
+
+size_t domino_train_workspace_bytes(domino_model_t m, int32_t batch, int32_t max_ctx, int32_t max_new) {
+  if (!m || batch < 1 || batch > 64 || max_ctx < 0 || max_new < 0 || max_new > max_ctx) return 0;
+  TrainLayout t;
+  train_layout(m, batch, max_ctx, max_new, t);
+  return t.total;
+}
+
+domino_status domino_train_forward(domino_model_t m, int32_t batch, const int32_t *anchor_ids,
+                                   const int32_t *ctx_lens, void *ctx_k, void *ctx_v, int32_t max_ctx,
+                                   const void *ctx_hidden_new, int32_t n_new, const int32_t *labels, float lambda,
+                                   float gamma, float *loss, float *ce, const domino_debug *debug, void *workspace,
+                                   size_t workspace_bytes, void *stream) {
+  domino_status s = check_step_args(m, batch, anchor_ids, ctx_lens, ctx_k, ctx_v, max_ctx, ctx_hidden_new, n_new);
+  if (s != DOMINO_OK) return s;
+  if (!labels) return fail(DOMINO_ERR_INVALID_ARG, "labels is NULL");
+  if (!loss) return fail(DOMINO_ERR_INVALID_ARG, "loss is NULL");
+  if (!(lambda >= 0.f && lambda <= 1.f)) return fail(DOMINO_ERR_INVALID_ARG, "lambda must be in [0, 1]");
+  if (!(gamma > 0.f) || !std::isfinite(gamma)) return fail(DOMINO_ERR_INVALID_ARG, "gamma must be positive and finite");
+  if (!workspace) return fail(DOMINO_ERR_WORKSPACE, "workspace is NULL");
+  TrainLayout tl;
+  train_layout(m, batch, max_ctx, n_new, tl);
+  if (workspace_bytes < tl.total)
+    return fail(DOMINO_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, tl.total);
+
+  hipStream_t st = (hipStream_t)stream;
+  char *ws = (char *)workspace;
+  const WsLayout &w = tl.w;
+  const Dims D = make_dims(m, batch);
+  const int depth = D.B - 1, Mr = batch * depth;
+  if (!m->side) {
+    HIP_TRY(hipStreamCreateWithFlags(&m->side, hipStreamNonBlocking));
+    HIP_TRY(hipEventCreateWithFlags(&m->fork, hipEventDisableTiming));
+    HIP_TRY(hipEventCreateWithFlags(&m->join, hipEventDisableTiming));
+  }
+
+  // the state recurrence depends on the labels only, not on the backbone: it
+  // runs on the side stream (after the error word is cleared) while the
+  // backbone streams its weights on the caller's stream
+  launch_fill_u32((uint32_t *)ws, w.hdr_words, 0u, st);
+  HIP_TRY(hipEventRecord(m->fork, st));
+  HIP_TRY(hipStreamWaitEvent(m->side, m->fork, 0));
+  HeadArgs h = head_args(m, batch, 1, ws, w, anchor_ids, labels, debug);
+  h.final_logits = nullptr;
+  h.states = (debug && debug->states) ? debug->states : (float *)(ws + tl.S);
+  h.skip_u = 1;
+  prof_begin(m, DOMINO_KC_HEADLOOP, m->side);
+  hipError_t he = launch_head_states(h, m->side);
+  prof_end(m, DOMINO_KC_HEADLOOP, m->side);
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "state recurrence launch: %s", hipGetErrorString(he));
+  HIP_TRY(hipEventRecord(m->join, m->side));
+
+  s = run_backbone(m, batch, anchor_ids, ctx_lens, ctx_k, ctx_v, max_ctx, ctx_hidden_new, n_new, debug, ws, w, st,
+                   false);
+  if (s != DOMINO_OK) {
+    (void)hipStreamWaitEvent(st, m->join, 0);
+    return s;
+  }
+  HIP_TRY(hipStreamWaitEvent(st, m->join, 0));
+
+  // Y = W1[:, d:] S for every (row, position) at once
+  prof_begin(m, DOMINO_KC_TRAINLOSS, st);
+  const GemmPlan py = plan_gemm(m->w1s.NT, m->w1s.KS, Mr, EPI_STORE, m->n_cu, 1);
+  const GemmArgs ga = gemm_args((const char *)m->mem + m->w1s.off, m->w1s, 0, m->w1s.NT, D.r, h.states, D.ds, Mr,
+                                D.ds, (float *)(ws + tl.Y), D.r, py);
+  launch_gemm(m->bf16, EPI_STORE, ga, py, st);
+
+  TrainArgs t;
+  t.V = D.V;
+  t.r = D.r;
+  t.Mr = batch * depth;
+  t.depth = depth;
+  t.w2p = (const char *)m->mem + m->w2.off;
+  t.P = (const float *)(ws + w.LP) + (w.ldl - D.r);
+  t.ldp = w.ldl;
+  t.Y = (const float *)(ws + tl.Y);
+  t.Lbase = (const float *)(ws + w.LP);
+  t.ldl = w.ldl;
+  t.labels = labels;
+  t.part = (float *)(ws + tl.part);
+  t.lab = (float *)(ws + tl.lab);
+  t.ce = ce ? ce : (float *)(ws + tl.ce);
+  t.loss = loss;
+  t.final_logits = debug ? debug->final_logits : nullptr;
+  t.lambda = lambda;
+  t.gamma = gamma;
+  t.err = (int32_t *)(ws + w.err);
+  he = launch_train_loss(t, m->bf16, st);
+  prof_end(m, DOMINO_KC_TRAINLOSS, st);
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "training loss launch: %s", hipGetErrorString(he));
+  return DOMINO_OK;
 }
 
 domino_status domino_build_tree(int32_t batch, int32_t depth, int32_t branch, const int32_t *topk_ids,

@@ -293,7 +293,7 @@ __global__ __launch_bounds__(256) void head_u_kernel(HeadArgs h, int j) {
     acc = wave_sum(acc);
     if (lane == 0) {
       const float x = h.P[((size_t)b * depth + (j - 1)) * h.ldp + k] + acc;
-      h.ubuf[(size_t)b * r + k] = x / (1.f + expf(-x));
+      h.ubuf[(size_t)b * h.u_ld + (size_t)(j - 1) * h.u_pos + k] = x / (1.f + expf(-x));
     }
   }
 }
@@ -322,6 +322,7 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
   __shared__ int ys[kFusedBatch];
   const int nchunk = ds / EPL;  // <= 256
   const int nrows = r + (j < depth ? 3 * ds : 0);
+  const int rbeg = h.skip_u ? r : 0;  // skip_u: only the W_hh rows (u is formed later, batched)
   const int nw = gridDim.x * kStateWaves;
   const int w0 = blockIdx.x * kStateWaves + wave;
   const WT *w1 = (const WT *)h.w1, *whh = (const WT *)h.w_hh;
@@ -350,7 +351,7 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
       }
     }
   };
-  load_rows(w0);
+  load_rows(rbeg + w0);
 
   // ---- y_{j-1}: the anchor, a forced token, or the decoded best key of position j-1
   if (tid < bs) {
@@ -407,8 +408,8 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
 
   // ---- rows of [W1[:, d:]; W_hh] against S_{j-1}
   float *ghn = h.ghbuf + (size_t)(j & 1) * bs * 3 * ds;  // W_hh S_{j-1}
-  for (int base = w0; base < nrows; base += 2 * nw) {
-    if (base != w0) load_rows(base);
+  for (int base = rbeg + w0; base < nrows; base += 2 * nw) {
+    if (base != rbeg + w0) load_rows(base);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       const int row = base + q * nw;
@@ -437,7 +438,7 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
         if (lane == 0) {
           if (row < r) {
             const float x = h.P[((size_t)b * depth + (j - 1)) * h.ldp + row] + acc;
-            h.ubuf[(size_t)b * r + row] = x / (1.f + expf(-x));
+            h.ubuf[(size_t)b * h.u_ld + (size_t)(j - 1) * h.u_pos + row] = x / (1.f + expf(-x));
           } else {
             ghn[(size_t)b * 3 * ds + (row - r)] = acc;
           }
@@ -488,7 +489,7 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
     // whose join drains every outstanding load, holding back the W2 stream
     // issued below.  Columns of padding rows (bb >= bs) only reach output
     // columns that are never read, so their values do not matter.
-    const float *src = h.ubuf + (size_t)min(bb, bs - 1) * r + k0;
+    const float *src = h.ubuf + (size_t)min(bb, bs - 1) * h.u_ld + (size_t)(j - 1) * h.u_pos + k0;
 #pragma unroll
     for (int e = 0; e < EPL / 4; ++e) uv[q][e] = *(const float4 *)(src + 4 * e);
   }
@@ -755,6 +756,34 @@ static void launch_loop(const HeadArgs &h, hipStream_t st) {
     hipLaunchKernelGGL((head_logits_kernel<WT, KS, MT>), dim3(h.GC), dim3(kLogitWaves * 64), lds, st, h, j);
   }
   hipLaunchKernelGGL(head_merge_kernel, dim3(depth, D.bs), dim3(64), 0, st, h);
+}
+
+template <typename WT>
+static void launch_states_t(const HeadArgs &h, hipStream_t st) {
+  const Dims &D = h.D;
+  const int ga = min((D.ds + 3) / 4, 256), gb = (D.r + 3) / 4;
+  const bool fused = D.bs <= kFusedBatch;
+  const size_t slds = sizeof(float) * (size_t)D.bs * D.ds;
+  const int rows = (h.skip_u ? 0 : D.r) + 3 * D.ds;
+  const int gs = min((rows + 2 * kStateWaves - 1) / (2 * kStateWaves), kStateMaxGrid);
+  if (fused)
+    (void)hipFuncSetAttribute((const void *)head_state_kernel<WT>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)slds);
+  for (int j = 1; j <= D.B - 1; ++j) {
+    if (fused) {
+      hipLaunchKernelGGL(head_state_kernel<WT>, dim3(gs), dim3(kStateWaves * 64), slds, st, h, j);
+    } else {
+      hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(ga), dim3(256), 0, st, h, j);
+      if (!h.skip_u) hipLaunchKernelGGL(head_u_kernel<WT>, dim3(gb), dim3(256), 0, st, h, j);
+    }
+  }
+}
+
+hipError_t launch_head_states(const HeadArgs &h, hipStream_t st) {
+  if (!h.forced) return hipErrorInvalidValue;
+  if (h.D.bf16) launch_states_t<bf16_t>(h, st);
+  else launch_states_t<float>(h, st);
+  return hipGetLastError();
 }
 
 template <typename WT, int KS>

@@ -88,7 +88,9 @@ struct HeadArgs {
   float *states;         // optional [bs][B-1][ds]
   float *hbuf;           // [2][bs][ds] states by parity of the position
   float *ghbuf;          // [2][bs][3ds] W_hh S by parity (fused small-batch path)
-  float *ubuf;           // [bs][r]
+  float *ubuf;           // u of batch row b, position j at ubuf + b*u_ld + (j-1)*u_pos
+  int u_ld, u_pos;       // (r, 0) while drafting; (r(B-1), r) keeps every position's u
+  int skip_u;            // state recurrence only (states to `states`); u is formed by the caller
   float *pval;           // [B-1][bs][GC][beta] per-workgroup top-beta lists
   int32_t *pid;
   unsigned long long *best;  // [B-1][bs][8] best (value, id) keys per position, zeroed per step
@@ -105,6 +107,30 @@ struct HeadArgs {
 int head_logits_grid(const Dims &D);
 int head_best_slots();
 hipError_t launch_head(const HeadArgs &h, hipStream_t st);
+// the state recurrence of every position, teacher-forced (no logits): u into
+// ubuf as above, or with skip_u only the states into `states`
+hipError_t launch_head_states(const HeadArgs &h, hipStream_t st);
+
+// ---- teacher-forced training loss (train.hip)
+struct TrainArgs {
+  int V, r, Mr, depth;    // Mr = bs (B-1) rows, row b (B-1) + k
+  const void *w2p;        // W2 packed
+  const float *P;         // [Mr] rows of stride ldp: W1[:, :d] H
+  int ldp;
+  const float *Y;         // [Mr][r]: W1[:, d:] S (u = SiLU(P + Y), formed while staging)
+  const float *Lbase;     // [Mr] rows of stride ldl
+  int ldl;
+  const int32_t *labels;  // [Mr]
+  float *part;            // [Mr][GC][4] per-workgroup (max, sum exp) of base and final logits
+  float *lab;             // [2][Mr] label logits (base, final)
+  float *ce;              // [2][Mr] cross-entropies (base, final)
+  float *loss;            // [3] total, base, final
+  float *final_logits;    // optional [Mr][V]
+  float lambda, gamma;
+  int32_t *err;
+};
+int train_ce_grid(int V, int r, bool bf16);
+hipError_t launch_train_loss(const TrainArgs &t, bool bf16, hipStream_t st);
 
 // ---- tree and acceptance (tree.hip)
 void launch_build_tree(int bs, int depth, int beta, const int32_t *topk, const int32_t *anchor,

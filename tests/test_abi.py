@@ -124,3 +124,12 @@ def test_sampling_entry_points_validation():
     assert lib.domino_verify_sample(*ok, 1.0, 1, p, p, p, p, 8, None) == bd.DOMINO_ERR_WORKSPACE
     assert lib.domino_philox4x32_10(None, 0, None, 4, None) == bd.DOMINO_ERR_INVALID_ARG
     assert lib.domino_philox4x32_10(None, 0, None, -1, None) == bd.DOMINO_ERR_INVALID_ARG
+
+
+def test_train_entry_points_validation():
+    lib = bd.load()
+    p = C.c_void_p(16)  # never dereferenced: validation fails first
+    assert lib.domino_train_workspace_bytes(None, 1, 16, 0) == 0
+    base = (None, 1, p, p, p, p, 16, None, 0)
+    st = lib.domino_train_forward(*base, p, 0.5, 15.0, p, None, None, p, 10**9, None)
+    assert st == bd.DOMINO_ERR_INVALID_ARG and "model" in bd.last_error()
