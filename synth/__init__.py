@@ -14,6 +14,7 @@ from .inputs import (  # noqa: F401
     make_random_topk,
     make_forced_tokens,
     make_append_hidden,
+    make_target_weights,
     weight_shapes,
     head_param_count,
 )

@@ -67,6 +67,13 @@ PRESETS = {
     "qwen3_32b": DominoConfig("qwen3_32b", hidden=5120, n_layers=5, n_q_heads=64,
                               n_kv_heads=8, head_dim=128, ffn=25600, vocab=151936,
                               batch=16, ctx=4096, branch=1),
+    # target models (the verify forward): a small fp32 decoder sharing the tiny
+    # drafter's vocabulary and width, and the Qwen3-8B-shaped target (36 layers)
+    "tiny_target": DominoConfig("tiny_target", hidden=256, n_layers=4, n_q_heads=4, n_kv_heads=2,
+                                head_dim=64, ffn=1024, vocab=4096, dtype="f32", batch=1, ctx=128),
+    "qwen3_8b_target": DominoConfig("qwen3_8b_target", hidden=4096, n_layers=36, n_q_heads=32,
+                                    n_kv_heads=8, head_dim=128, ffn=12288, vocab=151936,
+                                    batch=1, ctx=1024, branch=1),
 }
 
 

@@ -36,6 +36,7 @@ _LAYER_KEYS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down",
                "attn_norm", "ffn_norm", "q_norm", "k_norm")
 _T_ANCHOR, _T_CTX_K, _T_CTX_V, _T_CTX_H, _T_CTX_IDS, _T_TARGET = 1000, 1001, 1002, 1003, 1004, 1005
 _T_TOPK, _T_FORCED, _T_CTXLEN, _T_APPEND_H = 1006, 1007, 1008, 1009
+_TARGET_LAYER_BASE = 3000
 
 
 def _threads() -> int:
@@ -134,6 +135,41 @@ def make_weights(cfg: DominoConfig, seed: int = 0, gain_std: float = 0.0,
     }
     for li, ls in enumerate(s["layers"]):
         base = _LAYER_BASE + 16 * li
+        lw = {}
+        for k, shape in ls.items():
+            tid = base + _LAYER_KEYS.index(k)
+            if k.endswith("norm"):
+                lw[k] = gain(tid, shape)
+            elif zero_wo_wdown and k in ("wo", "w_down"):
+                lw[k] = np.zeros(shape, np.float32)
+            else:
+                lw[k] = _normal(seed, tid, shape, 0.02, bf)
+        w["layers"].append(lw)
+    return w
+
+
+def make_target_weights(cfg: DominoConfig, seed: int = 0, gain_std: float = 0.0,
+                        zero_wo_wdown: bool = False) -> dict:
+    """Random-init weights of a target decoder (the same recipe as the drafter's
+    layers).  The embedding, LM head and final norm use the drafter's tensor ids,
+    so a drafter and a target of the same width and vocabulary share them (the
+    drafter reuses the target's frozen embedding and LM head); the layers have
+    their own streams."""
+    bf = cfg.dtype == "bf16"
+    s = weight_shapes(cfg)
+
+    def gain(tid, shape):
+        if gain_std == 0.0:
+            return np.ones(shape, dtype=np.float32)
+        g = 1.0 + _normal(seed, tid, shape, gain_std, False)
+        return bf16_round(g) if bf else g
+
+    w = {"embed": _normal(seed, _T_EMBED, s["embed"], 0.02, bf),
+         "lm_head": _normal(seed, _T_LMHEAD, s["lm_head"], 0.02, bf),
+         "final_norm": gain(_T_FINAL_NORM, s["final_norm"]),
+         "layers": []}
+    for li, ls in enumerate(s["layers"]):
+        base = _TARGET_LAYER_BASE + 16 * li
         lw = {}
         for k, shape in ls.items():
             tid = base + _LAYER_KEYS.index(k)
