@@ -76,6 +76,9 @@ def main():
                          "reported per step (the write itself is not timed)")
     ap.add_argument("--train-steps", type=int, default=50,
                     help="extra pass timing the teacher-forced training forward + curriculum loss (0: skip)")
+    ap.add_argument("--cycle-steps", type=int, default=20,
+                    help="extra pass timing the full speculative cycle with a 36-layer Qwen3-8B-shaped target: "
+                         "draft step, tree, target verify forward, acceptance, cache commit (0: skip)")
     ap.add_argument("--config", default="qwen3_8b")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -298,6 +301,11 @@ def main():
                    "loss": [round(float(x), 5) for x in tloss.cpu().tolist()]}
         del tws
 
+    cycle = None
+    if args.cycle_steps > 0 and cfg.name == "qwen3_8b":
+        cycle = speculative_cycle(args, cfg, bd, torch, dev, stream, model, anchor, lens, ck, cv, max_ctx, ids, vals,
+                                  ws, hid, n_new, beta)
+
     breakdown = None
     if args.breakdown:
         classes = [c for c in bd.KERNEL_CLASSES]
@@ -359,6 +367,8 @@ def main():
         res["with_context_append"] = appended
     if trained:
         res["training_forward"] = trained
+    if cycle:
+        res["speculative_cycle"] = cycle
     if breakdown:
         res["breakdown_us_per_step"] = breakdown
 
@@ -379,6 +389,88 @@ def main():
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, w, inp, lg_seed=args.seed * 16, seconds=args.cpu_seconds)
     print(json.dumps(res), flush=True)
+
+
+def target_bytes(tc) -> int:
+    """Bytes a verify forward must move: every target weight once, the context
+    KV of every layer, the embedding rows of the nodes."""
+    d, dh, nq, nkv, F, V = tc.hidden, tc.head_dim, tc.n_q_heads, tc.n_kv_heads, tc.ffn, tc.vocab
+    layer = d * nq * dh + 2 * d * nkv * dh + nq * dh * d + 3 * d * F
+    return 2 * (tc.n_layers * layer + V * d) + tc.batch * tc.n_layers * tc.ctx * nkv * dh * 2 * 2 + 16 * d * 2
+
+
+def speculative_cycle(args, cfg, bd, torch, dev, stream, model, anchor, lens, ck, cv, max_ctx, ids, vals, ws, hid,
+                      n_new, beta):
+    """Draft step + tree + target verify forward + greedy acceptance + cache
+    commit, with a 36-layer Qwen3-8B-shaped target (random weights: only the
+    timing means anything; the target shares the drafter's embedding and LM head)."""
+    import synth
+    tc = synth.get_config("qwen3_8b_target").with_(batch=cfg.batch, ctx=cfg.ctx, branch=beta)
+    t0 = time.time()
+    tw = synth.make_target_weights(tc, seed=args.seed)
+    nn = tc.n_nodes
+    tinp = synth.make_inputs(tc, seed=args.seed, max_ctx=tc.ctx + nn)
+    tdw = bd.to_device_weights(tw, tc, dev)
+    del tw
+    target = bd.DominoModel(tc, tdw, target=True)
+    T = lambda a, dt=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
+    tck, tcv = T(tinp["ctx_k"], torch.bfloat16), T(tinp["ctx_v"], torch.bfloat16)
+    tmax = tinp["max_ctx"]
+    del tinp
+    print(f"# target ready in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    bs, D = cfg.batch, cfg.depth
+    tok, par, dep, pos = (torch.empty(bs, nn, dtype=torch.int32, device=dev) for _ in range(4))
+    mask = torch.empty(bs, nn, nn, dtype=torch.uint8, device=dev)
+    tws = torch.empty(bd.domino_target_workspace_bytes(target, bs, nn, tmax), dtype=torch.uint8, device=dev)
+    lg = torch.empty(bs, nn, cfg.vocab, dtype=torch.bfloat16, device=dev)
+    acc = torch.empty(bs, dtype=torch.int32, device=dev)
+    nodes = torch.empty(bs, D, dtype=torch.int32, device=dev)
+    out = torch.empty(bs, D + 1, dtype=torch.int32, device=dev)
+    vws = torch.empty(bd.domino_verify_workspace_bytes(bs, nn, cfg.vocab), dtype=torch.uint8, device=dev)
+    new_lens = torch.empty(bs, dtype=torch.int32, device=dev)
+
+    def one(ev=None):
+        bd.domino_draft_step(model, anchor, lens, ck, cv, max_ctx, ids, vals, ws, branch=beta,
+                             ctx_hidden_new=hid, n_new=n_new, stream=stream)
+        bd.domino_build_tree(ids, anchor, lens, tok, par, dep, pos, ancestor_mask=mask, stream=stream)
+        if ev:
+            ev[0].record(stream)
+        bd.domino_target_verify(target, tok, pos, mask, lens, tck, tcv, tmax, lg, tws, stream=stream)
+        if ev:
+            ev[1].record(stream)
+        bd.domino_verify_accept(tok, par, lg, cfg.block, acc, nodes, out, vws, stream=stream)
+        bd.domino_target_commit(target, nn, lens, acc, nodes, tck, tcv, tmax, new_lens, tws, stream=stream)
+
+    for _ in range(3):
+        one()
+    n = args.cycle_steps
+    ce = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ve = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    taus = torch.zeros(n, bs, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    ce[0].record(stream)
+    for i in range(n):
+        one(ve[i])
+        ce[i + 1].record(stream)
+        taus[i].copy_(acc)
+    torch.cuda.synchronize()
+    assert bd.domino_workspace_error(tws) == 0 and bd.domino_workspace_error(ws) == 0
+    cyc = [ce[i].elapsed_time(ce[i + 1]) for i in range(n)]
+    ver = [a.elapsed_time(b) for a, b in ve]
+    tb = target_bytes(tc)
+    v_s = statistics.median(ver) / 1e3
+    tau = float(taus.float().mean().item()) + 1.0
+    res = {"steps": n, "target": f"{tc.n_layers} layers, d {tc.hidden}, {tc.n_q_heads}q/{tc.n_kv_heads}kv, "
+                                 f"FFN {tc.ffn}, V {tc.vocab}, bf16, {nn} nodes, ctx {tc.ctx}",
+           "us_per_cycle_median": round(statistics.median(cyc) * 1e3, 1),
+           "us_verify_forward_median": round(v_s * 1e6, 1),
+           "verify_hbm_roofline_frac": round(tb / v_s / HBM_PEAK, 4), "verify_algorithmic_bytes": tb,
+           "mean_tau_random_target": round(tau, 3),
+           "tokens_per_s": round(bs * tau / (statistics.median(cyc) / 1e3), 1)}
+    target.close()
+    del target, tdw, tck, tcv
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(cfg, w, inp, lg_seed, seconds):

@@ -216,6 +216,63 @@ domino_status domino_train_forward(domino_model_t m, int32_t batch, const int32_
                                    void *stream);
 
 /*
+ * Target decoder for the verify side of a speculative cycle (Sec. 3.1: the
+ * target scores every drafted candidate in one forward pass).  Same config and
+ * weight structs as the drafter; the Domino-head fields (gru_*, w1, w2,
+ * gru_hidden, rank) are ignored and may be NULL / 0, and `block` is unused
+ * (the node count is given per call).  Layers, embedding and LM head are
+ * packed as for the drafter; the handle only serves domino_target_* calls.
+ */
+domino_status domino_target_create(const domino_config *cfg, const domino_weights *w, domino_model_t *out);
+
+/* Workspace for domino_target_verify (0 for invalid or unsupported arguments). */
+size_t domino_target_workspace_bytes(domino_model_t target, int32_t batch, int32_t n_nodes, int32_t max_ctx);
+
+/*
+ * Tree-verify forward: target logits of every node of the draft trees.
+ * Node i of batch row b (the arrays domino_build_tree writes) holds token
+ * node_token[b][i] at RoPE position node_pos[b][i]; in every layer it attends to
+ * the cached context positions [0, ctx_lens[b]) and to the nodes k with
+ * ancestor_mask[b][i][k] != 0 (its root-to-node path; the diagonal always
+ * counts), so each node is scored as plain causal decoding of its path would
+ * score it.  Every node's K (post k-norm and RoPE) and V are also written into
+ * the cache at position ctx_lens[b] + i of every layer, for domino_target_commit.
+ *  n_nodes         N + 1 in [1, 64], and at most the largest block the
+ *                  attention supports: (n_q_heads / n_kv_heads) * n_nodes <= 128
+ *                  after rounding n_nodes up to a supported size
+ *                  (DOMINO_ERR_UNSUPPORTED otherwise)
+ *  node_token, node_pos  device int32 [batch][n_nodes]; ancestor_mask device
+ *                  uint8 [batch][n_nodes][n_nodes]
+ *  ctx_lens        device int32 [batch]; ctx_lens[b] + n_nodes <= max_ctx (else
+ *                  DOMINO_DEV_BAD_CTX_LEN and the node K/V are not stored)
+ *  ctx_k, ctx_v    device [n_layers][batch][max_ctx][n_kv][d_h] storage type
+ *  logits          device [batch][n_nodes][vocab], fp32 or bf16 (RNE): row i is
+ *                  the target's next-token logits after node i's token
+ *  workspace       >= domino_target_workspace_bytes(target, batch, n_nodes, max_ctx)
+ */
+domino_status domino_target_verify(domino_model_t target, int32_t batch, int32_t n_nodes, const int32_t *node_token,
+                                   const int32_t *node_pos, const uint8_t *ancestor_mask, const int32_t *ctx_lens,
+                                   void *ctx_k, void *ctx_v, int32_t max_ctx, void *logits, domino_dtype logits_dtype,
+                                   void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Cache commit after acceptance: node 0 (the anchor, already at ctx_lens[b])
+ * and the accepted path (accepted_nodes[b][0 .. accept_len[b]-1], as
+ * domino_verify_accept writes them) become positions ctx_lens[b] ..
+ * ctx_lens[b] + accept_len[b] of every layer's cache; new_ctx_lens[b] =
+ * ctx_lens[b] + 1 + accept_len[b].  The node at depth d must have id >= d
+ * (breadth-first order) and be < n_nodes, else DOMINO_DEV_BAD_TREE and the row
+ * is left unchanged (new_ctx_lens[b] = ctx_lens[b]).
+ *  max_depth       B - 1: the row stride of accepted_nodes, in [1, 63]
+ *  new_ctx_lens    device int32 [batch], must not alias ctx_lens
+ *  workspace       the verify workspace (its error word)
+ */
+domino_status domino_target_commit(domino_model_t target, int32_t batch, int32_t n_nodes, int32_t max_depth,
+                                   const int32_t *ctx_lens, const int32_t *accept_len, const int32_t *accepted_nodes,
+                                   void *ctx_k, void *ctx_v, int32_t max_ctx, int32_t *new_ctx_lens, void *workspace,
+                                   void *stream);
+
+/*
  * Draft tree from the per-position top-beta tokens (spine-and-leaves, BFS
  * order).  Node 0 is the anchor (parent -1, depth 0, position n_b); node
  * 1 + (d-1)*branch + rho holds topk_ids[b][d-1][rho] at depth d, position

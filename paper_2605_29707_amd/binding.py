@@ -91,6 +91,10 @@ def load() -> C.CDLL:
                                        P]),
         "domino_philox4x32_10": (i32, [P, C.c_uint64, P, i32, P]),
         "domino_train_workspace_bytes": (sz, [P, i32, i32, i32]),
+        "domino_target_create": (i32, [C.POINTER(domino_config), C.POINTER(domino_weights), C.POINTER(P)]),
+        "domino_target_workspace_bytes": (sz, [P, i32, i32, i32]),
+        "domino_target_verify": (i32, [P, i32, i32, P, P, P, P, P, P, i32, P, C.c_int, P, sz, P]),
+        "domino_target_commit": (i32, [P, i32, i32, i32, P, P, P, P, P, i32, P, P, P]),
         "domino_train_forward": (i32, [P, i32, P, P, P, P, i32, P, i32, P, C.c_float, C.c_float, P, P,
                                        C.POINTER(domino_debug), P, sz, P]),
     }
@@ -108,7 +112,8 @@ def exported_symbols():
             "domino_verify_accept", "domino_workspace_error", "domino_workspace_clear_error",
             "domino_profile_enable", "domino_profile_read", "domino_profile_reset",
             "domino_draft_step_sampled", "domino_verify_sample_workspace_bytes", "domino_verify_sample",
-            "domino_philox4x32_10", "domino_train_workspace_bytes", "domino_train_forward"]
+            "domino_philox4x32_10", "domino_train_workspace_bytes", "domino_train_forward",
+            "domino_target_create", "domino_target_workspace_bytes", "domino_target_verify", "domino_target_commit"]
 
 
 def last_error() -> str:
@@ -148,7 +153,9 @@ def make_config(cfg) -> domino_config:
 class DominoModel:
     """Owns a domino_model_t; keeps the borrowed weight tensors alive."""
 
-    def __init__(self, cfg, dev_weights: dict):
+    def __init__(self, cfg, dev_weights: dict, target: bool = False):
+        """target=True creates a target decoder (domino_target_create): the
+        Domino-head weights are not needed."""
         lib = load()
         self.cfg = cfg
         self._w = dev_weights
@@ -166,12 +173,12 @@ class DominoModel:
             attn_norm=arr("attn_norm"), wq=arr("wq"), wk=arr("wk"), wv=arr("wv"),
             q_norm=arr("q_norm"), k_norm=arr("k_norm"), wo=arr("wo"), ffn_norm=arr("ffn_norm"),
             w_gate=arr("w_gate"), w_up=arr("w_up"), w_down=arr("w_down"),
-            gru_w_ih=dev_weights["gru_w_ih"].data_ptr(), gru_w_hh=dev_weights["gru_w_hh"].data_ptr(),
-            gru_b_ih=dev_weights["gru_b_ih"].data_ptr(), gru_b_hh=dev_weights["gru_b_hh"].data_ptr(),
-            w1=dev_weights["w1"].data_ptr(), w2=dev_weights["w2"].data_ptr())
+            **{k: (dev_weights[k].data_ptr() if k in dev_weights else None)
+               for k in ("gru_w_ih", "gru_w_hh", "gru_b_ih", "gru_b_hh", "w1", "w2")})
         self._cfg_struct = make_config(cfg)
         h = C.c_void_p()
-        _check(lib.domino_model_create(C.byref(self._cfg_struct), C.byref(w), C.byref(h)))
+        create = lib.domino_target_create if target else lib.domino_model_create
+        _check(create(C.byref(self._cfg_struct), C.byref(w), C.byref(h)))
         self.handle = h
 
     def close(self):
@@ -239,6 +246,31 @@ def domino_train_forward(model: DominoModel, anchor, ctx_lens, ctx_k, ctx_v, max
         int(max_ctx), _ptr(ctx_hidden_new), int(n_new), _ptr(labels), float(lam), float(gamma), _ptr(loss),
         _ptr(ce), C.byref(dbg) if dbg is not None else None, _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def domino_target_workspace_bytes(target: DominoModel, batch, n_nodes, max_ctx) -> int:
+    n = load().domino_target_workspace_bytes(target.handle, batch, n_nodes, max_ctx)
+    if n == 0:
+        raise DominoError(DOMINO_ERR_INVALID_ARG, "domino_target_workspace_bytes returned 0: " + last_error())
+    return int(n)
+
+
+def domino_target_verify(target: DominoModel, node_token, node_pos, ancestor_mask, ctx_lens, ctx_k, ctx_v, max_ctx,
+                         logits, workspace, stream=None):
+    import torch
+    bs, nn = node_token.shape
+    dt = DOMINO_BF16 if logits.dtype == torch.bfloat16 else DOMINO_F32
+    _check(load().domino_target_verify(target.handle, bs, nn, _ptr(node_token), _ptr(node_pos), _ptr(ancestor_mask),
+                                       _ptr(ctx_lens), _ptr(ctx_k), _ptr(ctx_v), int(max_ctx), _ptr(logits), dt,
+                                       _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def domino_target_commit(target: DominoModel, n_nodes, ctx_lens, accept_len, accepted_nodes, ctx_k, ctx_v, max_ctx,
+                         new_ctx_lens, workspace, stream=None):
+    bs, max_depth = accepted_nodes.shape
+    _check(load().domino_target_commit(target.handle, bs, int(n_nodes), int(max_depth), _ptr(ctx_lens),
+                                       _ptr(accept_len), _ptr(accepted_nodes), _ptr(ctx_k), _ptr(ctx_v), int(max_ctx),
+                                       _ptr(new_ctx_lens), _ptr(workspace), _stream(stream)))
 
 
 def domino_verify_sample_workspace_bytes(batch, block, vocab) -> int:

@@ -58,6 +58,7 @@ struct domino_model {
   void *mem = nullptr;
   size_t mem_bytes = 0;
   std::vector<Packed> qkv, wo, gateup, down;
+  bool has_head = true;  // false: a target decoder (layers, embedding, LM head only)
   Packed lm, w2, w1s;
   // training forward: the state recurrence runs on a second stream beside the backbone
   hipStream_t side = nullptr;
@@ -91,10 +92,10 @@ void prof_end(domino_model *m, int cls, hipStream_t st) {
   e.used++;
 }
 
-domino_status check_config(const domino_config *c) {
+domino_status check_config(const domino_config *c, bool with_head = true) {
   if (!c) return fail(DOMINO_ERR_INVALID_ARG, "config is NULL");
   if (c->hidden <= 0 || c->n_layers <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
-      c->ffn <= 0 || c->vocab <= 1 || c->gru_hidden <= 0 || c->rank <= 0)
+      c->ffn <= 0 || c->vocab <= 1 || (with_head && (c->gru_hidden <= 0 || c->rank <= 0)))
     return fail(DOMINO_ERR_INVALID_ARG, "config sizes must be positive");
   if (c->block < 2 || c->block > 64) return fail(DOMINO_ERR_INVALID_ARG, "block must be in [2, 64]");
   if (c->mask_token_id < 0 || c->mask_token_id >= c->vocab)
@@ -104,11 +105,13 @@ domino_status check_config(const domino_config *c) {
   if (c->head_dim != 64 && c->head_dim != 128) return fail(DOMINO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
   if (c->n_q_heads % c->n_kv_heads) return fail(DOMINO_ERR_UNSUPPORTED, "n_q_heads must be a multiple of n_kv_heads");
   const int ks = c->dtype == DOMINO_BF16 ? 32 : 16;
-  if (c->hidden % 32 || c->ffn % 32 || c->gru_hidden % 32 || (c->n_q_heads * c->head_dim) % 32)
-    return fail(DOMINO_ERR_UNSUPPORTED, "hidden, ffn, gru_hidden and n_q_heads*head_dim must be multiples of 32");
+  if (c->hidden % 32 || c->ffn % 32 || (c->n_q_heads * c->head_dim) % 32)
+    return fail(DOMINO_ERR_UNSUPPORTED, "hidden, ffn and n_q_heads*head_dim must be multiples of 32");
+  if (c->hidden > 8192) return fail(DOMINO_ERR_UNSUPPORTED, "hidden must be at most 8192");
+  if (!with_head) return DOMINO_OK;  // a target decoder: the node count is checked per call
+  if (c->gru_hidden % 32) return fail(DOMINO_ERR_UNSUPPORTED, "gru_hidden must be a multiple of 32");
   if (c->rank % ks || c->rank > 16 * ks)
     return fail(DOMINO_ERR_UNSUPPORTED, "rank must be a multiple of %d and at most %d", ks, 16 * ks);
-  if (c->hidden > 8192) return fail(DOMINO_ERR_UNSUPPORTED, "hidden must be at most 8192");
   if (!attn_supported(c->n_q_heads, c->n_kv_heads, c->block))
     return fail(DOMINO_ERR_UNSUPPORTED, "(n_q_heads/n_kv_heads)*block must be 32, 64 or 128");
   const int epl = c->dtype == DOMINO_BF16 ? 8 : 4;
@@ -137,18 +140,23 @@ struct Plans {
 
 constexpr int kMaxSplit = 16;
 
-Plans make_plans(const domino_model *m, int bs, int max_new) {
-  const Dims &D = m->D;
-  const int M = bs * D.B, Mh = bs * (D.B - 1);
+// Plans for M block rows, Mlm LM-head rows and Ma QKV rows (block rows, then
+// appended context rows)
+Plans make_plans_rows(const domino_model *m, int M, int Mlm, int Ma) {
   Plans p;
   // projections whose consumer is elementwise write K-split partial outputs
-  // QKV also projects the appended context rows (rows M .. M + bs*max_new - 1)
-  p.qkv = plan_gemm(m->qkv[0].NT, m->qkv[0].KS, M + bs * max_new, EPI_STORE, m->n_cu, kMaxSplit);
+  p.qkv = plan_gemm(m->qkv[0].NT, m->qkv[0].KS, Ma, EPI_STORE, m->n_cu, kMaxSplit);
   p.wo = plan_gemm(m->wo[0].NT, m->wo[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
   p.gateup = plan_gemm(m->gateup[0].NT, m->gateup[0].KS, M, EPI_SWIGLU, m->n_cu, 1);
   p.down = plan_gemm(m->down[0].NT, m->down[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
-  p.lm = plan_gemm(m->lm.NT, m->lm.KS, Mh, EPI_STORE, m->n_cu, 1);
+  p.lm = plan_gemm(m->lm.NT, m->lm.KS, Mlm, EPI_STORE, m->n_cu, 1);
   return p;
+}
+
+Plans make_plans(const domino_model *m, int bs, int max_new) {
+  const Dims &D = m->D;
+  // QKV also projects the appended context rows (rows M .. M + bs*max_new - 1)
+  return make_plans_rows(m, bs * D.B, bs * (D.B - 1), bs * D.B + bs * max_new);
 }
 
 bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, WsLayout &w) {
@@ -188,6 +196,64 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.pid = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
   w.praw = take((size_t)(D.B - 1) * bs * w.GC * 4);
   w.total = o;
+  return true;
+}
+
+// Rows per batch row of a verify forward: the smallest block size the
+// attention supports ((n_q / n_kv) * Bp in {32, 64, 128}, Bp a multiple of 4,
+// at most 64) that holds n_nodes; 0 if none does.
+int target_block(const domino_model *m, int nn) {
+  const int G = m->D.nq / m->D.nkv;
+  for (int R = 32; R <= 128; R *= 2)
+    if (R % G == 0) {
+      const int Bp = R / G;
+      if (Bp >= nn && Bp % 4 == 0 && Bp <= 64) return Bp;
+    }
+  return 0;
+}
+
+struct TargetLayout {
+  WsLayout w;
+  size_t tok, pos, mask, total;
+  int Bp;
+};
+
+bool target_layout(const domino_model *m, int bs, int nn, int max_ctx, TargetLayout &t) {
+  t.Bp = target_block(m, nn);
+  if (!t.Bp) return false;
+  Dims D = make_dims(m, bs);
+  D.B = t.Bp;
+  const int M = bs * t.Bp;
+  const Plans p = make_plans_rows(m, M, M, M);
+  WsLayout &w = t.w;
+  w = WsLayout();
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  w.err = take(256);
+  w.hdr_words = o / 4;
+  const int qkvw = (D.nq + 2 * D.nkv) * D.dh;
+  w.X = take((size_t)M * D.d * 4);
+  w.A = take((size_t)M * D.d * 4);
+  w.QKV = take((size_t)p.qkv.ksplit * M * qkvw * 4);
+  w.Q = take((size_t)M * D.nq * D.dh * 4);
+  w.Kb = take((size_t)M * D.nkv * D.dh * 4);
+  w.Vb = take((size_t)M * D.nkv * D.dh * 4);
+  w.attn = take(attn_part_floats(D, max_ctx) * 4);
+  w.O = take((size_t)M * D.nq * D.dh * 4);
+  w.WOp = take((size_t)p.wo.ksplit * M * D.d * 4);
+  w.F = take((size_t)M * D.ffn * 4);
+  w.DNp = take((size_t)p.down.ksplit * M * D.d * 4);
+  w.H = take((size_t)M * D.d * 4);
+  w.ldl = m->lm.NT * 16;
+  w.LP = take((size_t)M * w.ldl * 4);
+  t.tok = take((size_t)M * 4);
+  t.pos = take((size_t)M * 4);
+  t.mask = take((size_t)bs * t.Bp * t.Bp);
+  t.total = w.total = o;
   return true;
 }
 
@@ -257,15 +323,17 @@ extern "C" {
 
 const char *domino_last_error(void) { return g_err.c_str(); }
 
-domino_status domino_model_create(const domino_config *cfg, const domino_weights *w, domino_model_t *out) {
+namespace {
+domino_status create_impl(const domino_config *cfg, const domino_weights *w, domino_model_t *out, bool with_head) {
   if (!out) return fail(DOMINO_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
-  domino_status s = check_config(cfg);
+  domino_status s = check_config(cfg, with_head);
   if (s != DOMINO_OK) return s;
   if (!w) return fail(DOMINO_ERR_INVALID_ARG, "weights is NULL");
   const int L = cfg->n_layers;
-  if (!w->embed || !w->lm_head || !w->final_norm || !w->gru_w_ih || !w->gru_w_hh || !w->gru_b_ih ||
-      !w->gru_b_hh || !w->w1 || !w->w2)
+  if (!w->embed || !w->lm_head || !w->final_norm)
+    return fail(DOMINO_ERR_INVALID_ARG, "a weight pointer is NULL");
+  if (with_head && (!w->gru_w_ih || !w->gru_w_hh || !w->gru_b_ih || !w->gru_b_hh || !w->w1 || !w->w2))
     return fail(DOMINO_ERR_INVALID_ARG, "a weight pointer is NULL");
   const void *const *arrs[] = {w->attn_norm, w->wq, w->wk, w->wv, w->q_norm, w->k_norm,
                                w->wo, w->ffn_norm, w->w_gate, w->w_up, w->w_down};
@@ -277,6 +345,7 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
 
   domino_model *m = new domino_model();
   m->cfg = *cfg;
+  m->has_head = with_head;
   m->bf16 = cfg->dtype == DOMINO_BF16;
   m->esz = m->bf16 ? 2 : 4;
   Dims &D = m->D;
@@ -335,15 +404,17 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
     m->down.push_back(add(D.d, D.ffn));
   }
   // LM head and W1's H half share the input H: one packed matrix, W1 tiles after the vocabulary tiles
-  m->lm = add(((D.V + 15) / 16) * 16 + D.r, D.d);
-  m->w2 = add(D.V, D.r);
-  m->w1s = add(D.r, D.ds);  // W1's S half on its own, for the batched u of the training forward
-  m->gtab_off = off;
-  off = align_up(off + (size_t)D.V * 3 * D.ds * 4);
-  m->w_hh_off = off;
-  off = align_up(off + (size_t)3 * D.ds * D.ds * m->esz);
-  m->w1_off = off;
-  off = align_up(off + (size_t)D.r * (D.d + D.ds) * m->esz);
+  m->lm = add(((D.V + 15) / 16) * 16 + (with_head ? D.r : 0), D.d);
+  if (with_head) {
+    m->w2 = add(D.V, D.r);
+    m->w1s = add(D.r, D.ds);  // W1's S half on its own, for the batched u of the training forward
+    m->gtab_off = off;
+    off = align_up(off + (size_t)D.V * 3 * D.ds * 4);
+    m->w_hh_off = off;
+    off = align_up(off + (size_t)3 * D.ds * D.ds * m->esz);
+    m->w1_off = off;
+    off = align_up(off + (size_t)D.r * (D.d + D.ds) * m->esz);
+  }
   m->freq_off = off;
   off = align_up(off + (size_t)(D.dh / 2) * sizeof(double));
   m->mem_bytes = off;
@@ -376,21 +447,25 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
   }
   const int vt = (D.V + 15) / 16;
   launch_pack(bf, w->lm_head, D.V, D.d, D.d, base + m->lm.off, vt, m->lm.KS, 1, 0, st);
-  launch_pack(bf, w->w1, D.r, D.d, D.d + D.ds, base + m->lm.off + (size_t)vt * m->lm.KS * 1024, D.r / 16, m->lm.KS,
-              1, 0, st);
-  launch_pack(bf, w->w2, D.V, D.r, D.r, base + m->w2.off, m->w2.NT, m->w2.KS, 1, 0, st);
-  launch_pack(bf, (const char *)w->w1 + (size_t)D.d * m->esz, D.r, D.ds, D.d + D.ds, base + m->w1s.off, m->w1s.NT,
-              m->w1s.KS, 1, 0, st);
+  if (with_head) {
+    launch_pack(bf, w->w1, D.r, D.d, D.d + D.ds, base + m->lm.off + (size_t)vt * m->lm.KS * 1024, D.r / 16,
+                m->lm.KS, 1, 0, st);
+    launch_pack(bf, w->w2, D.V, D.r, D.r, base + m->w2.off, m->w2.NT, m->w2.KS, 1, 0, st);
+    launch_pack(bf, (const char *)w->w1 + (size_t)D.d * m->esz, D.r, D.ds, D.d + D.ds, base + m->w1s.off,
+                m->w1s.NT, m->w1s.KS, 1, 0, st);
+  }
   he = hipGetLastError();
-  if (he == hipSuccess) he = build_gtab(m, w->gru_w_ih);
+  if (he == hipSuccess && with_head) he = build_gtab(m, w->gru_w_ih);
   if (he == hipSuccess) {
     // RoPE inverse frequencies theta^(-2i/dh), exact in fp64 on the host
     std::vector<double> f(D.dh / 2);
     for (int i = 0; i < D.dh / 2; ++i) f[i] = std::pow((double)cfg->rope_theta, -2.0 * i / (double)D.dh);
     he = hipMemcpy(base + m->freq_off, f.data(), f.size() * sizeof(double), hipMemcpyHostToDevice);
   }
-  if (he == hipSuccess) he = hipMemcpy(base + m->w_hh_off, w->gru_w_hh, (size_t)3 * D.ds * D.ds * m->esz, hipMemcpyDeviceToDevice);
-  if (he == hipSuccess) he = hipMemcpy(base + m->w1_off, w->w1, (size_t)D.r * (D.d + D.ds) * m->esz, hipMemcpyDeviceToDevice);
+  if (he == hipSuccess && with_head)
+    he = hipMemcpy(base + m->w_hh_off, w->gru_w_hh, (size_t)3 * D.ds * D.ds * m->esz, hipMemcpyDeviceToDevice);
+  if (he == hipSuccess && with_head)
+    he = hipMemcpy(base + m->w1_off, w->w1, (size_t)D.r * (D.d + D.ds) * m->esz, hipMemcpyDeviceToDevice);
   if (he == hipSuccess) he = hipDeviceSynchronize();
   if (he != hipSuccess) {
     (void)hipFree(m->mem);
@@ -399,6 +474,15 @@ domino_status domino_model_create(const domino_config *cfg, const domino_weights
   }
   *out = m;
   return DOMINO_OK;
+}
+}  // namespace
+
+domino_status domino_model_create(const domino_config *cfg, const domino_weights *w, domino_model_t *out) {
+  return create_impl(cfg, w, out, true);
+}
+
+domino_status domino_target_create(const domino_config *cfg, const domino_weights *w, domino_model_t *out) {
+  return create_impl(cfg, w, out, false);
 }
 
 void domino_model_destroy(domino_model_t m) {
@@ -415,7 +499,9 @@ void domino_model_destroy(domino_model_t m) {
 }
 
 size_t domino_workspace_bytes(domino_model_t m, int32_t batch, int32_t max_ctx, int32_t max_new, int32_t branch) {
-  if (!m || batch < 1 || batch > 64 || max_ctx < 0 || max_new < 0 || max_new > max_ctx || branch < 1 || branch > 8) return 0;
+  if (!m || !m->has_head || batch < 1 || batch > 64 || max_ctx < 0 || max_new < 0 || max_new > max_ctx || branch < 1 ||
+      branch > 8)
+    return 0;
   WsLayout w;
   layout(m, batch, max_ctx, max_new, branch, w);
   return w.total;
@@ -430,6 +516,7 @@ struct SampleOpt {
 domino_status check_step_args(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
                               void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new) {
   if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
+  if (!m->has_head) return fail(DOMINO_ERR_INVALID_ARG, "model has no Domino head (created as a target decoder)");
   if (batch < 1 || batch > 64) return fail(DOMINO_ERR_INVALID_ARG, "batch must be in [1, 64]");
   if (!anchor_ids || !ctx_lens) return fail(DOMINO_ERR_INVALID_ARG, "anchor_ids/ctx_lens is NULL");
   if (max_ctx < 0) return fail(DOMINO_ERR_INVALID_ARG, "max_ctx must be >= 0");
@@ -441,16 +528,28 @@ domino_status check_step_args(domino_model_t m, int32_t batch, const int32_t *an
 
 // The masked block through the draft backbone, the final norm and the LM head
 // (with W1's H half): leaves [L_base | pad | P] in the workspace's LP.
-domino_status run_backbone(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
-                           void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new,
-                           const domino_debug *debug, char *ws, const WsLayout &w, hipStream_t st,
-                           bool clear_header = true) {
-  Dims D = make_dims(m, batch);
-  const Plans p = make_plans(m, batch, n_new);
+// How the B rows of each batch row enter the layers.  Default (the drafter):
+// the masked block [anchor, MASK, ...] at positions n + j, bidirectional block
+// attention, final norm and LM head over the B-1 draft rows.  A verify forward
+// gives a token and a position per row, a tree mask, stores its first n_store
+// rows' K/V into the cache at n + j, and takes every row through the LM head.
+struct RowSpec {
+  const int32_t *tokens = nullptr;
+  const int32_t *pos = nullptr;
+  const uint8_t *amask = nullptr;
+  int n_store = 0;
+  bool all_rows = false;
+};
+
+domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const RowSpec &spec,
+                         const int32_t *anchor_ids, const int32_t *ctx_lens, void *ctx_k, void *ctx_v,
+                         int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new, const domino_debug *debug,
+                         char *ws, const WsLayout &w, hipStream_t st, bool clear_header) {
+  const int batch = D.bs;
   auto F = [&](size_t off) { return (float *)(ws + off); };
   int32_t *err = (int32_t *)(ws + w.err);
   const char *base = (const char *)m->mem;
-  const int M = batch * D.B, Mh = batch * (D.B - 1);
+  const int M = batch * D.B, Mh = spec.all_rows ? M : batch * (D.B - 1);
   const int qd = D.nq * D.dh, kvd = D.nkv * D.dh, qkvw = qd + 2 * kvd;
   const size_t layer_elems = (size_t)batch * max_ctx * kvd;
 
@@ -474,7 +573,7 @@ domino_status run_backbone(domino_model_t m, int32_t batch, const int32_t *ancho
     prof_begin(m, DOMINO_KC_NORM, st);
     // (layer 0: the residual starts as the embedding of [anchor, MASK, ...])
     launch_add_norm(D, F(w.X), D.d, F(w.DNp), l > 0 ? p.down.ksplit : 0, rstride, m->attn_norm[l], F(w.A), D.d,
-                    M, D.d, false, l == 0 ? m->embed : nullptr, anchor_ids, err, st);
+                    M, D.d, false, l == 0 ? m->embed : nullptr, anchor_ids, err, st, spec.tokens);
     prof_end(m, DOMINO_KC_NORM, st);
 
     prof_begin(m, DOMINO_KC_QKV, st);
@@ -485,11 +584,11 @@ domino_status run_backbone(domino_model_t m, int32_t batch, const int32_t *ancho
 
     prof_begin(m, DOMINO_KC_ROPE, st);
     launch_qk_norm_rope(D, F(w.QKV), p.qkv.ksplit, (size_t)Ma * qkvw, m->q_norm[l], m->k_norm[l], ctx_lens, max_ctx,
-                        F(w.Q), F(w.Kb), F(w.Vb), n_new, (void *)ck, (void *)cv, err, st);
+                        F(w.Q), F(w.Kb), F(w.Vb), n_new, (void *)ck, (void *)cv, err, st, spec.pos, spec.n_store);
     prof_end(m, DOMINO_KC_ROPE, st);
 
     prof_begin(m, DOMINO_KC_ATTN, st);
-    launch_attention(D, F(w.Q), F(w.Kb), F(w.Vb), ck, cv, ctx_lens, max_ctx, F(w.attn), F(w.O), err, st);
+    launch_attention(D, F(w.Q), F(w.Kb), F(w.Vb), ck, cv, ctx_lens, max_ctx, F(w.attn), F(w.O), err, st, spec.amask);
     prof_end(m, DOMINO_KC_ATTN, st);
 
     prof_begin(m, DOMINO_KC_WO, st);
@@ -519,7 +618,7 @@ domino_status run_backbone(domino_model_t m, int32_t batch, const int32_t *ancho
   // residual += last down projection; final RMSNorm of the draft rows -> H
   float *H = (debug && debug->hidden) ? debug->hidden : F(w.H);
   prof_begin(m, DOMINO_KC_NORM, st);
-  launch_add_norm(D, F(w.X), D.d, F(w.DNp), p.down.ksplit, rstride, m->final_norm, H, D.d, Mh, D.d, true,
+  launch_add_norm(D, F(w.X), D.d, F(w.DNp), p.down.ksplit, rstride, m->final_norm, H, D.d, Mh, D.d, !spec.all_rows,
                   nullptr, nullptr, err, st);
   prof_end(m, DOMINO_KC_NORM, st);
 
@@ -529,13 +628,21 @@ domino_status run_backbone(domino_model_t m, int32_t batch, const int32_t *ancho
   GemmArgs a = gemm_args(base + m->lm.off, m->lm, 0, m->lm.NT, w.ldl, H, D.d, Mh, D.d, LP, w.ldl, p.lm);
   launch_gemm(m->bf16, EPI_STORE, a, p.lm, st);
   prof_end(m, DOMINO_KC_LMHEAD, st);
-  if (debug && debug->base_logits) {
+  if (!spec.all_rows && debug && debug->base_logits) {
     hipError_t ce = hipMemcpy2DAsync(debug->base_logits, (size_t)D.V * 4, LP, (size_t)w.ldl * 4, (size_t)D.V * 4, Mh,
                                      hipMemcpyDeviceToDevice, st);
     if (ce != hipSuccess) return fail(DOMINO_ERR_HIP, "copying base logits: %s", hipGetErrorString(ce));
   }
 
   return DOMINO_OK;
+}
+
+domino_status run_backbone(domino_model_t m, int32_t batch, const int32_t *anchor_ids, const int32_t *ctx_lens,
+                           void *ctx_k, void *ctx_v, int32_t max_ctx, const void *ctx_hidden_new, int32_t n_new,
+                           const domino_debug *debug, char *ws, const WsLayout &w, hipStream_t st,
+                           bool clear_header = true) {
+  return run_layers(m, make_dims(m, batch), make_plans(m, batch, n_new), RowSpec(), anchor_ids, ctx_lens, ctx_k, ctx_v,
+                    max_ctx, ctx_hidden_new, n_new, debug, ws, w, st, clear_header);
 }
 
 HeadArgs head_args(domino_model_t m, int32_t batch, int32_t branch, char *ws, const WsLayout &w,
@@ -674,7 +781,7 @@ void train_layout(const domino_model *m, int bs, int max_ctx, int max_new, Train
 }  // namespace
 
 size_t domino_train_workspace_bytes(domino_model_t m, int32_t batch, int32_t max_ctx, int32_t max_new) {
-  if (!m || batch < 1 || batch > 64 || max_ctx < 0 || max_new < 0 || max_new > max_ctx) return 0;
+  if (!m || !m->has_head || batch < 1 || batch > 64 || max_ctx < 0 || max_new < 0 || max_new > max_ctx) return 0;
   TrainLayout t;
   train_layout(m, batch, max_ctx, max_new, t);
   return t.total;
@@ -762,6 +869,85 @@ domino_status domino_train_forward(domino_model_t m, int32_t batch, const int32_
   he = launch_train_loss(t, m->bf16, st);
   prof_end(m, DOMINO_KC_TRAINLOSS, st);
   if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "training loss launch: %s", hipGetErrorString(he));
+  return DOMINO_OK;
+}
+
+size_t domino_target_workspace_bytes(domino_model_t m, int32_t batch, int32_t n_nodes, int32_t max_ctx) {
+  if (!m || m->has_head || batch < 1 || batch > 64 || n_nodes < 1 || n_nodes > 64 || max_ctx < n_nodes) return 0;
+  TargetLayout t;
+  if (!target_layout(m, batch, n_nodes, max_ctx, t)) return 0;
+  return t.total;
+}
+
+domino_status domino_target_verify(domino_model_t m, int32_t batch, int32_t n_nodes, const int32_t *node_token,
+                                   const int32_t *node_pos, const uint8_t *ancestor_mask, const int32_t *ctx_lens,
+                                   void *ctx_k, void *ctx_v, int32_t max_ctx, void *logits, domino_dtype logits_dtype,
+                                   void *workspace, size_t workspace_bytes, void *stream) {
+  if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
+  if (m->has_head) return fail(DOMINO_ERR_INVALID_ARG, "model is a drafter (create the target with domino_target_create)");
+  if (batch < 1 || batch > 64) return fail(DOMINO_ERR_INVALID_ARG, "batch must be in [1, 64]");
+  if (n_nodes < 1 || n_nodes > 64) return fail(DOMINO_ERR_INVALID_ARG, "n_nodes must be in [1, 64]");
+  if (!node_token || !node_pos || !ancestor_mask || !ctx_lens || !logits)
+    return fail(DOMINO_ERR_INVALID_ARG, "a node array, ctx_lens or logits is NULL");
+  if (max_ctx < n_nodes) return fail(DOMINO_ERR_INVALID_ARG, "max_ctx must leave room for the %d nodes", n_nodes);
+  if (!ctx_k || !ctx_v) return fail(DOMINO_ERR_INVALID_ARG, "ctx_k/ctx_v is NULL");
+  if (logits_dtype != DOMINO_F32 && logits_dtype != DOMINO_BF16) return fail(DOMINO_ERR_INVALID_ARG, "bad logits dtype");
+  if (!workspace) return fail(DOMINO_ERR_WORKSPACE, "workspace is NULL");
+  TargetLayout tl;
+  if (!target_layout(m, batch, n_nodes, max_ctx, tl))
+    return fail(DOMINO_ERR_UNSUPPORTED, "%d nodes exceed the largest block the attention supports for %d/%d heads",
+                n_nodes, m->D.nq, m->D.nkv);
+  if (workspace_bytes < tl.total)
+    return fail(DOMINO_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, tl.total);
+
+  hipStream_t st = (hipStream_t)stream;
+  char *ws = (char *)workspace;
+  const WsLayout &w = tl.w;
+  Dims D = make_dims(m, batch);
+  D.B = tl.Bp;
+  const int M = batch * tl.Bp;
+  const Plans p = make_plans_rows(m, M, M, M);
+  int32_t *err = (int32_t *)(ws + w.err);
+  int32_t *tok_p = (int32_t *)(ws + tl.tok), *pos_p = (int32_t *)(ws + tl.pos);
+  uint8_t *mask_p = (uint8_t *)(ws + tl.mask);
+  launch_fill_u32((uint32_t *)ws, w.hdr_words, 0u, st);
+  launch_target_prep(batch, n_nodes, tl.Bp, D.V, node_token, node_pos, ancestor_mask, tok_p, pos_p, mask_p, err, st);
+  RowSpec spec;
+  spec.tokens = tok_p;
+  spec.pos = pos_p;
+  spec.amask = mask_p;
+  spec.n_store = n_nodes;
+  spec.all_rows = true;
+  domino_status s = run_layers(m, D, p, spec, nullptr, ctx_lens, ctx_k, ctx_v, max_ctx, nullptr, 0, nullptr, ws, w, st,
+                               false);
+  if (s != DOMINO_OK) return s;
+  launch_target_out(batch, n_nodes, tl.Bp, D.V, (const float *)(ws + w.LP), w.ldl, logits,
+                    logits_dtype == DOMINO_BF16, st);
+  hipError_t he = hipGetLastError();
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "verify forward launch: %s", hipGetErrorString(he));
+  return DOMINO_OK;
+}
+
+domino_status domino_target_commit(domino_model_t m, int32_t batch, int32_t n_nodes, int32_t max_depth,
+                                   const int32_t *ctx_lens, const int32_t *accept_len, const int32_t *accepted_nodes,
+                                   void *ctx_k, void *ctx_v, int32_t max_ctx, int32_t *new_ctx_lens, void *workspace,
+                                   void *stream) {
+  if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
+  if (m->has_head) return fail(DOMINO_ERR_INVALID_ARG, "model is a drafter (create the target with domino_target_create)");
+  if (batch < 1 || batch > 64) return fail(DOMINO_ERR_INVALID_ARG, "batch must be in [1, 64]");
+  if (n_nodes < 1 || n_nodes > 64 || max_depth < 1 || max_depth > 63)
+    return fail(DOMINO_ERR_INVALID_ARG, "n_nodes must be in [1, 64] and max_depth in [1, 63]");
+  if (!ctx_lens || !accept_len || !accepted_nodes || !ctx_k || !ctx_v || !new_ctx_lens)
+    return fail(DOMINO_ERR_INVALID_ARG, "an argument array is NULL");
+  if ((const void *)new_ctx_lens == (const void *)ctx_lens)
+    return fail(DOMINO_ERR_INVALID_ARG, "new_ctx_lens must not alias ctx_lens");
+  if (max_ctx < n_nodes) return fail(DOMINO_ERR_INVALID_ARG, "max_ctx must be at least n_nodes");
+  if (!workspace) return fail(DOMINO_ERR_WORKSPACE, "workspace is NULL");
+  const Dims &D = m->D;
+  launch_target_commit(m->bf16, m->cfg.n_layers, batch, n_nodes, max_depth, ctx_lens, accept_len, accepted_nodes,
+                       ctx_k, ctx_v, max_ctx, D.nkv * D.dh, new_ctx_lens, (int32_t *)workspace, (hipStream_t)stream);
+  hipError_t he = hipGetLastError();
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "commit launch: %s", hipGetErrorString(he));
   return DOMINO_OK;
 }
 

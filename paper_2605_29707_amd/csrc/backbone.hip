@@ -31,8 +31,9 @@ __global__ __launch_bounds__(256) void embed_block_kernel(const WT *__restrict__
 // x[in_row] += sum of the `np` (<= 16) partial outputs (split order), then
 // y[i] = RMSNorm(x[in_row]) * gain.  With skip_anchor, output row i reads
 // input row i + i/(B-1) + 1 (the draft rows of each block) and x is not
-// written back.  With `tok` given, the row is first replaced by the embedding
-// row of its token (the anchor for block position 0, MASK otherwise).  One
+// written back.  With `embed` given, the row is first replaced by the embedding
+// row of its token: tokens[row] when `tokens` is given, else the anchor for
+// block position 0 and MASK otherwise.  One
 // workgroup per output row; a thread keeps its 16 columns in registers and
 // issues all of its loads together.
 template <typename WT, int MAXP>
@@ -42,7 +43,7 @@ __global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, in
                                                        float *__restrict__ y, int ldy, int width, float eps,
                                                        int skip_anchor, int depth, const WT *__restrict__ embed,
                                                        const int32_t *__restrict__ anchor, int mask_id, int V,
-                                                       int32_t *err) {
+                                                       int32_t *err, const int32_t *__restrict__ tokens) {
   const int i = blockIdx.x;
   const int in_row = skip_anchor ? i + i / depth + 1 : i;
   float *xr = x + (size_t)in_row * ldx;
@@ -52,7 +53,13 @@ __global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, in
   if (embed) {
     const int B = depth + 1;
     int tok = mask_id;
-    if (in_row % B == 0) {
+    if (tokens) {  // one token per row (a tree's nodes)
+      tok = tokens[in_row];
+      if (tok < 0 || tok >= V) {
+        if (threadIdx.x == 0) raise_error(err, DEV_BAD_TOKEN);
+        tok = tok < 0 ? 0 : V - 1;
+      }
+    } else if (in_row % B == 0) {
       tok = anchor[in_row / B];
       if (tok < 0 || tok >= V) {
         if (threadIdx.x == 0) raise_error(err, DEV_BAD_TOKEN);
@@ -164,7 +171,8 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
                                                            int nkv, int dh, float eps,
                                                            const double *__restrict__ inv_freq, int n_new,
                                                            WT *__restrict__ ck, WT *__restrict__ cv,
-                                                           int32_t *err) {
+                                                           int32_t *err, const int32_t *__restrict__ pos_rows,
+                                                           int n_store) {
   const int lane = threadIdx.x & 63;
   const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int nh = nq + 2 * nkv;
@@ -220,7 +228,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
   const int b = m / B, j = m % B;
   int n = ctx_lens[b];
   n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
-  const int pos = n + j;
+  const int pos = pos_rows ? pos_rows[m] : n + j;
   float *dst;
   if (hh < nq) {
     norm_rope_head<WT>(v, dh, qn, eps, pos, inv_freq, true, lane);
@@ -232,6 +240,17 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
     dst = Vb + ((size_t)m * nkv + (hh - nq - nkv)) * dh;
   }
   for (int q = 0; q < per; ++q) dst[lane + 64 * q] = v[q];
+  // the first n_store rows of each block also go to the cache at n + j (a
+  // verify forward leaves every node's K/V there for the commit)
+  if (j < n_store && hh >= nq) {
+    if (n + j < max_ctx) {
+      const bool isk = hh < nq + nkv;
+      WT *cd = (isk ? ck : cv) + (((size_t)b * max_ctx + n + j) * nkv + (hh - nq - (isk ? 0 : nkv))) * dh;
+      for (int q = 0; q < per; ++q) store_as(cd + lane + 64 * q, v[q]);
+    } else if (lane == 0) {
+      raise_error(err, DEV_BAD_CTX_LEN);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -255,8 +274,9 @@ DEVI float4 ld4_f32(const bf16_t *p) {
                      __uint_as_float(u.y & 0xffff0000u));
 }
 
-static int attn_ch(int G) { return G <= 4 ? 64 : 32; }
-int attn_chunk_len() { return 64; }
+// keys per chunk, by the query rows R = (n_q / n_kv) * B of a workgroup (the
+// partial kernel's dispatch and the merge must agree)
+static int attn_ch(int R) { return R >= 128 ? 32 : 64; }
 int attn_nchunks(int max_ctx, int B) { return (max_ctx + B + 31) / 32; }  // upper bound for any G
 size_t attn_part_floats(const Dims &D, int max_ctx) {
   return (size_t)D.bs * D.nq * D.B * attn_nchunks(max_ctx, D.B) * (D.dh + 2);
@@ -282,11 +302,16 @@ DEVI floatx4 mfma3(const bf16x8 &ah, const bf16x8 &al, const bf16x8 &bh, const b
 //   hi + lo bf16 parts (three passes, the lo*lo term dropped: ~2^-16 relative).
 // Q, K, P live in LDS row-major; V is staged transposed so a B fragment (8
 // consecutive keys of one dim) is one contiguous read.
-template <typename WT, int QT, int CH, int DH>
+// MASKED: block key k is visible to block query j only where amask[b][j][k] is
+// set (a verify forward's tree mask, [bs][B][B] bytes, B a multiple of 4);
+// context keys are always visible.  Rows whose keys in a chunk are all hidden
+// leave (max -inf, sum 0), which the merge weighs as zero.
+template <typename WT, int QT, int CH, int DH, bool MASKED>
 __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     const float *__restrict__ Q, const float *__restrict__ Kb, const float *__restrict__ Vb,
     const WT *__restrict__ ck, const WT *__restrict__ cv, const int32_t *__restrict__ ctx_lens,
-    int max_ctx, float *__restrict__ part, int B, int nq, int nkv, int nch, float scale) {
+    int max_ctx, float *__restrict__ part, int B, int nq, int nkv, int nch, float scale,
+    const uint8_t *__restrict__ amask) {
   constexpr int R = QT * 16;      // query rows of the group
   constexpr int KT = CH / 16;     // key tiles
   constexpr int DT = DH / 16;     // output dim tiles
@@ -300,6 +325,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   float *Ps = Vt + DH * CP;       // [R][CP]
   float *Rm = Ps + R * CP;        // [KT][R] partial row max
   float *Rl = Rm + KT * R;        // [KT][R] partial row sum
+  uint32_t *Ms = (uint32_t *)(Rl + KT * R);  // MASKED: [B][B] bytes of this batch row's tree mask
+  constexpr int kMaskIt = 64 * 64 / 4 / kAttnThreads;  // words per thread for B <= 64
 
   const int c = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int G = nq / nkv;
@@ -347,6 +374,13 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
       vc[q] = ld4_f32(cvb + vrow + 4 * dv);
       vbk[q] = *(const float4 *)(Vb + ((((size_t)b * B + min(max(kv2 - n, 0), B - 1)) * nkv) + kvh) * DH + 4 * dv);
     }
+    uint32_t mw[MASKED ? kMaskIt : 1];
+    if constexpr (MASKED) {  // unconditional loads at clamped word indices
+      const int words = B * B / 4;
+      const uint32_t *src = (const uint32_t *)amask + (size_t)b * words;
+#pragma unroll
+      for (int q = 0; q < kMaskIt; ++q) mw[q] = src[min(tid + q * kAttnThreads, words - 1)];
+    }
     float4 kv[NE], vv[NE];
 #pragma unroll
     for (int q = 0; q < NE; ++q) {
@@ -374,6 +408,11 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
       Vt[(4 * dv + 2) * CP + tv] = v.z;
       Vt[(4 * dv + 3) * CP + tv] = v.w;
     }
+    if constexpr (MASKED) {
+#pragma unroll
+      for (int q = 0; q < kMaskIt; ++q)
+        if (tid + q * kAttnThreads < B * B / 4) Ms[tid + q * kAttnThreads] = mw[q];
+    }
   }
   __syncthreads();
 
@@ -397,10 +436,16 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
 #pragma unroll
   for (int i = 0; i < QTW; ++i) {
     float m = -INFINITY;
+    const int jq = (16 * (qt0 + i) + cc) % B;  // the query's block row
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int key = 16 * kt + 4 * g + e;
-      sacc[i][e] = key < nk ? sacc[i][e] * scale : -INFINITY;
+      bool ok = key < nk;
+      if constexpr (MASKED) {
+        const int kb = c0 + key - n;  // block key index (< 0: a context key; < B wherever key < nk)
+        ok = ok && (kb < 0 || ((const uint8_t *)Ms)[jq * B + min(kb, B - 1)] != 0);
+      }
+      sacc[i][e] = ok ? sacc[i][e] * scale : -INFINITY;
       m = fmaxf(m, sacc[i][e]);
     }
     m = fmaxf(m, __shfl_xor(m, 16, 64));
@@ -418,7 +463,10 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int key = 16 * kt + 4 * g + e;
-      p[e] = key < nk ? expf(sacc[i][e] - m) : 0.f;
+      if constexpr (MASKED)  // hidden keys hold -inf (and m too if all of them are hidden)
+        p[e] = sacc[i][e] != -INFINITY ? expf(sacc[i][e] - m) : 0.f;
+      else
+        p[e] = key < nk ? expf(sacc[i][e] - m) : 0.f;
       l += p[e];
     }
     *(float4 *)(Ps + q * CP + 16 * kt + 4 * g) = make_float4(p[0], p[1], p[2], p[3]);
@@ -536,77 +584,90 @@ void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor,
 template <typename WT, int MAXP>
 static void add_norm_t(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
                        const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
-                       const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st) {
+                       const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st,
+                       const int32_t *tokens) {
   hipLaunchKernelGGL((add_norm_kernel<WT, MAXP>), dim3(rows), dim3(512), 0, st, x, ldx, parts, np, pstride,
                      (const WT *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1, (const WT *)embed, anchor,
-                     D.mask_id, D.V, err);
+                     D.mask_id, D.V, err, tokens);
 }
 
 void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
                      const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
-                     const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st) {
+                     const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st,
+                     const int32_t *tokens) {
   if (rows <= 0) return;
   if (np < 0 || np > 16) return;  // partial counts come from the GEMM planner (<= 16)
   if (D.bf16) {
-    if (np <= 8) add_norm_t<bf16_t, 8>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st);
-    else add_norm_t<bf16_t, 16>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st);
+    if (np <= 8) add_norm_t<bf16_t, 8>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
+    else add_norm_t<bf16_t, 16>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
   } else {
-    if (np <= 8) add_norm_t<float, 8>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st);
-    else add_norm_t<float, 16>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st);
+    if (np <= 8) add_norm_t<float, 8>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
+    else add_norm_t<float, 16>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
   }
 }
 
 template <typename WT, int MAXP>
 static void qk_norm_rope_t(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,
                            const void *k_norm, const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb, float *Vb,
-                           int n_new, void *ck, void *cv, int32_t *err, hipStream_t st) {
+                           int n_new, void *ck, void *cv, int32_t *err, hipStream_t st, const int32_t *pos_rows,
+                           int n_store) {
   const int M = D.bs * D.B;
   const int items = M * (D.nq + 2 * D.nkv) + D.bs * n_new * 2 * D.nkv;
   hipLaunchKernelGGL((qk_norm_rope_kernel<WT, MAXP>), dim3((items + 3) / 4), dim3(256), 0, st, qkv, np, pstride,
                      (const WT *)q_norm, (const WT *)k_norm, ctx_lens, max_ctx, Q, Kb, Vb, M, D.B, D.nq, D.nkv, D.dh,
-                     D.eps, D.inv_freq, n_new, (WT *)ck, (WT *)cv, err);
+                     D.eps, D.inv_freq, n_new, (WT *)ck, (WT *)cv, err, pos_rows, n_store);
 }
 
 void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,
                          const void *k_norm, const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb,
-                         float *Vb, int n_new, void *ck, void *cv, int32_t *err, hipStream_t st) {
+                         float *Vb, int n_new, void *ck, void *cv, int32_t *err, hipStream_t st,
+                         const int32_t *pos_rows, int n_store) {
   if (np < 1 || np > 16) return;  // partial counts come from the GEMM planner (1..16)
   if (D.bf16) {
-    if (np <= 8) qk_norm_rope_t<bf16_t, 8>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st);
-    else qk_norm_rope_t<bf16_t, 16>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st);
+    if (np <= 8) qk_norm_rope_t<bf16_t, 8>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st, pos_rows, n_store);
+    else qk_norm_rope_t<bf16_t, 16>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st, pos_rows, n_store);
   } else {
-    if (np <= 8) qk_norm_rope_t<float, 8>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st);
-    else qk_norm_rope_t<float, 16>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st);
+    if (np <= 8) qk_norm_rope_t<float, 8>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st, pos_rows, n_store);
+    else qk_norm_rope_t<float, 16>(D, qkv, np, pstride, q_norm, k_norm, ctx_lens, max_ctx, Q, Kb, Vb, n_new, ck, cv, err, st, pos_rows, n_store);
   }
 }
 
-template <typename WT, int RPT, int CH, int DH>
+template <typename WT, int RPT, int CH, int DH, bool MASKED>
 static void attn_launch_t(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
                           const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
-                          hipStream_t st) {
+                          const uint8_t *amask, hipStream_t st) {
   constexpr int R = RPT * 16, DP = DH + 4, CP = CH + 4, KT = CH / 16;
   const size_t lds =
-      sizeof(float) * ((size_t)R * DP + (size_t)CH * DP + (size_t)DH * CP + (size_t)R * CP + 2 * KT * R);
+      sizeof(float) * ((size_t)R * DP + (size_t)CH * DP + (size_t)DH * CP + (size_t)R * CP + 2 * KT * R) +
+      (MASKED ? (size_t)64 * 64 : 0);
   const float scale = 1.0f / sqrtf((float)DH);
   const int nc = (max_ctx + D.B + CH - 1) / CH;
-  (void)hipFuncSetAttribute((const void *)attn_partial_kernel<WT, RPT, CH, DH>,
+  (void)hipFuncSetAttribute((const void *)attn_partial_kernel<WT, RPT, CH, DH, MASKED>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  hipLaunchKernelGGL((attn_partial_kernel<WT, RPT, CH, DH>), dim3(nc, D.nkv, D.bs), dim3(kAttnThreads), lds, st,
-                     Q, Kb, Vb, (const WT *)ck, (const WT *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv, nch,
-                     scale);
+  hipLaunchKernelGGL((attn_partial_kernel<WT, RPT, CH, DH, MASKED>), dim3(nc, D.nkv, D.bs), dim3(kAttnThreads), lds,
+                     st, Q, Kb, Vb, (const WT *)ck, (const WT *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv, nch,
+                     scale, amask);
+}
+
+template <typename WT, int DH, bool MASKED>
+static bool attn_dispatch(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
+                          const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
+                          const uint8_t *amask, hipStream_t st) {
+  const int R = (D.nq / D.nkv) * D.B;
+  switch (R) {
+    case 32: attn_launch_t<WT, 2, 64, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st); return true;
+    case 64: attn_launch_t<WT, 4, 64, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st); return true;
+    case 128: attn_launch_t<WT, 8, 32, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st); return true;
+    default: return false;
+  }
 }
 
 template <typename WT, int DH>
-static bool attn_dispatch(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
-                          const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
-                          hipStream_t st) {
-  const int R = (D.nq / D.nkv) * D.B;
-  switch (R) {
-    case 32: attn_launch_t<WT, 2, 64, DH>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st); return true;
-    case 64: attn_launch_t<WT, 4, 64, DH>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st); return true;
-    case 128: attn_launch_t<WT, 8, 32, DH>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st); return true;
-    default: return false;
-  }
+static bool attn_dispatch_m(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
+                            const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
+                            const uint8_t *amask, hipStream_t st) {
+  if (amask) return attn_dispatch<WT, DH, true>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st);
+  return attn_dispatch<WT, DH, false>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, nullptr, st);
 }
 
 bool attn_supported(int nq, int nkv, int B) {
@@ -616,17 +677,16 @@ bool attn_supported(int nq, int nkv, int B) {
 
 void launch_attention(const Dims &D, const float *Q, const float *Kb, const float *Vb,
                       const void *ck, const void *cv, const int32_t *ctx_lens, int max_ctx,
-                      float *part, float *O, int32_t *err, hipStream_t st) {
+                      float *part, float *O, int32_t *err, hipStream_t st, const uint8_t *amask) {
   (void)err;
   const int nch = attn_nchunks(max_ctx, D.B);
-  const int G = D.nq / D.nkv;
-  const int CH = attn_ch(G);
+  const int CH = attn_ch((D.nq / D.nkv) * D.B);
   if (D.dh == 128) {
-    if (D.bf16) attn_dispatch<bf16_t, 128>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st);
-    else attn_dispatch<float, 128>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st);
+    if (D.bf16) attn_dispatch_m<bf16_t, 128>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st);
+    else attn_dispatch_m<float, 128>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st);
   } else {
-    if (D.bf16) attn_dispatch<bf16_t, 64>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st);
-    else attn_dispatch<float, 64>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, st);
+    if (D.bf16) attn_dispatch_m<bf16_t, 64>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st);
+    else attn_dispatch_m<float, 64>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st);
   }
   const int items = D.bs * D.nq * D.B;
   if (D.dh == 128)

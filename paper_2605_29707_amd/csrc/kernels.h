@@ -49,21 +49,27 @@ void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor,
 // input row i + i/(B-1) + 1 (the draft rows of each block) and x is left as is.
 // With `embed` given, x rows are first set to the embedding rows of the masked
 // block ([anchor, MASK, ...]) before the (empty) partial sum.
+// With `tokens` given (and `embed`), row i's token is tokens[i] instead.
 void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
                      const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
-                     const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st);
+                     const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st,
+                     const int32_t *tokens = nullptr);
 // q/k RMSNorm + RoPE on the QKV projection (sum of np partials); writes
 // Q [M][nq][dh], Kb/Vb [M][nkv][dh].  The projection's rows M + b*n_new + i
 // (n_new appended context rows per batch row) have their K (k-norm, RoPE at
 // n_b - n_new + i) and V stored into this layer's cache ck/cv.
+// With pos_rows, block row m is rotated at pos_rows[m] instead of n_b + j; the
+// first n_store rows of each block also store their K/V into the cache at n_b + j.
 void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride, const void *q_norm,
                          const void *k_norm, const int32_t *ctx_lens, int max_ctx, float *Q, float *Kb,
-                         float *Vb, int n_new, void *ck, void *cv, int32_t *err, hipStream_t st);
-int attn_chunk_len();
+                         float *Vb, int n_new, void *ck, void *cv, int32_t *err, hipStream_t st,
+                         const int32_t *pos_rows = nullptr, int n_store = 0);
 int attn_nchunks(int max_ctx, int B);
+// amask (optional, [bs][B][B] bytes, B a multiple of 4 and at most 64): block
+// query j sees block key k only where amask[b][j][k] is set.
 void launch_attention(const Dims &D, const float *Q, const float *Kb, const float *Vb,
                       const void *ck, const void *cv, const int32_t *ctx_lens, int max_ctx,
-                      float *part, float *O, int32_t *err, hipStream_t st);
+                      float *part, float *O, int32_t *err, hipStream_t st, const uint8_t *amask = nullptr);
 size_t attn_part_floats(const Dims &D, int max_ctx);
 bool attn_supported(int nq, int nkv, int B);
 
@@ -131,6 +137,15 @@ struct TrainArgs {
 };
 int train_ce_grid(int V, int r, bool bf16);
 hipError_t launch_train_loss(const TrainArgs &t, bool bf16, hipStream_t st);
+
+// ---- target verify forward: input preparation, output copy, cache commit (target.hip)
+void launch_target_prep(int bs, int nn, int Bp, int V, const int32_t *tok, const int32_t *pos, const uint8_t *mask,
+                        int32_t *tok_p, int32_t *pos_p, uint8_t *mask_p, int32_t *err, hipStream_t st);
+void launch_target_out(int bs, int nn, int Bp, int V, const float *lg, int ldl, void *out, bool out_bf16,
+                       hipStream_t st);
+void launch_target_commit(bool bf16, int L, int bs, int nn, int max_depth, const int32_t *ctx_lens,
+                          const int32_t *accept_len, const int32_t *accepted_nodes, void *ck, void *cv, int max_ctx,
+                          int width, int32_t *new_lens, int32_t *err, hipStream_t st);
 
 // ---- tree and acceptance (tree.hip)
 void launch_build_tree(int bs, int depth, int beta, const int32_t *topk, const int32_t *anchor,

@@ -133,3 +133,19 @@ def test_train_entry_points_validation():
     base = (None, 1, p, p, p, p, 16, None, 0)
     st = lib.domino_train_forward(*base, p, 0.5, 15.0, p, None, None, p, 10**9, None)
     assert st == bd.DOMINO_ERR_INVALID_ARG and "model" in bd.last_error()
+
+
+def test_target_entry_points_validation():
+    lib = bd.load()
+    p = C.c_void_p(16)  # never dereferenced: validation fails first
+    h = C.c_void_p()
+    cfg = _cfg(gru_hidden=0, rank=0)        # head sizes are ignored for a target decoder
+    assert lib.domino_target_create(C.byref(cfg), None, C.byref(h)) == bd.DOMINO_ERR_INVALID_ARG
+    assert "weights" in bd.last_error() and h.value is None
+    cfg = _cfg(head_dim=96)
+    assert lib.domino_target_create(C.byref(cfg), None, C.byref(h)) == bd.DOMINO_ERR_UNSUPPORTED
+    assert lib.domino_target_workspace_bytes(None, 1, 16, 1024) == 0
+    st = lib.domino_target_verify(None, 1, 16, p, p, p, p, p, p, 1024, p, bd.DOMINO_BF16, p, 10**9, None)
+    assert st == bd.DOMINO_ERR_INVALID_ARG and "model" in bd.last_error()
+    st = lib.domino_target_commit(None, 1, 16, 15, p, p, p, p, p, 1024, p, p, None)
+    assert st == bd.DOMINO_ERR_INVALID_ARG

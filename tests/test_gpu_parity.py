@@ -77,6 +77,23 @@ def test_tiny_bf16_batches(batch, beta):
     run.close()
 
 
+@pytest.mark.parametrize("nq,block", [(8, 32), (4, 64)])
+def test_tiny_large_blocks(nq, block):
+    """(n_q / n_kv) * block = 128 query rows per workgroup: the attention uses
+    32-key chunks there, and the chunk merge must use the same length (it once
+    took 64 whenever n_q / n_kv <= 4)."""
+    cfg = synth.get_config("tiny").with_(n_q_heads=nq, block=block, ctx_from_hidden=False, batch=2)
+    w = synth.make_weights(cfg, seed=12, gain_std=0.1)
+    inp = synth.make_inputs(cfg, seed=12, ctx_lens=np.array([128, 45], np.int32), max_ctx=128)
+    log(f"tiny nq={nq} block={block}")
+    run = GpuRun(cfg, w, 128, beta=1)
+    gpu = run.step(inp)
+    assert gpu["err"] == 0
+    ref = oracle_for(cfg, oracle.as_f64_weights(w), inp, gpu, 1)
+    check_against_oracle(cfg, gpu, ref, 1e-4, 1)
+    run.close()
+
+
 def test_teacher_forcing_and_perturbation_causality():
     cfg = synth.get_config("tiny").with_(ctx_from_hidden=False, batch=2)
     w = synth.make_weights(cfg, seed=3)
