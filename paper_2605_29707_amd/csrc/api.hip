@@ -129,7 +129,7 @@ Dims make_dims(const domino_model *m, int bs) {
 
 // ---- workspace layout of the draft step
 struct WsLayout {
-  size_t err, best, hdr_words, X, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
+  size_t err, best, hdr_words, X, X2, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
       praw, total;
   int GC, ldl;
 };
@@ -175,6 +175,7 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.hdr_words = o / 4;  // error word and best keys: cleared at every step
   const int qkvw = (D.nq + 2 * D.nkv) * D.dh;
   w.X = take((size_t)M * D.d * 4);
+  w.X2 = take((size_t)M * D.d * 4);
   const int Ma = M + bs * max_new;  // block rows, then the appended context rows
   w.A = take((size_t)Ma * D.d * 4);
   w.QKV = take((size_t)p.qkv.ksplit * Ma * qkvw * 4);
@@ -237,6 +238,7 @@ bool target_layout(const domino_model *m, int bs, int nn, int max_ctx, TargetLay
   w.hdr_words = o / 4;
   const int qkvw = (D.nq + 2 * D.nkv) * D.dh;
   w.X = take((size_t)M * D.d * 4);
+  w.X2 = take((size_t)M * D.d * 4);
   w.A = take((size_t)M * D.d * 4);
   w.QKV = take((size_t)p.qkv.ksplit * M * qkvw * 4);
   w.Q = take((size_t)M * D.nq * D.dh * 4);
@@ -566,14 +568,18 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
   }
 
   const size_t rstride = (size_t)M * D.d;  // partial-output stride of the residual projections
+  // the residual stream ping-pongs between two buffers: every RMSNorm launch
+  // reads one and writes the updated residual to the other
+  float *xc = F(w.X), *xn = F(w.X2);
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const char *ck = (const char *)ctx_k + l * layer_elems * m->esz;
     const char *cv = (const char *)ctx_v + l * layer_elems * m->esz;
     // residual += previous layer's down projection, then the attention RMSNorm
     prof_begin(m, DOMINO_KC_NORM, st);
     // (layer 0: the residual starts as the embedding of [anchor, MASK, ...])
-    launch_add_norm(D, F(w.X), D.d, F(w.DNp), l > 0 ? p.down.ksplit : 0, rstride, m->attn_norm[l], F(w.A), D.d,
+    launch_add_norm(D, xc, xn, D.d, F(w.DNp), l > 0 ? p.down.ksplit : 0, rstride, m->attn_norm[l], F(w.A), D.d,
                     M, D.d, false, l == 0 ? m->embed : nullptr, anchor_ids, err, st, spec.tokens);
+    std::swap(xc, xn);
     prof_end(m, DOMINO_KC_NORM, st);
 
     prof_begin(m, DOMINO_KC_QKV, st);
@@ -598,8 +604,9 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
 
     // residual += attention output, then the FFN RMSNorm
     prof_begin(m, DOMINO_KC_NORM, st);
-    launch_add_norm(D, F(w.X), D.d, F(w.WOp), p.wo.ksplit, rstride, m->ffn_norm[l], F(w.A), D.d, M, D.d, false,
+    launch_add_norm(D, xc, xn, D.d, F(w.WOp), p.wo.ksplit, rstride, m->ffn_norm[l], F(w.A), D.d, M, D.d, false,
                     nullptr, nullptr, err, st);
+    std::swap(xc, xn);
     prof_end(m, DOMINO_KC_NORM, st);
 
     prof_begin(m, DOMINO_KC_GATEUP, st);
@@ -618,7 +625,7 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
   // residual += last down projection; final RMSNorm of the draft rows -> H
   float *H = (debug && debug->hidden) ? debug->hidden : F(w.H);
   prof_begin(m, DOMINO_KC_NORM, st);
-  launch_add_norm(D, F(w.X), D.d, F(w.DNp), p.down.ksplit, rstride, m->final_norm, H, D.d, Mh, D.d, !spec.all_rows,
+  launch_add_norm(D, xc, nullptr, D.d, F(w.DNp), p.down.ksplit, rstride, m->final_norm, H, D.d, Mh, D.d, !spec.all_rows,
                   nullptr, nullptr, err, st);
   prof_end(m, DOMINO_KC_NORM, st);
 

@@ -28,25 +28,31 @@ __global__ __launch_bounds__(256) void embed_block_kernel(const WT *__restrict__
   for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = to_f32(src[c]);
 }
 
-// x[in_row] += sum of the `np` (<= 16) partial outputs (split order), then
-// y[i] = RMSNorm(x[in_row]) * gain.  With skip_anchor, output row i reads
-// input row i + i/(B-1) + 1 (the draft rows of each block) and x is not
-// written back.  With `embed` given, the row is first replaced by the embedding
+// x_out[in_row] = x[in_row] + the `np` (<= 16) partial outputs (split order),
+// y[i] = RMSNorm(x_out[in_row]) * gain.  With skip_anchor, output row i reads
+// input row i + i/(B-1) + 1 (the draft rows of each block); a null x_out skips
+// the residual write.  x and x_out are distinct buffers (ping-pong): the
+// workgroups of one row each write a slice while the others still read x.  With `embed` given, the row is first replaced by the embedding
 // row of its token: tokens[row] when `tokens` is given, else the anchor for
 // block position 0 and MASK otherwise.  One
 // workgroup per output row; a thread keeps its 16 columns in registers and
 // issues all of its loads together.
 template <typename WT, int MAXP>
-__global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, int ldx,
+__global__ __launch_bounds__(512) void add_norm_kernel(const float *__restrict__ x, float *__restrict__ x_out,
+                                                       int ldx,
                                                        const float *__restrict__ parts, int np,
                                                        size_t pstride, const WT *__restrict__ gain,
                                                        float *__restrict__ y, int ldy, int width, float eps,
                                                        int skip_anchor, int depth, const WT *__restrict__ embed,
                                                        const int32_t *__restrict__ anchor, int mask_id, int V,
-                                                       int32_t *err, const int32_t *__restrict__ tokens) {
-  const int i = blockIdx.x;
+                                                       int32_t *err, const int32_t *__restrict__ tokens,
+                                                       int nsplit) {
+  // nsplit workgroups per row: each forms the whole row's sum of squares but
+  // writes only its slice of the columns
+  const int i = blockIdx.x / nsplit, part = blockIdx.x % nsplit;
+  const int cs = width / nsplit;  // columns per slice (a multiple of 8)
   const int in_row = skip_anchor ? i + i / depth + 1 : i;
-  float *xr = x + (size_t)in_row * ldx;
+  const float *xr = x + (size_t)in_row * ldx;
   const float *pr = parts + (size_t)in_row * ldx;
   constexpr int PER = 8, IT = 2;
   const WT *er = nullptr;
@@ -98,9 +104,10 @@ __global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, in
         v[it][0] += pa[p].x; v[it][1] += pa[p].y; v[it][2] += pa[p].z; v[it][3] += pa[p].w;
         v[it][4] += pc[p].x; v[it][5] += pc[p].y; v[it][6] += pc[p].z; v[it][7] += pc[p].w;
       }
-    if ((np > 0 || er) && !skip_anchor) {
-      *(float4 *)(xr + c0) = make_float4(v[it][0], v[it][1], v[it][2], v[it][3]);
-      *(float4 *)(xr + c0 + 4) = make_float4(v[it][4], v[it][5], v[it][6], v[it][7]);
+    if (x_out && c0 / cs == part) {  // the updated residual goes to the other buffer (other slices still read x)
+      float *xo = x_out + (size_t)in_row * ldx;
+      *(float4 *)(xo + c0) = make_float4(v[it][0], v[it][1], v[it][2], v[it][3]);
+      *(float4 *)(xo + c0 + 4) = make_float4(v[it][4], v[it][5], v[it][6], v[it][7]);
     }
 #pragma unroll
     for (int e = 0; e < PER; ++e) ss = fmaf(v[it][e], v[it][e], ss);
@@ -115,7 +122,7 @@ __global__ __launch_bounds__(512) void add_norm_kernel(float *__restrict__ x, in
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     const int c0 = (threadIdx.x + it * blockDim.x) * PER;
-    if (c0 >= width) continue;
+    if (c0 >= width || c0 / cs != part) continue;
     float o[PER];
 #pragma unroll
     for (int e = 0; e < PER; ++e) o[e] = v[it][e] * inv * to_f32(gain[c0 + e]);
@@ -582,27 +589,32 @@ void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor,
 }
 
 template <typename WT, int MAXP>
-static void add_norm_t(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
+static void add_norm_t(const Dims &D, const float *x, float *x_out, int ldx, const float *parts, int np, size_t pstride,
                        const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
                        const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st,
                        const int32_t *tokens) {
-  hipLaunchKernelGGL((add_norm_kernel<WT, MAXP>), dim3(rows), dim3(512), 0, st, x, ldx, parts, np, pstride,
+  // a few workgroups per row when there are few rows: a GEMM that reads rows
+  // written by one workgroup each was measured ~5 us slower (QKV after the
+  // attention RMSNorm at 16 rows), with two or more per row it is not
+  int split = 1;
+  while (split < 4 && rows * split < 64 && width % (2 * split * 8) == 0) split *= 2;
+  hipLaunchKernelGGL((add_norm_kernel<WT, MAXP>), dim3(rows * split), dim3(512), 0, st, x, x_out, ldx, parts, np, pstride,
                      (const WT *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1, (const WT *)embed, anchor,
-                     D.mask_id, D.V, err, tokens);
+                     D.mask_id, D.V, err, tokens, split);
 }
 
-void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
+void launch_add_norm(const Dims &D, const float *x, float *x_out, int ldx, const float *parts, int np, size_t pstride,
                      const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
                      const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st,
                      const int32_t *tokens) {
   if (rows <= 0) return;
   if (np < 0 || np > 16) return;  // partial counts come from the GEMM planner (<= 16)
   if (D.bf16) {
-    if (np <= 8) add_norm_t<bf16_t, 8>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
-    else add_norm_t<bf16_t, 16>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
+    if (np <= 8) add_norm_t<bf16_t, 8>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
+    else add_norm_t<bf16_t, 16>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
   } else {
-    if (np <= 8) add_norm_t<float, 8>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
-    else add_norm_t<float, 16>(D, x, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
+    if (np <= 8) add_norm_t<float, 8>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
+    else add_norm_t<float, 16>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
   }
 }
 

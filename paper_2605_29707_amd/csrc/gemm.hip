@@ -15,7 +15,8 @@
 // per fragment; products are exact in fp32), so the GEMM keeps fp32 accuracy.
 //
 // Work split: a workgroup of 8 waves owns 8/WPT consecutive tiles (WPT waves
-// per tile) and a range of K chunks of KCM k-steps.  The activations of a
+// per tile) and a range of K chunks of KCM k-steps (16/MT, or 8/MT: half the
+// registers, two workgroups per CU, finer K splits).  The activations of a
 // chunk are staged once per workgroup into LDS, already split into hi/lo
 // fragments, and shared by all its waves; weight fragments of the next chunk
 // are in flight while the current chunk is multiplied.  Loads are issued
@@ -85,11 +86,10 @@ DEVI void load_xfrag(const float *__restrict__ X, int ldx, int M, int K, int m, 
 
 constexpr int kWaves = 8;
 
-template <typename WT, int MT, int WPT, int EPI>
+template <typename WT, int MT, int WPT, int EPI, int KCM>
 __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
   constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP;
   constexpr int XF = XStage<WT>::XF;
-  constexpr int KCM = 16 / MT;           // k-steps per chunk
   constexpr int KW = KCM / WPT;          // k-steps per wave per chunk
   constexpr int TW = kWaves / WPT;       // tiles per workgroup
   constexpr int ITEMS = KCM * MT * 64;   // staged fragments per chunk
@@ -247,38 +247,51 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
 GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu, int max_split) {
   GemmPlan p;
   p.MT = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-  const int kcm = 16 / p.MT;
-  const int nch = (KS + kcm - 1) / kcm;
   p.mgroups = (M + 16 * p.MT - 1) / (16 * p.MT);
   p.WPT = 1;
-  // Two waves per tile (more workgroups for grids that leave CUs idle) was
-  // measured slower: it doubles the activation staging per weight byte.
-  (void)kcm;
-  if (max_split > 1) p.WPT = 1;
-  const int tw = 8 / p.WPT;
-  p.groups = (ntiles + tw - 1) / tw;
+  p.groups = (ntiles + 7) / 8;
   p.ksplit = 1;
-  // split K (largest divisor of the chunk count) until about 1.5 workgroups per CU
-  for (int s = 2; s <= std::min(nch, max_split); ++s)
-    if (nch % s == 0 && p.groups * p.mgroups * s <= (3 * n_cu) / 2) p.ksplit = s;
+  p.kcm = 16 / p.MT;
   (void)epi;
+  // Cost model (bytes through the busiest CU): workgroups land evenly over the
+  // CUs, so a CU streams ceil(W / n_cu) workgroups' weight slices; K-split
+  // partial outputs are written and read back once (spread over all CUs).
+  // Candidates: chunks of 16/MT or 8/MT k-steps, any split dividing the chunk count.
+  const int N = ntiles * 16;
+  double best = 1e300;
+  for (int kcm : {16 / p.MT, 8 / p.MT}) {
+    const int nch = (KS + kcm - 1) / kcm;
+    for (int s = 1; s <= std::min(nch, max_split); ++s) {
+      if (nch % s) continue;
+      const long W = (long)p.groups * p.mgroups * s;
+      const double wg_bytes = 8.0 * (nch / s) * kcm * 1024.0;
+      const double cost = (double)((W + n_cu - 1) / n_cu) * wg_bytes +
+                          (s > 1 ? 2.0 * s * (double)M * N * 4.0 / n_cu : 0.0);
+      if (cost < best * 0.999) {
+        best = cost;
+        p.ksplit = s;
+        p.kcm = kcm;
+      }
+    }
+  }
   return p;
 }
 
-template <typename WT, int MT, int WPT, int EPI>
+template <typename WT, int MT, int WPT, int EPI, int KCM>
 static void launch_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
   dim3 grid(p.groups, p.ksplit, p.mgroups);
-  hipLaunchKernelGGL((gemm_kernel<WT, MT, WPT, EPI>), grid, dim3(kWaves * 64), 0, st, a);
+  hipLaunchKernelGGL((gemm_kernel<WT, MT, WPT, EPI, KCM>), grid, dim3(kWaves * 64), 0, st, a);
 }
 
 template <typename WT, int MT>
 static void launch_m(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
-  if (p.WPT == 1) {
-    if (epi == EPI_SWIGLU) launch_t<WT, MT, 1, EPI_SWIGLU>(a, p, st);
-    else launch_t<WT, MT, 1, EPI_STORE>(a, p, st);
+  constexpr int K1 = 16 / MT, K2 = 8 / MT;
+  if (p.kcm == K2) {
+    if (epi == EPI_SWIGLU) launch_t<WT, MT, 1, EPI_SWIGLU, K2>(a, p, st);
+    else launch_t<WT, MT, 1, EPI_STORE, K2>(a, p, st);
   } else {
-    if (epi == EPI_SWIGLU) launch_t<WT, MT, 2, EPI_SWIGLU>(a, p, st);
-    else launch_t<WT, MT, 2, EPI_STORE>(a, p, st);
+    if (epi == EPI_SWIGLU) launch_t<WT, MT, 1, EPI_SWIGLU, K1>(a, p, st);
+    else launch_t<WT, MT, 1, EPI_STORE, K1>(a, p, st);
   }
 }
 

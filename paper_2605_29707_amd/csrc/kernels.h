@@ -24,6 +24,7 @@ struct GemmArgs {
 
 struct GemmPlan {
   int MT, WPT, groups, mgroups, ksplit;
+  int kcm;  // k-steps per staged chunk (16/MT, or 8/MT for finer K splits)
 };
 
 // max_split = 1: one workgroup covers all of K (direct output); otherwise K
@@ -44,13 +45,14 @@ struct Dims {
 
 void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor, float *X,
                         int32_t *err, hipStream_t st);
-// x[map(row)] += sum of np partials (pstride floats apart), then
-// y[row] = rmsnorm(x[map(row)]) * gain; with skip_anchor, output row i reads
-// input row i + i/(B-1) + 1 (the draft rows of each block) and x is left as is.
+// x_out[map(row)] = x[map(row)] + sum of np partials (pstride floats apart),
+// y[row] = rmsnorm(x_out[map(row)]) * gain; with skip_anchor, output row i
+// reads input row i + i/(B-1) + 1 (the draft rows of each block).  x_out
+// (null: not written) must not alias x.
 // With `embed` given, x rows are first set to the embedding rows of the masked
 // block ([anchor, MASK, ...]) before the (empty) partial sum.
 // With `tokens` given (and `embed`), row i's token is tokens[i] instead.
-void launch_add_norm(const Dims &D, float *x, int ldx, const float *parts, int np, size_t pstride,
+void launch_add_norm(const Dims &D, const float *x, float *x_out, int ldx, const float *parts, int np, size_t pstride,
                      const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
                      const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st,
                      const int32_t *tokens = nullptr);
