@@ -283,7 +283,7 @@ DEVI float4 ld4_f32(const bf16_t *p) {
 
 // keys per chunk, by the query rows R = (n_q / n_kv) * B of a workgroup (the
 // partial kernel's dispatch and the merge must agree)
-static int attn_ch(int R) { return R >= 128 ? 32 : 64; }
+static int attn_ch(int R) { return R >= 64 ? 32 : 64; }
 int attn_nchunks(int max_ctx, int B) { return (max_ctx + B + 31) / 32; }  // upper bound for any G
 size_t attn_part_floats(const Dims &D, int max_ctx) {
   return (size_t)D.bs * D.nq * D.B * attn_nchunks(max_ctx, D.B) * (D.dh + 2);
@@ -668,7 +668,7 @@ static bool attn_dispatch(const Dims &D, const float *Q, const float *Kb, const 
   const int R = (D.nq / D.nkv) * D.B;
   switch (R) {
     case 32: attn_launch_t<WT, 2, 64, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st); return true;
-    case 64: attn_launch_t<WT, 4, 64, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st); return true;
+    case 64: attn_launch_t<WT, 4, 32, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st); return true;
     case 128: attn_launch_t<WT, 8, 32, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st); return true;
     default: return false;
   }

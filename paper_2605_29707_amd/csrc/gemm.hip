@@ -84,17 +84,14 @@ DEVI void load_xfrag(const float *__restrict__ X, int ldx, int M, int K, int m, 
   }
 }
 
-constexpr int kWaves = 8;
-
-template <typename WT, int MT, int WPT, int EPI, int KCM>
+template <typename WT, int MT, int WPT, int EPI, int KCM, int kWaves>
 __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
   constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP;
   constexpr int XF = XStage<WT>::XF;
   constexpr int KW = KCM / WPT;          // k-steps per wave per chunk
   constexpr int TW = kWaves / WPT;       // tiles per workgroup
   constexpr int ITEMS = KCM * MT * 64;   // staged fragments per chunk
-  constexpr int IPT = ITEMS / (kWaves * 64);
-  static_assert(ITEMS % (kWaves * 64) == 0, "staging split");
+  constexpr int IPT = (ITEMS + kWaves * 64 - 1) / (kWaves * 64);
 
   __shared__ u32x4 xs[2][KCM][MT][64][XF];
   __shared__ floatx4 xch[kWaves][MT][64];
@@ -126,7 +123,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
   auto load_x = [&](float4 (&v)[IPT][EPL / 4], int c) {
 #pragma unroll
     for (int q = 0; q < IPT; ++q) {
-      const int it = tid + q * kWaves * 64;
+      const int it = min(tid + q * kWaves * 64, ITEMS - 1);  // clamped: loads stay unconditional
       const int l = it & 63, mt = (it >> 6) % MT, s = (it >> 6) / MT;
       const int m = mbase + mt * 16 + (l & 15);
       const int k0 = (c * KCM + s) * KSTEP + (l >> 4) * EPL;
@@ -137,6 +134,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int q = 0; q < IPT; ++q) {
       const int it = tid + q * kWaves * 64;
+      if (ITEMS % (kWaves * 64) != 0 && it >= ITEMS) continue;
       const int l = it & 63, mt = (it >> 6) % MT, s = (it >> 6) / MT;
       XStage<WT>::put(&xs[buf][s][mt][l][0], v[q]);
     }
@@ -257,41 +255,52 @@ GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu, int max_split) 
   // CUs, so a CU streams ceil(W / n_cu) workgroups' weight slices; K-split
   // partial outputs are written and read back once (spread over all CUs).
   // Candidates: chunks of 16/MT or 8/MT k-steps, any split dividing the chunk count.
+  // Workgroups of 8 or 6 waves (a wave per tile; 6 lets 1536 gate/up tiles
+  // fill 256 CUs exactly).
   const int N = ntiles * 16;
   double best = 1e300;
-  for (int kcm : {16 / p.MT, 8 / p.MT}) {
-    const int nch = (KS + kcm - 1) / kcm;
-    for (int s = 1; s <= std::min(nch, max_split); ++s) {
-      if (nch % s) continue;
-      const long W = (long)p.groups * p.mgroups * s;
-      const double wg_bytes = 8.0 * (nch / s) * kcm * 1024.0;
-      const double cost = (double)((W + n_cu - 1) / n_cu) * wg_bytes +
-                          (s > 1 ? 2.0 * s * (double)M * N * 4.0 / n_cu : 0.0);
-      if (cost < best * 0.999) {
-        best = cost;
-        p.ksplit = s;
-        p.kcm = kcm;
+  p.nw = 8;
+  for (int nw : {8, 6}) {
+    const int groups = (ntiles + nw - 1) / nw;
+    for (int kcm : {16 / p.MT, 8 / p.MT}) {
+      const int nch = (KS + kcm - 1) / kcm;
+      for (int s = 1; s <= std::min(nch, max_split); ++s) {
+        if (nch % s) continue;
+        const long W = (long)groups * p.mgroups * s;
+        const double wg_bytes = (double)nw * (nch / s) * kcm * 1024.0;
+        const double cost = (double)((W + n_cu - 1) / n_cu) * wg_bytes +
+                            (s > 1 ? 2.0 * s * (double)M * N * 4.0 / n_cu : 0.0);
+        if (cost < best * 0.999) {
+          best = cost;
+          p.ksplit = s;
+          p.kcm = kcm;
+          p.nw = nw;
+          p.groups = groups;
+        }
       }
     }
   }
   return p;
 }
 
-template <typename WT, int MT, int WPT, int EPI, int KCM>
+template <typename WT, int MT, int EPI, int KCM>
 static void launch_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
   dim3 grid(p.groups, p.ksplit, p.mgroups);
-  hipLaunchKernelGGL((gemm_kernel<WT, MT, WPT, EPI, KCM>), grid, dim3(kWaves * 64), 0, st, a);
+  if (p.nw == 6)
+    hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 6>), grid, dim3(6 * 64), 0, st, a);
+  else
+    hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 8>), grid, dim3(8 * 64), 0, st, a);
 }
 
 template <typename WT, int MT>
 static void launch_m(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
   constexpr int K1 = 16 / MT, K2 = 8 / MT;
   if (p.kcm == K2) {
-    if (epi == EPI_SWIGLU) launch_t<WT, MT, 1, EPI_SWIGLU, K2>(a, p, st);
-    else launch_t<WT, MT, 1, EPI_STORE, K2>(a, p, st);
+    if (epi == EPI_SWIGLU) launch_t<WT, MT, EPI_SWIGLU, K2>(a, p, st);
+    else launch_t<WT, MT, EPI_STORE, K2>(a, p, st);
   } else {
-    if (epi == EPI_SWIGLU) launch_t<WT, MT, 1, EPI_SWIGLU, K1>(a, p, st);
-    else launch_t<WT, MT, 1, EPI_STORE, K1>(a, p, st);
+    if (epi == EPI_SWIGLU) launch_t<WT, MT, EPI_SWIGLU, K1>(a, p, st);
+    else launch_t<WT, MT, EPI_STORE, K1>(a, p, st);
   }
 }
 
