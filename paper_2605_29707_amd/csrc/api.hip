@@ -5,6 +5,7 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <algorithm>
 #include <cmath>
 #include <cstring>
@@ -52,18 +53,19 @@ struct domino_model {
   int n_cu;
   int esz;
   // borrowed
-  const void *embed, *final_norm, *b_ih, *b_hh;
+  const void *embed, *final_norm;
   std::vector<const void *> attn_norm, q_norm, k_norm, ffn_norm;
   // owned
   void *mem = nullptr;
   size_t mem_bytes = 0;
   std::vector<Packed> qkv, wo, gateup, down;
   bool has_head = true;  // false: a target decoder (layers, embedding, LM head only)
+  bool persistent = true;  // DOMINO_ROLLOUT=loop selects the launch-pair rollout everywhere
   Packed lm, w2, w1s;
   // training forward: the state recurrence runs on a second stream beside the backbone
   hipStream_t side = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
-  size_t gtab_off, w_hh_off, w1_off, freq_off;
+  size_t gtab_off, w_hh_off, w1_off, bhh_off, freq_off;
   // profiling
   uint32_t prof_mask = 0;
   struct Ev {
@@ -129,7 +131,7 @@ Dims make_dims(const domino_model *m, int bs) {
 
 // ---- workspace layout of the draft step
 struct WsLayout {
-  size_t err, best, hdr_words, X, X2, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
+  size_t err, best, slots, hdr_words, X, X2, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
       praw, total;
   int GC, ldl;
 };
@@ -172,7 +174,8 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   };
   w.err = take(256);
   w.best = take((size_t)(D.B - 1) * bs * head_best_slots() * 8);
-  w.hdr_words = o / 4;  // error word and best keys: cleared at every step
+  w.slots = take((size_t)bs * (D.r + w.GC) * 8);  // persistent rollout: u and key slots
+  w.hdr_words = o / 4;  // error word (+ rollout abort flag), best keys, slots: cleared at every step
   const int qkvw = (D.nq + 2 * D.nkv) * D.dh;
   w.X = take((size_t)M * D.d * 4);
   w.X2 = take((size_t)M * D.d * 4);
@@ -282,10 +285,10 @@ GemmArgs gemm_args(const void *P, const Packed &pk, int tile0, int ntiles, int N
 
 namespace {
 
-// G = E W_ih^T for every vocabulary row (fp32), so the GRU input half of a
-// rollout step is a row gather.  Built with the same matrix-core GEMM as the
+// G = E W_ih^T + b_ih for every vocabulary row (fp32), so the GRU input half
+// of a rollout step is a row gather.  Built with the same matrix-core GEMM as the
 // projections, over the embedding in row chunks.
-hipError_t build_gtab(domino_model *m, const void *w_ih) {
+hipError_t build_gtab(domino_model *m, const void *w_ih, const void *b_ih) {
   const Dims &D = m->D;
   const int KSTEP = kstep(m);
   const int N = 3 * D.ds, K = D.d;
@@ -311,6 +314,7 @@ hipError_t build_gtab(domino_model *m, const void *w_ih) {
     const GemmPlan pl = plan_gemm(pk.NT, pk.KS, rows, EPI_STORE, m->n_cu, 1);
     const GemmArgs a = gemm_args(P, pk, 0, pk.NT, N, X, K, rows, K, G + (size_t)r0 * N, N, pl);
     launch_gemm(m->bf16, EPI_STORE, a, pl, nullptr);
+    launch_add_row_bias(G + (size_t)r0 * N, rows, N, b_ih, m->bf16, nullptr);
   }
   e = hipGetLastError();
   if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -348,6 +352,10 @@ domino_status create_impl(const domino_config *cfg, const domino_weights *w, dom
   domino_model *m = new domino_model();
   m->cfg = *cfg;
   m->has_head = with_head;
+  {
+    const char *ro = std::getenv("DOMINO_ROLLOUT");
+    m->persistent = !(ro && std::strcmp(ro, "loop") == 0);
+  }
   m->bf16 = cfg->dtype == DOMINO_BF16;
   m->esz = m->bf16 ? 2 : 4;
   Dims &D = m->D;
@@ -368,8 +376,6 @@ domino_status create_impl(const domino_config *cfg, const domino_weights *w, dom
   D.inv_freq = nullptr;  // set once the model memory exists
   m->embed = w->embed;
   m->final_norm = w->final_norm;
-  m->b_ih = w->gru_b_ih;
-  m->b_hh = w->gru_b_hh;
   for (int l = 0; l < L; ++l) {
     m->attn_norm.push_back(w->attn_norm[l]);
     m->q_norm.push_back(w->q_norm[l]);
@@ -416,6 +422,8 @@ domino_status create_impl(const domino_config *cfg, const domino_weights *w, dom
     off = align_up(off + (size_t)3 * D.ds * D.ds * m->esz);
     m->w1_off = off;
     off = align_up(off + (size_t)D.r * (D.d + D.ds) * m->esz);
+    m->bhh_off = off;
+    off = align_up(off + (size_t)3 * D.ds * 4);
   }
   m->freq_off = off;
   off = align_up(off + (size_t)(D.dh / 2) * sizeof(double));
@@ -457,7 +465,11 @@ domino_status create_impl(const domino_config *cfg, const domino_weights *w, dom
                 m->w1s.NT, m->w1s.KS, 1, 0, st);
   }
   he = hipGetLastError();
-  if (he == hipSuccess && with_head) he = build_gtab(m, w->gru_w_ih);
+  if (he == hipSuccess && with_head) he = build_gtab(m, w->gru_w_ih, w->gru_b_ih);
+  if (he == hipSuccess && with_head) {
+    launch_to_f32(w->gru_b_hh, m->bf16, (float *)(base + m->bhh_off), (size_t)3 * D.ds, nullptr);
+    he = hipGetLastError();
+  }
   if (he == hipSuccess) {
     // RoPE inverse frequencies theta^(-2i/dh), exact in fp64 on the host
     std::vector<double> f(D.dh / 2);
@@ -663,8 +675,7 @@ HeadArgs head_args(domino_model_t m, int32_t batch, int32_t branch, char *ws, co
   h.beta = branch;
   h.gtab = (const float *)(base + m->gtab_off);
   h.w_hh = base + m->w_hh_off;
-  h.b_ih = m->b_ih;
-  h.b_hh = m->b_hh;
+  h.bhh = (const float *)(base + m->bhh_off);
   h.w1 = base + m->w1_off;
   h.w2p = base + m->w2.off;
   h.P = LP + (w.ldl - D.r);
@@ -693,6 +704,9 @@ HeadArgs head_args(domino_model_t m, int32_t batch, int32_t branch, char *ws, co
   h.seed_lo = 0u;
   h.seed_hi = 0u;
   h.praw = F(w.praw);
+  h.uslot = (unsigned long long *)(ws + w.slots);
+  h.kslot = h.uslot + (size_t)batch * D.r;
+  h.abort_flag = (unsigned *)(ws + w.err + 128);
   return h;
 }
 
@@ -724,7 +738,10 @@ domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *an
   h.seed_lo = smp ? (uint32_t)smp->seed : 0u;
   h.seed_hi = smp ? (uint32_t)(smp->seed >> 32) : 0u;
   prof_begin(m, DOMINO_KC_HEADLOOP, st);
-  hipError_t he = launch_head(h, st);
+  hipError_t he = hipSuccess;
+  // one cooperative launch for the whole rollout where it applies, else a
+  // launch pair per position
+  if (!m->persistent || !launch_head_persistent(h, m->n_cu, st)) he = launch_head(h, st);
   prof_end(m, DOMINO_KC_HEADLOOP, st);
   if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "head loop launch: %s", hipGetErrorString(he));
   he = hipGetLastError();

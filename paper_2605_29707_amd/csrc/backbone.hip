@@ -3,6 +3,8 @@
 // context hidden states into the KV cache, and split-KV block attention.
 // All arithmetic is fp32; RoPE angles are formed and range-reduced in fp64 so
 // that positions in the thousands keep full fp32 accuracy in the rotated values.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -719,6 +721,18 @@ void launch_to_f32(const void *src, bool bf16, float *dst, size_t n, hipStream_t
   const unsigned blocks = (unsigned)((n + 255) / 256);
   if (bf16) hipLaunchKernelGGL(to_f32_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st, (const bf16_t *)src, dst, n);
   else hipLaunchKernelGGL(to_f32_kernel<float>, dim3(blocks), dim3(256), 0, st, (const float *)src, dst, n);
+}
+
+template <typename WT>
+__global__ void add_row_bias_kernel(float *__restrict__ Y, size_t n, int N, const WT *__restrict__ bias) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    Y[i] += to_f32(bias[i % N]);
+}
+void launch_add_row_bias(float *Y, size_t rows, int N, const void *bias, bool bf16, hipStream_t st) {
+  const size_t n = rows * (size_t)N;
+  const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 65536);
+  if (bf16) hipLaunchKernelGGL(add_row_bias_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st, Y, n, N, (const bf16_t *)bias);
+  else hipLaunchKernelGGL(add_row_bias_kernel<float>, dim3(blocks), dim3(256), 0, st, Y, n, N, (const float *)bias);
 }
 
 __global__ void fill_u32_kernel(uint32_t *p, size_t n, uint32_t v) {

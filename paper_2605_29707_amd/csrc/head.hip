@@ -186,7 +186,6 @@ __global__ __launch_bounds__(256) void head_gru_kernel(HeadArgs h, int j) {
   const float *hprev = h.hbuf + (size_t)((j - 1) & 1) * bs * ds;
   float *hnext = h.hbuf + (size_t)(j & 1) * bs * ds;
   const WT *whh = (const WT *)h.w_hh;
-  const WT *bih = (const WT *)h.b_ih, *bhh = (const WT *)h.b_hh;
   const int nchunk = ds / EPL;  // EPL-element chunks per row
   for (int i0 = blockIdx.x * 4; i0 < ds; i0 += gridDim.x * 4) {
     const int i = i0 + wave;
@@ -235,10 +234,8 @@ __global__ __launch_bounds__(256) void head_gru_kernel(HeadArgs h, int j) {
         float hn = 0.f;
         if (live) {
           const float *gy = h.gtab + (size_t)ys[b] * 3 * ds;
-          const float gir = gy[i] + to_f32(bih[i]), giz = gy[ds + i] + to_f32(bih[ds + i]),
-                      gin = gy[2 * ds + i] + to_f32(bih[2 * ds + i]);
-          const float ghr = acc[0] + to_f32(bhh[i]), ghz = acc[1] + to_f32(bhh[ds + i]),
-                      ghn = acc[2] + to_f32(bhh[2 * ds + i]);
+          const float gir = gy[i], giz = gy[ds + i], gin = gy[2 * ds + i];  // b_ih is in G
+          const float ghr = acc[0] + h.bhh[i], ghz = acc[1] + h.bhh[ds + i], ghn = acc[2] + h.bhh[2 * ds + i];
           const float rg = sigm(gir + ghr), zg = sigm(giz + ghz);
           const float ng = tanhf(gin + rg * ghn);
           const float hold = j > 1 ? hprev[(size_t)b * ds + i] : 0.f;
@@ -368,9 +365,11 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
   }
   __syncthreads();
 
-  // ---- S_{j-1} = GRU(x = E[y_{j-1}], S_{j-2}), four state indices per item
-  const WT *bih = (const WT *)h.b_ih, *bhh = (const WT *)h.b_hh;
-  const float *ghp = h.ghbuf + (size_t)((j - 1) & 1) * bs * 3 * ds;  // W_hh S_{j-2}
+  // ---- S_{j-1} = GRU(x = E[y_{j-1}], S_{j-2}), four state indices per item.
+  // G holds E W_ih^T + b_ih; the stored gates hold W_hh S_{j-2} + b_hh (at j = 1,
+  // S = 0: the gates are b_hh).  Every load is unconditional (the position-1
+  // values are selected after), so none waits behind a branch.
+  const float *ghp = h.ghbuf + (size_t)((j - 1) & 1) * bs * 3 * ds;  // W_hh S_{j-2} + b_hh
   const float *sprev = h.hbuf + (size_t)(j & 1) * bs * ds;            // S_{j-2}
   float *scur = h.hbuf + (size_t)((j - 1) & 1) * bs * ds;             // S_{j-1}
   for (int it = tid; it < bs * ds / 4; it += kStateWaves * 64) {
@@ -380,21 +379,23 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
 #pragma unroll
     for (int q = 0; q < 3; ++q) {
       const float4 a = *(const float4 *)(gy + q * ds + i);
-      const float4 c = j > 1 ? *(const float4 *)(ghp + (size_t)b * 3 * ds + q * ds + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 c = *(const float4 *)(ghp + (size_t)b * 3 * ds + q * ds + i);
+      const float4 c0 = *(const float4 *)(h.bhh + q * ds + i);
       gi[q][0] = a.x; gi[q][1] = a.y; gi[q][2] = a.z; gi[q][3] = a.w;
-      gh[q][0] = c.x; gh[q][1] = c.y; gh[q][2] = c.z; gh[q][3] = c.w;
+      gh[q][0] = j > 1 ? c.x : c0.x; gh[q][1] = j > 1 ? c.y : c0.y;
+      gh[q][2] = j > 1 ? c.z : c0.z; gh[q][3] = j > 1 ? c.w : c0.w;
     }
     {
-      const float4 c = j > 1 ? *(const float4 *)(sprev + (size_t)b * ds + i) : make_float4(0.f, 0.f, 0.f, 0.f);
-      hold[0] = c.x; hold[1] = c.y; hold[2] = c.z; hold[3] = c.w;
+      const float4 c = *(const float4 *)(sprev + (size_t)b * ds + i);
+      hold[0] = j > 1 ? c.x : 0.f; hold[1] = j > 1 ? c.y : 0.f;
+      hold[2] = j > 1 ? c.z : 0.f; hold[3] = j > 1 ? c.w : 0.f;
     }
     float out[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int ii = i + e;
-      const float rg = sigm(gi[0][e] + to_f32(bih[ii]) + gh[0][e] + to_f32(bhh[ii]));
-      const float zg = sigm(gi[1][e] + to_f32(bih[ds + ii]) + gh[1][e] + to_f32(bhh[ds + ii]));
-      const float ng = tanhf(gi[2][e] + to_f32(bih[2 * ds + ii]) + rg * (gh[2][e] + to_f32(bhh[2 * ds + ii])));
+      const float rg = sigm(gi[0][e] + gh[0][e]);
+      const float zg = sigm(gi[1][e] + gh[1][e]);
+      const float ng = tanhf(gi[2][e] + rg * gh[2][e]);
       out[e] = (1.f - zg) * ng + zg * hold[e];
     }
     const float4 o = make_float4(out[0], out[1], out[2], out[3]);
@@ -440,7 +441,7 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
             const float x = h.P[((size_t)b * depth + (j - 1)) * h.ldp + row] + acc;
             h.ubuf[(size_t)b * h.u_ld + (size_t)(j - 1) * h.u_pos + row] = x / (1.f + expf(-x));
           } else {
-            ghn[(size_t)b * 3 * ds + (row - r)] = acc;
+            ghn[(size_t)b * 3 * ds + (row - r)] = acc + h.bhh[row - r];
           }
         }
       }
@@ -719,6 +720,415 @@ __global__ __launch_bounds__(64) void head_merge_kernel(HeadArgs h) {
     h.topk_ids[((size_t)b * depth + j) * beta + lane] = mi;
     h.topk_vals[((size_t)b * depth + j) * beta + lane] = mv;
   }
+}
+
+// ---------------------------------------------------------------------------
+// Persistent rollout (bf16 weights, r = 256, one or two batch rows, greedy): one
+// cooperative launch runs all B-1 positions.  Each workgroup keeps its slice
+// of W2 resident for the whole rollout (kPersTiles tiles per wave, the last
+// one in LDS, the rest in registers: 77.8 MB over 238 workgroups at the Qwen3
+// vocabulary) and its rows of [W1[:, d:]; W_hh] in LDS, so W2 leaves HBM once
+// per step instead of once per position.
+//
+// Workgroups exchange data through tagged 64-bit slots in the workspace
+// header (zeroed at every step), written with device-scope atomic stores and
+// polled with device-scope atomic loads by one wave; a slot is ready when its
+// top bits carry the position's tag, so a poll both waits and delivers:
+//   u slot [b][k]   (j << 32) | bits of u_j[k], written by the owner of row k
+//   key slot [b][g] (j << 50) | value(32) << 18 | (2^18 - 1 - id): workgroup
+//                   g's top-1 for position j; the maximum over g is the argmax
+//                   under (value desc, id asc)
+// The hidden gates W_hh S_{j-1} go out as plain device-scope stores before the
+// u slots (each thread waits for its own stores first), and every workgroup
+// owns a u row, so "all u slots ready" also means "all gates stored".
+// Waits are bounded: a timeout sets DEV_BARRIER_TIMEOUT and the abort flag,
+// and every workgroup leaves; the kernel always ends.
+// ---------------------------------------------------------------------------
+constexpr int kPersWaves = 8, kPersTiles = 5, kPersKS = 8, kPersRegTiles = kPersTiles - 1;
+constexpr unsigned kPollLimit = 1u << 22;
+constexpr int kKeyIdBits = 18;
+
+DEVI float ld_coherent(const float *p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+DEVI void st_coherent(float *p, float v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+DEVI unsigned long long ld_slot(const unsigned long long *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+DEVI void st_slot(unsigned long long *p, unsigned long long v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+DEVI unsigned long long pack_key50(float v, int id) {
+  uint32_t u = __float_as_uint(order_val(v));
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((unsigned long long)u << kKeyIdBits) | (unsigned long long)((1 << kKeyIdBits) - 1 - id);
+}
+DEVI int key50_id(unsigned long long k) { return (1 << kKeyIdBits) - 1 - (int)(k & ((1ull << kKeyIdBits) - 1)); }
+
+// Wave 0 polls `n` slots until each carries `tag` (top bits from `shift`);
+// lane l holds slots l, l+64, ... in w[].  Returns false on timeout / abort.
+template <int MAXQ>
+DEVI bool poll_tagged(const unsigned long long *slots, int n, unsigned long long tag, int shift,
+                      unsigned *abort_flag, int32_t *err, unsigned long long (&w)[MAXQ]) {
+  const int lane = threadIdx.x & 63;
+  unsigned spins = 0;
+  while (true) {
+#pragma unroll
+    for (int q = 0; q < MAXQ; ++q) w[q] = ld_slot(slots + min(lane + 64 * q, n - 1));
+    bool ready = true;
+#pragma unroll
+    for (int q = 0; q < MAXQ; ++q) ready = ready && (w[q] >> shift) == tag;
+    if (__all(ready)) return true;
+    if ((++spins & 63) == 0) {
+      if (__hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
+      if (spins > kPollLimit) {
+        if (lane == 0) {
+          __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          raise_error(err, DEV_BARRIER_TIMEOUT);
+        }
+        return false;
+      }
+    }
+  }
+}
+
+// BS: the largest batch the instantiation serves (1 or 2; arrays sized by it)
+template <int BS>
+__global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs h, int nr) {
+  using WT = bf16_t;
+  constexpr int EPL = 8, KSTEP = 32, XF = 2;
+  const Dims &D = h.D;
+  const int bs = D.bs, ds = D.ds, r = D.r, d = D.d, depth = D.B - 1, V = D.V;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, cc = lane & 15;
+  const int G = gridDim.x, NT = (V + 15) / 16;
+  const int nchunk = ds / EPL;  // 16-byte chunks of a row (<= 256 by the config check)
+  const int nrows_all = r + 3 * ds;
+  extern __shared__ __align__(16) unsigned char smem[];
+  u32x4 *rows = (u32x4 *)smem;                          // [nr][nchunk] rows of [W1s; W_hh]
+  float *S = (float *)(rows + (size_t)nr * nchunk);     // [bs][ds] the state
+  u32x4 *us = (u32x4 *)(S + (size_t)bs * ds);           // [KS][64][XF] u as B fragments
+  u32x4 *w2s = us + kPersKS * 64 * XF;                  // [waves][KS][64] each wave's last W2 tile
+  float4 *lbs = (float4 *)(w2s + kPersWaves * kPersKS * 64);  // [waves][tiles][64] this lane's L_base values
+  float *u_s = (float *)(lbs + kPersWaves * kPersTiles * 64);  // [bs][r] u of the position
+  __shared__ float best_v[kPersWaves][16], best_r[kPersWaves][16];
+  __shared__ int best_i[kPersWaves][16];
+  __shared__ int ys[kFusedBatch];
+  __shared__ int s_ok;
+  const WT *w1 = (const WT *)h.w1, *whh = (const WT *)h.w_hh;
+  const int tile0 = (blockIdx.x * kPersWaves + wave) * kPersTiles;  // this wave's tiles tile0 + q
+
+  // ---- resident operands, loaded once: W2 tiles, rows, b_ih
+  u32x4 wf[kPersRegTiles][kPersKS];
+  {
+    const u32x4 *w2p = (const u32x4 *)h.w2p;
+#pragma unroll
+    for (int q = 0; q < kPersTiles; ++q) {
+      const int t = min(tile0 + q, NT - 1);
+#pragma unroll
+      for (int s = 0; s < kPersKS; ++s) {
+        const u32x4 v = w2p[((size_t)t * kPersKS + s) * 64 + lane];
+        if (q < kPersRegTiles) wf[q < kPersRegTiles ? q : 0][s] = v;
+        else w2s[((size_t)wave * kPersKS + s) * 64 + lane] = v;
+      }
+    }
+  }
+  for (int e = tid; e < nr * nchunk; e += kPersWaves * 64) {
+    const int k = e / nchunk, ch = e % nchunk;
+    const int R = min(blockIdx.x + k * G, nrows_all - 1);
+    const WT *src = R < r ? w1 + (size_t)R * (d + ds) + d : whh + (size_t)(R - r) * ds;
+    rows[e] = *(const u32x4 *)(src + (size_t)ch * EPL);
+  }
+  for (int e = tid; e < bs * ds; e += kPersWaves * 64) S[e] = 0.f;
+  __syncthreads();
+
+  const int nit = bs * ds / 4;  // state items: four indices of one batch row
+  for (int j = 1; j <= depth; ++j) {
+    // L_base of this lane's row and tiles, straight from memory into LDS (no
+    // registers held; complete by the wait before the u slots are published)
+    {
+      const int bb = min(cc, bs - 1);
+#pragma unroll
+      for (int q = 0; q < kPersTiles; ++q) {
+        const int t = min(tile0 + q, NT - 1);
+        __builtin_amdgcn_global_load_lds(
+            (const void *)(h.Lbase + ((size_t)bb * depth + (j - 1)) * h.ldl + t * 16 + 4 * g),
+            (void __attribute__((address_space(3))) *)(lbs + ((size_t)wave * kPersTiles + q) * 64), 16, 0, 0);
+      }
+    }
+    // ---- y_{j-1}: anchor, forced token, or the argmax the previous wait delivered
+    if (tid < bs) {
+      int y;
+      if (j == 1) y = clamp_token(h.anchor[tid], V, h.err);
+      else if (h.forced) y = clamp_token(h.forced[(size_t)tid * depth + (j - 2)], V, h.err);
+      else y = ys[tid];
+      ys[tid] = y;
+    }
+    __syncthreads();
+    // ---- S_{j-1} = GRU(E[y_{j-1}], S_{j-2}) in place; items beyond one per thread
+    // (batches above 2 at d_s = 1024) load their gates here
+    for (int it = tid; it < nit; it += kPersWaves * 64) {
+      const int b = it / (ds / 4), i = (it % (ds / 4)) * 4;
+      // W_hh S_{j-2} + b_hh (stored by the previous position's row owners) and the G row, loaded together
+      float ghv[3][4];
+      {
+        const float *gb = h.ghbuf + (size_t)((j - 1) & 1) * bs * 3 * ds + (size_t)b * 3 * ds + i;
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+          const float4 c0 = *(const float4 *)(h.bhh + q * ds + i);  // the gates at j = 1 (S = 0)
+          const float v0 = ld_coherent(gb + q * ds), v1 = ld_coherent(gb + q * ds + 1);
+          const float v2 = ld_coherent(gb + q * ds + 2), v3 = ld_coherent(gb + q * ds + 3);
+          ghv[q][0] = j > 1 ? v0 : c0.x;
+          ghv[q][1] = j > 1 ? v1 : c0.y;
+          ghv[q][2] = j > 1 ? v2 : c0.z;
+          ghv[q][3] = j > 1 ? v3 : c0.w;
+        }
+      }
+      const float *gy = h.gtab + (size_t)ys[b] * 3 * ds + i;
+      const float4 g0 = *(const float4 *)gy, g1 = *(const float4 *)(gy + ds), g2 = *(const float4 *)(gy + 2 * ds);
+      const float gi[3][4] = {{g0.x, g0.y, g0.z, g0.w}, {g1.x, g1.y, g1.z, g1.w}, {g2.x, g2.y, g2.z, g2.w}};
+      float4 s4 = *(const float4 *)(S + (size_t)b * ds + i);
+      const float hold[4] = {s4.x, s4.y, s4.z, s4.w};
+      float out[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float rg = sigm(gi[0][e] + ghv[0][e]), zg = sigm(gi[1][e] + ghv[1][e]);
+        const float ng = tanhf(gi[2][e] + rg * ghv[2][e]);
+        out[e] = (1.f - zg) * ng + zg * hold[e];
+      }
+      s4 = make_float4(out[0], out[1], out[2], out[3]);
+      *(float4 *)(S + (size_t)b * ds + i) = s4;
+      if (blockIdx.x == 0 && h.states) *(float4 *)(h.states + ((size_t)b * depth + (j - 1)) * ds + i) = s4;
+    }
+    __syncthreads();
+    // ---- this workgroup's rows against S_{j-1}: gates of the next position (plain
+    // device-scope stores, b_hh added), then u into the tagged slots
+    float *gh_out = h.ghbuf + (size_t)(j & 1) * bs * 3 * ds;
+    for (int k = wave; k < nr; k += kPersWaves) {
+      const int R = blockIdx.x + k * G;
+      if (R >= nrows_all || (R >= r && j == depth)) continue;  // wave-uniform
+      float accb[BS];
+#pragma unroll
+      for (int b = 0; b < BS; ++b) accb[b] = 0.f;
+      for (int c = 0; c < 4; ++c) {
+        const int ch = lane + 64 * c;
+        if (ch >= nchunk) break;
+        float wfl[EPL];
+        unpack16<WT>(rows[(size_t)k * nchunk + ch], wfl);
+#pragma unroll
+        for (int b = 0; b < BS; ++b) {
+          if (b >= bs) break;
+          const float *sb = S + (size_t)b * ds + (size_t)ch * EPL;
+          const float4 s0 = *(const float4 *)sb, s1 = *(const float4 *)(sb + 4);
+          accb[b] = fmaf(wfl[0], s0.x, accb[b]);
+          accb[b] = fmaf(wfl[1], s0.y, accb[b]);
+          accb[b] = fmaf(wfl[2], s0.z, accb[b]);
+          accb[b] = fmaf(wfl[3], s0.w, accb[b]);
+          accb[b] = fmaf(wfl[4], s1.x, accb[b]);
+          accb[b] = fmaf(wfl[5], s1.y, accb[b]);
+          accb[b] = fmaf(wfl[6], s1.z, accb[b]);
+          accb[b] = fmaf(wfl[7], s1.w, accb[b]);
+        }
+      }
+      if (R >= r) {
+        const float bias = h.bhh[R - r];
+#pragma unroll
+        for (int b = 0; b < BS; ++b) {
+          if (b >= bs) break;
+          const float acc = wave_sum(accb[b]);
+          if (lane == 0) st_coherent(gh_out + (size_t)b * 3 * ds + (R - r), acc + bias);
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's gate stores are done
+    __syncthreads();                // ... and every thread's
+    for (int k = wave; k < nr; k += kPersWaves) {
+      const int R = blockIdx.x + k * G;
+      if (R >= r) continue;  // wave-uniform
+      for (int b = 0; b < bs; ++b) {
+        float acc = 0.f;
+        for (int c = 0; c < 4; ++c) {
+          const int ch = lane + 64 * c;
+          if (ch >= nchunk) break;
+          float wfl[EPL];
+          unpack16<WT>(rows[(size_t)k * nchunk + ch], wfl);
+          const float *sb = S + (size_t)b * ds + (size_t)ch * EPL;
+          const float4 s0 = *(const float4 *)sb, s1 = *(const float4 *)(sb + 4);
+          acc = fmaf(wfl[0], s0.x, acc);
+          acc = fmaf(wfl[1], s0.y, acc);
+          acc = fmaf(wfl[2], s0.z, acc);
+          acc = fmaf(wfl[3], s0.w, acc);
+          acc = fmaf(wfl[4], s1.x, acc);
+          acc = fmaf(wfl[5], s1.y, acc);
+          acc = fmaf(wfl[6], s1.z, acc);
+          acc = fmaf(wfl[7], s1.w, acc);
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) {
+          const float x = h.P[((size_t)b * depth + (j - 1)) * h.ldp + R] + acc;
+          const float u = x / (1.f + expf(-x));
+          st_slot(h.uslot + (size_t)b * r + R, ((unsigned long long)j << 32) | __float_as_uint(u));
+        }
+      }
+    }
+    // ---- wait for u (wave 0 polls all u slots; the slots deliver the values)
+    if (wave == 0) {
+      unsigned long long w[4 * BS];
+      const bool ok = poll_tagged<4 * BS>(h.uslot, bs * r, (unsigned long long)j, 32, h.abort_flag, h.err, w);
+#pragma unroll
+      for (int q = 0; q < 4 * BS; ++q) {
+        const int e = lane + 64 * q;
+        if (e < bs * r) u_s[e] = __uint_as_float((uint32_t)(w[q] & 0xffffffffu));
+      }
+      if (lane == 0) s_ok = ok;
+    }
+    __syncthreads();
+    if (!s_ok) return;
+    // ---- logits: u as B fragments (batch rows as the 16 columns) against the resident W2
+    {
+      const int l = tid & 63, s = tid >> 6;  // kPersKS * 64 == kPersWaves * 64 items, one per thread
+      const int bb = min(l & 15, bs - 1);
+      const float *src = u_s + (size_t)bb * r + s * KSTEP + (l >> 4) * EPL;
+      float4 uv[2] = {*(const float4 *)src, *(const float4 *)(src + 4)};
+      XStage<WT>::put(us + (size_t)tid * XF, uv);
+    }
+    __syncthreads();
+    floatx4 acc[kPersTiles][1];
+#pragma unroll
+    for (int q = 0; q < kPersTiles; ++q) acc[q][0] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < kPersKS; ++s) {
+      u32x4 xf[XF];
+#pragma unroll
+      for (int f = 0; f < XF; ++f) xf[f] = us[((size_t)s * 64 + lane) * XF + f];
+#pragma unroll
+      for (int q = 0; q < kPersRegTiles; ++q) Mac2<WT, 1>::step(wf[q][s], xf, acc[q]);
+      Mac2<WT, 1>::step(w2s[((size_t)wave * kPersKS + s) * 64 + lane], xf, acc[kPersRegTiles]);
+    }
+    // lane (g, cc) holds vocabulary ids 16 (tile0 + q) + 4 g + e of batch row cc
+    const bool rowok = cc < bs;
+    if (h.final_logits) {  // debug output
+#pragma unroll
+      for (int q = 0; q < kPersTiles; ++q) {
+        const float4 l4 = lbs[((size_t)wave * kPersTiles + q) * 64 + lane];
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int n = (tile0 + q) * 16 + 4 * g + e;
+          if (rowok && n < V) h.final_logits[((size_t)cc * depth + (j - 1)) * V + n] = lv[e] + acc[q][0][e];
+        }
+      }
+    }
+    {
+      float bv = -INFINITY;
+      int bi = INT_MAX;
+#pragma unroll
+      for (int q = 0; q < kPersTiles; ++q) {
+        const float4 l4 = lbs[((size_t)wave * kPersTiles + q) * 64 + lane];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int n = (tile0 + q) * 16 + 4 * g + e;
+          const float lbe = e == 0 ? l4.x : (e == 1 ? l4.y : (e == 2 ? l4.z : l4.w));
+          const float val = lbe + acc[q][0][e];
+          const bool ok = rowok && n < V;
+          const float ov = ok ? order_val(val) : -INFINITY;
+          const int nid = ok ? n : INT_MAX;
+          const bool take = better(ov, nid, bv, bi);
+          bv = take ? ov : bv;
+          bi = take ? nid : bi;
+        }
+      }
+#pragma unroll
+      for (int o = 16; o <= 32; o <<= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        const bool take = better(ov, oi, bv, bi);
+        bv = take ? ov : bv;
+        bi = take ? oi : bi;
+      }
+      if (g == 0) {
+        best_v[wave][cc] = bv;
+        best_i[wave][cc] = bi;
+      }
+    }
+    __syncthreads();
+    if (tid < bs) {
+      const int bb = tid;
+      float v = best_v[0][bb];
+      int id = best_i[0][bb];
+#pragma unroll
+      for (int w = 1; w < kPersWaves; ++w)
+        if (better(best_v[w][bb], best_i[w][bb], v, id)) {
+          v = best_v[w][bb];
+          id = best_i[w][bb];
+        }
+      const size_t o = ((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x;
+      h.pval[o] = v;
+      h.pid[o] = id;
+      // an empty slice (no valid id) publishes the smallest key
+      const unsigned long long key = id == INT_MAX ? 0ull : pack_key50(v, id);
+      st_slot(h.kslot + (size_t)bb * G + blockIdx.x, ((unsigned long long)j << 50) | key);
+    }
+    // ---- wait for every workgroup's top-1: the maximum key is y_j.  Also the
+    // guard that no workgroup writes the next position's slots while another
+    // still polls this position's, so it runs with forced tokens as well.
+    if (j < depth) {
+      if (wave == 0) {
+        unsigned long long w[4 * BS];
+        const bool ok = poll_tagged<4 * BS>(h.kslot, bs * G, (unsigned long long)j, 50, h.abort_flag, h.err, w);
+        // lane holds slots lane + 64 q: slot e = b * G + g
+        for (int b = 0; b < bs; ++b) {
+          unsigned long long best = 0;
+#pragma unroll
+          for (int q = 0; q < 4 * BS; ++q) {
+            const int e = lane + 64 * q;
+            const unsigned long long k = w[q] & ((1ull << 50) - 1);
+            if (e >= b * G && e < (b + 1) * G && e < bs * G) best = k > best ? k : best;
+          }
+#pragma unroll
+          for (int o = 32; o >= 1; o >>= 1) {
+            const unsigned long long other = __shfl_xor(best, o, 64);
+            best = other > best ? other : best;
+          }
+          if (lane == 0) ys[b] = min(max(key50_id(best), 0), V - 1);
+        }
+        if (lane == 0) s_ok = ok;
+      }
+      __syncthreads();
+      if (!s_ok) return;
+    }
+  }
+}
+
+bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st) {
+  const Dims &D = h.D;
+  // greedy, one or two batch rows (larger batches and temperature sampling run
+  // the launch-pair rollout: their register demand would spill here)
+  if (!D.bf16 || D.r != kPersKS * 32 || D.bs > 2 || h.beta != 1 || h.sample || D.ds % 32 || D.ds > 256 * 8 ||
+      D.V >= (1 << kKeyIdBits) || !h.uslot || !h.kslot || !h.abort_flag)
+    return false;
+  const int NT = (D.V + 15) / 16;
+  const int G = (NT + kPersWaves * kPersTiles - 1) / (kPersWaves * kPersTiles);
+  // every workgroup must own a u row (its u slot doubles as its "gates stored" signal),
+  // and the polls cover at most 4 * kFusedBatch slots per lane
+  if (G != h.GC || G > n_cu || G > D.r || G > 256) return false;  // polls: 4 slots per lane per batch row
+  const int nr = (D.r + 3 * D.ds + G - 1) / G;
+  const size_t lds = (size_t)nr * (D.ds / 8) * 16 + sizeof(float) * (size_t)D.bs * D.ds +
+                     sizeof(u32x4) * kPersKS * 64 * 2 + sizeof(u32x4) * kPersWaves * kPersKS * 64 +
+                     sizeof(float4) * kPersWaves * kPersTiles * 64 + sizeof(float) * (size_t)D.bs * D.r;
+  if (lds > 160 * 1024) return false;
+  const void *fn = D.bs == 1 ? (const void *)head_persist_kernel<1> : (const void *)head_persist_kernel<2>;
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  HeadArgs a = h;
+  int nrv = nr;
+  void *args[] = {&a, &nrv};
+  if (hipLaunchCooperativeKernel(fn, dim3(G), dim3(kPersWaves * 64), args, lds, st) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  hipLaunchKernelGGL(head_merge_kernel, dim3(D.B - 1, D.bs), dim3(64), 0, st, h);
+  return true;
 }
 
 static int logit_rows(const Dims &D) {

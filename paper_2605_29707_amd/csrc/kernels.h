@@ -80,9 +80,9 @@ bool attn_supported(int nq, int nkv, int B);
 struct HeadArgs {
   Dims D;
   int beta;
-  const float *gtab;     // [V][3ds] = E W_ih^T (built at model creation)
+  const float *gtab;     // [V][3ds] = E W_ih^T + b_ih (built at model creation)
   const void *w_hh;      // [3ds][ds]
-  const void *b_ih, *b_hh;
+  const float *bhh;      // b_hh in fp32 [3ds] (b_ih is folded into gtab)
   const void *w1;        // [r][d+ds]; the S half starts at column d
   const void *w2p;       // W2 packed (tile-major, KS = r / KSTEP)
   const float *P;        // [bs][B-1] rows of stride ldp: W1[:, :d] H_j
@@ -112,10 +112,19 @@ struct HeadArgs {
   float *praw;
   int32_t *err;
   int GC;                // workgroups of the logits kernel
+  // persistent rollout exchange (workspace header, zeroed at every step):
+  // u slots [bs][r] and per-workgroup best-key slots [bs][GC], each a 64-bit
+  // word tagged with the position; abort flag of its bounded waits
+  unsigned long long *uslot, *kslot;
+  unsigned *abort_flag;
 };
 int head_logits_grid(const Dims &D);
 int head_best_slots();
 hipError_t launch_head(const HeadArgs &h, hipStream_t st);
+// One cooperative launch for the whole rollout where the shapes allow it (bf16,
+// r = 256, batch <= 2, greedy branch 1, a grid that fits the device at one
+// workgroup per CU, vocabulary < 2^18); returns false (nothing launched) otherwise.
+bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st);
 // the state recurrence of every position, teacher-forced (no logits): u into
 // ubuf as above, or with skip_u only the states into `states`
 hipError_t launch_head_states(const HeadArgs &h, hipStream_t st);
@@ -168,6 +177,8 @@ void launch_philox_words(const uint32_t *ctr, uint64_t key, uint32_t *out, int n
 
 // misc
 void launch_to_f32(const void *src, bool bf16, float *dst, size_t n, hipStream_t st);
+// Y[r][n] += bias[n] for r < rows, n < N (row stride N)
+void launch_add_row_bias(float *Y, size_t rows, int N, const void *bias, bool bf16, hipStream_t st);
 void launch_fill_u32(uint32_t *p, size_t n, uint32_t v, hipStream_t st);
 
 }  // namespace dk

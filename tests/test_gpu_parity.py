@@ -274,3 +274,49 @@ def test_qwen3_8b_bs1_full_size_parity():
     n = check_against_oracle(cfg, gpu, ref, 2e-2, 1)
     log(f"top-1 positions checked: {n}")
     assert n >= 12
+
+
+@pytest.mark.parametrize("batch", [1, 2])
+def test_persistent_rollout_matches_launch_pair_rollout(batch, monkeypatch):
+    """bf16, r = 256, one or two batch rows, greedy: the rollout runs as one
+    cooperative launch with the W2 slice held on chip.  It must agree with the
+    launch-pair rollout (DOMINO_ROLLOUT=loop at model creation): the backbone
+    outputs bit for bit, states and logits to fp32 summation order, the drafted
+    tokens exactly away from near-ties; free-running and teacher-forced."""
+    cfg = synth.get_config("tiny").with_(dtype="bf16", batch=batch, ctx_from_hidden=False)
+    w = synth.make_weights(cfg, seed=21, gain_std=0.1)
+    inp = synth.make_inputs(cfg, seed=21)
+    f = synth.make_forced_tokens(cfg, seed=21)
+    monkeypatch.delenv("DOMINO_ROLLOUT", raising=False)
+    run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
+    a, af = run.step(inp), run.step(inp, forced=f)
+    run.close()
+    monkeypatch.setenv("DOMINO_ROLLOUT", "loop")
+    run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
+    b, bf = run.step(inp), run.step(inp, forced=f)
+    run.close()
+    for x, y, forced in ((a, b, False), (af, bf, True)):
+        assert x["err"] == 0 and y["err"] == 0
+        for k in ("hidden", "base_logits"):
+            np.testing.assert_array_equal(x[k], y[k], err_msg=k)
+        # a free-running rollout follows its own tokens: positions after the first
+        # differing token (a near-tie, which must be one) are not comparable
+        upto = np.full(batch, cfg.depth)
+        if not forced:
+            for r in range(batch):
+                diff = np.nonzero(x["topk_ids"][r, :, 0] != y["topk_ids"][r, :, 0])[0]
+                if diff.size:
+                    j = diff[0]
+                    s = np.sort(y["final_logits"][r, j])
+                    assert s[-1] - s[-2] < 1e-3, (r, j)
+                    upto[r] = j + 1
+        for r in range(batch):
+            n = upto[r]
+            es = float(np.abs(x["states"][r, :n] - y["states"][r, :n]).max())
+            el = float(np.abs(x["final_logits"][r, :n] - y["final_logits"][r, :n]).max())
+            log(f"persistent vs launch-pair ({'forced' if forced else 'free'}, row {r}, {n} positions): "
+                f"states within {es:.2e}, final logits within {el:.2e}")
+            assert es < 1e-5 and el < 1e-4
+            np.testing.assert_allclose(x["topk_vals"][r, :n], y["topk_vals"][r, :n], atol=1e-4, rtol=0)
+    ref = oracle_for(cfg, oracle.as_f64_weights(w), inp, a, 1)
+    check_against_oracle(cfg, a, ref, 2e-2, 1)
