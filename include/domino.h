@@ -56,7 +56,7 @@ enum {
   DOMINO_DEV_BAD_TOKEN = 1,       /* an anchor / forced / tree token id outside [0, vocab) (clamped) */
   DOMINO_DEV_BAD_CTX_LEN = 2,     /* ctx_lens[b] outside [n_new, max_ctx] (clamped) */
   DOMINO_DEV_BAD_TREE = 4,        /* a node_parent entry that is not an earlier node (ignored) */
-  DOMINO_DEV_BARRIER_TIMEOUT = 8  /* a grid barrier in the head loop exceeded its spin bound */
+  DOMINO_DEV_BARRIER_TIMEOUT = 8  /* a bounded cross-workgroup wait of the rollout exceeded its spin bound */
 };
 
 /*
