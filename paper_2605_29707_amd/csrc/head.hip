@@ -738,9 +738,10 @@ __global__ __launch_bounds__(64) void head_merge_kernel(HeadArgs h) {
 //   key slot [b][g] (j << 50) | value(32) << 18 | (2^18 - 1 - id): workgroup
 //                   g's top-1 for position j; the maximum over g is the argmax
 //                   under (value desc, id asc)
-// The hidden gates W_hh S_{j-1} go out as plain device-scope stores before the
-// u slots (each thread waits for its own stores first), and every workgroup
-// owns a u row, so "all u slots ready" also means "all gates stored".
+// The hidden gates W_hh S for the next position go out as plain device-scope
+// stores while one wave waits for u; each thread waits for its own stores
+// before its workgroup publishes its key, so "all key slots ready" also means
+// "all gates stored".
 // Waits are bounded: a timeout sets DEV_BARRIER_TIMEOUT and the abort flag,
 // and every workgroup leaves; the kernel always ends.
 // ---------------------------------------------------------------------------
@@ -790,11 +791,12 @@ DEVI bool poll_tagged(const unsigned long long *slots, int n, unsigned long long
   }
 }
 
-// BS: the largest batch the instantiation serves (1 or 2; arrays sized by it)
-template <int BS>
+// BS: the largest batch the instantiation serves (1 or 2; arrays sized by it);
+// DBG: the final logits are also written out (h.final_logits)
+template <int BS, bool DBG>
 __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs h, int nr) {
   using WT = bf16_t;
-  constexpr int EPL = 8, KSTEP = 32, XF = 2;
+  constexpr int EPL = 8, KSTEP = 32;
   const Dims &D = h.D;
   const int bs = D.bs, ds = D.ds, r = D.r, d = D.d, depth = D.B - 1, V = D.V;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -805,10 +807,12 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
   extern __shared__ __align__(16) unsigned char smem[];
   u32x4 *rows = (u32x4 *)smem;                          // [nr][nchunk] rows of [W1s; W_hh]
   float *S = (float *)(rows + (size_t)nr * nchunk);     // [bs][ds] the state
-  u32x4 *us = (u32x4 *)(S + (size_t)bs * ds);           // [KS][64][XF] u as B fragments
-  u32x4 *w2s = us + kPersKS * 64 * XF;                  // [waves][KS][64] each wave's last W2 tile
+  u32x4 *us = (u32x4 *)(S + (size_t)bs * ds);           // [KS][64] u as B fragments
+  u32x4 *w2s = us + kPersKS * 64;                       // [waves][KS][64] each wave's last W2 tile
   float4 *lbs = (float4 *)(w2s + kPersWaves * kPersKS * 64);  // [waves][tiles][64] this lane's L_base values
   float *u_s = (float *)(lbs + kPersWaves * kPersTiles * 64);  // [bs][r] u of the position
+  const int nu = (r + G - 1) / G;                              // u rows per workgroup: k < nu (R < r)
+  float *P_s = u_s + (size_t)bs * r;                           // [depth][bs][nu] W1[:, :d] H at the u rows
   __shared__ float best_v[kPersWaves][16], best_r[kPersWaves][16];
   __shared__ int best_i[kPersWaves][16];
   __shared__ int ys[kFusedBatch];
@@ -838,6 +842,11 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
     rows[e] = *(const u32x4 *)(src + (size_t)ch * EPL);
   }
   for (int e = tid; e < bs * ds; e += kPersWaves * 64) S[e] = 0.f;
+  for (int e = tid; e < depth * bs * nu; e += kPersWaves * 64) {
+    const int k = e % nu, b = (e / nu) % bs, jj = e / (nu * bs);
+    const int R = min(blockIdx.x + k * G, r - 1);
+    P_s[e] = h.P[((size_t)b * depth + jj) * h.ldp + R];
+  }
   __syncthreads();
 
   const int nit = bs * ds / 4;  // state items: four indices of one batch row
@@ -899,73 +908,73 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
       if (blockIdx.x == 0 && h.states) *(float4 *)(h.states + ((size_t)b * depth + (j - 1)) * ds + i) = s4;
     }
     __syncthreads();
-    // ---- this workgroup's rows against S_{j-1}: gates of the next position (plain
-    // device-scope stores, b_hh added), then u into the tagged slots
-    float *gh_out = h.ghbuf + (size_t)(j & 1) * bs * 3 * ds;
-    for (int k = wave; k < nr; k += kPersWaves) {
+    // ---- this workgroup's u rows against S_{j-1} into the tagged u slots
+    for (int it = wave; it < nu * bs; it += kPersWaves) {
+      const int k = it / bs, b = it % bs;
       const int R = blockIdx.x + k * G;
-      if (R >= nrows_all || (R >= r && j == depth)) continue;  // wave-uniform
-      float accb[BS];
-#pragma unroll
-      for (int b = 0; b < BS; ++b) accb[b] = 0.f;
+      if (R >= r) continue;  // wave-uniform
+      float acc = 0.f;
       for (int c = 0; c < 4; ++c) {
         const int ch = lane + 64 * c;
         if (ch >= nchunk) break;
         float wfl[EPL];
         unpack16<WT>(rows[(size_t)k * nchunk + ch], wfl);
-#pragma unroll
-        for (int b = 0; b < BS; ++b) {
-          if (b >= bs) break;
-          const float *sb = S + (size_t)b * ds + (size_t)ch * EPL;
-          const float4 s0 = *(const float4 *)sb, s1 = *(const float4 *)(sb + 4);
-          accb[b] = fmaf(wfl[0], s0.x, accb[b]);
-          accb[b] = fmaf(wfl[1], s0.y, accb[b]);
-          accb[b] = fmaf(wfl[2], s0.z, accb[b]);
-          accb[b] = fmaf(wfl[3], s0.w, accb[b]);
-          accb[b] = fmaf(wfl[4], s1.x, accb[b]);
-          accb[b] = fmaf(wfl[5], s1.y, accb[b]);
-          accb[b] = fmaf(wfl[6], s1.z, accb[b]);
-          accb[b] = fmaf(wfl[7], s1.w, accb[b]);
-        }
+        const float *sb = S + (size_t)b * ds + (size_t)ch * EPL;
+        const float4 s0 = *(const float4 *)sb, s1 = *(const float4 *)(sb + 4);
+        acc = fmaf(wfl[0], s0.x, acc);
+        acc = fmaf(wfl[1], s0.y, acc);
+        acc = fmaf(wfl[2], s0.z, acc);
+        acc = fmaf(wfl[3], s0.w, acc);
+        acc = fmaf(wfl[4], s1.x, acc);
+        acc = fmaf(wfl[5], s1.y, acc);
+        acc = fmaf(wfl[6], s1.z, acc);
+        acc = fmaf(wfl[7], s1.w, acc);
       }
-      if (R >= r) {
+      acc = wave_sum(acc);
+      if (lane == 0) {
+        const float x = P_s[((size_t)(j - 1) * bs + b) * nu + k] + acc;
+        const float u = x / (1.f + expf(-x));
+        st_slot(h.uslot + (size_t)b * r + R, ((unsigned long long)j << 32) | __float_as_uint(u));
+      }
+    }
+    // ---- gates of the next position, W_hh S_{j-1} + b_hh (plain device-scope
+    // stores), by waves 1.. while wave 0 waits for u; the stores are waited for
+    // before this workgroup publishes its top-1, so "every key slot of position
+    // j ready" also means "every gate of position j + 1 stored"
+    if (wave > 0 && j < depth) {
+      float *gh_out = h.ghbuf + (size_t)(j & 1) * bs * 3 * ds;
+      for (int k = wave - 1; k < nr; k += kPersWaves - 1) {
+        const int R = blockIdx.x + k * G;
+        if (R < r || R >= nrows_all) continue;  // wave-uniform
+        float accb[BS];
+#pragma unroll
+        for (int b = 0; b < BS; ++b) accb[b] = 0.f;
+        for (int c = 0; c < 4; ++c) {
+          const int ch = lane + 64 * c;
+          if (ch >= nchunk) break;
+          float wfl[EPL];
+          unpack16<WT>(rows[(size_t)k * nchunk + ch], wfl);
+#pragma unroll
+          for (int b = 0; b < BS; ++b) {
+            if (b >= bs) break;
+            const float *sb = S + (size_t)b * ds + (size_t)ch * EPL;
+            const float4 s0 = *(const float4 *)sb, s1 = *(const float4 *)(sb + 4);
+            accb[b] = fmaf(wfl[0], s0.x, accb[b]);
+            accb[b] = fmaf(wfl[1], s0.y, accb[b]);
+            accb[b] = fmaf(wfl[2], s0.z, accb[b]);
+            accb[b] = fmaf(wfl[3], s0.w, accb[b]);
+            accb[b] = fmaf(wfl[4], s1.x, accb[b]);
+            accb[b] = fmaf(wfl[5], s1.y, accb[b]);
+            accb[b] = fmaf(wfl[6], s1.z, accb[b]);
+            accb[b] = fmaf(wfl[7], s1.w, accb[b]);
+          }
+        }
         const float bias = h.bhh[R - r];
 #pragma unroll
         for (int b = 0; b < BS; ++b) {
           if (b >= bs) break;
           const float acc = wave_sum(accb[b]);
           if (lane == 0) st_coherent(gh_out + (size_t)b * 3 * ds + (R - r), acc + bias);
-        }
-      }
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // this thread's gate stores are done
-    __syncthreads();                // ... and every thread's
-    for (int k = wave; k < nr; k += kPersWaves) {
-      const int R = blockIdx.x + k * G;
-      if (R >= r) continue;  // wave-uniform
-      for (int b = 0; b < bs; ++b) {
-        float acc = 0.f;
-        for (int c = 0; c < 4; ++c) {
-          const int ch = lane + 64 * c;
-          if (ch >= nchunk) break;
-          float wfl[EPL];
-          unpack16<WT>(rows[(size_t)k * nchunk + ch], wfl);
-          const float *sb = S + (size_t)b * ds + (size_t)ch * EPL;
-          const float4 s0 = *(const float4 *)sb, s1 = *(const float4 *)(sb + 4);
-          acc = fmaf(wfl[0], s0.x, acc);
-          acc = fmaf(wfl[1], s0.y, acc);
-          acc = fmaf(wfl[2], s0.z, acc);
-          acc = fmaf(wfl[3], s0.w, acc);
-          acc = fmaf(wfl[4], s1.x, acc);
-          acc = fmaf(wfl[5], s1.y, acc);
-          acc = fmaf(wfl[6], s1.z, acc);
-          acc = fmaf(wfl[7], s1.w, acc);
-        }
-        acc = wave_sum(acc);
-        if (lane == 0) {
-          const float x = h.P[((size_t)b * depth + (j - 1)) * h.ldp + R] + acc;
-          const float u = x / (1.f + expf(-x));
-          st_slot(h.uslot + (size_t)b * r + R, ((unsigned long long)j << 32) | __float_as_uint(u));
         }
       }
     }
@@ -982,59 +991,91 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
     }
     __syncthreads();
     if (!s_ok) return;
-    // ---- logits: u as B fragments (batch rows as the 16 columns) against the resident W2
+    // ---- logits: u as B fragments against the resident W2.  Column b holds the
+    // bf16 high part of batch row b's u, column bs + b its low part (u - hi), so
+    // one product per tile and k-step carries both; the two columns are summed
+    // after the k loop.
     {
       const int l = tid & 63, s = tid >> 6;  // kPersKS * 64 == kPersWaves * 64 items, one per thread
-      const int bb = min(l & 15, bs - 1);
+      const int n = l & 15;
+      const int bb = n < bs ? n : min(n - bs, bs - 1);
       const float *src = u_s + (size_t)bb * r + s * KSTEP + (l >> 4) * EPL;
-      float4 uv[2] = {*(const float4 *)src, *(const float4 *)(src + 4)};
-      XStage<WT>::put(us + (size_t)tid * XF, uv);
+      const float4 v0 = *(const float4 *)src, v1 = *(const float4 *)(src + 4);
+      const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+      bf16x8 hi, lo;
+      split8(f, hi, lo);
+      u32x4 frag = n < bs ? __builtin_bit_cast(u32x4, hi) : __builtin_bit_cast(u32x4, lo);
+      if (n >= 2 * bs) frag = u32x4{0u, 0u, 0u, 0u};
+      us[tid] = frag;
     }
     __syncthreads();
-    floatx4 acc[kPersTiles][1];
+    floatx4 acc[kPersTiles];
 #pragma unroll
-    for (int q = 0; q < kPersTiles; ++q) acc[q][0] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < kPersTiles; ++q) acc[q] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < kPersKS; ++s) {
-      u32x4 xf[XF];
+      const bf16x8 xb = __builtin_bit_cast(bf16x8, us[(size_t)s * 64 + lane]);
 #pragma unroll
-      for (int f = 0; f < XF; ++f) xf[f] = us[((size_t)s * 64 + lane) * XF + f];
-#pragma unroll
-      for (int q = 0; q < kPersRegTiles; ++q) Mac2<WT, 1>::step(wf[q][s], xf, acc[q]);
-      Mac2<WT, 1>::step(w2s[((size_t)wave * kPersKS + s) * 64 + lane], xf, acc[kPersRegTiles]);
+      for (int q = 0; q < kPersRegTiles; ++q)
+        acc[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wf[q][s]), xb, acc[q], 0, 0, 0);
+      acc[kPersRegTiles] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          __builtin_bit_cast(bf16x8, w2s[((size_t)wave * kPersKS + s) * 64 + lane]), xb, acc[kPersRegTiles], 0, 0, 0);
     }
-    // lane (g, cc) holds vocabulary ids 16 (tile0 + q) + 4 g + e of batch row cc
-    const bool rowok = cc < bs;
-    if (h.final_logits) {  // debug output
+    // lane (g, cc) holds vocabulary ids 16 (tile0 + q) + 4 g + e: column cc < bs
+    // adds the low-part column of lane cc + bs (a row shift within 16 lanes)
+    float val[kPersTiles][4];
 #pragma unroll
-      for (int q = 0; q < kPersTiles; ++q) {
-        const float4 l4 = lbs[((size_t)wave * kPersTiles + q) * 64 + lane];
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+    for (int q = 0; q < kPersTiles; ++q) {
+      const float4 l4 = lbs[((size_t)wave * kPersTiles + q) * 64 + lane];
+      const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int n = (tile0 + q) * 16 + 4 * g + e;
-          if (rowok && n < V) h.final_logits[((size_t)cc * depth + (j - 1)) * V + n] = lv[e] + acc[q][0][e];
-        }
+      for (int e = 0; e < 4; ++e) {
+        const int a = __float_as_int(acc[q][e]);
+        const int lo1 = __builtin_amdgcn_update_dpp(0, a, 0x101, 0xf, 0xf, false);  // lane + 1
+        const int lo2 = __builtin_amdgcn_update_dpp(0, a, 0x102, 0xf, 0xf, false);  // lane + 2
+        val[q][e] = lv[e] + (acc[q][e] + __int_as_float(BS == 1 || bs == 1 ? lo1 : lo2));
       }
     }
-    {
-      float bv = -INFINITY;
-      int bi = INT_MAX;
+    const bool rowok = cc < bs;
+    if (DBG) {  // debug output
 #pragma unroll
-      for (int q = 0; q < kPersTiles; ++q) {
-        const float4 l4 = lbs[((size_t)wave * kPersTiles + q) * 64 + lane];
+      for (int q = 0; q < kPersTiles; ++q)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int n = (tile0 + q) * 16 + 4 * g + e;
-          const float lbe = e == 0 ? l4.x : (e == 1 ? l4.y : (e == 2 ? l4.z : l4.w));
-          const float val = lbe + acc[q][0][e];
-          const bool ok = rowok && n < V;
-          const float ov = ok ? order_val(val) : -INFINITY;
-          const int nid = ok ? n : INT_MAX;
-          const bool take = better(ov, nid, bv, bi);
-          bv = take ? ov : bv;
-          bi = take ? nid : bi;
+          if (rowok && n < V) h.final_logits[((size_t)cc * depth + (j - 1)) * V + n] = val[q][e];
         }
+    }
+    {
+      // ids grow along (q, e) within a lane, so a strict comparison keeps the
+      // smallest id of equal values; ids past V occur only in the last workgroup
+      float bv = -INFINITY;
+      int bi = (tile0 * 16 + 4 * g) < V ? tile0 * 16 + 4 * g : INT_MAX;
+      if ((tile0 + kPersTiles) * 16 <= V) {
+#pragma unroll
+        for (int q = 0; q < kPersTiles; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float ov = order_val(val[q][e]);
+            const bool take = ov > bv;
+            bv = take ? ov : bv;
+            bi = take ? (tile0 + q) * 16 + 4 * g + e : bi;
+          }
+      } else {
+#pragma unroll
+        for (int q = 0; q < kPersTiles; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int n = (tile0 + q) * 16 + 4 * g + e;
+            const float ov = n < V ? order_val(val[q][e]) : -INFINITY;
+            const bool take = ov > bv;
+            bv = take ? ov : bv;
+            bi = take ? n : bi;
+          }
+      }
+      if (!rowok) {
+        bv = -INFINITY;
+        bi = INT_MAX;
       }
 #pragma unroll
       for (int o = 16; o <= 32; o <<= 1) {
@@ -1049,7 +1090,8 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
         best_i[wave][cc] = bi;
       }
     }
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's gate stores are done
+    __syncthreads();                // ... and every thread's
     if (tid < bs) {
       const int bb = tid;
       float v = best_v[0][bb];
@@ -1112,10 +1154,13 @@ bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st) {
   if (G != h.GC || G > n_cu || G > D.r || G > 256) return false;  // polls: 4 slots per lane per batch row
   const int nr = (D.r + 3 * D.ds + G - 1) / G;
   const size_t lds = (size_t)nr * (D.ds / 8) * 16 + sizeof(float) * (size_t)D.bs * D.ds +
-                     sizeof(u32x4) * kPersKS * 64 * 2 + sizeof(u32x4) * kPersWaves * kPersKS * 64 +
-                     sizeof(float4) * kPersWaves * kPersTiles * 64 + sizeof(float) * (size_t)D.bs * D.r;
+                     sizeof(u32x4) * kPersKS * 64 + sizeof(u32x4) * kPersWaves * kPersKS * 64 +
+                     sizeof(float4) * kPersWaves * kPersTiles * 64 + sizeof(float) * (size_t)D.bs * D.r +
+                     sizeof(float) * (size_t)(D.B - 1) * D.bs * ((D.r + G - 1) / G);
   if (lds > 160 * 1024) return false;
-  const void *fn = D.bs == 1 ? (const void *)head_persist_kernel<1> : (const void *)head_persist_kernel<2>;
+  const bool dbg = h.final_logits != nullptr;
+  const void *fn = D.bs == 1 ? (dbg ? (const void *)head_persist_kernel<1, true> : (const void *)head_persist_kernel<1, false>)
+                             : (dbg ? (const void *)head_persist_kernel<2, true> : (const void *)head_persist_kernel<2, false>);
   if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
     (void)hipGetLastError();
     return false;
