@@ -739,7 +739,7 @@ domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *an
   h.seed_hi = smp ? (uint32_t)(smp->seed >> 32) : 0u;
   prof_begin(m, DOMINO_KC_HEADLOOP, st);
   hipError_t he = hipSuccess;
-  // one cooperative launch for the whole rollout where it applies, else a
+  // one persistent launch for the whole rollout where it applies, else a
   // launch pair per position
   if (!m->persistent || !launch_head_persistent(h, m->n_cu, st)) he = launch_head(h, st);
   prof_end(m, DOMINO_KC_HEADLOOP, st);

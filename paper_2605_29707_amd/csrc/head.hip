@@ -724,7 +724,7 @@ __global__ __launch_bounds__(64) void head_merge_kernel(HeadArgs h) {
 
 // ---------------------------------------------------------------------------
 // Persistent rollout (bf16 weights, r = 256, one or two batch rows, greedy): one
-// cooperative launch runs all B-1 positions.  Each workgroup keeps its slice
+// launch of at most one workgroup per CU runs all B-1 positions.  Each workgroup keeps its slice
 // of W2 resident for the whole rollout (kPersTiles tiles per wave, the last
 // one in LDS, the rest in registers: 77.8 MB over 238 workgroups at the Qwen3
 // vocabulary) and its rows of [W1[:, d:]; W_hh] in LDS, so W2 leaves HBM once
@@ -743,7 +743,8 @@ __global__ __launch_bounds__(64) void head_merge_kernel(HeadArgs h) {
 // before its workgroup publishes its key, so "all key slots ready" also means
 // "all gates stored".
 // Waits are bounded: a timeout sets DEV_BARRIER_TIMEOUT and the abort flag,
-// and every workgroup leaves; the kernel always ends.
+// and every workgroup leaves; the kernel always ends.  Workgroup 0 writes the
+// drafted token and its value of every position (no merge kernel).
 // ---------------------------------------------------------------------------
 constexpr int kPersWaves = 8, kPersTiles = 5, kPersKS = 8, kPersRegTiles = kPersTiles - 1;
 constexpr unsigned kPollLimit = 1u << 22;
@@ -1102,9 +1103,6 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
           v = best_v[w][bb];
           id = best_i[w][bb];
         }
-      const size_t o = ((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x;
-      h.pval[o] = v;
-      h.pid[o] = id;
       // an empty slice (no valid id) publishes the smallest key
       const unsigned long long key = id == INT_MAX ? 0ull : pack_key50(v, id);
       st_slot(h.kslot + (size_t)bb * G + blockIdx.x, ((unsigned long long)j << 50) | key);
@@ -1112,7 +1110,8 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
     // ---- wait for every workgroup's top-1: the maximum key is y_j.  Also the
     // guard that no workgroup writes the next position's slots while another
     // still polls this position's, so it runs with forced tokens as well.
-    if (j < depth) {
+    // Workgroup 0 reports (y_j, its value) for every position, the last included.
+    if (j < depth || blockIdx.x == 0) {
       if (wave == 0) {
         unsigned long long w[4 * BS];
         const bool ok = poll_tagged<4 * BS>(h.kslot, bs * G, (unsigned long long)j, 50, h.abort_flag, h.err, w);
@@ -1130,7 +1129,15 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
             const unsigned long long other = __shfl_xor(best, o, 64);
             best = other > best ? other : best;
           }
-          if (lane == 0) ys[b] = min(max(key50_id(best), 0), V - 1);
+          if (lane == 0) {
+            const int id = key50_id(best);
+            ys[b] = min(max(id, 0), V - 1);
+            if (blockIdx.x == 0) {
+              const uint32_t u = (uint32_t)(best >> kKeyIdBits);
+              h.topk_ids[(size_t)b * depth + (j - 1)] = id;
+              h.topk_vals[(size_t)b * depth + (j - 1)] = __uint_as_float((u & 0x80000000u) ? (u ^ 0x80000000u) : ~u);
+            }
+          }
         }
         if (lane == 0) s_ok = ok;
       }
@@ -1165,14 +1172,24 @@ bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st) {
     (void)hipGetLastError();
     return false;
   }
-  HeadArgs a = h;
-  int nrv = nr;
-  void *args[] = {&a, &nrv};
-  if (hipLaunchCooperativeKernel(fn, dim3(G), dim3(kPersWaves * 64), args, lds, st) != hipSuccess) {
+  // Every workgroup waits for all others, so the grid must be resident at once:
+  // one workgroup per CU at most (its LDS share allows no second), G <= CUs.  An
+  // ordinary launch is used (a cooperative one cost ~60 us per step in
+  // queue synchronisation); it gets the whole device once the previous kernel
+  // on the stream has drained.  Should other work hold CUs, the waits are
+  // bounded and end in DEV_BARRIER_TIMEOUT rather than a hang.
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kPersWaves * 64, lds) != hipSuccess || per_cu < 1) {
     (void)hipGetLastError();
     return false;
   }
-  hipLaunchKernelGGL(head_merge_kernel, dim3(D.B - 1, D.bs), dim3(64), 0, st, h);
+  HeadArgs a = h;
+  int nrv = nr;
+  void *args[] = {&a, &nrv};
+  if (hipLaunchKernel(fn, dim3(G), dim3(kPersWaves * 64), args, lds, st) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
   return true;
 }
 

@@ -121,7 +121,7 @@ struct HeadArgs {
 int head_logits_grid(const Dims &D);
 int head_best_slots();
 hipError_t launch_head(const HeadArgs &h, hipStream_t st);
-// One cooperative launch for the whole rollout where the shapes allow it (bf16,
+// One persistent launch for the whole rollout where the shapes allow it (bf16,
 // r = 256, batch <= 2, greedy branch 1, a grid that fits the device at one
 // workgroup per CU, vocabulary < 2^18); returns false (nothing launched) otherwise.
 bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st);
