@@ -28,6 +28,9 @@ LMHEAD_TRAFFIC = {"gemm_sha1": "700f9722713674283b019da6e19b720930abe556", "byte
                   "config": "qwen3_8b"}
 
 
+PROF_EVERY = 10  # timed steps per LM-head launch bracketed by events
+
+
 def lmhead_traffic(cfg_name):
     import hashlib
     src = os.path.join(ROOT, "paper_2605_29707_amd", "csrc", "gemm.hip")
@@ -159,7 +162,8 @@ def main():
     torch.cuda.synchronize()
     assert bd.domino_workspace_error(ws) == 0, "device error word set"
 
-    # timed region: K steps, per-step events, the LM-head launches bracketed by library events
+    # timed region: K steps, per-step events; the LM-head launch of every PROF_EVERY-th step is
+    # bracketed by library events (an event pair costs a few us of queue time, so not every step)
     dom = "lmhead"
     bd.domino_profile_enable(model, [dom])
     bd.domino_profile_reset(model)
@@ -167,6 +171,7 @@ def main():
     torch.cuda.synchronize()
     evs[0].record(stream)
     for i in range(args.steps):
+        bd.domino_profile_enable(model, [dom] if i % PROF_EVERY == 0 else [])
         step()
         evs[i + 1].record(stream)
     torch.cuda.synchronize()

@@ -567,8 +567,8 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
   const int qd = D.nq * D.dh, kvd = D.nkv * D.dh, qkvw = qd + 2 * kvd;
   const size_t layer_elems = (size_t)batch * max_ctx * kvd;
 
-  // clear the error word and the rollout's best keys
-  if (clear_header) launch_fill_u32((uint32_t *)ws, w.hdr_words, 0u, st);
+  // the error word, the rollout's best keys and exchange slots are cleared by
+  // layer 0's RMSNorm launch (clear_header)
   // appended context rows (target hidden states) ride along in the QKV
   // projection: they sit after the block rows of its input, and the RMSNorms
   // only ever rewrite the block rows
@@ -590,7 +590,8 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
     prof_begin(m, DOMINO_KC_NORM, st);
     // (layer 0: the residual starts as the embedding of [anchor, MASK, ...])
     launch_add_norm(D, xc, xn, D.d, F(w.DNp), l > 0 ? p.down.ksplit : 0, rstride, m->attn_norm[l], F(w.A), D.d,
-                    M, D.d, false, l == 0 ? m->embed : nullptr, anchor_ids, err, st, spec.tokens);
+                    M, D.d, false, l == 0 ? m->embed : nullptr, anchor_ids, err, st, spec.tokens,
+                    l == 0 && clear_header ? (uint32_t *)ws : nullptr, (int)w.hdr_words);
     std::swap(xc, xn);
     prof_end(m, DOMINO_KC_NORM, st);
 
@@ -1011,7 +1012,6 @@ domino_status domino_verify_accept(int32_t batch, int32_t n_nodes, int32_t vocab
   const size_t need = accept_ws_bytes(batch, n_nodes, vocab);
   if (workspace_bytes < need) return fail(DOMINO_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
   hipStream_t st = (hipStream_t)stream;
-  launch_fill_u32((uint32_t *)workspace, 1, 0u, st);
   launch_accept(batch, n_nodes, vocab, block, node_token, node_parent, target_logits, logits_dtype == DOMINO_BF16,
                 accept_len, accepted_nodes, out_tokens, workspace, st);
   hipError_t he = hipGetLastError();

@@ -48,10 +48,26 @@ __global__ __launch_bounds__(512) void add_norm_kernel(const float *__restrict__
                                                        int skip_anchor, int depth, const WT *__restrict__ embed,
                                                        const int32_t *__restrict__ anchor, int mask_id, int V,
                                                        int32_t *err, const int32_t *__restrict__ tokens,
-                                                       int nsplit) {
+                                                       int nsplit, uint32_t *hdr, int hdr_words) {
   // nsplit workgroups per row: each forms the whole row's sum of squares but
   // writes only its slice of the columns
   const int i = blockIdx.x / nsplit, part = blockIdx.x % nsplit;
+  // hdr: the step's workspace header (word 0 the error word) is cleared here
+  // instead of by a launch of its own; then only thread 0 of workgroup 0 checks
+  // the tokens, after clearing the error word, so no error raised in this launch
+  // is lost to the clear
+  if (hdr) {
+    for (int e = blockIdx.x * blockDim.x + threadIdx.x + 1; e < hdr_words; e += gridDim.x * blockDim.x) hdr[e] = 0u;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      hdr[0] = 0u;
+      const int B = depth + 1;
+      for (int row = 0; row < (int)gridDim.x / nsplit; ++row) {
+        const int tk = tokens ? tokens[row] : (row % B == 0 ? anchor[row / B] : 0);
+        if (tk < 0 || tk >= V) raise_error(err, DEV_BAD_TOKEN);
+      }
+    }
+  }
+  const bool raise = hdr == nullptr;
   const int cs = width / nsplit;  // columns per slice (a multiple of 8)
   const int in_row = skip_anchor ? i + i / depth + 1 : i;
   const float *xr = x + (size_t)in_row * ldx;
@@ -64,13 +80,13 @@ __global__ __launch_bounds__(512) void add_norm_kernel(const float *__restrict__
     if (tokens) {  // one token per row (a tree's nodes)
       tok = tokens[in_row];
       if (tok < 0 || tok >= V) {
-        if (threadIdx.x == 0) raise_error(err, DEV_BAD_TOKEN);
+        if (threadIdx.x == 0 && raise) raise_error(err, DEV_BAD_TOKEN);
         tok = tok < 0 ? 0 : V - 1;
       }
     } else if (in_row % B == 0) {
       tok = anchor[in_row / B];
       if (tok < 0 || tok >= V) {
-        if (threadIdx.x == 0) raise_error(err, DEV_BAD_TOKEN);
+        if (threadIdx.x == 0 && raise) raise_error(err, DEV_BAD_TOKEN);
         tok = tok < 0 ? 0 : V - 1;
       }
     }
@@ -594,7 +610,7 @@ template <typename WT, int MAXP>
 static void add_norm_t(const Dims &D, const float *x, float *x_out, int ldx, const float *parts, int np, size_t pstride,
                        const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
                        const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st,
-                       const int32_t *tokens) {
+                       const int32_t *tokens, uint32_t *hdr, int hdr_words) {
   // a few workgroups per row when there are few rows: a GEMM that reads rows
   // written by one workgroup each was measured ~5 us slower (QKV after the
   // attention RMSNorm at 16 rows), with two or more per row it is not
@@ -602,21 +618,21 @@ static void add_norm_t(const Dims &D, const float *x, float *x_out, int ldx, con
   while (split < 4 && rows * split < 64 && width % (2 * split * 8) == 0) split *= 2;
   hipLaunchKernelGGL((add_norm_kernel<WT, MAXP>), dim3(rows * split), dim3(512), 0, st, x, x_out, ldx, parts, np, pstride,
                      (const WT *)gain, y, ldy, width, D.eps, (int)skip_anchor, D.B - 1, (const WT *)embed, anchor,
-                     D.mask_id, D.V, err, tokens, split);
+                     D.mask_id, D.V, err, tokens, split, hdr, hdr_words);
 }
 
 void launch_add_norm(const Dims &D, const float *x, float *x_out, int ldx, const float *parts, int np, size_t pstride,
                      const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
                      const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st,
-                     const int32_t *tokens) {
+                     const int32_t *tokens, uint32_t *hdr, int hdr_words) {
   if (rows <= 0) return;
   if (np < 0 || np > 16) return;  // partial counts come from the GEMM planner (<= 16)
   if (D.bf16) {
-    if (np <= 8) add_norm_t<bf16_t, 8>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
-    else add_norm_t<bf16_t, 16>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
+    if (np <= 8) add_norm_t<bf16_t, 8>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens, hdr, hdr_words);
+    else add_norm_t<bf16_t, 16>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens, hdr, hdr_words);
   } else {
-    if (np <= 8) add_norm_t<float, 8>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
-    else add_norm_t<float, 16>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens);
+    if (np <= 8) add_norm_t<float, 8>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens, hdr, hdr_words);
+    else add_norm_t<float, 16>(D, x, x_out, ldx, parts, np, pstride, gain, y, ldy, rows, width, skip_anchor, embed, anchor, err, st, tokens, hdr, hdr_words);
   }
 }
 

@@ -53,10 +53,13 @@ void launch_embed_block(const Dims &D, const void *embed, const int32_t *anchor,
 // With `embed` given, x rows are first set to the embedding rows of the masked
 // block ([anchor, MASK, ...]) before the (empty) partial sum.
 // With `tokens` given (and `embed`), row i's token is tokens[i] instead.
+// With `hdr` given (and `embed`, no skip_anchor), the launch also zeroes
+// hdr[0 .. hdr_words) (the step's workspace header; hdr[0] is `err`) before
+// any error of its own is raised.
 void launch_add_norm(const Dims &D, const float *x, float *x_out, int ldx, const float *parts, int np, size_t pstride,
                      const void *gain, float *y, int ldy, int rows, int width, bool skip_anchor,
                      const void *embed, const int32_t *anchor, int32_t *err, hipStream_t st,
-                     const int32_t *tokens = nullptr);
+                     const int32_t *tokens = nullptr, uint32_t *hdr = nullptr, int hdr_words = 0);
 // q/k RMSNorm + RoPE on the QKV projection (sum of np partials); writes
 // Q [M][nq][dh], Kb/Vb [M][nkv][dh].  The projection's rows M + b*n_new + i
 // (n_new appended context rows per batch row) have their K (k-norm, RoPE at

@@ -59,18 +59,18 @@ void launch_build_tree(int bs, int depth, int beta, const int32_t *topk, const i
 }
 
 // ---------------------------------------------------------------------------
-// acceptance
-// workspace: [err:int32][pad to 256 B][flags: uint8 bs*nn (padded)][partials: (float,int) bs*nn*nchunk]
+// acceptance: two launches.  (1) the argmax of every node row, split into
+// vocabulary chunks (all rows, so the walk never scans a row itself; a leaf
+// row costs one more pass over V values, read once); (2) one workgroup per
+// batch row checks the tree and walks it from the root.
+// workspace: [err:int32][pad to 256 B][partials: (float,int) bs*nn*nchunk]
 // ---------------------------------------------------------------------------
 constexpr int ACH = 4096;  // vocabulary elements per argmax chunk
 
-static size_t acc_flags_off() { return 256; }
-static size_t acc_part_off(int bs, int nn) {
-  return (acc_flags_off() + (size_t)bs * nn + 255) & ~(size_t)255;
-}
+static size_t acc_part_off() { return 256; }
 size_t accept_ws_bytes(int bs, int nn, int V) {
   const int nch = (V + ACH - 1) / ACH;
-  return acc_part_off(bs, nn) + (size_t)bs * nn * nch * 8;
+  return acc_part_off() + (size_t)bs * nn * nch * 8;
 }
 
 template <typename LT>
@@ -84,39 +84,29 @@ DEVI float ld_logit<bf16_t>(const bf16_t *p) {
   return to_f32(*p);
 }
 
-// Mark the nodes that have children (their rows are needed by the walk).
-__global__ __launch_bounds__(256) void mark_internal_kernel(int nn, const int32_t *__restrict__ par,
-                                                            uint8_t *flags, int32_t *err) {
-  const int b = blockIdx.x;
-  for (int i = threadIdx.x; i < nn; i += blockDim.x) flags[(size_t)b * nn + i] = 0;
-  __syncthreads();
-  for (int c = threadIdx.x; c < nn; c += blockDim.x) {
-    const int p = par[(size_t)b * nn + c];
-    const bool ok = (c == 0) ? (p == -1) : (p >= 0 && p < c);
-    if (!ok) {
-      raise_error(err, DEV_BAD_TREE);
-      continue;
-    }
-    if (c > 0) flags[(size_t)b * nn + p] = 1;
-  }
-}
-
-// Partial argmax of row (b, m) over one vocabulary chunk, for marked rows.
+// Partial argmax of row (b, m) over one vocabulary chunk.  The first workgroup
+// also clears the error word (only the walk, a later launch, raises errors).
 template <typename LT>
 __global__ __launch_bounds__(256) void argmax_partial_kernel(int nn, int V, const LT *__restrict__ logits,
-                                                             const uint8_t *__restrict__ flags,
-                                                             float *part_v, int32_t *part_i) {
+                                                             float *part_v, int32_t *part_i, int32_t *err) {
   const int ch = blockIdx.x, m = blockIdx.y, b = blockIdx.z;
   const int nch = gridDim.x;
-  if (!flags[(size_t)b * nn + m]) return;
+  if ((ch | m | b) == 0 && threadIdx.x == 0) *err = 0;
   const LT *row = logits + ((size_t)b * nn + m) * V;
   const int v0 = ch * ACH, v1 = min(V, v0 + ACH);
+  // ACH / 256 = 16 values per thread, loaded together at clamped addresses
+  constexpr int PER = ACH / 256;
+  float x[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) x[q] = ld_logit<LT>(row + min(v0 + (int)threadIdx.x + q * 256, v1 - 1));
   float bv = -INFINITY;
   int bi = INT_MAX;
-  for (int v = v0 + threadIdx.x; v < v1; v += 256) {
-    const float x = order_val(ld_logit<LT>(row + v));
-    if (better(x, v, bv, bi)) {
-      bv = x;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int v = v0 + (int)threadIdx.x + q * 256;  // increasing in q: a strict > keeps the smallest id
+    const float o = v < v1 ? order_val(x[q]) : -INFINITY;
+    if (v < v1 && (o > bv || bi == INT_MAX)) {
+      bv = o;
       bi = v;
     }
   }
@@ -140,80 +130,48 @@ __global__ __launch_bounds__(256) void argmax_partial_kernel(int nn, int V, cons
   }
 }
 
-// Block-wide argmax of a whole row (for the final node when it is a leaf).
-template <typename LT>
-DEVI int row_argmax(const LT *row, int V, float *sv, int *si) {
-  float bv = -INFINITY;
-  int bi = INT_MAX;
-  for (int v = threadIdx.x; v < V; v += blockDim.x) {
-    const float x = order_val(ld_logit<LT>(row + v));
-    if (better(x, v, bv, bi)) {
-      bv = x;
-      bi = v;
-    }
-  }
-  wave_best(bv, bi);
-  if ((threadIdx.x & 63) == 0) {
-    sv[threadIdx.x >> 6] = bv;
-    si[threadIdx.x >> 6] = bi;
-  }
-  __syncthreads();
-  bv = sv[0];
-  bi = si[0];
-  for (int w = 1; w < (int)(blockDim.x >> 6); ++w)
-    if (better(sv[w], si[w], bv, bi)) {
-      bv = sv[w];
-      bi = si[w];
-    }
-  __syncthreads();
-  return bi;
-}
-
-template <typename LT>
 __global__ __launch_bounds__(256) void accept_walk_kernel(int nn, int V, int B, const int32_t *__restrict__ tok,
                                                           const int32_t *__restrict__ par,
-                                                          const LT *__restrict__ logits,
-                                                          const uint8_t *__restrict__ flags,
                                                           const float *__restrict__ part_v,
                                                           const int32_t *__restrict__ part_i,
                                                           int32_t *acc_len, int32_t *acc_nodes,
-                                                          int32_t *out_tok) {
+                                                          int32_t *out_tok, int32_t *err) {
   const int b = blockIdx.x;
   const int nch = (V + ACH - 1) / ACH;
   __shared__ float sv[4];
   __shared__ int si[4];
   __shared__ int s_next;
+  // the tree: node 0 is the root, every other node's parent comes before it
+  for (int c = threadIdx.x; c < nn; c += blockDim.x) {
+    const int p = par[(size_t)b * nn + c];
+    if (!((c == 0) ? (p == -1) : (p >= 0 && p < c))) raise_error(err, DEV_BAD_TREE);
+  }
   int cur = 0, a = 0;
   int R = 0;
   while (true) {
-    // R = argmax of row cur
-    if (flags[(size_t)b * nn + cur]) {
-      float bv = -INFINITY;
-      int bi = INT_MAX;
-      const size_t o = ((size_t)b * nn + cur) * nch;
-      for (int c = threadIdx.x; c < nch; c += blockDim.x)
-        if (better(part_v[o + c], part_i[o + c], bv, bi)) {
-          bv = part_v[o + c];
-          bi = part_i[o + c];
-        }
-      wave_best(bv, bi);
-      if ((threadIdx.x & 63) == 0) {
-        sv[threadIdx.x >> 6] = bv;
-        si[threadIdx.x >> 6] = bi;
+    // R = argmax of row cur, from its chunk partials
+    float bv = -INFINITY;
+    int bi = INT_MAX;
+    const size_t o = ((size_t)b * nn + cur) * nch;
+    for (int c = threadIdx.x; c < nch; c += blockDim.x)
+      if (better(part_v[o + c], part_i[o + c], bv, bi)) {
+        bv = part_v[o + c];
+        bi = part_i[o + c];
       }
-      __syncthreads();
-      bv = sv[0];
-      bi = si[0];
-      for (int w = 1; w < 4; ++w)
-        if (better(sv[w], si[w], bv, bi)) {
-          bv = sv[w];
-          bi = si[w];
-        }
-      __syncthreads();
-      R = bi;
-    } else {
-      R = row_argmax<LT>(logits + ((size_t)b * nn + cur) * V, V, sv, si);
+    wave_best(bv, bi);
+    if ((threadIdx.x & 63) == 0) {
+      sv[threadIdx.x >> 6] = bv;
+      si[threadIdx.x >> 6] = bi;
     }
+    __syncthreads();
+    bv = sv[0];
+    bi = si[0];
+    for (int w = 1; w < 4; ++w)
+      if (better(sv[w], si[w], bv, bi)) {
+        bv = sv[w];
+        bi = si[w];
+      }
+    R = bi;
     if (a >= B - 1) break;  // walk bound
     // the child of cur whose token is R (children have distinct tokens; take the first)
     if (threadIdx.x == 0) s_next = INT_MAX;
@@ -244,23 +202,18 @@ void launch_accept(int bs, int nn, int V, int B, const int32_t *tok, const int32
                    int32_t *out_tok, void *ws, hipStream_t st) {
   unsigned char *w = (unsigned char *)ws;
   int32_t *err = (int32_t *)w;
-  uint8_t *flags = w + acc_flags_off();
   const int nch = (V + ACH - 1) / ACH;
-  float *pv = (float *)(w + acc_part_off(bs, nn));
+  float *pv = (float *)(w + acc_part_off());
   int32_t *pi = (int32_t *)(pv + (size_t)bs * nn * nch);
-  hipLaunchKernelGGL(mark_internal_kernel, dim3(bs), dim3(256), 0, st, nn, par, flags, err);
   dim3 grid(nch, nn, bs);
-  if (bf16) {
-    hipLaunchKernelGGL(argmax_partial_kernel<bf16_t>, grid, dim3(256), 0, st, nn, V, (const bf16_t *)logits,
-                       flags, pv, pi);
-    hipLaunchKernelGGL(accept_walk_kernel<bf16_t>, dim3(bs), dim3(256), 0, st, nn, V, B, tok, par,
-                       (const bf16_t *)logits, flags, pv, pi, acc_len, acc_nodes, out_tok);
-  } else {
-    hipLaunchKernelGGL(argmax_partial_kernel<float>, grid, dim3(256), 0, st, nn, V, (const float *)logits,
-                       flags, pv, pi);
-    hipLaunchKernelGGL(accept_walk_kernel<float>, dim3(bs), dim3(256), 0, st, nn, V, B, tok, par,
-                       (const float *)logits, flags, pv, pi, acc_len, acc_nodes, out_tok);
-  }
+  if (bf16)
+    hipLaunchKernelGGL(argmax_partial_kernel<bf16_t>, grid, dim3(256), 0, st, nn, V, (const bf16_t *)logits, pv, pi,
+                       err);
+  else
+    hipLaunchKernelGGL(argmax_partial_kernel<float>, grid, dim3(256), 0, st, nn, V, (const float *)logits, pv, pi,
+                       err);
+  hipLaunchKernelGGL(accept_walk_kernel, dim3(bs), dim3(256), 0, st, nn, V, B, tok, par, pv, pi, acc_len, acc_nodes,
+                     out_tok, err);
 }
 
 }  // namespace dk

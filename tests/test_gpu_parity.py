@@ -230,6 +230,37 @@ def test_verify_accept_bit_exact(beta, dtype, kind):
     log(f"tau values: {taus}")
 
 
+def test_verify_accept_bad_tree_sets_error_word_then_clears():
+    """A parent that does not precede its node raises DEV_BAD_TREE (the walk
+    still ends); the next call on the same workspace starts from a clear error
+    word and matches the oracle."""
+    from paper_2605_29707_amd import binding as bd
+    V = 5000
+    cfg = synth.get_config("qwen3_8b").with_(batch=2, branch=2, vocab=V)
+    topk = synth.make_random_topk(cfg, seed=7)
+    tree = oracle.build_tree(topk, np.arange(2, dtype=np.int32), np.full(2, 9, np.int32))
+    lg = synth.make_target_logits(cfg, tree["node_token"], tree["node_parent"], seed=7, dtype="f32")
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    bs, nn = tree["node_token"].shape
+    acc = torch.empty(bs, dtype=torch.int32, device=dev)
+    nodes = torch.empty(bs, cfg.block - 1, dtype=torch.int32, device=dev)
+    out = torch.empty(bs, cfg.block, dtype=torch.int32, device=dev)
+    ws = torch.empty(bd.domino_verify_workspace_bytes(bs, nn, V), dtype=torch.uint8, device=dev)
+    bad = tree["node_parent"].copy()
+    bad[1, 3] = 7
+    bd.domino_verify_accept(t(tree["node_token"]), t(bad), t(lg), cfg.block, acc, nodes, out, ws)
+    torch.cuda.synchronize()
+    assert bd.domino_workspace_error(ws) & bd.DEV_BAD_TREE
+    bd.domino_verify_accept(t(tree["node_token"]), t(tree["node_parent"]), t(lg), cfg.block, acc, nodes, out, ws)
+    torch.cuda.synchronize()
+    assert bd.domino_workspace_error(ws) == 0
+    want = oracle.verify_accept(tree["node_token"], tree["node_parent"], lg, cfg.block)
+    np.testing.assert_array_equal(acc.cpu().numpy(), want["accept_len"])
+    np.testing.assert_array_equal(nodes.cpu().numpy(), want["accepted_nodes"])
+    np.testing.assert_array_equal(out.cpu().numpy(), want["out_tokens"])
+
+
 def test_tiny_pipeline_draft_tree_accept():
     cfg = synth.get_config("tiny").with_(ctx_from_hidden=False, batch=2, branch=4)
     w = synth.make_weights(cfg, seed=7)
