@@ -545,7 +545,11 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
 }
 
 // Merge the chunks of one (batch, query head, block row) with log-sum-exp
-// weights; one wave per row, lane c reads chunk c's statistics.
+// weights; one wave per row.  The first CB chunks' output rows and maxima are
+// loaded together with the statistics pass, so a context of up to CB chunks
+// costs one memory round trip: lane c folds chunks c, c + 64, ... into a
+// running (max, sum) pair, the wave combines the pairs, then the rows are
+// weighted and summed in chunk order.
 template <int DH>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float *__restrict__ part,
                                                            const int32_t *__restrict__ ctx_lens,
@@ -559,21 +563,37 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float *__restri
   n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
   const int nc = (n + B + CH - 1) / CH;
   const float *base = part + (((size_t)b * nq + qh) * B + j) * nch * (DH + 2);
-  // chunk statistics: lane c holds chunk c (and c + 64, ...)
-  float M = -INFINITY;
-  for (int c = lane; c < nc; c += 64) M = fmaxf(M, base[c * (DH + 2) + DH]);
-  M = wave_max(M);
-  float den = 0.f;
-  for (int c = lane; c < nc; c += 64) den += expf(base[c * (DH + 2) + DH] - M) * base[c * (DH + 2) + DH + 1];
-  den = wave_sum(den);
-  constexpr int PER = DH / 64, CB = 16;
+  constexpr int PER = DH / 64, CB = 40;
+  float w[CB], v[CB][PER];
+#pragma unroll
+  for (int u = 0; u < CB; ++u) {  // chunk u's max and this lane's output values (clamped, in flight together)
+    const int cu = min(u, nc - 1);
+    w[u] = base[cu * (DH + 2) + DH];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) v[u][q] = base[cu * (DH + 2) + lane + 64 * q];
+  }
+  float M = -INFINITY, den = 0.f;
+  for (int c = lane; c < nc; c += 64) {
+    const float m = base[c * (DH + 2) + DH], l = base[c * (DH + 2) + DH + 1];
+    const float Mn = fmaxf(M, m);
+    den = (M == -INFINITY ? 0.f : den * expf(M - Mn)) + (m == -INFINITY ? 0.f : l * expf(m - Mn));
+    M = Mn;
+  }
+  const float Mw = wave_max(M);
+  den = wave_sum(M == -INFINITY ? 0.f : den * expf(M - Mw));
+  M = Mw;
   float acc[PER];
 #pragma unroll
   for (int q = 0; q < PER; ++q) acc[q] = 0.f;
-  for (int c0 = 0; c0 < nc; c0 += CB) {
-    float w[CB], v[CB][PER];
 #pragma unroll
-    for (int u = 0; u < CB; ++u) {  // all loads of the batch in flight together
+  for (int u = 0; u < CB; ++u) {
+    const float wu = u < nc ? expf(w[u] - M) : 0.f;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) acc[q] = fmaf(wu, v[u][q], acc[q]);
+  }
+  for (int c0 = CB; c0 < nc; c0 += CB) {  // longer contexts: further batches
+#pragma unroll
+    for (int u = 0; u < CB; ++u) {
       const int cu = min(c0 + u, nc - 1);
       w[u] = base[cu * (DH + 2) + DH];
 #pragma unroll

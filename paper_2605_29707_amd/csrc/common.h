@@ -25,6 +25,13 @@ DEVI bf16_t f32_to_bf16(float f) {
   u += 0x7fffu + ((u >> 16) & 1u);
   return bf16_t{(uint16_t)(u >> 16)};
 }
+// Device-scope (all XCDs) loads and stores of single values, for data one
+// workgroup hands to another within a launch: the store is complete at the
+// device coherence point once the storing thread's vector-memory count drains,
+// and the load does not hit a stale line in a CU or XCD cache.
+DEVI float ld_coherent(const float *p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+DEVI void st_coherent(float *p, float v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+
 DEVI void store_as(float *p, float v) { *p = v; }
 DEVI void store_as(bf16_t *p, float v) { *p = f32_to_bf16(v); }
 
