@@ -358,7 +358,7 @@ def main():
                    "batch": bs, "ctx": cfg.ctx, "block": cfg.block, "branch": beta,
                    "hidden": cfg.hidden, "layers": cfg.n_layers, "vocab": V,
                    "storage": cfg.dtype},
-        "roofline": {"kernel": "LM-head GEMM (gemm_kernel<bf16_t, 1, 1, 0>, W1 H-half fused)", "bound": "hbm",
+        "roofline": {"kernel": "LM-head GEMM (gemm_stream_kernel<bf16_t, 1, 16, 8>, W1 H-half fused)", "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                      "frac": round(achieved * 1e9 / HBM_PEAK, 4), "traffic": lmhead_traffic(cfg.name),
                      "launch_us": round(dom_launch_s * 1e6, 2), "launches": dom_n,

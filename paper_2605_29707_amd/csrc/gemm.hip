@@ -25,7 +25,9 @@
 // just prefetched.  When K is split across workgroups (ksplit > 1) each
 // split writes its own partial output and the consuming kernel adds the
 // partials in split order: no workgroup ever waits on another, and the sums
-// are bitwise reproducible.
+// are bitwise reproducible.  Grids larger than the device (the LM head: 1189
+// groups of 8 tiles) run as one workgroup per CU looping over its groups with a
+// single pipeline, which saves the pipeline fill of every further workgroup.
 #include "common.h"
 #include "kernels.h"
 #include "mfma.h"
@@ -239,11 +241,138 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
   }
 }
 
+// Stored-output variant for grids larger than the device: pgrid workgroups
+// each take groups blockIdx.x, blockIdx.x + pgrid, ... one after another with a
+// single double-buffered pipeline over (group, chunk), so a workgroup never
+// restarts it (the fill of a fresh workgroup costs a memory round trip).
+template <typename WT, int MT, int KCM, int kWaves>
+__global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(GemmArgs a, int ngroups) {
+  constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP;
+  constexpr int XF = XStage<WT>::XF;
+  constexpr int KW = KCM;
+  constexpr int ITEMS = KCM * MT * 64;
+  constexpr int IPT = (ITEMS + kWaves * 64 - 1) / (kWaves * 64);
+  __shared__ u32x4 xs[2][KCM][MT][64][XF];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ky = blockIdx.y, mz = blockIdx.z;
+  const int KS = a.KS;
+  const int nch = (KS + KCM - 1) / KCM;
+  const int cpw = (nch + a.ksplit - 1) / a.ksplit;
+  const int c0 = min(nch, ky * cpw), c1 = min(nch, c0 + cpw);
+  const int nck = c1 - c0;
+  const int mine = (int)blockIdx.x < ngroups ? (ngroups - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
+  const int total = mine * nck;
+  if (total <= 0) return;
+  const int mbase = mz * MT * 16;
+  float *Y = a.Y + (size_t)ky * a.ysplit;
+
+  auto tile_of = [&](int it) { return ((int)blockIdx.x + (it / nck) * (int)gridDim.x) * kWaves + wave; };
+  auto load_w = [&](u32x4 (&w)[KW], int it) {
+    const int t = min(tile_of(it), a.ntiles - 1);
+    const u32x4 *Pv = (const u32x4 *)a.P + ((size_t)(a.tile0 + t) * KS) * 64 + lane;
+    const int c = c0 + it % nck;
+#pragma unroll
+    for (int u = 0; u < KW; ++u) {
+      const int s = min(c * KCM + u, KS - 1);
+      w[u] = __builtin_nontemporal_load(Pv + (size_t)s * 64);
+    }
+  };
+  auto load_x = [&](float4 (&v)[IPT][EPL / 4], int it) {
+    const int c = c0 + it % nck;
+#pragma unroll
+    for (int q = 0; q < IPT; ++q) {
+      const int i2 = min(tid + q * kWaves * 64, ITEMS - 1);
+      const int l = i2 & 63, mt = (i2 >> 6) % MT, s = (i2 >> 6) / MT;
+      const int m = mbase + mt * 16 + (l & 15);
+      const int k0 = (c * KCM + s) * KSTEP + (l >> 4) * EPL;
+      load_xfrag<EPL>(a.X, a.ldx, a.M, a.K, m, k0, v[q]);
+    }
+  };
+  auto store_x = [&](const float4 (&v)[IPT][EPL / 4], int buf) {
+#pragma unroll
+    for (int q = 0; q < IPT; ++q) {
+      const int i2 = tid + q * kWaves * 64;
+      if (ITEMS % (kWaves * 64) != 0 && i2 >= ITEMS) continue;
+      const int l = i2 & 63, mt = (i2 >> 6) % MT, s = (i2 >> 6) / MT;
+      XStage<WT>::put(&xs[buf][s][mt][l][0], v[q]);
+    }
+  };
+  floatx4 acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](const u32x4 (&w)[KW], int it, int buf) {
+    const int c = c0 + it % nck;
+#pragma unroll
+    for (int u = 0; u < KW; ++u) {
+      if (c * KCM + u < KS) {
+        u32x4 xf[MT * XF];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int f = 0; f < XF; ++f) xf[mt * XF + f] = xs[buf][u][mt][lane][f];
+        Mac2<WT, MT>::step(w[u], xf, acc);
+      }
+    }
+  };
+  auto finish = [&](int it) {  // after the last chunk of an item: store and restart the sums
+    if (it % nck != nck - 1) return;
+    const int tile = tile_of(it);
+    if (tile < a.ntiles) {
+      const int n = tile * 16 + 4 * (lane >> 4);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = mbase + mt * 16 + (lane & 15);
+        if (m >= a.M) continue;
+        float *y = Y + (size_t)m * a.ldy + n;
+        if (n + 4 <= a.N && ((a.ldy & 3) == 0)) {
+          *(floatx4 *)y = acc[mt];
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (n + e < a.N) y[e] = acc[mt][e];
+        }
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  };
+
+  u32x4 wa[KW], wb[KW];
+  float4 xr[IPT][EPL / 4];
+  load_x(xr, 0);
+  load_w(wa, 0);
+  store_x(xr, 0);
+  __syncthreads();
+  for (int it = 0; it < total; it += 2) {
+    const bool n1 = it + 1 < total;
+    if (n1) {
+      load_x(xr, it + 1);
+      load_w(wb, it + 1);
+    }
+    compute(wa, it, 0);
+    finish(it);
+    if (n1) store_x(xr, 1);
+    __syncthreads();
+    if (!n1) break;
+    const bool n2 = it + 2 < total;
+    if (n2) {
+      load_x(xr, it + 2);
+      load_w(wa, it + 2);
+    }
+    compute(wb, it + 1, 1);
+    finish(it + 1);
+    if (n2) store_x(xr, 0);
+    __syncthreads();
+  }
+}
+
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
 GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu, int max_split) {
   GemmPlan p;
+  p.pgrid = 0;
   p.MT = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   p.mgroups = (M + 16 * p.MT - 1) / (16 * p.MT);
   p.WPT = 1;
@@ -280,11 +409,28 @@ GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu, int max_split) 
       }
     }
   }
+  // more workgroups than CUs (8 waves and 16-k-step chunks fill a CU): a
+  // grid of at most n_cu workgroups loops over the groups instead, sized so
+  // that every workgroup takes the same number of groups (or one fewer) and
+  // rounded up to a multiple of 8 (the XCDs)
+  p.pgrid = 0;
+  const long wgs = (long)p.groups * p.ksplit * p.mgroups;
+  if (epi == EPI_STORE && p.nw == 8 && p.kcm == 16 / p.MT && wgs > n_cu) {
+    const int per = std::max(1, n_cu / (p.ksplit * p.mgroups));  // CUs per (split, m-group)
+    const int rounds = (p.groups + per - 1) / per;
+    const int pg = std::min(per, ((p.groups + rounds - 1) / rounds + 7) / 8 * 8);
+    if (pg < p.groups) p.pgrid = pg;
+  }
   return p;
 }
 
 template <typename WT, int MT, int EPI, int KCM>
 static void launch_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
+  if (EPI == EPI_STORE && p.pgrid > 0 && p.nw == 8) {
+    hipLaunchKernelGGL((gemm_stream_kernel<WT, MT, KCM, 8>), dim3(p.pgrid, p.ksplit, p.mgroups), dim3(8 * 64), 0, st,
+                       a, p.groups);
+    return;
+  }
   dim3 grid(p.groups, p.ksplit, p.mgroups);
   if (p.nw == 6)
     hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 6>), grid, dim3(6 * 64), 0, st, a);

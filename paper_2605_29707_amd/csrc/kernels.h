@@ -26,6 +26,7 @@ struct GemmPlan {
   int MT, WPT, groups, mgroups, ksplit;
   int kcm;  // k-steps per staged chunk (16/MT, or 8/MT for finer K splits)
   int nw;   // waves (= tiles) per workgroup: 8 or 6
+  int pgrid;  // > 0: that many workgroups loop over the groups (one pipeline across groups)
 };
 
 // max_split = 1: one workgroup covers all of K (direct output); otherwise K
