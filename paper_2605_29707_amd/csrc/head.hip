@@ -929,7 +929,7 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
         acc = fmaf(wfl[6], s1.z, acc);
         acc = fmaf(wfl[7], s1.w, acc);
       }
-      acc = wave_sum(acc);
+      acc = wave_sum_dpp(acc);
       if (lane == 0) {
         const float x = P_s[((size_t)(j - 1) * bs + b) * nu + k] + acc;
         const float u = x / (1.f + expf(-x));
@@ -972,7 +972,7 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
 #pragma unroll
         for (int b = 0; b < BS; ++b) {
           if (b >= bs) break;
-          const float acc = wave_sum(accb[b]);
+          const float acc = wave_sum_dpp(accb[b]);
           if (lane == 0) st_coherent(gh_out + (size_t)b * 3 * ds + (R - r), acc + bias);
         }
       }
