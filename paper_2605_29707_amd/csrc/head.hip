@@ -791,8 +791,11 @@ DEVI bool poll_tagged(const unsigned long long *slots, int n, unsigned long long
 }
 
 // BS: the largest batch the instantiation serves (1 or 2; arrays sized by it);
-// DBG: the final logits are also written out (h.final_logits)
-template <int BS, bool DBG>
+// DBG: the final logits are also written out (h.final_logits);
+// SAMPLE: temperature sampling, the selection key is L / T + Gumbel noise
+// (Philox stream RNG_DRAFT, as in the launch-pair rollout) and the reported
+// value is the chosen token's raw logit
+template <int BS, bool DBG, bool SAMPLE>
 __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs h, int nr) {
   using WT = bf16_t;
   constexpr int EPL = 8, KSTEP = 32;
@@ -812,8 +815,9 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
   float *u_s = (float *)(lbs + kPersWaves * kPersTiles * 64);  // [bs][r] u of the position
   const int nu = (r + G - 1) / G;                              // u rows per workgroup: k < nu (R < r)
   float *P_s = u_s + (size_t)bs * r;                           // [depth][bs][nu] W1[:, :d] H at the u rows
-  __shared__ float best_v[kPersWaves][16], best_r[kPersWaves][16];
+  __shared__ float best_v[kPersWaves][16], best_r[SAMPLE ? kPersWaves : 1][16];
   __shared__ int best_i[kPersWaves][16];
+  __shared__ int win_id[SAMPLE ? 64 : 1][BS];  // workgroup 0: each position's drafted token
   __shared__ int ys[kFusedBatch];
   __shared__ int s_ok;
   const WT *w1 = (const WT *)h.w1, *whh = (const WT *)h.w_hh;
@@ -1047,30 +1051,24 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
     }
     {
       // ids grow along (q, e) within a lane, so a strict comparison keeps the
-      // smallest id of equal values; ids past V occur only in the last workgroup
-      float bv = -INFINITY;
+      // smallest id of equal keys; ids past V occur only in the last workgroup
+      float bv = -INFINITY, br = 0.f;
       int bi = (tile0 * 16 + 4 * g) < V ? tile0 * 16 + 4 * g : INT_MAX;
-      if ((tile0 + kPersTiles) * 16 <= V) {
+      const bool full = (tile0 + kPersTiles) * 16 <= V;
 #pragma unroll
-        for (int q = 0; q < kPersTiles; ++q)
+      for (int q = 0; q < kPersTiles; ++q) {
+        Philox4 noise = {{0u, 0u, 0u, 0u}};
+        if (SAMPLE) noise = rng_block(h.seed_lo, h.seed_hi, RNG_DRAFT, cc, j, (tile0 + q) * 4 + g);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float ov = order_val(val[q][e]);
-            const bool take = ov > bv;
-            bv = take ? ov : bv;
-            bi = take ? (tile0 + q) * 16 + 4 * g + e : bi;
-          }
-      } else {
-#pragma unroll
-        for (int q = 0; q < kPersTiles; ++q)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int n = (tile0 + q) * 16 + 4 * g + e;
-            const float ov = n < V ? order_val(val[q][e]) : -INFINITY;
-            const bool take = ov > bv;
-            bv = take ? ov : bv;
-            bi = take ? n : bi;
-          }
+        for (int e = 0; e < 4; ++e) {
+          const int n = (tile0 + q) * 16 + 4 * g + e;
+          const float key = SAMPLE ? val[q][e] * h.inv_temp + rng_gumbel(noise.x[e]) : val[q][e];
+          const float ov = (full || n < V) ? order_val(key) : -INFINITY;
+          const bool take = ov > bv;
+          bv = take ? ov : bv;
+          bi = take ? n : bi;
+          if (SAMPLE) br = take ? val[q][e] : br;
+        }
       }
       if (!rowok) {
         bv = -INFINITY;
@@ -1080,27 +1078,35 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
       for (int o = 16; o <= 32; o <<= 1) {
         const float ov = __shfl_xor(bv, o, 64);
         const int oi = __shfl_xor(bi, o, 64);
+        const float orw = SAMPLE ? __shfl_xor(br, o, 64) : 0.f;
         const bool take = better(ov, oi, bv, bi);
         bv = take ? ov : bv;
         bi = take ? oi : bi;
+        if (SAMPLE) br = take ? orw : br;
       }
       if (g == 0) {
         best_v[wave][cc] = bv;
         best_i[wave][cc] = bi;
+        if (SAMPLE) best_r[SAMPLE ? wave : 0][cc] = br;
       }
     }
     __builtin_amdgcn_s_waitcnt(0);  // this thread's gate stores are done
     __syncthreads();                // ... and every thread's
     if (tid < bs) {
       const int bb = tid;
-      float v = best_v[0][bb];
+      float v = best_v[0][bb], raw = SAMPLE ? best_r[0][bb] : 0.f;
       int id = best_i[0][bb];
 #pragma unroll
       for (int w = 1; w < kPersWaves; ++w)
         if (better(best_v[w][bb], best_i[w][bb], v, id)) {
           v = best_v[w][bb];
           id = best_i[w][bb];
+          if (SAMPLE) raw = best_r[SAMPLE ? w : 0][bb];
         }
+      if (SAMPLE) {  // the raw logit goes out before the key that announces it
+        st_coherent(h.praw + ((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x, raw);
+        __builtin_amdgcn_s_waitcnt(0);
+      }
       // an empty slice (no valid id) publishes the smallest key
       const unsigned long long key = id == INT_MAX ? 0ull : pack_key50(v, id);
       st_slot(h.kslot + (size_t)bb * G + blockIdx.x, ((unsigned long long)j << 50) | key);
@@ -1133,7 +1139,8 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
             if (blockIdx.x == 0) {
               const uint32_t u = (uint32_t)(best >> kKeyIdBits);
               h.topk_ids[(size_t)b * depth + (j - 1)] = id;
-              h.topk_vals[(size_t)b * depth + (j - 1)] = __uint_as_float((u & 0x80000000u) ? (u ^ 0x80000000u) : ~u);
+              if (SAMPLE) win_id[SAMPLE ? j - 1 : 0][b] = id;
+              else h.topk_vals[(size_t)b * depth + (j - 1)] = __uint_as_float((u & 0x80000000u) ? (u ^ 0x80000000u) : ~u);
             }
           }
         }
@@ -1143,14 +1150,23 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
       if (!s_ok) return;
     }
   }
+  if (SAMPLE && blockIdx.x == 0) {  // reported values: the drafted tokens' raw logits, from their owners
+    __syncthreads();
+    for (int e = tid; e < depth * bs; e += kPersWaves * 64) {
+      const int jj = e / bs, b = e % bs;
+      const int id = win_id[SAMPLE ? jj : 0][b];
+      const int owner = min(max(id, 0), V - 1) / (16 * kPersWaves * kPersTiles);
+      h.topk_vals[(size_t)b * depth + jj] = ld_coherent(h.praw + ((size_t)jj * bs + b) * h.GC + owner);
+    }
+  }
 }
 
 bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st) {
   const Dims &D = h.D;
-  // greedy, one or two batch rows (larger batches and temperature sampling run
-  // the launch-pair rollout: their register demand would spill here)
-  if (!D.bf16 || D.r != kPersKS * 32 || D.bs > 2 || h.beta != 1 || h.sample || D.ds % 32 || D.ds > 256 * 8 ||
-      D.V >= (1 << kKeyIdBits) || !h.uslot || !h.kslot || !h.abort_flag)
+  // one or two batch rows, branch 1 (larger batches run the launch-pair
+  // rollout: their register demand would spill here)
+  if (!D.bf16 || D.r != kPersKS * 32 || D.bs > 2 || h.beta != 1 || D.ds % 32 || D.ds > 256 * 8 ||
+      D.V >= (1 << kKeyIdBits) || D.B > 64 || !h.uslot || !h.kslot || !h.abort_flag || (h.sample && !h.praw))
     return false;
   const int NT = (D.V + 15) / 16;
   const int G = (NT + kPersWaves * kPersTiles - 1) / (kPersWaves * kPersTiles);
@@ -1163,9 +1179,18 @@ bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st) {
                      sizeof(float4) * kPersWaves * kPersTiles * 64 + sizeof(float) * (size_t)D.bs * D.r +
                      sizeof(float) * (size_t)(D.B - 1) * D.bs * ((D.r + G - 1) / G);
   if (lds > 160 * 1024) return false;
-  const bool dbg = h.final_logits != nullptr;
-  const void *fn = D.bs == 1 ? (dbg ? (const void *)head_persist_kernel<1, true> : (const void *)head_persist_kernel<1, false>)
-                             : (dbg ? (const void *)head_persist_kernel<2, true> : (const void *)head_persist_kernel<2, false>);
+  const bool dbg = h.final_logits != nullptr, smp = h.sample != 0;
+  const void *fn;
+  switch ((D.bs == 1 ? 0 : 4) + (dbg ? 2 : 0) + (smp ? 1 : 0)) {
+    case 0: fn = (const void *)head_persist_kernel<1, false, false>; break;
+    case 1: fn = (const void *)head_persist_kernel<1, false, true>; break;
+    case 2: fn = (const void *)head_persist_kernel<1, true, false>; break;
+    case 3: fn = (const void *)head_persist_kernel<1, true, true>; break;
+    case 4: fn = (const void *)head_persist_kernel<2, false, false>; break;
+    case 5: fn = (const void *)head_persist_kernel<2, false, true>; break;
+    case 6: fn = (const void *)head_persist_kernel<2, true, false>; break;
+    default: fn = (const void *)head_persist_kernel<2, true, true>; break;
+  }
   if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
     (void)hipGetLastError();
     return false;

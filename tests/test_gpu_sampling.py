@@ -91,8 +91,11 @@ def _check_sampled(cfg, gpu, inp, w64, T, seed, tol):
     return int(mask.sum()), mask.size
 
 
-@pytest.mark.parametrize("dtype,batch,T", [("f32", 3, 1.0), ("f32", 1, 0.6), ("bf16", 5, 1.0), ("bf16", 12, 1.3)])
+@pytest.mark.parametrize("dtype,batch,T", [("f32", 3, 1.0), ("f32", 1, 0.6), ("bf16", 5, 1.0), ("bf16", 12, 1.3),
+                                           ("bf16", 1, 1.0), ("bf16", 2, 0.7)])
 def test_sampled_drafting_tiny(dtype, batch, T):
+    """bf16 with one or two batch rows runs the persistent rollout (its sampled
+    variant), the other cases the launch-pair rollout."""
     cfg = synth.get_config("tiny").with_(dtype=dtype, batch=batch, branch=1, ctx_from_hidden=False)
     w = synth.make_weights(cfg, seed=21, gain_std=0.1)
     inp = synth.make_inputs(cfg, seed=21)
