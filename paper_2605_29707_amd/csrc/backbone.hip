@@ -307,12 +307,27 @@ size_t attn_part_floats(const Dims &D, int max_ctx) {
   return (size_t)D.bs * D.nq * D.B * attn_nchunks(max_ctx, D.B) * (D.dh + 2);
 }
 
-// Split 8 consecutive fp32 values (two 16-byte LDS vectors) into hi/lo bf16
-// matrix-core fragments.
-DEVI void frag_split(const float *p, bf16x8 &hi, bf16x8 &lo) {
-  const float4 a = *(const float4 *)p, c = *(const float4 *)(p + 4);
-  const float f[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
-  split8(f, hi, lo);
+// Four fp32 values as hi and lo bf16 quads (8 bytes each), the split of split8.
+DEVI void split4(const float4 &v, uint2 &hi, uint2 &lo) {
+  const float f[8] = {v.x, v.y, v.z, v.w, 0.f, 0.f, 0.f, 0.f};
+  bf16x8 h, l;
+  split8(f, h, l);
+  const u32x4 hu = __builtin_bit_cast(u32x4, h), lu = __builtin_bit_cast(u32x4, l);
+  hi = make_uint2(hu[0], hu[1]);
+  lo = make_uint2(lu[0], lu[1]);
+}
+DEVI bf16x8 ld_frag(const uint16_t *p) { return __builtin_bit_cast(bf16x8, *(const u32x4 *)p); }
+// the product with an exact bf16 first operand (its lo part is zero)
+DEVI floatx4 mfma2(const bf16x8 &ah, const bf16x8 &bh, const bf16x8 &bl, floatx4 acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, acc, 0, 0, 0);
+  return acc;
+}
+// the product with an exact bf16 second operand, in mfma3's order without its zero term
+DEVI floatx4 mfma2b(const bf16x8 &ah, const bf16x8 &al, const bf16x8 &bh, floatx4 acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, acc, 0, 0, 0);
+  return acc;
 }
 DEVI floatx4 mfma3(const bf16x8 &ah, const bf16x8 &al, const bf16x8 &bh, const bf16x8 &bl, floatx4 acc) {
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, acc, 0, 0, 0);
@@ -325,8 +340,10 @@ DEVI floatx4 mfma3(const bf16x8 &ah, const bf16x8 &al, const bf16x8 &bh, const b
 //   S^T = K Q^T  (16-key x 16-query tiles), softmax statistics per query row,
 //   O   = P V    (16-query x 16-dim tiles), with every fp32 operand split into
 //   hi + lo bf16 parts (three passes, the lo*lo term dropped: ~2^-16 relative).
-// Q, K, P live in LDS row-major; V is staged transposed so a B fragment (8
-// consecutive keys of one dim) is one contiguous read.
+// Q, K, P live in LDS row-major as bf16 hi and lo parts (split once, when
+// staged or produced; P takes K's place once the scores are formed); V is staged transposed so a B fragment (8 consecutive
+// keys of one dim) is one contiguous read.  A chunk of bf16 cache keys has
+// exact K and V (zero lo parts): the products with them are skipped.
 // MASKED: block key k is visible to block query j only where amask[b][j][k] is
 // set (a verify forward's tree mask, [bs][B][B] bytes, B a multiple of 4);
 // context keys are always visible.  Rows whose keys in a chunk are all hidden
@@ -342,14 +359,18 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   constexpr int DT = DH / 16;     // output dim tiles
   constexpr int QTW = QT * KT / 4;  // query tiles per wave in the score phase
   constexpr int DTW = DT / 4;     // dim tiles per wave in the output phase
-  constexpr int DP = DH + 4, CP = CH + 4;
+  // operands are held as bf16 hi and lo parts, split once while staging
+  constexpr int DP = DH + 8, CP = CH + 8;  // row strides in bf16 values (16-byte rows, staggered banks)
   extern __shared__ __align__(16) float smem[];
-  float *Qs = smem;               // [R][DP]
-  float *Ks = Qs + R * DP;        // [CH][DP]
-  float *Vt = Ks + CH * DP;       // [DH][CP]  (transposed)
-  float *Ps = Vt + DH * CP;       // [R][CP]
-  float *Rm = Ps + R * CP;        // [KT][R] partial row max
-  float *Rl = Rm + KT * R;        // [KT][R] partial row sum
+  uint16_t *Qh = (uint16_t *)smem, *Ql = Qh + R * DP;  // [R][DP]
+  uint16_t *Kh = Ql + R * DP, *Kl = Kh + CH * DP;        // [CH][DP]
+  uint16_t *Vh = Kl + CH * DP, *Vl = Vh + DH * CP;       // [DH][CP]  (transposed)
+  // [R][CP], over K where it fits: P is written after the barrier that
+  // follows the last read of K
+  constexpr bool kPinK = R * CP <= CH * DP;
+  uint16_t *Ph = kPinK ? Kh : Vl + DH * CP, *Pl = Ph + R * CP;
+  float *Rm = (float *)(kPinK ? Vl + DH * CP : Pl + R * CP);  // [KT][R] partial row max
+  float *Rl = Rm + KT * R;             // [KT][R] partial row sum
   uint32_t *Ms = (uint32_t *)(Rl + KT * R);  // MASKED: [B][B] bytes of this batch row's tree mask
   constexpr int kMaskIt = 64 * 64 / 4 / kAttnThreads;  // words per thread for B <= 64
 
@@ -364,7 +385,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, cc = lane & 15;
 
-  // ---- stage Q rows, K chunk (row-major) and V chunk (transposed), fp32
+  // ---- stage Q rows, the K chunk (row-major) and the V chunk (transposed)
   {
     constexpr int NQ = R * DH / 4 / kAttnThreads;
     float4 qv[NQ];
@@ -419,19 +440,29 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     for (int q = 0; q < NQ; ++q) {
       const int e = tid + q * kAttnThreads;
       const int qi = e / (DH / 4), d4 = e % (DH / 4);
-      *(float4 *)(Qs + qi * DP + 4 * d4) = qv[q];
+      uint2 hi, lo;
+      split4(qv[q], hi, lo);
+      *(uint2 *)(Qh + qi * DP + 4 * d4) = hi;
+      *(uint2 *)(Ql + qi * DP + 4 * d4) = lo;
     }
 #pragma unroll
     for (int q = 0; q < NE; ++q) {
       const int e = tid + q * kAttnThreads;
       const int t = e / (DH / 4), d4 = e % (DH / 4);
-      *(float4 *)(Ks + t * DP + 4 * d4) = keep4(t < nk, kv[q]);
+      uint2 hi, lo;
+      split4(keep4(t < nk, kv[q]), hi, lo);
+      *(uint2 *)(Kh + t * DP + 4 * d4) = hi;
+      *(uint2 *)(Kl + t * DP + 4 * d4) = lo;
       const int tv = e % CH, dv = e / CH;
-      const float4 v = keep4(tv < nk, vv[q]);
-      Vt[(4 * dv + 0) * CP + tv] = v.x;
-      Vt[(4 * dv + 1) * CP + tv] = v.y;
-      Vt[(4 * dv + 2) * CP + tv] = v.z;
-      Vt[(4 * dv + 3) * CP + tv] = v.w;
+      split4(keep4(tv < nk, vv[q]), hi, lo);
+      Vh[(4 * dv + 0) * CP + tv] = (uint16_t)hi.x;
+      Vh[(4 * dv + 1) * CP + tv] = (uint16_t)(hi.x >> 16);
+      Vh[(4 * dv + 2) * CP + tv] = (uint16_t)hi.y;
+      Vh[(4 * dv + 3) * CP + tv] = (uint16_t)(hi.y >> 16);
+      Vl[(4 * dv + 0) * CP + tv] = (uint16_t)lo.x;
+      Vl[(4 * dv + 1) * CP + tv] = (uint16_t)(lo.x >> 16);
+      Vl[(4 * dv + 2) * CP + tv] = (uint16_t)lo.y;
+      Vl[(4 * dv + 3) * CP + tv] = (uint16_t)(lo.y >> 16);
     }
     if constexpr (MASKED) {
 #pragma unroll
@@ -441,20 +472,23 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   }
   __syncthreads();
 
-  // ---- scores: wave w owns key tile kt = w % KT and QTW query tiles
+  // ---- scores: wave w owns key tile kt = w % KT and QTW query tiles.  A
+  // chunk of bf16 cache keys only has exact keys: their lo parts are zero,
+  // so those products are skipped (the sums are the same bits).
+  const bool exact = sizeof(WT) == 2 && c0 + CH <= n;
   const int kt = wave % KT, qt0 = (wave / KT) * QTW;
   floatx4 sacc[QTW];
 #pragma unroll
   for (int i = 0; i < QTW; ++i) sacc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < DH / 32; ++s) {
-    bf16x8 kh, kl;
-    frag_split(Ks + (16 * kt + cc) * DP + 32 * s + 8 * g, kh, kl);
+    const bf16x8 kh = ld_frag(Kh + (16 * kt + cc) * DP + 32 * s + 8 * g);
+    const bf16x8 kl = ld_frag(Kl + (16 * kt + cc) * DP + 32 * s + 8 * g);
 #pragma unroll
     for (int i = 0; i < QTW; ++i) {
-      bf16x8 qh, ql;
-      frag_split(Qs + (16 * (qt0 + i) + cc) * DP + 32 * s + 8 * g, qh, ql);
-      sacc[i] = mfma3(kh, kl, qh, ql, sacc[i]);
+      const bf16x8 qh = ld_frag(Qh + (16 * (qt0 + i) + cc) * DP + 32 * s + 8 * g);
+      const bf16x8 ql = ld_frag(Ql + (16 * (qt0 + i) + cc) * DP + 32 * s + 8 * g);
+      sacc[i] = exact ? mfma2(kh, qh, ql, sacc[i]) : mfma3(kh, kl, qh, ql, sacc[i]);
     }
   }
   // lane (g, cc) holds S[q = 16*qt + cc][key = 16*kt + 4g + e]
@@ -494,7 +528,10 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
         p[e] = key < nk ? expf(sacc[i][e] - m) : 0.f;
       l += p[e];
     }
-    *(float4 *)(Ps + q * CP + 16 * kt + 4 * g) = make_float4(p[0], p[1], p[2], p[3]);
+    uint2 hi, lo;
+    split4(make_float4(p[0], p[1], p[2], p[3]), hi, lo);
+    *(uint2 *)(Ph + q * CP + 16 * kt + 4 * g) = hi;
+    *(uint2 *)(Pl + q * CP + 16 * kt + 4 * g) = lo;
     l += __shfl_xor(l, 16, 64);
     l += __shfl_xor(l, 32, 64);
     if (g == 0) Rl[kt * R + q] = l;
@@ -521,14 +558,17 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   for (int s = 0; s < CH / 32; ++s) {
     bf16x8 vh[DTW], vl[DTW];
 #pragma unroll
-    for (int x = 0; x < DTW; ++x)
-      frag_split(Vt + (16 * (wave * DTW + x) + cc) * CP + 32 * s + 8 * g, vh[x], vl[x]);
+    for (int x = 0; x < DTW; ++x) {
+      vh[x] = ld_frag(Vh + (16 * (wave * DTW + x) + cc) * CP + 32 * s + 8 * g);
+      vl[x] = ld_frag(Vl + (16 * (wave * DTW + x) + cc) * CP + 32 * s + 8 * g);
+    }
 #pragma unroll
     for (int i = 0; i < QT; ++i) {
-      bf16x8 ph, pl;
-      frag_split(Ps + (16 * i + cc) * CP + 32 * s + 8 * g, ph, pl);
+      const bf16x8 ph = ld_frag(Ph + (16 * i + cc) * CP + 32 * s + 8 * g);
+      const bf16x8 pl = ld_frag(Pl + (16 * i + cc) * CP + 32 * s + 8 * g);
 #pragma unroll
-      for (int x = 0; x < DTW; ++x) oacc[i][x] = mfma3(ph, pl, vh[x], vl[x], oacc[i][x]);
+      for (int x = 0; x < DTW; ++x)  // exact V (zero lo part): the zero product is left out
+        oacc[i][x] = exact ? mfma2b(ph, pl, vh[x], oacc[i][x]) : mfma3(ph, pl, vh[x], vl[x], oacc[i][x]);
     }
   }
   // lane (g, cc) holds O[q = 16*i + 4g + e][dim = 16*dt + cc]
@@ -686,10 +726,10 @@ template <typename WT, int RPT, int CH, int DH, bool MASKED>
 static void attn_launch_t(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
                           const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
                           const uint8_t *amask, hipStream_t st) {
-  constexpr int R = RPT * 16, DP = DH + 4, CP = CH + 4, KT = CH / 16;
-  const size_t lds =
-      sizeof(float) * ((size_t)R * DP + (size_t)CH * DP + (size_t)DH * CP + (size_t)R * CP + 2 * KT * R) +
-      (MASKED ? (size_t)64 * 64 : 0);
+  constexpr int R = RPT * 16, DP = DH + 8, CP = CH + 8, KT = CH / 16;
+  const size_t ps = R * CP <= CH * DP ? 0 : (size_t)R * CP;  // P over K where it fits
+  const size_t lds = 2 * sizeof(uint16_t) * ((size_t)R * DP + (size_t)CH * DP + (size_t)DH * CP + ps) +
+                     sizeof(float) * 2 * KT * R + (MASKED ? (size_t)64 * 64 : 0);
   const float scale = 1.0f / sqrtf((float)DH);
   const int nc = (max_ctx + D.B + CH - 1) / CH;
   (void)hipFuncSetAttribute((const void *)attn_partial_kernel<WT, RPT, CH, DH, MASKED>,
