@@ -92,6 +92,14 @@ __global__ __launch_bounds__(512) void add_norm_kernel(const float *__restrict__
     }
     er = embed + (size_t)tok * width;
   }
+  // the gains of this thread's columns, loaded with the inputs (not after the reduction)
+  float gv[IT][PER];
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int c0 = min((int)(threadIdx.x + it * blockDim.x) * PER, width - PER);
+#pragma unroll
+    for (int e = 0; e < PER; ++e) gv[it][e] = to_f32(gain[c0 + e]);
+  }
   float v[IT][PER];
   float ss = 0.f;
 #pragma unroll
@@ -130,7 +138,7 @@ __global__ __launch_bounds__(512) void add_norm_kernel(const float *__restrict__
 #pragma unroll
     for (int e = 0; e < PER; ++e) ss = fmaf(v[it][e], v[it][e], ss);
   }
-  ss = wave_sum(ss);
+  ss = wave_sum_dpp(ss);
   __shared__ float red[8];
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
@@ -143,7 +151,7 @@ __global__ __launch_bounds__(512) void add_norm_kernel(const float *__restrict__
     if (c0 >= width || c0 / cs != part) continue;
     float o[PER];
 #pragma unroll
-    for (int e = 0; e < PER; ++e) o[e] = v[it][e] * inv * to_f32(gain[c0 + e]);
+    for (int e = 0; e < PER; ++e) o[e] = v[it][e] * inv * gv[it][e];
     float *yr = y + (size_t)i * ldy + c0;
     *(float4 *)(yr) = make_float4(o[0], o[1], o[2], o[3]);
     *(float4 *)(yr + 4) = make_float4(o[4], o[5], o[6], o[7]);
@@ -152,20 +160,19 @@ __global__ __launch_bounds__(512) void add_norm_kernel(const float *__restrict__
 
 // One wave per (row, head).  Lane l holds elements l and l+64 (dh = 128) or
 // l (dh = 64); RoPE pairs element i with i + dh/2.
-template <typename WT>
-DEVI void norm_rope_head(float (&v)[2], int dh, const WT *__restrict__ gain, float eps, int pos,
-                         const double *__restrict__ inv_freq, bool rotate, int lane) {
+DEVI void norm_rope_head(float (&v)[2], int dh, const float (&gain)[2], float eps, int pos, double freq,
+                         bool rotate, int lane) {
   const int per = dh / 64;
   float ss = 0.f;
   for (int q = 0; q < per; ++q) ss = fmaf(v[q], v[q], ss);
-  ss = wave_sum(ss);
+  ss = wave_sum_dpp(ss);
   const float inv = 1.0f / sqrtf(ss / (float)dh + eps);
-  for (int q = 0; q < per; ++q) v[q] = v[q] * inv * to_f32(gain[lane + 64 * q]);
+  for (int q = 0; q < per; ++q) v[q] = v[q] * inv * gain[q];
   if (!rotate) return;
-  // angle pos * theta^(-2i/dh): formed and reduced modulo 2*pi in fp64, then an
-  // fp32 sine/cosine of the reduced angle (|error| ~ 1e-7 at positions of 10^4)
-  const int i = dh == 128 ? lane : (lane & 31);
-  const double ang = (double)pos * inv_freq[i];
+  // angle pos * theta^(-2i/dh) (freq = theta^(-2i/dh) of this lane's pair):
+  // formed and reduced modulo 2*pi in fp64, then an fp32 sine/cosine of the
+  // reduced angle (|error| ~ 1e-7 at positions of 10^4)
+  const double ang = (double)pos * freq;
   const double k = rint(ang * 0.15915494309189535);
   const double red = fma(-k, 6.283185307179586, ang) - k * 2.4492935982947064e-16;
   float s, c;
@@ -215,6 +222,19 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
   const float *src = qkv + (size_t)m * nh * dh + (size_t)hh * dh;
   float v[2] = {0.f, 0.f};
   const int per = dh / 64;
+  // everything the head needs besides the projection, loaded with it: the
+  // context length, the row's position, the norm gains, the RoPE frequency
+  const bool appended = m >= M;
+  const int b = appended ? (m - M) / n_new : m / B;
+  const int n_raw = ctx_lens[b];
+  const int prow = (!appended && pos_rows) ? pos_rows[m] : 0;
+  float gv[2];
+  {
+    const WT *gp = hh < nq ? qn : kn;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) gv[q] = to_f32(gp[lane + 64 * min(q, per - 1)]);
+  }
+  const double freq = inv_freq[dh == 128 ? lane : (lane & 31)];
   {
     // K-split partial outputs, added in split order; all loads issued together
     // (MAXP slots, clamped to a valid partial, added only below np)
@@ -231,9 +251,9 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
 #pragma unroll
         for (int q = 0; q < 2; ++q) v[q] += q < per ? t[p][q] : 0.f;
   }
-  if (m >= M) {
-    const int r = m - M, b = r / n_new, i = r % n_new;
-    int n = ctx_lens[b];
+  if (appended) {
+    const int i = (m - M) % n_new;
+    int n = n_raw;
     if (n < n_new || n > max_ctx) {
       if (lane == 0 && i == 0 && hh == nq) raise_error(err, DEV_BAD_CTX_LEN);
       n = n < n_new ? n_new : max_ctx;
@@ -242,7 +262,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
     const size_t off = (((size_t)b * max_ctx + pos) * nkv) * dh;
     WT *dst;
     if (hh < nq + nkv) {
-      norm_rope_head<WT>(v, dh, kn, eps, pos, inv_freq, true, lane);
+      norm_rope_head(v, dh, gv, eps, pos, freq, true, lane);
       dst = ck + off + (size_t)(hh - nq) * dh;
     } else {
       dst = cv + off + (size_t)(hh - nq - nkv) * dh;
@@ -250,16 +270,16 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const float *__restri
     for (int q = 0; q < per; ++q) store_as(dst + lane + 64 * q, v[q]);
     return;
   }
-  const int b = m / B, j = m % B;
-  int n = ctx_lens[b];
+  const int j = m % B;
+  int n = n_raw;
   n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
-  const int pos = pos_rows ? pos_rows[m] : n + j;
+  const int pos = pos_rows ? prow : n + j;
   float *dst;
   if (hh < nq) {
-    norm_rope_head<WT>(v, dh, qn, eps, pos, inv_freq, true, lane);
+    norm_rope_head(v, dh, gv, eps, pos, freq, true, lane);
     dst = Q + ((size_t)m * nq + hh) * dh;
   } else if (hh < nq + nkv) {
-    norm_rope_head<WT>(v, dh, kn, eps, pos, inv_freq, true, lane);
+    norm_rope_head(v, dh, gv, eps, pos, freq, true, lane);
     dst = Kb + ((size_t)m * nkv + (hh - nq)) * dh;
   } else {
     dst = Vb + ((size_t)m * nkv + (hh - nq - nkv)) * dh;
