@@ -349,7 +349,7 @@ domino_status domino_verify_sample(int32_t batch, int32_t block, int32_t vocab, 
 domino_status domino_philox4x32_10(const uint32_t *counters, uint64_t key, uint32_t *out, int32_t n,
                                    void *stream);
 
-/* Copy the device error word at the start of a draft or verify workspace to/* Copy the device error word at the start of a draft or verify workspace to
+/* Copy the device error word at the start of a draft or verify workspace to
  * *out (synchronises `stream`).  Returns DOMINO_ERR_DEVICE when it is set. */
 domino_status domino_workspace_error(const void *workspace, void *stream, int32_t *out);
 
@@ -374,6 +374,17 @@ domino_status domino_profile_enable(domino_model_t m, uint32_t class_mask);
 domino_status domino_profile_read(domino_model_t m, int32_t kernel_class, double *total_ms,
                                   int32_t *launches);
 domino_status domino_profile_reset(domino_model_t m);
+
+/*
+ * Test hook for the failure path of the persistent rollout (greedy or sampled
+ * drafting with bf16 weights, rank 256 and one or two batch rows): the number
+ * of polls a cross-workgroup wait may make before it gives up, raising
+ * DOMINO_DEV_BARRIER_TIMEOUT in the error word and letting every workgroup
+ * leave (the step's outputs are then undefined); 0 makes every wait give up at
+ * once.  A negative value restores the default (2^22 polls, seconds).  Applies
+ * to the model's later draft steps.
+ */
+domino_status domino_debug_set_poll_limit(domino_model_t m, int32_t polls);
 
 #ifdef __cplusplus
 }

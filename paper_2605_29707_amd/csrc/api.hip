@@ -61,6 +61,7 @@ struct domino_model {
   std::vector<Packed> qkv, wo, gateup, down;
   bool has_head = true;  // false: a target decoder (layers, embedding, LM head only)
   bool persistent = true;  // DOMINO_ROLLOUT=loop selects the launch-pair rollout everywhere
+  uint32_t poll_limit = kDefaultPollLimit;  // persistent rollout: polls a wait makes before it gives up
   Packed lm, w2, w1s;
   // training forward: the state recurrence runs on a second stream beside the backbone
   hipStream_t side = nullptr;
@@ -708,6 +709,7 @@ HeadArgs head_args(domino_model_t m, int32_t batch, int32_t branch, char *ws, co
   h.uslot = (unsigned long long *)(ws + w.slots);
   h.kslot = h.uslot + (size_t)batch * D.r;
   h.abort_flag = (unsigned *)(ws + w.err + 128);
+  h.poll_limit = m->poll_limit;
   return h;
 }
 
@@ -1094,6 +1096,12 @@ domino_status domino_profile_enable(domino_model_t m, uint32_t class_mask) {
 domino_status domino_profile_reset(domino_model_t m) {
   if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
   for (auto &e : m->ev) e.used = 0;
+  return DOMINO_OK;
+}
+
+domino_status domino_debug_set_poll_limit(domino_model_t m, int32_t polls) {
+  if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
+  m->poll_limit = polls < 0 ? kDefaultPollLimit : (uint32_t)polls;
   return DOMINO_OK;
 }
 

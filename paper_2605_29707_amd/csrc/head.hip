@@ -747,7 +747,6 @@ __global__ __launch_bounds__(64) void head_merge_kernel(HeadArgs h) {
 // drafted token and its value of every position (no merge kernel).
 // ---------------------------------------------------------------------------
 constexpr int kPersWaves = 8, kPersTiles = 5, kPersKS = 8, kPersRegTiles = kPersTiles - 1;
-constexpr unsigned kPollLimit = 1u << 22;
 constexpr int kKeyIdBits = 18;
 
 DEVI unsigned long long ld_slot(const unsigned long long *p) {
@@ -764,29 +763,28 @@ DEVI unsigned long long pack_key50(float v, int id) {
 DEVI int key50_id(unsigned long long k) { return (1 << kKeyIdBits) - 1 - (int)(k & ((1ull << kKeyIdBits) - 1)); }
 
 // Wave 0 polls `n` slots until each carries `tag` (top bits from `shift`);
-// lane l holds slots l, l+64, ... in w[].  Returns false on timeout / abort.
+// lane l holds slots l, l+64, ... in w[].  Returns false on timeout (`limit`
+// polls made, none complete) or when another workgroup has aborted.
 template <int MAXQ>
 DEVI bool poll_tagged(const unsigned long long *slots, int n, unsigned long long tag, int shift,
-                      unsigned *abort_flag, int32_t *err, unsigned long long (&w)[MAXQ]) {
+                      unsigned *abort_flag, int32_t *err, unsigned limit, unsigned long long (&w)[MAXQ]) {
   const int lane = threadIdx.x & 63;
-  unsigned spins = 0;
+  unsigned polls = 0;
   while (true) {
+    if (polls++ >= limit) {  // this wait gives up: every workgroup is told to leave
+      if (lane == 0) {
+        __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        raise_error(err, DEV_BARRIER_TIMEOUT);
+      }
+      return false;
+    }
 #pragma unroll
     for (int q = 0; q < MAXQ; ++q) w[q] = ld_slot(slots + min(lane + 64 * q, n - 1));
     bool ready = true;
 #pragma unroll
     for (int q = 0; q < MAXQ; ++q) ready = ready && (w[q] >> shift) == tag;
     if (__all(ready)) return true;
-    if ((++spins & 63) == 0) {
-      if (__hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
-      if (spins > kPollLimit) {
-        if (lane == 0) {
-          __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          raise_error(err, DEV_BARRIER_TIMEOUT);
-        }
-        return false;
-      }
-    }
+    if ((polls & 63) == 0 && __hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
   }
 }
 
@@ -984,7 +982,7 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
     // ---- wait for u (wave 0 polls all u slots; the slots deliver the values)
     if (wave == 0) {
       unsigned long long w[4 * BS];
-      const bool ok = poll_tagged<4 * BS>(h.uslot, bs * r, (unsigned long long)j, 32, h.abort_flag, h.err, w);
+      const bool ok = poll_tagged<4 * BS>(h.uslot, bs * r, (unsigned long long)j, 32, h.abort_flag, h.err, h.poll_limit, w);
 #pragma unroll
       for (int q = 0; q < 4 * BS; ++q) {
         const int e = lane + 64 * q;
@@ -1118,7 +1116,7 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
     if (j < depth || blockIdx.x == 0) {
       if (wave == 0) {
         unsigned long long w[4 * BS];
-        const bool ok = poll_tagged<4 * BS>(h.kslot, bs * G, (unsigned long long)j, 50, h.abort_flag, h.err, w);
+        const bool ok = poll_tagged<4 * BS>(h.kslot, bs * G, (unsigned long long)j, 50, h.abort_flag, h.err, h.poll_limit, w);
         // lane holds slots lane + 64 q: slot e = b * G + g
         for (int b = 0; b < bs; ++b) {
           unsigned long long best = 0;

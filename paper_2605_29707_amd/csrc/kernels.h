@@ -81,6 +81,7 @@ size_t attn_part_floats(const Dims &D, int max_ctx);
 bool attn_supported(int nq, int nkv, int B);
 
 // ---- Domino head rollout (head.hip)
+constexpr uint32_t kDefaultPollLimit = 1u << 22;  // polls a rollout wait makes before it gives up
 struct HeadArgs {
   Dims D;
   int beta;
@@ -121,6 +122,7 @@ struct HeadArgs {
   // word tagged with the position; abort flag of its bounded waits
   unsigned long long *uslot, *kslot;
   unsigned *abort_flag;
+  unsigned poll_limit;  // polls a wait makes before it gives up
 };
 int head_logits_grid(const Dims &D);
 int head_best_slots();

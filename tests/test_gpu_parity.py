@@ -307,6 +307,16 @@ def test_qwen3_8b_bs1_full_size_parity():
     assert n >= 12
 
 
+def persistent_config(batch):
+    """The tiny drafter with d_s = 256 and a 8192-token vocabulary, bf16: the
+    persistent rollout takes it (13 workgroups of 640 vocabulary rows, whose
+    share of the 1024 rows of [W1 S-half; W_hh] fits in LDS; at d_s = 1024 and
+    4096 tokens its 7 workgroups could not hold theirs, and the launch-pair
+    rollout runs)."""
+    return synth.get_config("tiny").with_(dtype="bf16", batch=batch, gru_hidden=256, vocab=8192,
+                                          ctx_from_hidden=False)
+
+
 @pytest.mark.parametrize("batch", [1, 2])
 def test_persistent_rollout_matches_launch_pair_rollout(batch, monkeypatch):
     """bf16, r = 256, one or two batch rows, greedy: the rollout runs as one
@@ -314,7 +324,7 @@ def test_persistent_rollout_matches_launch_pair_rollout(batch, monkeypatch):
     launch-pair rollout (DOMINO_ROLLOUT=loop at model creation): the backbone
     outputs bit for bit, states and logits to fp32 summation order, the drafted
     tokens exactly away from near-ties; free-running and teacher-forced."""
-    cfg = synth.get_config("tiny").with_(dtype="bf16", batch=batch, ctx_from_hidden=False)
+    cfg = persistent_config(batch)
     w = synth.make_weights(cfg, seed=21, gain_std=0.1)
     inp = synth.make_inputs(cfg, seed=21)
     f = synth.make_forced_tokens(cfg, seed=21)
@@ -351,3 +361,28 @@ def test_persistent_rollout_matches_launch_pair_rollout(batch, monkeypatch):
             np.testing.assert_allclose(x["topk_vals"][r, :n], y["topk_vals"][r, :n], atol=1e-4, rtol=0)
     ref = oracle_for(cfg, oracle.as_f64_weights(w), inp, a, 1)
     check_against_oracle(cfg, a, ref, 2e-2, 1)
+
+
+def test_persistent_rollout_wait_gives_up_then_recovers():
+    """The failure path of the persistent rollout, forced from the host: with a
+    poll limit of 0 every wait gives up at once, raises DEV_BARRIER_TIMEOUT and
+    every workgroup leaves (the launch ends); with
+    the default restored, the next step on the same workspace is clean and
+    matches a run that never failed."""
+    from paper_2605_29707_amd import binding as bd
+    cfg = persistent_config(1)
+    w = synth.make_weights(cfg, seed=22, gain_std=0.1)
+    inp = synth.make_inputs(cfg, seed=22)
+    run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
+    good = run.step(inp)
+    assert good["err"] == 0
+    bd.domino_debug_set_poll_limit(run.model, 0)
+    bad = run.step(inp)
+    log(f"forced timeout: error word {bad['err']:#x}")
+    assert bad["err"] & bd.DEV_BARRIER_TIMEOUT
+    bd.domino_debug_set_poll_limit(run.model, -1)
+    again = run.step(inp)
+    run.close()
+    assert again["err"] == 0
+    for k in ("topk_ids", "topk_vals", "final_logits", "states"):
+        np.testing.assert_array_equal(again[k], good[k], err_msg=k)

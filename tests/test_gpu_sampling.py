@@ -91,12 +91,16 @@ def _check_sampled(cfg, gpu, inp, w64, T, seed, tol):
     return int(mask.sum()), mask.size
 
 
-@pytest.mark.parametrize("dtype,batch,T", [("f32", 3, 1.0), ("f32", 1, 0.6), ("bf16", 5, 1.0), ("bf16", 12, 1.3),
-                                           ("bf16", 1, 1.0), ("bf16", 2, 0.7)])
-def test_sampled_drafting_tiny(dtype, batch, T):
-    """bf16 with one or two batch rows runs the persistent rollout (its sampled
-    variant), the other cases the launch-pair rollout."""
+@pytest.mark.parametrize("dtype,batch,T,wide", [("f32", 3, 1.0, False), ("f32", 1, 0.6, False),
+                                                ("bf16", 5, 1.0, False), ("bf16", 12, 1.3, False),
+                                                ("bf16", 1, 1.0, True), ("bf16", 2, 0.7, True)])
+def test_sampled_drafting_tiny(dtype, batch, T, wide):
+    """wide: d_s = 256 and 8192 tokens, where bf16 with one or two batch rows
+    runs the persistent rollout (its sampled variant); the other cases run the
+    launch-pair rollout."""
     cfg = synth.get_config("tiny").with_(dtype=dtype, batch=batch, branch=1, ctx_from_hidden=False)
+    if wide:
+        cfg = cfg.with_(gru_hidden=256, vocab=8192)
     w = synth.make_weights(cfg, seed=21, gain_std=0.1)
     inp = synth.make_inputs(cfg, seed=21)
     run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
