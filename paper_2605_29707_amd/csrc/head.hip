@@ -1038,14 +1038,20 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
       }
     }
     const bool rowok = cc < bs;
-    if (DBG) {  // debug output
+    if (DBG && rowok) {  // the final logits (output of sampled drafting, debug output otherwise)
+      float *fl = h.final_logits + ((size_t)cc * depth + (j - 1)) * V;
+      const bool vec = (V & 3) == 0;  // rows start 16-byte aligned: four ids per store
 #pragma unroll
-      for (int q = 0; q < kPersTiles; ++q)
+      for (int q = 0; q < kPersTiles; ++q) {
+        const int n = (tile0 + q) * 16 + 4 * g;
+        if (vec && n + 4 <= V) {
+          *(float4 *)(fl + n) = make_float4(val[q][0], val[q][1], val[q][2], val[q][3]);
+        } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int n = (tile0 + q) * 16 + 4 * g + e;
-          if (rowok && n < V) h.final_logits[((size_t)cc * depth + (j - 1)) * V + n] = val[q][e];
+          for (int e = 0; e < 4; ++e)
+            if (n + e < V) fl[n + e] = val[q][e];
         }
+      }
     }
     {
       // ids grow along (q, e) within a lane, so a strict comparison keeps the
