@@ -111,6 +111,21 @@ def attention(q, k, v):
 # ----------------------------------------------------------------------------
 # backbone (Sec. 4.1.1)
 # ----------------------------------------------------------------------------
+def fuse_context(cfg, w, hidden):
+    """Context features C_t (Sec. 4.1.1) from the target's hidden states.
+
+    With cfg.ctx_fuse_layers = k > 0 a context row is the concatenation of the
+    hidden states of k target layers, [n, k*d]; one linear map ctx_fc [d, k*d]
+    fuses it to width d.  The paper gives the fusion no formula: this is the
+    reading that the +5.3% parameter figure of Sec. 1 implies (an ~84M map at
+    the Qwen3-8B shape with k = 5).  With k = 0 the rows are used as they are.
+    """
+    c = np.asarray(hidden, F64)
+    if cfg.ctx_fuse_layers <= 0:
+        return c
+    return c @ np.asarray(w["ctx_fc"], F64).T
+
+
 def project_context_kv(cfg, lw, hidden, positions):
     """Context K/V of one layer from target hidden states.
 
@@ -267,8 +282,9 @@ def draft_step(cfg, w, anchor, ctx_lens, ctx_k, ctx_v, beta, forced=None,
     """Full draft step.
 
     anchor, ctx_lens: [bs]; ctx_k/ctx_v: [L, bs, max_ctx, nkv, d_h]; forced:
-    optional [bs, B-1]; ctx_hidden: optional [bs, n_new, d] projected into
-    positions [ctx_len - n_new, ctx_len) of every layer before drafting.
+    optional [bs, B-1]; ctx_hidden: optional [bs, n_new, cfg.ctx_width] target
+    hidden states, fused (fuse_context) and projected into positions
+    [ctx_len - n_new, ctx_len) of every layer before drafting.
     sampling: optional (temperature, seed) for sampled drafting; `rows` gives
     the batch-row index each row's random streams use (default 0..bs-1).
     Returns a dict of arrays with a leading batch axis ("sample_gap" [bs, B-1]
@@ -284,8 +300,9 @@ def draft_step(cfg, w, anchor, ctx_lens, ctx_k, ctx_v, beta, forced=None,
         if ctx_hidden is not None and ctx_hidden.shape[1] > 0:
             n_new = ctx_hidden.shape[1]
             pos = np.arange(n - n_new, n, dtype=F64)
+            c = fuse_context(cfg, w, ctx_hidden[b])
             for l, lw in enumerate(w["layers"]):
-                k, v = project_context_kv(cfg, lw, ctx_hidden[b], pos)
+                k, v = project_context_kv(cfg, lw, c, pos)
                 ctx_k[l, b, n - n_new:n] = k
                 ctx_v[l, b, n - n_new:n] = v
         h = draft_backbone(cfg, w, anchor[b], ctx_k[:, b], ctx_v[:, b], n)

@@ -29,10 +29,18 @@ class DominoConfig:
     ctx: int = 1024
     branch: int = 1        # beta: top-k per position used by the tree
     ctx_from_hidden: bool = False  # context KV built by projecting hidden states
+    # k > 0: a context row is the concatenation of k target layers' hidden
+    # states ([k*d]), fused to width d by ctx_fc before the K/V projections
+    ctx_fuse_layers: int = 0
 
     @property
     def mask_id(self) -> int:
         return self.vocab - 1 if self.mask_token_id < 0 else self.mask_token_id
+
+    @property
+    def ctx_width(self) -> int:
+        """Width of one target-hidden-state context row."""
+        return self.hidden * self.ctx_fuse_layers if self.ctx_fuse_layers > 0 else self.hidden
 
     @property
     def depth(self) -> int:
@@ -54,19 +62,19 @@ PRESETS = {
     # Qwen3-8B-shaped bf16 drafter, bs 1, ctx 1024 (latency setting)
     "qwen3_8b": DominoConfig("qwen3_8b", hidden=4096, n_layers=5, n_q_heads=32,
                              n_kv_heads=8, head_dim=128, ffn=12288, vocab=151936,
-                             batch=1, ctx=1024, branch=1),
+                             batch=1, ctx=1024, branch=1, ctx_fuse_layers=5),
     # serving-style: bs 32, ctx 2048, tree branch 4
     "qwen3_8b_bs32": DominoConfig("qwen3_8b_bs32", hidden=4096, n_layers=5, n_q_heads=32,
                                   n_kv_heads=8, head_dim=128, ffn=12288, vocab=151936,
-                                  batch=32, ctx=2048, branch=4),
+                                  batch=32, ctx=2048, branch=4, ctx_fuse_layers=5),
     # Qwen3-4B-shaped, long context
     "qwen3_4b_ctx8k": DominoConfig("qwen3_4b_ctx8k", hidden=2560, n_layers=5, n_q_heads=32,
                                    n_kv_heads=8, head_dim=128, ffn=9728, vocab=151936,
-                                   batch=4, ctx=8192, branch=1),
+                                   batch=4, ctx=8192, branch=1, ctx_fuse_layers=5),
     # Qwen3-32B-shaped
     "qwen3_32b": DominoConfig("qwen3_32b", hidden=5120, n_layers=5, n_q_heads=64,
                               n_kv_heads=8, head_dim=128, ffn=25600, vocab=151936,
-                              batch=16, ctx=4096, branch=1),
+                              batch=16, ctx=4096, branch=1, ctx_fuse_layers=5),
     # target models (the verify forward): a small fp32 decoder sharing the tiny
     # drafter's vocabulary and width, and the Qwen3-8B-shaped target (36 layers)
     "tiny_target": DominoConfig("tiny_target", hidden=256, n_layers=4, n_q_heads=4, n_kv_heads=2,

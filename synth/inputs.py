@@ -31,6 +31,7 @@ _CHUNK = 1 << 22
 # stable tensor ids
 _T_EMBED, _T_LMHEAD, _T_FINAL_NORM = 0, 1, 2
 _T_GRU_WIH, _T_GRU_WHH, _T_GRU_BIH, _T_GRU_BHH, _T_W1, _T_W2 = 10, 11, 12, 13, 14, 15
+_T_CTX_FC = 16
 _LAYER_BASE = 100
 _LAYER_KEYS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down",
                "attn_norm", "ffn_norm", "q_norm", "k_norm")
@@ -88,13 +89,16 @@ def weight_shapes(cfg: DominoConfig) -> dict:
         "w_gate": (F, d), "w_up": (F, d), "w_down": (d, F),
         "attn_norm": (d,), "ffn_norm": (d,), "q_norm": (dh,), "k_norm": (dh,),
     }
-    return {
+    out = {
         "embed": (V, d), "lm_head": (V, d), "final_norm": (d,),
         "layers": [dict(layer) for _ in range(cfg.n_layers)],
         "gru_w_ih": (3 * ds, d), "gru_w_hh": (3 * ds, ds),
         "gru_b_ih": (3 * ds,), "gru_b_hh": (3 * ds,),
         "w1": (r, d + ds), "w2": (V, r),
     }
+    if cfg.ctx_fuse_layers > 0:
+        out["ctx_fc"] = (d, cfg.ctx_width)  # context fusion: k target layers -> d
+    return out
 
 
 def head_param_count(cfg: DominoConfig, with_gru_bias: bool = False) -> int:
@@ -133,6 +137,8 @@ def make_weights(cfg: DominoConfig, seed: int = 0, gain_std: float = 0.0,
                else _normal(seed, _T_W2, s["w2"], 0.02, bf)),
         "layers": [],
     }
+    if "ctx_fc" in s:
+        w["ctx_fc"] = _normal(seed, _T_CTX_FC, s["ctx_fc"], 0.02, bf)
     for li, ls in enumerate(s["layers"]):
         base = _LAYER_BASE + 16 * li
         lw = {}
@@ -190,7 +196,7 @@ def make_inputs(cfg: DominoConfig, seed: int = 0, ctx_lens=None, max_ctx: int | 
       anchor   int32 [bs]
       ctx_lens int32 [bs]
       ctx_k, ctx_v  fp32 [L, bs, max_ctx, n_kv, d_h] (zeros when ctx_from_hidden)
-      ctx_hidden    fp32 [bs, n_new, d] or None, n_new = min(ctx_lens)
+      ctx_hidden    fp32 [bs, n_new, cfg.ctx_width] or None, n_new = min(ctx_lens)
     """
     bs, V = cfg.batch, cfg.vocab
     mask = cfg.mask_id
@@ -207,7 +213,7 @@ def make_inputs(cfg: DominoConfig, seed: int = 0, ctx_lens=None, max_ctx: int | 
         out["ctx_k"] = np.zeros(shape, np.float32)
         out["ctx_v"] = np.zeros(shape, np.float32)
         n_new = int(ctx_lens.min(initial=0))
-        out["ctx_hidden"] = _normal(seed, _T_CTX_H, (bs, n_new, cfg.hidden), 1.0, bf)
+        out["ctx_hidden"] = _normal(seed, _T_CTX_H, (bs, n_new, cfg.ctx_width), 1.0, bf)
         out["ctx_ids"] = _rng(seed, _T_CTX_IDS).integers(0, V - 1, size=(bs, n_new)).astype(np.int32)
     else:
         out["ctx_k"] = _normal(seed, _T_CTX_K, shape, 1.0, bf)
@@ -217,9 +223,9 @@ def make_inputs(cfg: DominoConfig, seed: int = 0, ctx_lens=None, max_ctx: int | 
 
 
 def make_append_hidden(cfg: DominoConfig, n_new: int, seed: int = 0) -> np.ndarray:
-    """Target hidden states of the tokens accepted last cycle, [bs, n_new, d] N(0, 1)
-    (storage-type values), to be appended to a KV-cache context."""
-    return _normal(seed, _T_APPEND_H, (cfg.batch, n_new, cfg.hidden), 1.0, cfg.dtype == "bf16")
+    """Target hidden states of the tokens accepted last cycle, [bs, n_new, cfg.ctx_width]
+    N(0, 1) (storage-type values), to be appended to a KV-cache context."""
+    return _normal(seed, _T_APPEND_H, (cfg.batch, n_new, cfg.ctx_width), 1.0, cfg.dtype == "bf16")
 
 
 def make_forced_tokens(cfg: DominoConfig, seed: int = 0) -> np.ndarray:

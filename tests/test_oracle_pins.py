@@ -400,3 +400,68 @@ def test_context_projection_matches_layer_kv():
                                np.linalg.norm(O.rms_norm(kk, lw["k_norm"], cfg.rms_eps), axis=-1),
                                rtol=1e-12)
     np.testing.assert_allclose(v, (c @ lw["wv"].T).reshape(3, cfg.n_kv_heads, cfg.head_dim), rtol=1e-13)
+
+
+# ---------------------------------------------------------------- context fusion
+def _drafter_own_params(cfg):
+    """Parameters the drafter trains itself: backbone layers, final norm and the
+    context-fusion map (the embedding and LM head are the target's, frozen)."""
+    s = synth.weight_shapes(cfg)
+    n = sum(int(np.prod(v)) for lw in s["layers"] for v in lw.values())
+    n += int(np.prod(s["final_norm"]))
+    if "ctx_fc" in s:
+        n += int(np.prod(s["ctx_fc"]))
+    return n
+
+
+def test_context_fusion_makes_the_head_5_3_percent_of_the_drafter():
+    # Sec. 1: the head adds 56M parameters, +5.3% over the drafter without it.
+    # Five fused target layers (an ~84M map) give 5.33%, the fusion width
+    # closest to 5.3%; without a fusion map the head would be 5.8%.
+    gold = json.load(open(os.path.join(GOLDEN, "paper_constants.json")))
+    pct = gold["head_params_relative_percent"]
+    cfg = synth.get_config("qwen3_8b")
+    assert cfg.ctx_fuse_layers == 5
+    head = synth.head_param_count(cfg)
+    assert round(int(np.prod(synth.weight_shapes(cfg)["ctx_fc"])) / 1e6) == 84
+    share = {k: 100 * head / _drafter_own_params(cfg.with_(ctx_fuse_layers=k)) for k in range(9)}
+    assert round(share[5], 1) == pct
+    assert min(share, key=lambda k: abs(share[k] - pct)) == 5
+    assert round(share[0], 1) == 5.8
+
+
+def _fused_vs_plain(k, fc_blocks, hidden_blocks):
+    """Draft step with k fused layers and ctx_fc = [fc_blocks...] against the
+    plain (unfused) step fed the given hidden states."""
+    cfg = tiny_cfg(batch=1, ctx=9, ctx_from_hidden=True, ctx_fuse_layers=k)
+    plain = cfg.with_(ctx_fuse_layers=0)
+    w, inp = _tiny_step(plain)
+    d = cfg.hidden
+    rng = np.random.default_rng(21)
+    blocks = [rng.standard_normal((1, 9, d)) for _ in range(k)]
+    cat = np.concatenate(blocks, axis=-1)
+    wf = dict(w)
+    wf["ctx_fc"] = np.concatenate([np.asarray(b, np.float64) for b in fc_blocks], axis=1)
+    lens = np.array([9], np.int32)
+    r = O.draft_step(cfg, wf, inp["anchor"], lens, inp["ctx_k"], inp["ctx_v"], 1, ctx_hidden=cat)
+    r2 = O.draft_step(plain, w, inp["anchor"], lens, inp["ctx_k"], inp["ctx_v"], 1,
+                      ctx_hidden=hidden_blocks(blocks))
+    return r, r2
+
+
+@pytest.mark.parametrize("pick", [0, 1, 2])
+def test_context_fusion_selecting_one_layer_is_that_layer(pick):
+    # ctx_fc = [0 .. I .. 0] picks layer `pick` of the concatenation: the step
+    # equals the unfused step fed that layer's hidden states
+    d = tiny_cfg().hidden
+    fc = [np.eye(d) if i == pick else np.zeros((d, d)) for i in range(3)]
+    r, r2 = _fused_vs_plain(3, fc, lambda b: b[pick])
+    np.testing.assert_allclose(r["base_logits"], r2["base_logits"], rtol=1e-12, atol=1e-13)
+    np.testing.assert_array_equal(r["topk_ids"], r2["topk_ids"])
+
+
+def test_context_fusion_equal_weights_is_the_mean_of_layers():
+    d = tiny_cfg().hidden
+    r, r2 = _fused_vs_plain(3, [np.eye(d) / 3] * 3, lambda b: (b[0] + b[1] + b[2]) / 3)
+    np.testing.assert_allclose(r["base_logits"], r2["base_logits"], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(r["final_logits"], r2["final_logits"], rtol=1e-11, atol=1e-12)
