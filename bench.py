@@ -270,8 +270,24 @@ def main():
         torch.cuda.synchronize()
         assert bd.domino_workspace_error(aws) == 0
         aper = [ae[i].elapsed_time(ae[i + 1]) for i in range(50)]
-        appended = {"rows": na, "steps": 50, "ms_per_step": round(ae[0].elapsed_time(ae[-1]) / 50, 4),
+        appended = {"rows": na, "fused_target_layers": cfg.ctx_fuse_layers, "steps": 50,
+                    "ms_per_step": round(ae[0].elapsed_time(ae[-1]) / 50, 4),
                     "us_per_step_median": round(statistics.median(aper) * 1e3, 1)}
+        if cfg.ctx_fuse_layers > 0:
+            # the fusion launches (K-split GEMM + partial sum) bracketed by library events
+            bd.domino_profile_enable(model, ["ctxproj"])
+            for _ in range(10):
+                step_append()
+            torch.cuda.synchronize()
+            fms, fn = bd.domino_profile_read(model, "ctxproj")
+            bd.domino_profile_enable(model, [])
+            kf = cfg.ctx_fuse_layers * cfg.hidden
+            esz = 2 if cfg.dtype == "bf16" else 4
+            fbytes = cfg.hidden * kf * esz + bs * na * (kf + cfg.hidden) * 4  # ctx_fc once, rows in and out
+            fus = fms * 1e3 / max(fn, 1)
+            appended["fusion"] = {"us": round(fus, 2), "launches": fn, "algorithmic_bytes": fbytes,
+                                  "achieved_GBps": round(fbytes / (fus * 1e-6) / 1e9, 1),
+                                  "hbm_frac": round(fbytes / (fus * 1e-6) / 8e12, 4)}
         del aws
 
     trained = None

@@ -70,12 +70,20 @@ enum {
  * n_kv_heads with (n_q_heads/n_kv_heads)*block <= 128; block in [2, 64];
  * mask_token_id in [0, vocab).  domino_model_create also builds the table
  * G = embed * gru_w_ih^T ([vocab, 3*gru_hidden] fp32) used by the rollout.
+ * ctx_fuse_layers k in [0, 8]: with k > 0 a projected context row is the
+ * concatenation of k target layers' hidden states ([k*hidden]), fused to
+ * width hidden by the weight ctx_fc before each layer's K/V projections (the
+ * context features C_t of Sec. 4.1.1; the paper states no formula for them:
+ * k = 5 at the Qwen3-8B shape is the ~84M map its +5.3% parameter figure of
+ * Sec. 1 implies).  k = 0: rows are hidden wide and used as they are.
+ * domino_target_create ignores it.
  */
 typedef struct {
   int32_t hidden, n_layers, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
   int32_t block, gru_hidden, rank, mask_token_id;
   float rms_eps, rope_theta;
   domino_dtype dtype;
+  int32_t ctx_fuse_layers;
 } domino_config;
 
 /*
@@ -88,7 +96,9 @@ typedef struct {
  *   w_gate [ffn, d], w_up [ffn, d], w_down [d, ffn];
  *   GRU (reset-after form, gate order r, z, n): gru_w_ih [3ds, d],
  *   gru_w_hh [3ds, ds], gru_b_ih [3ds], gru_b_hh [3ds];
- *   correction: w1 [r, d + ds] with columns [H | S], w2 [V, r].
+ *   correction: w1 [r, d + ds] with columns [H | S], w2 [V, r];
+ *   context fusion (only when ctx_fuse_layers k > 0, else ignored):
+ *   ctx_fc [d, k*d], its column block i acting on the i-th concatenated layer.
  * domino_model_create copies every matrix into its own device memory in a
  * matrix-core tile order; it keeps borrowing embed, the norm gains and the
  * GRU biases, which the caller keeps alive until domino_model_destroy.
@@ -99,6 +109,7 @@ typedef struct {
       *const *k_norm, *const *wo, *const *ffn_norm, *const *w_gate, *const *w_up, *const *w_down;
   const void *gru_w_ih, *gru_w_hh, *gru_b_ih, *gru_b_hh;
   const void *w1, *w2;
+  const void *ctx_fc;
 } domino_weights;
 
 /* Optional per-step debug outputs (device fp32; any field may be NULL).
@@ -136,9 +147,11 @@ const char *domino_last_error(void);
  *                  the block are n_b .. n_b+B-1), in [n_new, max_ctx]
  *  ctx_k, ctx_v    device [n_layers][batch][max_ctx][n_kv][d_h] in the storage
  *                  type; K is post k-norm and RoPE.  Read-only unless n_new > 0.
- *  ctx_hidden_new  optional device [batch][n_new][d] target hidden states; when
- *                  given, row i is projected with each layer's W_k (k-norm,
- *                  RoPE) and W_v and written at position n_b - n_new + i.
+ *  ctx_hidden_new  optional device fp32 [batch][n_new][w] target hidden states,
+ *                  w = k*d with ctx_fuse_layers k > 0 (fused by ctx_fc first),
+ *                  else d; when given, row i is projected with each layer's
+ *                  W_k (k-norm, RoPE) and W_v and written at position
+ *                  n_b - n_new + i.
  *  branch          beta in [1, 8]: entries kept per position
  *  forced_tokens   optional device int32 [batch][B-1]: teacher forcing — the
  *                  token fed to the causal encoder after position j is
@@ -362,8 +375,9 @@ domino_status domino_workspace_clear_error(void *workspace, void *stream);
  * domino_profile_read synchronises and returns the summed milliseconds and
  * the number of launches timed since the last reset.  Classes that currently
  * have no launches of their own (EMBED: the embedding gather is part of the
- * first NORM launch; W1H: W1's H half shares the LMHEAD launch; CTXPROJ: the
- * appended context rows ride in the QKV launches) read back zero launches.
+ * first NORM launch; W1H: W1's H half shares the LMHEAD launch) read back zero
+ * launches.  CTXPROJ times the context fusion (ctx_fc) of appended rows; their
+ * K/V projections ride in the QKV launches.
  */
 enum {
   DOMINO_KC_EMBED = 0, DOMINO_KC_NORM, DOMINO_KC_QKV, DOMINO_KC_ROPE, DOMINO_KC_ATTN,

@@ -32,7 +32,8 @@ class domino_config(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "hidden", "n_layers", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "vocab",
         "block", "gru_hidden", "rank", "mask_token_id")] + [
-        ("rms_eps", C.c_float), ("rope_theta", C.c_float), ("dtype", C.c_int)]
+        ("rms_eps", C.c_float), ("rope_theta", C.c_float), ("dtype", C.c_int),
+        ("ctx_fuse_layers", C.c_int32)]
 
 
 _VP = C.c_void_p
@@ -43,7 +44,7 @@ class domino_weights(C.Structure):
     _fields_ = [("embed", _VP), ("lm_head", _VP), ("final_norm", _VP)] + [
         (n, _PP) for n in ("attn_norm", "wq", "wk", "wv", "q_norm", "k_norm", "wo", "ffn_norm",
                            "w_gate", "w_up", "w_down")] + [
-        (n, _VP) for n in ("gru_w_ih", "gru_w_hh", "gru_b_ih", "gru_b_hh", "w1", "w2")]
+        (n, _VP) for n in ("gru_w_ih", "gru_w_hh", "gru_b_ih", "gru_b_hh", "w1", "w2", "ctx_fc")]
 
 
 class domino_debug(C.Structure):
@@ -149,7 +150,8 @@ def make_config(cfg) -> domino_config:
         head_dim=cfg.head_dim, ffn=cfg.ffn, vocab=cfg.vocab, block=cfg.block,
         gru_hidden=cfg.gru_hidden, rank=cfg.rank, mask_token_id=cfg.mask_id,
         rms_eps=cfg.rms_eps, rope_theta=cfg.rope_theta,
-        dtype=DOMINO_BF16 if cfg.dtype == "bf16" else DOMINO_F32)
+        dtype=DOMINO_BF16 if cfg.dtype == "bf16" else DOMINO_F32,
+        ctx_fuse_layers=getattr(cfg, "ctx_fuse_layers", 0))
 
 
 class DominoModel:
@@ -176,7 +178,7 @@ class DominoModel:
             q_norm=arr("q_norm"), k_norm=arr("k_norm"), wo=arr("wo"), ffn_norm=arr("ffn_norm"),
             w_gate=arr("w_gate"), w_up=arr("w_up"), w_down=arr("w_down"),
             **{k: (dev_weights[k].data_ptr() if k in dev_weights else None)
-               for k in ("gru_w_ih", "gru_w_hh", "gru_b_ih", "gru_b_hh", "w1", "w2")})
+               for k in ("gru_w_ih", "gru_w_hh", "gru_b_ih", "gru_b_hh", "w1", "w2", "ctx_fc")})
         self._cfg_struct = make_config(cfg)
         h = C.c_void_p()
         create = lib.domino_target_create if target else lib.domino_model_create
@@ -201,6 +203,23 @@ class DominoModel:
         return n
 
 
+def _check_ctx_hidden(model: DominoModel, batch, ctx_hidden_new, n_new):
+    """The appended rows must be fp32 and hold batch * n_new rows of the
+    model's context width (k*d with k fused layers, else d)."""
+    if ctx_hidden_new is None or int(n_new) <= 0:
+        return
+    import torch
+    cfg = model.cfg
+    k = getattr(cfg, "ctx_fuse_layers", 0)
+    width = cfg.hidden * k if k > 0 else cfg.hidden
+    need = int(batch) * int(n_new) * width
+    if ctx_hidden_new.dtype != torch.float32 or not ctx_hidden_new.is_contiguous() \
+            or ctx_hidden_new.numel() < need:
+        raise DominoError(DOMINO_ERR_INVALID_ARG,
+                          f"ctx_hidden_new must be contiguous fp32 with >= {need} elements "
+                          f"([{batch}][{n_new}][{width}])")
+
+
 def domino_draft_step(model: DominoModel, anchor, ctx_lens, ctx_k, ctx_v, max_ctx, topk_ids, topk_vals,
                       workspace, branch=1, ctx_hidden_new=None, n_new=0, forced=None, debug=None,
                       stream=None):
@@ -208,6 +227,7 @@ def domino_draft_step(model: DominoModel, anchor, ctx_lens, ctx_k, ctx_v, max_ct
     if debug:
         dbg = domino_debug(**{k: (debug[k].data_ptr() if debug.get(k) is not None else None)
                               for k in ("hidden", "base_logits", "final_logits", "states")})
+    _check_ctx_hidden(model, anchor.shape[0], ctx_hidden_new, n_new)
     _check(load().domino_draft_step(
         model.handle, int(anchor.shape[0]), _ptr(anchor), _ptr(ctx_lens), _ptr(ctx_k), _ptr(ctx_v),
         int(max_ctx), _ptr(ctx_hidden_new), int(n_new), int(branch), _ptr(forced), _ptr(topk_ids),
@@ -222,6 +242,7 @@ def domino_draft_step_sampled(model: DominoModel, anchor, ctx_lens, ctx_k, ctx_v
     if debug:
         dbg = domino_debug(**{k: (debug[k].data_ptr() if debug.get(k) is not None else None)
                               for k in ("hidden", "base_logits", "final_logits", "states")})
+    _check_ctx_hidden(model, anchor.shape[0], ctx_hidden_new, n_new)
     _check(load().domino_draft_step_sampled(
         model.handle, int(anchor.shape[0]), _ptr(anchor), _ptr(ctx_lens), _ptr(ctx_k), _ptr(ctx_v),
         int(max_ctx), _ptr(ctx_hidden_new), int(n_new), float(temperature), int(seed) & (2**64 - 1),
@@ -243,6 +264,7 @@ def domino_train_forward(model: DominoModel, anchor, ctx_lens, ctx_k, ctx_v, max
     if debug:
         dbg = domino_debug(**{k: (debug[k].data_ptr() if debug.get(k) is not None else None)
                               for k in ("hidden", "base_logits", "final_logits", "states")})
+    _check_ctx_hidden(model, anchor.shape[0], ctx_hidden_new, n_new)
     _check(load().domino_train_forward(
         model.handle, int(anchor.shape[0]), _ptr(anchor), _ptr(ctx_lens), _ptr(ctx_k), _ptr(ctx_v),
         int(max_ctx), _ptr(ctx_hidden_new), int(n_new), _ptr(labels), float(lam), float(gamma), _ptr(loss),

@@ -63,6 +63,8 @@ struct domino_model {
   bool persistent = true;  // DOMINO_ROLLOUT=loop selects the launch-pair rollout everywhere
   uint32_t poll_limit = kDefaultPollLimit;  // persistent rollout: polls a wait makes before it gives up
   Packed lm, w2, w1s;
+  int fuse_k = 0;  // context fusion: appended rows are fuse_k*d wide, fused by fc
+  Packed fc;
   // training forward: the state recurrence runs on a second stream beside the backbone
   hipStream_t side = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
@@ -111,7 +113,9 @@ domino_status check_config(const domino_config *c, bool with_head = true) {
   if (c->hidden % 32 || c->ffn % 32 || (c->n_q_heads * c->head_dim) % 32)
     return fail(DOMINO_ERR_UNSUPPORTED, "hidden, ffn and n_q_heads*head_dim must be multiples of 32");
   if (c->hidden > 8192) return fail(DOMINO_ERR_UNSUPPORTED, "hidden must be at most 8192");
-  if (!with_head) return DOMINO_OK;  // a target decoder: the node count is checked per call
+  if (!with_head) return DOMINO_OK;
+  if (c->ctx_fuse_layers < 0 || c->ctx_fuse_layers > 8)
+    return fail(DOMINO_ERR_INVALID_ARG, "ctx_fuse_layers must be in [0, 8]");  // a target decoder: the node count is checked per call
   if (c->gru_hidden % 32) return fail(DOMINO_ERR_UNSUPPORTED, "gru_hidden must be a multiple of 32");
   if (c->rank % ks || c->rank > 16 * ks)
     return fail(DOMINO_ERR_UNSUPPORTED, "rank must be a multiple of %d and at most %d", ks, 16 * ks);
@@ -132,13 +136,14 @@ Dims make_dims(const domino_model *m, int bs) {
 
 // ---- workspace layout of the draft step
 struct WsLayout {
-  size_t err, best, slots, hdr_words, X, X2, A, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
+  size_t err, best, slots, hdr_words, X, X2, A, FC, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
       praw, total;
   int GC, ldl;
 };
 
 struct Plans {
   GemmPlan qkv, wo, gateup, down, lm;
+  GemmPlan fc;  // context fusion of the appended rows (fc.ksplit = 0: none)
 };
 
 constexpr int kMaxSplit = 16;
@@ -153,13 +158,18 @@ Plans make_plans_rows(const domino_model *m, int M, int Mlm, int Ma) {
   p.gateup = plan_gemm(m->gateup[0].NT, m->gateup[0].KS, M, EPI_SWIGLU, m->n_cu, 1);
   p.down = plan_gemm(m->down[0].NT, m->down[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
   p.lm = plan_gemm(m->lm.NT, m->lm.KS, Mlm, EPI_STORE, m->n_cu, 1);
+  p.fc = GemmPlan();
+  p.fc.ksplit = 0;
   return p;
 }
 
 Plans make_plans(const domino_model *m, int bs, int max_new) {
   const Dims &D = m->D;
   // QKV also projects the appended context rows (rows M .. M + bs*max_new - 1)
-  return make_plans_rows(m, bs * D.B, bs * (D.B - 1), bs * D.B + bs * max_new);
+  Plans p = make_plans_rows(m, bs * D.B, bs * (D.B - 1), bs * D.B + bs * max_new);
+  // the fusion's K-split partials are summed into those rows of the QKV input
+  if (m->fuse_k > 0 && max_new > 0) p.fc = plan_gemm(m->fc.NT, m->fc.KS, bs * max_new, EPI_STORE, m->n_cu, kMaxSplit);
+  return p;
 }
 
 bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, WsLayout &w) {
@@ -182,6 +192,7 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.X2 = take((size_t)M * D.d * 4);
   const int Ma = M + bs * max_new;  // block rows, then the appended context rows
   w.A = take((size_t)Ma * D.d * 4);
+  w.FC = take((size_t)p.fc.ksplit * bs * max_new * D.d * 4);
   w.QKV = take((size_t)p.qkv.ksplit * Ma * qkvw * 4);
   w.Q = take((size_t)M * D.nq * D.dh * 4);
   w.Kb = take((size_t)M * D.nkv * D.dh * 4);
@@ -342,6 +353,8 @@ domino_status create_impl(const domino_config *cfg, const domino_weights *w, dom
     return fail(DOMINO_ERR_INVALID_ARG, "a weight pointer is NULL");
   if (with_head && (!w->gru_w_ih || !w->gru_w_hh || !w->gru_b_ih || !w->gru_b_hh || !w->w1 || !w->w2))
     return fail(DOMINO_ERR_INVALID_ARG, "a weight pointer is NULL");
+  if (with_head && cfg->ctx_fuse_layers > 0 && !w->ctx_fc)
+    return fail(DOMINO_ERR_INVALID_ARG, "ctx_fc is NULL (ctx_fuse_layers > 0)");
   const void *const *arrs[] = {w->attn_norm, w->wq, w->wk, w->wv, w->q_norm, w->k_norm,
                                w->wo, w->ffn_norm, w->w_gate, w->w_up, w->w_down};
   for (auto a : arrs) {
@@ -417,6 +430,8 @@ domino_status create_impl(const domino_config *cfg, const domino_weights *w, dom
   if (with_head) {
     m->w2 = add(D.V, D.r);
     m->w1s = add(D.r, D.ds);  // W1's S half on its own, for the batched u of the training forward
+    m->fuse_k = cfg->ctx_fuse_layers;
+    if (m->fuse_k > 0) m->fc = add(D.d, m->fuse_k * D.d);
     m->gtab_off = off;
     off = align_up(off + (size_t)D.V * 3 * D.ds * 4);
     m->w_hh_off = off;
@@ -464,6 +479,10 @@ domino_status create_impl(const domino_config *cfg, const domino_weights *w, dom
     launch_pack(bf, w->w2, D.V, D.r, D.r, base + m->w2.off, m->w2.NT, m->w2.KS, 1, 0, st);
     launch_pack(bf, (const char *)w->w1 + (size_t)D.d * m->esz, D.r, D.ds, D.d + D.ds, base + m->w1s.off,
                 m->w1s.NT, m->w1s.KS, 1, 0, st);
+    if (m->fuse_k > 0) {
+      const int kf = m->fuse_k * D.d;
+      launch_pack(bf, w->ctx_fc, D.d, kf, kf, base + m->fc.off, m->fc.NT, m->fc.KS, 1, 0, st);
+    }
   }
   he = hipGetLastError();
   if (he == hipSuccess && with_head) he = build_gtab(m, w->gru_w_ih, w->gru_b_ih);
@@ -572,9 +591,19 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
   // layer 0's RMSNorm launch (clear_header)
   // appended context rows (target hidden states) ride along in the QKV
   // projection: they sit after the block rows of its input, and the RMSNorms
-  // only ever rewrite the block rows
+  // only ever rewrite the block rows.  With context fusion the rows are
+  // k*d wide and enter as ctx_fc times the row (K-split GEMM, then the sum of
+  // its partials written into place).
   const int Ma = M + batch * n_new;
-  if (n_new > 0) {
+  if (n_new > 0 && m->fuse_k > 0) {
+    const int kf = m->fuse_k * D.d, rows = batch * n_new;
+    prof_begin(m, DOMINO_KC_CTXPROJ, st);
+    GemmArgs a = gemm_args(base + m->fc.off, m->fc, 0, m->fc.NT, D.d, (const float *)ctx_hidden_new, kf, rows, kf,
+                           F(w.FC), D.d, p.fc);
+    launch_gemm(m->bf16, EPI_STORE, a, p.fc, st);
+    launch_sum_parts(F(w.FC), p.fc.ksplit, (size_t)rows * D.d, rows, D.d, F(w.A) + (size_t)M * D.d, D.d, st);
+    prof_end(m, DOMINO_KC_CTXPROJ, st);
+  } else if (n_new > 0) {
     hipError_t ce = hipMemcpyAsync(F(w.A) + (size_t)M * D.d, ctx_hidden_new, (size_t)batch * n_new * D.d * 4,
                                    hipMemcpyDeviceToDevice, st);
     if (ce != hipSuccess) return fail(DOMINO_ERR_HIP, "staging ctx_hidden_new: %s", hipGetErrorString(ce));

@@ -831,6 +831,34 @@ void launch_add_row_bias(float *Y, size_t rows, int N, const void *bias, bool bf
   else hipLaunchKernelGGL(add_row_bias_kernel<float>, dim3(blocks), dim3(256), 0, st, Y, n, N, (const float *)bias);
 }
 
+// y[r][c] = sum over p < np of parts[p * pstride + r * width + c], four
+// columns per thread (width % 4 == 0, pstride % 4 == 0, ldy % 4 == 0)
+__global__ void sum_parts_kernel(const float *__restrict__ parts, int np, size_t pstride, int rows, int width,
+                                 float *__restrict__ y, int ldy) {
+  const int w4 = width / 4;
+  const size_t n = (size_t)rows * w4;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t r = i / w4, c = (i % w4) * 4;
+    const float *src = parts + r * width + c;
+    float4 acc = *(const float4 *)src;
+    for (int p = 1; p < np; ++p) {
+      const float4 v = *(const float4 *)(src + (size_t)p * pstride);
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
+    }
+    *(float4 *)(y + r * ldy + c) = acc;
+  }
+}
+void launch_sum_parts(const float *parts, int np, size_t pstride, int rows, int width, float *y, int ldy,
+                      hipStream_t st) {
+  const size_t n = (size_t)rows * (width / 4);
+  if (n == 0) return;
+  const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(sum_parts_kernel, dim3(blocks), dim3(256), 0, st, parts, np, pstride, rows, width, y, ldy);
+}
+
 __global__ void fill_u32_kernel(uint32_t *p, size_t n, uint32_t v) {
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = v;

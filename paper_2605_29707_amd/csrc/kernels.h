@@ -186,5 +186,9 @@ void launch_to_f32(const void *src, bool bf16, float *dst, size_t n, hipStream_t
 // Y[r][n] += bias[n] for r < rows, n < N (row stride N)
 void launch_add_row_bias(float *Y, size_t rows, int N, const void *bias, bool bf16, hipStream_t st);
 void launch_fill_u32(uint32_t *p, size_t n, uint32_t v, hipStream_t st);
+// y[r][c] = sum of np K-split partial outputs parts[p*pstride + r*width + c]
+// (width, pstride and ldy multiples of 4; y must not alias parts)
+void launch_sum_parts(const float *parts, int np, size_t pstride, int rows, int width, float *y, int ldy,
+                      hipStream_t st);
 
 }  // namespace dk

@@ -212,7 +212,7 @@ def make_inputs(cfg: DominoConfig, seed: int = 0, ctx_lens=None, max_ctx: int | 
     if cfg.ctx_from_hidden:
         out["ctx_k"] = np.zeros(shape, np.float32)
         out["ctx_v"] = np.zeros(shape, np.float32)
-        n_new = int(ctx_lens.min(initial=0))
+        n_new = int(ctx_lens.min()) if ctx_lens.size else 0
         out["ctx_hidden"] = _normal(seed, _T_CTX_H, (bs, n_new, cfg.ctx_width), 1.0, bf)
         out["ctx_ids"] = _rng(seed, _T_CTX_IDS).integers(0, V - 1, size=(bs, n_new)).astype(np.int32)
     else:

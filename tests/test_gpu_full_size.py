@@ -102,8 +102,9 @@ def test_full_size_sampled_rows(name, rows):
 
 def test_context_append_qwen3_8b():
     """Context-KV append at full size: the hidden states of tau = 4 accepted
-    tokens are projected by every layer's W_k (k-norm, RoPE) and W_v into a bf16
-    cache of 1024 positions, then the block is drafted over the updated cache."""
+    tokens, taken from 5 target layers ([4][5*4096]), are fused by ctx_fc and
+    projected by every layer's W_k (k-norm, RoPE) and W_v into a bf16 cache of
+    1024 positions, then the block is drafted over the updated cache."""
     cfg = synth.get_config("qwen3_8b")
     n_new = 4
     w = synth.make_weights(cfg, seed=0)
@@ -119,9 +120,11 @@ def test_context_append_qwen3_8b():
     del w
     n = int(inp["ctx_lens"][0])
     pos = np.arange(n - n_new, n, dtype=np.float64)
+    assert cfg.ctx_fuse_layers == 5 and inp["ctx_hidden"].shape == (1, n_new, 5 * cfg.hidden)
+    c = oracle.fuse_context(cfg, w64, inp["ctx_hidden"][0])
     worst = 0.0
     for l, lw in enumerate(w64["layers"]):
-        k, v = oracle.project_context_kv(cfg, lw, inp["ctx_hidden"][0], pos)
+        k, v = oracle.project_context_kv(cfg, lw, c, pos)
         for got, want in ((gpu["ctx_k"][l, 0, n - n_new:n], k), (gpu["ctx_v"][l, 0, n - n_new:n], v)):
             # stored in bf16: round-to-nearest error at most 2^-9 relative, plus the fp32 arithmetic
             assert np.all(np.abs(got - want) <= np.abs(want) * 2.0 ** -8 + 1e-4)

@@ -43,6 +43,34 @@ def test_tiny_parity_context_from_hidden_states():
     run.close()
 
 
+@pytest.mark.parametrize("dtype,k,lens", [("f32", 3, [128]), ("f32", 2, [128, 77]), ("bf16", 5, [101, 128, 64])])
+def test_context_fusion_parity(dtype, k, lens):
+    """Appended rows of k concatenated target layers ([n_new][k*d]) are fused by
+    ctx_fc (a K-split GEMM over k*d columns and the sum of its partials) before
+    each layer's K/V projections; ragged context lengths put them at different
+    cache positions per batch row."""
+    cfg = synth.get_config("tiny").with_(dtype=dtype, ctx_fuse_layers=k, batch=len(lens))
+    log(f"context fusion: {dtype} k={k} lens={lens}")
+    w = synth.make_weights(cfg, seed=4)
+    inp = synth.make_inputs(cfg, seed=4, ctx_lens=np.array(lens, np.int32))
+    n_new = inp["ctx_hidden"].shape[1]
+    assert inp["ctx_hidden"].shape == (len(lens), n_new, k * cfg.hidden) and n_new == min(lens)
+    run = GpuRun(cfg, w, inp["max_ctx"], beta=1, n_new=n_new)
+    gpu = run.step(inp)
+    assert gpu["err"] == 0
+    ref = oracle_for(cfg, oracle.as_f64_weights(w), inp, gpu, 1)
+    if dtype == "f32":
+        np.testing.assert_allclose(gpu["ctx_k"], ref["ctx_k"], atol=1e-5, rtol=0)
+        np.testing.assert_allclose(gpu["ctx_v"], ref["ctx_v"], atol=1e-5, rtol=0)
+    else:
+        # stored in bf16: round-to-nearest error at most 2^-9 relative, plus the fp32 arithmetic
+        for got, want in ((gpu["ctx_k"], ref["ctx_k"]), (gpu["ctx_v"], ref["ctx_v"])):
+            assert np.all(np.abs(got - want) <= np.abs(want) * 2.0 ** -8 + 1e-4)
+    n = check_against_oracle(cfg, gpu, ref, 1e-4 if dtype == "f32" else 2e-2, 1)
+    assert n >= 10 * len(lens)
+    run.close()
+
+
 @pytest.mark.parametrize("beta,lens", [(3, [128, 37, 0]), (8, [5, 128, 64]),
                                        (2, [128 - 3 * i for i in range(20)]),
                                        (1, [(37 * i) % 129 for i in range(40)])])
