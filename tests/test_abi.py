@@ -46,6 +46,8 @@ def _cfg(**kw):
     ({"rank": 1000}, bd.DOMINO_ERR_UNSUPPORTED),
     ({"rank": 64}, bd.DOMINO_ERR_UNSUPPORTED),
     ({"gru_hidden": 2048}, bd.DOMINO_ERR_UNSUPPORTED),
+    ({"ctx_fuse_layers": -1}, bd.DOMINO_ERR_INVALID_ARG),
+    ({"ctx_fuse_layers": 9}, bd.DOMINO_ERR_INVALID_ARG),
     ({}, bd.DOMINO_ERR_INVALID_ARG),  # valid config, NULL weights
 ])
 def test_model_create_validation(kw, status):
@@ -55,6 +57,24 @@ def test_model_create_validation(kw, status):
     assert lib.domino_model_create(C.byref(cfg), None, C.byref(h)) == status
     assert h.value is None
     assert bd.last_error()
+
+
+def test_context_fusion_needs_its_weight():
+    # every pointer set (never dereferenced: validation precedes any HIP call)
+    # except ctx_fc, which a config with fused context layers requires
+    lib = bd.load()
+    fake = 4096
+    arr = (C.c_void_p * 2)(fake, fake)
+    pp = C.cast(arr, C.POINTER(C.c_void_p))
+    w = bd.domino_weights(embed=fake, lm_head=fake, final_norm=fake,
+                          **{k: pp for k in ("attn_norm", "wq", "wk", "wv", "q_norm", "k_norm", "wo",
+                                             "ffn_norm", "w_gate", "w_up", "w_down")},
+                          **{k: fake for k in ("gru_w_ih", "gru_w_hh", "gru_b_ih", "gru_b_hh", "w1", "w2")},
+                          ctx_fc=None)
+    h = C.c_void_p()
+    cfg = _cfg(ctx_fuse_layers=3)
+    assert lib.domino_model_create(C.byref(cfg), C.byref(w), C.byref(h)) == bd.DOMINO_ERR_INVALID_ARG
+    assert h.value is None and "ctx_fc" in bd.last_error()
 
 
 def test_null_config_and_out():
