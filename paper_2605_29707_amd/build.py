@@ -11,7 +11,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libdomino.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["api.hip", "gemm.hip", "backbone.hip", "head.hip", "tree.hip", "sample.hip", "train.hip", "target.hip"]
+SOURCES = ["api.hip", "gemm.hip", "gemm_wide.hip", "backbone.hip", "head.hip", "tree.hip", "sample.hip", "train.hip", "target.hip"]
 ARCH = os.environ.get("DOMINO_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = [

@@ -148,16 +148,28 @@ struct Plans {
 
 constexpr int kMaxSplit = 16;
 
+// bf16 projections of more than kSkinnyMaxRows rows (K a multiple of 32, as
+// the config checks make every K here) run the wide-activation kernel;
+// everything else the skinny weight-streaming kernel
+GemmPlan plan_proj(const domino_model *m, const Packed &pk, int M, int epi, int max_split) {
+  if (m->bf16 && M > kSkinnyMaxRows) return plan_gemm_wide(pk.NT, pk.KS, M, epi, m->n_cu, max_split);
+  return plan_gemm(pk.NT, pk.KS, M, epi, m->n_cu, max_split);
+}
+void launch_proj(const domino_model *m, int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
+  if (p.wide) launch_gemm_wide(epi, a, p, st);  // a.K == a.KS * 32
+  else launch_gemm(m->bf16, epi, a, p, st);
+}
+
 // Plans for M block rows, Mlm LM-head rows and Ma QKV rows (block rows, then
 // appended context rows)
 Plans make_plans_rows(const domino_model *m, int M, int Mlm, int Ma) {
   Plans p;
   // projections whose consumer is elementwise write K-split partial outputs
-  p.qkv = plan_gemm(m->qkv[0].NT, m->qkv[0].KS, Ma, EPI_STORE, m->n_cu, kMaxSplit);
-  p.wo = plan_gemm(m->wo[0].NT, m->wo[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
-  p.gateup = plan_gemm(m->gateup[0].NT, m->gateup[0].KS, M, EPI_SWIGLU, m->n_cu, 1);
-  p.down = plan_gemm(m->down[0].NT, m->down[0].KS, M, EPI_STORE, m->n_cu, kMaxSplit);
-  p.lm = plan_gemm(m->lm.NT, m->lm.KS, Mlm, EPI_STORE, m->n_cu, 1);
+  p.qkv = plan_proj(m, m->qkv[0], Ma, EPI_STORE, kMaxSplit);
+  p.wo = plan_proj(m, m->wo[0], M, EPI_STORE, kMaxSplit);
+  p.gateup = plan_proj(m, m->gateup[0], M, EPI_SWIGLU, 1);
+  p.down = plan_proj(m, m->down[0], M, EPI_STORE, kMaxSplit);
+  p.lm = plan_proj(m, m->lm, Mlm, EPI_STORE, 1);
   p.fc = GemmPlan();
   p.fc.ksplit = 0;
   return p;
@@ -168,7 +180,7 @@ Plans make_plans(const domino_model *m, int bs, int max_new) {
   // QKV also projects the appended context rows (rows M .. M + bs*max_new - 1)
   Plans p = make_plans_rows(m, bs * D.B, bs * (D.B - 1), bs * D.B + bs * max_new);
   // the fusion's K-split partials are summed into those rows of the QKV input
-  if (m->fuse_k > 0 && max_new > 0) p.fc = plan_gemm(m->fc.NT, m->fc.KS, bs * max_new, EPI_STORE, m->n_cu, kMaxSplit);
+  if (m->fuse_k > 0 && max_new > 0) p.fc = plan_proj(m, m->fc, bs * max_new, EPI_STORE, kMaxSplit);
   return p;
 }
 
@@ -323,9 +335,9 @@ hipError_t build_gtab(domino_model *m, const void *w_ih, const void *b_ih) {
   for (int r0 = 0; r0 < D.V; r0 += CH) {
     const int rows = std::min(CH, D.V - r0);
     launch_to_f32((const char *)m->embed + (size_t)r0 * K * m->esz, m->bf16, X, (size_t)rows * K, nullptr);
-    const GemmPlan pl = plan_gemm(pk.NT, pk.KS, rows, EPI_STORE, m->n_cu, 1);
+    const GemmPlan pl = plan_proj(m, pk, rows, EPI_STORE, 1);
     const GemmArgs a = gemm_args(P, pk, 0, pk.NT, N, X, K, rows, K, G + (size_t)r0 * N, N, pl);
-    launch_gemm(m->bf16, EPI_STORE, a, pl, nullptr);
+    launch_proj(m, EPI_STORE, a, pl, nullptr);
     launch_add_row_bias(G + (size_t)r0 * N, rows, N, b_ih, m->bf16, nullptr);
   }
   e = hipGetLastError();
@@ -600,7 +612,7 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
     prof_begin(m, DOMINO_KC_CTXPROJ, st);
     GemmArgs a = gemm_args(base + m->fc.off, m->fc, 0, m->fc.NT, D.d, (const float *)ctx_hidden_new, kf, rows, kf,
                            F(w.FC), D.d, p.fc);
-    launch_gemm(m->bf16, EPI_STORE, a, p.fc, st);
+    launch_proj(m, EPI_STORE, a, p.fc, st);
     launch_sum_parts(F(w.FC), p.fc.ksplit, (size_t)rows * D.d, rows, D.d, F(w.A) + (size_t)M * D.d, D.d, st);
     prof_end(m, DOMINO_KC_CTXPROJ, st);
   } else if (n_new > 0) {
@@ -628,7 +640,7 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
     prof_begin(m, DOMINO_KC_QKV, st);
     GemmArgs a = gemm_args(base + m->qkv[l].off, m->qkv[l], 0, m->qkv[l].NT, qkvw, F(w.A), D.d, Ma, D.d, F(w.QKV),
                            qkvw, p.qkv);
-    launch_gemm(m->bf16, EPI_STORE, a, p.qkv, st);
+    launch_proj(m, EPI_STORE, a, p.qkv, st);
     prof_end(m, DOMINO_KC_QKV, st);
 
     prof_begin(m, DOMINO_KC_ROPE, st);
@@ -642,7 +654,7 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
 
     prof_begin(m, DOMINO_KC_WO, st);
     a = gemm_args(base + m->wo[l].off, m->wo[l], 0, m->wo[l].NT, D.d, F(w.O), qd, M, qd, F(w.WOp), D.d, p.wo);
-    launch_gemm(m->bf16, EPI_STORE, a, p.wo, st);
+    launch_proj(m, EPI_STORE, a, p.wo, st);
     prof_end(m, DOMINO_KC_WO, st);
 
     // residual += attention output, then the FFN RMSNorm
@@ -655,13 +667,13 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
     prof_begin(m, DOMINO_KC_GATEUP, st);
     a = gemm_args(base + m->gateup[l].off, m->gateup[l], 0, m->gateup[l].NT, D.ffn, F(w.A), D.d, M, D.d, F(w.F),
                   D.ffn, p.gateup);
-    launch_gemm(m->bf16, EPI_SWIGLU, a, p.gateup, st);
+    launch_proj(m, EPI_SWIGLU, a, p.gateup, st);
     prof_end(m, DOMINO_KC_GATEUP, st);
 
     prof_begin(m, DOMINO_KC_DOWN, st);
     a = gemm_args(base + m->down[l].off, m->down[l], 0, m->down[l].NT, D.d, F(w.F), D.ffn, M, D.ffn, F(w.DNp), D.d,
                   p.down);
-    launch_gemm(m->bf16, EPI_STORE, a, p.down, st);
+    launch_proj(m, EPI_STORE, a, p.down, st);
     prof_end(m, DOMINO_KC_DOWN, st);
   }
 
@@ -676,7 +688,7 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
   float *LP = F(w.LP);
   prof_begin(m, DOMINO_KC_LMHEAD, st);
   GemmArgs a = gemm_args(base + m->lm.off, m->lm, 0, m->lm.NT, w.ldl, H, D.d, Mh, D.d, LP, w.ldl, p.lm);
-  launch_gemm(m->bf16, EPI_STORE, a, p.lm, st);
+  launch_proj(m, EPI_STORE, a, p.lm, st);
   prof_end(m, DOMINO_KC_LMHEAD, st);
   if (!spec.all_rows && debug && debug->base_logits) {
     hipError_t ce = hipMemcpy2DAsync(debug->base_logits, (size_t)D.V * 4, LP, (size_t)w.ldl * 4, (size_t)D.V * 4, Mh,
@@ -897,10 +909,10 @@ domino_status domino_train_forward(domino_model_t m, int32_t batch, const int32_
 
   // Y = W1[:, d:] S for every (row, position) at once
   prof_begin(m, DOMINO_KC_TRAINLOSS, st);
-  const GemmPlan py = plan_gemm(m->w1s.NT, m->w1s.KS, Mr, EPI_STORE, m->n_cu, 1);
+  const GemmPlan py = plan_proj(m, m->w1s, Mr, EPI_STORE, 1);
   const GemmArgs ga = gemm_args((const char *)m->mem + m->w1s.off, m->w1s, 0, m->w1s.NT, D.r, h.states, D.ds, Mr,
                                 D.ds, (float *)(ws + tl.Y), D.r, py);
-  launch_gemm(m->bf16, EPI_STORE, ga, py, st);
+  launch_proj(m, EPI_STORE, ga, py, st);
 
   TrainArgs t;
   t.V = D.V;

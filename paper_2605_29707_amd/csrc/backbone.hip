@@ -368,12 +368,12 @@ DEVI floatx4 mfma3(const bf16x8 &ah, const bf16x8 &al, const bf16x8 &bh, const b
 // set (a verify forward's tree mask, [bs][B][B] bytes, B a multiple of 4);
 // context keys are always visible.  Rows whose keys in a chunk are all hidden
 // leave (max -inf, sum 0), which the merge weighs as zero.
-template <typename WT, int QT, int CH, int DH, bool MASKED>
+template <typename WT, int QT, int CH, int DH, bool MASKED, bool MULTI>
 __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     const float *__restrict__ Q, const float *__restrict__ Kb, const float *__restrict__ Vb,
     const WT *__restrict__ ck, const WT *__restrict__ cv, const int32_t *__restrict__ ctx_lens,
     int max_ctx, float *__restrict__ part, int B, int nq, int nkv, int nch, float scale,
-    const uint8_t *__restrict__ amask) {
+    const uint8_t *__restrict__ amask, int cpw) {
   constexpr int R = QT * 16;      // query rows of the group
   constexpr int KT = CH / 16;     // key tiles
   constexpr int DT = DH / 16;     // output dim tiles
@@ -391,7 +391,10 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   uint16_t *Ph = kPinK ? Kh : Vl + DH * CP, *Pl = Ph + R * CP;
   float *Rm = (float *)(kPinK ? Vl + DH * CP : Pl + R * CP);  // [KT][R] partial row max
   float *Rl = Rm + KT * R;             // [KT][R] partial row sum
-  uint32_t *Ms = (uint32_t *)(Rl + KT * R);  // MASKED: [B][B] bytes of this batch row's tree mask
+  // MULTI: running row max and sum over the chunks folded so far, and each
+  // row's rescale factor for the current chunk
+  float *Mrun = Rl + KT * R, *Lrun = Mrun + R, *Alpha = Lrun + R;
+  uint32_t *Ms = (uint32_t *)(Rl + KT * R + (MULTI ? 3 * R : 0));  // MASKED: [B][B] bytes of this batch row's tree mask
   constexpr int kMaskIt = 64 * 64 / 4 / kAttnThreads;  // words per thread for B <= 64
 
   const int c = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
@@ -399,22 +402,40 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   int n = ctx_lens[b];
   n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
   const int total = n + B;
-  const int c0 = c * CH;
-  if (c0 >= total) return;
-  const int nk = min(CH, total - c0);
+  // MULTI: this workgroup folds chunks c*cpw .. c*cpw + cpw - 1 into one
+  // partial with a running (online) softmax; otherwise it takes chunk c alone
+  const int nsub = MULTI ? cpw : 1;
+  if (c * nsub * CH >= total) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, cc = lane & 15;
+  if constexpr (MULTI)
+    for (int q = tid; q < R; q += kAttnThreads) {
+      Mrun[q] = -INFINITY;
+      Lrun[q] = 0.f;
+    }
+  floatx4 oacc[QT][DTW];
+#pragma unroll
+  for (int i = 0; i < QT; ++i)
+#pragma unroll
+    for (int x = 0; x < DTW; ++x) oacc[i][x] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // ---- stage Q rows, the K chunk (row-major) and the V chunk (transposed)
+  for (int cs = 0; cs < nsub; ++cs) {
+  const int c0 = (c * nsub + cs) * CH;
+  if (c0 >= total) break;  // uniform over the workgroup
+  const int nk = min(CH, total - c0);
+
+  // ---- stage Q rows (first chunk only), the K chunk (row-major) and the V chunk (transposed)
   {
     constexpr int NQ = R * DH / 4 / kAttnThreads;
     float4 qv[NQ];
+    if (cs == 0) {
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int e = tid + q * kAttnThreads;
-      const int qi = e / (DH / 4), d4 = e % (DH / 4);
-      const int qh = kvh * G + qi / B, j = qi % B;
-      qv[q] = *(const float4 *)(Q + (((size_t)b * B + j) * nq + qh) * DH + 4 * d4);
+      for (int q = 0; q < NQ; ++q) {
+        const int e = tid + q * kAttnThreads;
+        const int qi = e / (DH / 4), d4 = e % (DH / 4);
+        const int qh = kvh * G + qi / B, j = qi % B;
+        qv[q] = *(const float4 *)(Q + (((size_t)b * B + j) * nq + qh) * DH + 4 * d4);
+      }
     }
     // Each key comes from the cache (index < n) or the block (index >= n).
     // Both candidates are loaded unconditionally at clamped, valid addresses
@@ -456,14 +477,16 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
       kv[q] = kk < n ? kc[q] : kbk[q];
       vv[q] = kv2 < n ? vc[q] : vbk[q];
     }
+    if (cs == 0) {
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int e = tid + q * kAttnThreads;
-      const int qi = e / (DH / 4), d4 = e % (DH / 4);
-      uint2 hi, lo;
-      split4(qv[q], hi, lo);
-      *(uint2 *)(Qh + qi * DP + 4 * d4) = hi;
-      *(uint2 *)(Ql + qi * DP + 4 * d4) = lo;
+      for (int q = 0; q < NQ; ++q) {
+        const int e = tid + q * kAttnThreads;
+        const int qi = e / (DH / 4), d4 = e % (DH / 4);
+        uint2 hi, lo;
+        split4(qv[q], hi, lo);
+        *(uint2 *)(Qh + qi * DP + 4 * d4) = hi;
+        *(uint2 *)(Ql + qi * DP + 4 * d4) = lo;
+      }
     }
 #pragma unroll
     for (int q = 0; q < NE; ++q) {
@@ -532,12 +555,27 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     if (g == 0) Rm[kt * R + 16 * (qt0 + i) + cc] = m;
   }
   __syncthreads();
+  if constexpr (MULTI) {  // running max and the rescale of what was folded before
+    for (int q = tid; q < R; q += kAttnThreads) {
+      float mc = Rm[q];
+      for (int k2 = 1; k2 < KT; ++k2) mc = fmaxf(mc, Rm[k2 * R + q]);
+      const float mo = Mrun[q], mn = fmaxf(mo, mc);
+      Alpha[q] = mo == -INFINITY ? 0.f : expf(mo - mn);
+      Mrun[q] = mn;
+    }
+    __syncthreads();
+  }
 #pragma unroll
   for (int i = 0; i < QTW; ++i) {
     const int q = 16 * (qt0 + i) + cc;
-    float m = Rm[q];
+    float m;
+    if constexpr (MULTI) {
+      m = Mrun[q];
+    } else {
+      m = Rm[q];
 #pragma unroll
-    for (int k2 = 1; k2 < KT; ++k2) m = fmaxf(m, Rm[k2 * R + q]);
+      for (int k2 = 1; k2 < KT; ++k2) m = fmaxf(m, Rm[k2 * R + q]);
+    }
     float p[4], l = 0.f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -558,22 +596,35 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
   }
   __syncthreads();
   // softmax statistics of the chunk per query row
-  for (int q = tid; q < R; q += kAttnThreads) {
-    float m = Rm[q], l = 0.f;
-    for (int k2 = 1; k2 < KT; ++k2) m = fmaxf(m, Rm[k2 * R + q]);
-    for (int k2 = 0; k2 < KT; ++k2) l += Rl[k2 * R + q];
-    const int qh = kvh * G + q / B, j = q % B;
-    float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2);
-    dst[DH] = m;
-    dst[DH + 1] = l;
+  if constexpr (MULTI) {
+    for (int q = tid; q < R; q += kAttnThreads) {
+      float l = 0.f;
+      for (int k2 = 0; k2 < KT; ++k2) l += Rl[k2 * R + q];
+      Lrun[q] = Alpha[q] * Lrun[q] + l;
+    }
+  } else {
+    for (int q = tid; q < R; q += kAttnThreads) {
+      float m = Rm[q], l = 0.f;
+      for (int k2 = 1; k2 < KT; ++k2) m = fmaxf(m, Rm[k2 * R + q]);
+      for (int k2 = 0; k2 < KT; ++k2) l += Rl[k2 * R + q];
+      const int qh = kvh * G + q / B, j = q % B;
+      float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2);
+      dst[DH] = m;
+      dst[DH + 1] = l;
+    }
   }
 
   // ---- output: wave w owns DTW dim tiles, all query tiles
-  floatx4 oacc[QT][DTW];
+  if constexpr (MULTI) {  // what was folded before is rescaled to the new running max
 #pragma unroll
-  for (int i = 0; i < QT; ++i)
+    for (int i = 0; i < QT; ++i)
 #pragma unroll
-    for (int x = 0; x < DTW; ++x) oacc[i][x] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int e = 0; e < 4; ++e) {
+        const float al = Alpha[16 * i + 4 * g + e];
+#pragma unroll
+        for (int x = 0; x < DTW; ++x) oacc[i][x][e] *= al;
+      }
+  }
 #pragma unroll
   for (int s = 0; s < CH / 32; ++s) {
     bf16x8 vh[DTW], vl[DTW];
@@ -591,6 +642,9 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
         oacc[i][x] = exact ? mfma2b(ph, pl, vh[x], oacc[i][x]) : mfma3(ph, pl, vh[x], vl[x], oacc[i][x]);
     }
   }
+  if constexpr (MULTI) __syncthreads();  // K/P, V and the row statistics are reused by the next chunk
+  }  // chunks
+
   // lane (g, cc) holds O[q = 16*i + 4g + e][dim = 16*dt + cc]
 #pragma unroll
   for (int i = 0; i < QT; ++i)
@@ -601,6 +655,13 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
       float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2);
 #pragma unroll
       for (int x = 0; x < DTW; ++x) dst[16 * (wave * DTW + x) + cc] = oacc[i][x][e];
+    }
+  if constexpr (MULTI)
+    for (int q = tid; q < R; q += kAttnThreads) {
+      const int qh = kvh * G + q / B, j = q % B;
+      float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2);
+      dst[DH] = Mrun[q];
+      dst[DH + 1] = Lrun[q];
     }
 }
 
@@ -742,32 +803,43 @@ void launch_qk_norm_rope(const Dims &D, const float *qkv, int np, size_t pstride
   }
 }
 
-template <typename WT, int RPT, int CH, int DH, bool MASKED>
-static void attn_launch_t(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
-                          const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
-                          const uint8_t *amask, hipStream_t st) {
+template <typename WT, int RPT, int CH, int DH, bool MASKED, bool MULTI>
+static void attn_launch_mt(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
+                           const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
+                           const uint8_t *amask, int cpw, hipStream_t st) {
   constexpr int R = RPT * 16, DP = DH + 8, CP = CH + 8, KT = CH / 16;
   const size_t ps = R * CP <= CH * DP ? 0 : (size_t)R * CP;  // P over K where it fits
   const size_t lds = 2 * sizeof(uint16_t) * ((size_t)R * DP + (size_t)CH * DP + (size_t)DH * CP + ps) +
-                     sizeof(float) * 2 * KT * R + (MASKED ? (size_t)64 * 64 : 0);
+                     sizeof(float) * (2 * KT * R + (MULTI ? 3 * R : 0)) + (MASKED ? (size_t)64 * 64 : 0);
   const float scale = 1.0f / sqrtf((float)DH);
   const int nc = (max_ctx + D.B + CH - 1) / CH;
-  (void)hipFuncSetAttribute((const void *)attn_partial_kernel<WT, RPT, CH, DH, MASKED>,
+  const int ngrp = (nc + cpw - 1) / cpw;
+  (void)hipFuncSetAttribute((const void *)attn_partial_kernel<WT, RPT, CH, DH, MASKED, MULTI>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  hipLaunchKernelGGL((attn_partial_kernel<WT, RPT, CH, DH, MASKED>), dim3(nc, D.nkv, D.bs), dim3(kAttnThreads), lds,
-                     st, Q, Kb, Vb, (const WT *)ck, (const WT *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv, nch,
-                     scale, amask);
+  hipLaunchKernelGGL((attn_partial_kernel<WT, RPT, CH, DH, MASKED, MULTI>), dim3(ngrp, D.nkv, D.bs),
+                     dim3(kAttnThreads), lds, st, Q, Kb, Vb, (const WT *)ck, (const WT *)cv, ctx_lens, max_ctx, part,
+                     D.B, D.nq, D.nkv, nch, scale, amask, cpw);
+}
+
+template <typename WT, int RPT, int CH, int DH, bool MASKED>
+static void attn_launch_t(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
+                          const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
+                          const uint8_t *amask, int cpw, hipStream_t st) {
+  if (cpw > 1)
+    attn_launch_mt<WT, RPT, CH, DH, MASKED, true>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, cpw, st);
+  else
+    attn_launch_mt<WT, RPT, CH, DH, MASKED, false>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, 1, st);
 }
 
 template <typename WT, int DH, bool MASKED>
 static bool attn_dispatch(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
                           const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
-                          const uint8_t *amask, hipStream_t st) {
+                          const uint8_t *amask, int cpw, hipStream_t st) {
   const int R = (D.nq / D.nkv) * D.B;
   switch (R) {
-    case 32: attn_launch_t<WT, 2, 64, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st); return true;
-    case 64: attn_launch_t<WT, 4, 32, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st); return true;
-    case 128: attn_launch_t<WT, 8, 32, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st); return true;
+    case 32: attn_launch_t<WT, 2, 64, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, cpw, st); return true;
+    case 64: attn_launch_t<WT, 4, 32, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, cpw, st); return true;
+    case 128: attn_launch_t<WT, 8, 32, DH, MASKED>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, cpw, st); return true;
     default: return false;
   }
 }
@@ -775,9 +847,29 @@ static bool attn_dispatch(const Dims &D, const float *Q, const float *Kb, const 
 template <typename WT, int DH>
 static bool attn_dispatch_m(const Dims &D, const float *Q, const float *Kb, const float *Vb, const void *ck,
                             const void *cv, const int32_t *ctx_lens, int max_ctx, float *part, int nch,
-                            const uint8_t *amask, hipStream_t st) {
-  if (amask) return attn_dispatch<WT, DH, true>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st);
-  return attn_dispatch<WT, DH, false>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, nullptr, st);
+                            const uint8_t *amask, int cpw, hipStream_t st) {
+  if (amask) return attn_dispatch<WT, DH, true>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, cpw, st);
+  return attn_dispatch<WT, DH, false>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, nullptr, cpw, st);
+}
+
+// Chunks folded per workgroup: 1 (a workgroup per chunk, the lowest latency)
+// unless the grid has enough (batch row, kv head) pairs that, doubling the
+// chunks per workgroup, it still holds at least four workgroups per CU; then
+// the partial outputs and the merge shrink by that factor.
+static int attn_chunks_per_wg(const Dims &D, int nc) {
+  static int n_cu = 0;
+  if (n_cu == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      n_cu = v;
+    else
+      n_cu = 256;
+  }
+  const long pairs = (long)D.bs * D.nkv;
+  int cpw = 1;
+  while (cpw < 64 && pairs * ((nc + 2 * cpw - 1) / (2 * cpw)) >= 4L * n_cu) cpw *= 2;
+  return cpw;
 }
 
 bool attn_supported(int nq, int nkv, int B) {
@@ -790,13 +882,15 @@ void launch_attention(const Dims &D, const float *Q, const float *Kb, const floa
                       float *part, float *O, int32_t *err, hipStream_t st, const uint8_t *amask) {
   (void)err;
   const int nch = attn_nchunks(max_ctx, D.B);
-  const int CH = attn_ch((D.nq / D.nkv) * D.B);
+  const int CH0 = attn_ch((D.nq / D.nkv) * D.B);
+  const int cpw = attn_chunks_per_wg(D, (max_ctx + D.B + CH0 - 1) / CH0);
+  const int CH = CH0 * cpw;  // keys per partial, as the merge sees them
   if (D.dh == 128) {
-    if (D.bf16) attn_dispatch_m<bf16_t, 128>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st);
-    else attn_dispatch_m<float, 128>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st);
+    if (D.bf16) attn_dispatch_m<bf16_t, 128>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, cpw, st);
+    else attn_dispatch_m<float, 128>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, cpw, st);
   } else {
-    if (D.bf16) attn_dispatch_m<bf16_t, 64>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st);
-    else attn_dispatch_m<float, 64>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, st);
+    if (D.bf16) attn_dispatch_m<bf16_t, 64>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, cpw, st);
+    else attn_dispatch_m<float, 64>(D, Q, Kb, Vb, ck, cv, ctx_lens, max_ctx, part, nch, amask, cpw, st);
   }
   const int items = D.bs * D.nq * D.B;
   if (D.dh == 128)

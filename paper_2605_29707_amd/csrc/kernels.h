@@ -27,12 +27,20 @@ struct GemmPlan {
   int kcm;  // k-steps per staged chunk (16/MT, or 8/MT for finer K splits)
   int nw;   // waves (= tiles) per workgroup: 8 or 6
   int pgrid;  // > 0: that many workgroups loop over the groups (one pipeline across groups)
+  int wide = 0;  // 1: the wide-activation kernel (gemm_wide.hip) runs this plan
 };
 
 // max_split = 1: one workgroup covers all of K (direct output); otherwise K
 // may be split up to max_split ways into partial outputs.
 GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu, int max_split);
 void launch_gemm(bool bf16, int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st);
+// Wide activations (bf16 weights; more rows than the skinny kernel's 64 per
+// m-group): workgroup tiles of 128 columns x 256 rows, same packed weights,
+// same hi/lo activation split, K-split partials as above.
+GemmPlan plan_gemm_wide(int ntiles, int KS, int M, int epi, int n_cu, int max_split);
+void launch_gemm_wide(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st);
+// above this many rows a bf16 GEMM whose K is a multiple of 32 runs the wide kernel
+constexpr int kSkinnyMaxRows = 64;
 void launch_pack(bool bf16, const void *W, int N, int K, int ldw, void *P, int NT, int KS,
                  int tile_mul, int tile_off, hipStream_t st);
 inline int kstep_of(bool bf16) { return bf16 ? 32 : 16; }

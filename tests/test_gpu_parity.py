@@ -105,6 +105,29 @@ def test_tiny_bf16_batches(batch, beta):
     run.close()
 
 
+@pytest.mark.parametrize("dtype,nq", [("bf16", 4), ("f32", 8), ("bf16", 16)])
+def test_long_context_folded_chunks(dtype, nq):
+    """16 batch rows over contexts of up to 4096 keys: enough (batch row, kv
+    head) pairs that each attention workgroup folds two key chunks into one
+    partial with a running softmax (the long-context path); ragged lengths
+    leave some workgroups one chunk, some partial chunks and one row with no
+    context at all.  nq = 4, 8, 16 over 2 kv heads: 32, 64 and 128 query rows
+    per workgroup."""
+    lens = [4096, 100, 0, 37, 4095, 64, 65, 2048, 1, 3000, 4000, 129, 127, 500, 4096, 33]
+    cfg = synth.get_config("tiny").with_(dtype=dtype, n_q_heads=nq, batch=len(lens), ctx=4096,
+                                         ctx_from_hidden=False)
+    w = synth.make_weights(cfg, seed=13, gain_std=0.1)
+    inp = synth.make_inputs(cfg, seed=13, ctx_lens=np.array(lens, np.int32), max_ctx=4096)
+    log(f"long context: {dtype} nq={nq} bs={len(lens)}")
+    run = GpuRun(cfg, w, 4096, beta=1)
+    gpu = run.step(inp)
+    assert gpu["err"] == 0
+    ref = oracle_for(cfg, oracle.as_f64_weights(w), inp, gpu, 1)
+    n = check_against_oracle(cfg, gpu, ref, 1e-4 if dtype == "f32" else 2e-2, 1)
+    assert n >= 10 * len(lens)
+    run.close()
+
+
 @pytest.mark.parametrize("nq,block", [(8, 32), (4, 64)])
 def test_tiny_large_blocks(nq, block):
     """(n_q / n_kv) * block = 128 query rows per workgroup: the attention uses
