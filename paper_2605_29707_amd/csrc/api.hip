@@ -65,6 +65,7 @@ struct domino_model {
   Packed lm, w2, w1s;
   int fuse_k = 0;  // context fusion: appended rows are fuse_k*d wide, fused by fc
   Packed fc;
+  Packed whh;  // W_hh packed, for the state GEMM of batches above kHeadFusedBatch
   // training forward: the state recurrence runs on a second stream beside the backbone
   hipStream_t side = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
@@ -136,7 +137,7 @@ Dims make_dims(const domino_model *m, int bs) {
 
 // ---- workspace layout of the draft step
 struct WsLayout {
-  size_t err, best, slots, hdr_words, X, X2, A, FC, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
+  size_t err, best, slots, hdr_words, X, X2, A, FC, HP, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
       praw, total;
   int GC, ldl;
 };
@@ -205,6 +206,7 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   const int Ma = M + bs * max_new;  // block rows, then the appended context rows
   w.A = take((size_t)Ma * D.d * 4);
   w.FC = take((size_t)p.fc.ksplit * bs * max_new * D.d * 4);
+  w.HP = take(head_part_floats(D) * 4);  // state GEMM partials (batches above kHeadFusedBatch)
   w.QKV = take((size_t)p.qkv.ksplit * Ma * qkvw * 4);
   w.Q = take((size_t)M * D.nq * D.dh * 4);
   w.Kb = take((size_t)M * D.nkv * D.dh * 4);
@@ -441,7 +443,8 @@ domino_status create_impl(const domino_config *cfg, const domino_weights *w, dom
   m->lm = add(((D.V + 15) / 16) * 16 + (with_head ? D.r : 0), D.d);
   if (with_head) {
     m->w2 = add(D.V, D.r);
-    m->w1s = add(D.r, D.ds);  // W1's S half on its own, for the batched u of the training forward
+    m->w1s = add(D.r, D.ds);  // W1's S half on its own (training forward; state GEMMs of large batches)
+    m->whh = add(3 * D.ds, D.ds);
     m->fuse_k = cfg->ctx_fuse_layers;
     if (m->fuse_k > 0) m->fc = add(D.d, m->fuse_k * D.d);
     m->gtab_off = off;
@@ -491,6 +494,7 @@ domino_status create_impl(const domino_config *cfg, const domino_weights *w, dom
     launch_pack(bf, w->w2, D.V, D.r, D.r, base + m->w2.off, m->w2.NT, m->w2.KS, 1, 0, st);
     launch_pack(bf, (const char *)w->w1 + (size_t)D.d * m->esz, D.r, D.ds, D.d + D.ds, base + m->w1s.off,
                 m->w1s.NT, m->w1s.KS, 1, 0, st);
+    launch_pack(bf, w->gru_w_hh, 3 * D.ds, D.ds, D.ds, base + m->whh.off, m->whh.NT, m->whh.KS, 1, 0, st);
     if (m->fuse_k > 0) {
       const int kf = m->fuse_k * D.d;
       launch_pack(bf, w->ctx_fc, D.d, kf, kf, base + m->fc.off, m->fc.NT, m->fc.KS, 1, 0, st);
@@ -751,6 +755,14 @@ HeadArgs head_args(domino_model_t m, int32_t batch, int32_t branch, char *ws, co
   h.kslot = h.uslot + (size_t)batch * D.r;
   h.abort_flag = (unsigned *)(ws + w.err + 128);
   h.poll_limit = m->poll_limit;
+  h.whh_p = base + m->whh.off;
+  h.w1s_p = base + m->w1s.off;
+  h.whh_NT = m->whh.NT;
+  h.whh_KS = m->whh.KS;
+  h.w1s_NT = m->w1s.NT;
+  h.w1s_KS = m->w1s.KS;
+  h.hpart = head_part_floats(D) ? F(w.HP) : nullptr;
+  h.n_cu = m->n_cu;
   return h;
 }
 

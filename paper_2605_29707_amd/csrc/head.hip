@@ -305,7 +305,7 @@ __global__ __launch_bounds__(256) void head_u_kernel(HeadArgs h, int j) {
 // update is the only step repeated per workgroup and no launch sits between
 // the state and u.  Weight rows are loaded before the state is formed.
 // ---------------------------------------------------------------------------
-constexpr int kFusedBatch = 8;
+constexpr int kFusedBatch = kHeadFusedBatch;
 constexpr int kStateWaves = 8;
 constexpr int kStateMaxGrid = 256;
 
@@ -447,6 +447,67 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
       }
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Batches above kFusedBatch: W_hh S_{j-1} and W1[:, d:] S_j run as K-split
+// GEMMs (the projections' weight-streaming kernel over packed copies of the
+// two matrices), which stage the states once per workgroup; these kernels add
+// the partials in split order and finish each step elementwise.
+// ---------------------------------------------------------------------------
+// S_j = GRU(G[y_{j-1}], S_{j-1}), one workgroup row per batch row
+__global__ __launch_bounds__(256) void head_gru_elem_kernel(HeadArgs h, int j, const float *__restrict__ gp, int np,
+                                                            size_t pstride) {
+  const Dims &D = h.D;
+  const int bs = D.bs, ds = D.ds, depth = D.B - 1, V = D.V;
+  const int b = blockIdx.y;
+  __shared__ int ysh;
+  if (threadIdx.x == 0) {  // y_{j-1}: the anchor, a forced token, or the decoded best key of position j-1
+    int y;
+    if (j == 1) y = clamp_token(h.anchor[b], V, h.err);
+    else if (h.forced) y = clamp_token(h.forced[(size_t)b * depth + (j - 2)], V, h.err);
+    else {
+      const unsigned long long *bk = h.best + ((size_t)(j - 2) * bs + b) * kBestSlots;
+      unsigned long long key = bk[0];
+#pragma unroll
+      for (int q = 1; q < kBestSlots; ++q) key = bk[q] > key ? bk[q] : key;
+      y = decode_best_id(key, V);
+    }
+    ysh = y;
+  }
+  __syncthreads();
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= ds) return;
+  const float *hprev = h.hbuf + (size_t)((j - 1) & 1) * bs * ds;
+  float *hnext = h.hbuf + (size_t)(j & 1) * bs * ds;
+  float gh[3];
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    float acc = 0.f;  // W_hh S_{j-1} (S_0 = 0: no product at j = 1)
+    for (int p = 0; p < np; ++p) acc += gp[(size_t)p * pstride + (size_t)b * 3 * ds + q * ds + i];
+    gh[q] = acc + h.bhh[q * ds + i];
+  }
+  const float *gy = h.gtab + (size_t)ysh * 3 * ds;  // b_ih is in G
+  const float rg = sigm(gy[i] + gh[0]), zg = sigm(gy[ds + i] + gh[1]);
+  const float ng = tanhf(gy[2 * ds + i] + rg * gh[2]);
+  const float hold = j > 1 ? hprev[(size_t)b * ds + i] : 0.f;
+  const float hn = (1.f - zg) * ng + zg * hold;
+  hnext[(size_t)b * ds + i] = hn;
+  if (h.states) h.states[((size_t)b * depth + (j - 1)) * ds + i] = hn;
+}
+
+// u_j = SiLU(W1[:, :d] H_j + W1[:, d:] S_j) from the summed partials
+__global__ __launch_bounds__(256) void head_u_elem_kernel(HeadArgs h, int j, const float *__restrict__ up, int np,
+                                                          size_t pstride) {
+  const Dims &D = h.D;
+  const int r = D.r, depth = D.B - 1;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= D.bs * r) return;
+  const int b = e / r, k = e % r;
+  float acc = 0.f;
+  for (int p = 0; p < np; ++p) acc += up[(size_t)p * pstride + e];
+  const float x = h.P[((size_t)b * depth + (j - 1)) * h.ldp + k] + acc;
+  h.ubuf[(size_t)b * h.u_ld + (size_t)(j - 1) * h.u_pos + k] = x / (1.f + expf(-x));
 }
 
 // ---------------------------------------------------------------------------
@@ -1229,6 +1290,58 @@ int head_logits_grid(const Dims &D) { return (D.V + logit_rows(D) - 1) / logit_r
 
 
 
+// One position's state (and u) for batches above kFusedBatch: the two GEMMs
+// and their elementwise finishes
+static void states_gemm_step(const HeadArgs &h, int j, bool with_u, hipStream_t st) {
+  const Dims &D = h.D;
+  const int bs = D.bs, ds = D.ds, r = D.r;
+  float *gp = h.hpart, *up = h.hpart + (size_t)kHeadMaxSplit * bs * 3 * ds;
+  int npg = 0;
+  if (j > 1) {
+    const GemmPlan pg = plan_gemm(h.whh_NT, h.whh_KS, bs, EPI_STORE, h.n_cu, kHeadMaxSplit);
+    GemmArgs a;
+    a.P = h.whh_p;
+    a.KS = h.whh_KS;
+    a.tile0 = 0;
+    a.ntiles = h.whh_NT;
+    a.N = 3 * ds;
+    a.X = h.hbuf + (size_t)((j - 1) & 1) * bs * ds;
+    a.ldx = ds;
+    a.M = bs;
+    a.K = ds;
+    a.Y = gp;
+    a.ldy = 3 * ds;
+    a.ysplit = (size_t)bs * 3 * ds;
+    a.ksplit = pg.ksplit;
+    launch_gemm(D.bf16, EPI_STORE, a, pg, st);
+    npg = pg.ksplit;
+  }
+  hipLaunchKernelGGL(head_gru_elem_kernel, dim3((ds + 255) / 256, bs), dim3(256), 0, st, h, j, gp, npg,
+                     (size_t)bs * 3 * ds);
+  if (!with_u) return;
+  const GemmPlan pu = plan_gemm(h.w1s_NT, h.w1s_KS, bs, EPI_STORE, h.n_cu, kHeadMaxSplit);
+  GemmArgs a;
+  a.P = h.w1s_p;
+  a.KS = h.w1s_KS;
+  a.tile0 = 0;
+  a.ntiles = h.w1s_NT;
+  a.N = r;
+  a.X = h.hbuf + (size_t)(j & 1) * bs * ds;
+  a.ldx = ds;
+  a.M = bs;
+  a.K = ds;
+  a.Y = up;
+  a.ldy = r;
+  a.ysplit = (size_t)bs * r;
+  a.ksplit = pu.ksplit;
+  launch_gemm(D.bf16, EPI_STORE, a, pu, st);
+  hipLaunchKernelGGL(head_u_elem_kernel, dim3((bs * r + 255) / 256), dim3(256), 0, st, h, j, up, pu.ksplit,
+                     (size_t)bs * r);
+}
+static bool states_by_gemm(const HeadArgs &h) {
+  return h.D.bs > kFusedBatch && h.whh_p && h.w1s_p && h.hpart && h.n_cu > 0;
+}
+
 template <typename WT, int KS, int MT>
 static void launch_loop(const HeadArgs &h, hipStream_t st) {
   const Dims &D = h.D;
@@ -1245,9 +1358,12 @@ static void launch_loop(const HeadArgs &h, hipStream_t st) {
   if (fused)
     (void)hipFuncSetAttribute((const void *)head_state_kernel<WT>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)slds);
+  const bool by_gemm = !fused && states_by_gemm(h);
   for (int j = 1; j <= depth; ++j) {
     if (fused) {
       hipLaunchKernelGGL(head_state_kernel<WT>, dim3(gs), dim3(kStateWaves * 64), slds, st, h, j);
+    } else if (by_gemm) {
+      states_gemm_step(h, j, true, st);
     } else {
       hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(ga), dim3(256), 0, st, h, j);
       hipLaunchKernelGGL(head_u_kernel<WT>, dim3(gb), dim3(256), 0, st, h, j);
@@ -1268,9 +1384,12 @@ static void launch_states_t(const HeadArgs &h, hipStream_t st) {
   if (fused)
     (void)hipFuncSetAttribute((const void *)head_state_kernel<WT>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)slds);
+  const bool by_gemm = !fused && states_by_gemm(h);
   for (int j = 1; j <= D.B - 1; ++j) {
     if (fused) {
       hipLaunchKernelGGL(head_state_kernel<WT>, dim3(gs), dim3(kStateWaves * 64), slds, st, h, j);
+    } else if (by_gemm) {
+      states_gemm_step(h, j, !h.skip_u, st);
     } else {
       hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(ga), dim3(256), 0, st, h, j);
       if (!h.skip_u) hipLaunchKernelGGL(head_u_kernel<WT>, dim3(gb), dim3(256), 0, st, h, j);

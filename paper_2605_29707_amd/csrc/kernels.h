@@ -131,7 +131,19 @@ struct HeadArgs {
   unsigned long long *uslot, *kslot;
   unsigned *abort_flag;
   unsigned poll_limit;  // polls a wait makes before it gives up
+  // batches above kHeadFusedBatch: W_hh S and W1[:, d:] S run as K-split
+  // GEMMs over packed copies of the two matrices (partials in hpart:
+  // [kHeadMaxSplit][bs][3ds], then [kHeadMaxSplit][bs][r])
+  const void *whh_p, *w1s_p;
+  int whh_NT, whh_KS, w1s_NT, w1s_KS;
+  float *hpart;
+  int n_cu;
 };
+constexpr int kHeadFusedBatch = 8;  // batches up to this run the fused state kernel
+constexpr int kHeadMaxSplit = 16;
+inline size_t head_part_floats(const Dims &D) {
+  return D.bs > kHeadFusedBatch ? (size_t)kHeadMaxSplit * D.bs * (3 * D.ds + D.r) : 0;
+}
 int head_logits_grid(const Dims &D);
 int head_best_slots();
 hipError_t launch_head(const HeadArgs &h, hipStream_t st);
