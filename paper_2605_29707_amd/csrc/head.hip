@@ -156,146 +156,6 @@ DEVI void unpack16<float>(const u32x4 &w, float *f) {
 }
 
 // ---------------------------------------------------------------------------
-// gru: choose y_{j-1} and advance this workgroup's slice of the state.
-// ---------------------------------------------------------------------------
-template <typename WT>
-__global__ __launch_bounds__(256) void head_gru_kernel(HeadArgs h, int j) {
-  constexpr int EPL = 16 / sizeof(WT);
-  const Dims &D = h.D;
-  const int bs = D.bs, ds = D.ds, depth = D.B - 1, beta = h.beta, V = D.V;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  __shared__ int ys[64];
-
-  // ---- y_{j-1}: the anchor, a forced token, or the decoded best key of position j-1
-  for (int b = threadIdx.x; b < bs; b += blockDim.x) {
-    int y;
-    if (j == 1) y = clamp_token(h.anchor[b], V, h.err);
-    else if (h.forced) y = clamp_token(h.forced[(size_t)b * depth + (j - 2)], V, h.err);
-    else {
-      const unsigned long long *bk = h.best + ((size_t)(j - 2) * bs + b) * kBestSlots;
-      unsigned long long key = bk[0];
-#pragma unroll
-      for (int q = 1; q < kBestSlots; ++q) key = bk[q] > key ? bk[q] : key;
-      y = decode_best_id(key, V);
-    }
-    ys[b] = y;
-  }
-  __syncthreads();
-
-  // ---- state slice: one wave per state index (4 per round); lanes stride over d_s
-  const float *hprev = h.hbuf + (size_t)((j - 1) & 1) * bs * ds;
-  float *hnext = h.hbuf + (size_t)(j & 1) * bs * ds;
-  const WT *whh = (const WT *)h.w_hh;
-  const int nchunk = ds / EPL;  // EPL-element chunks per row
-  for (int i0 = blockIdx.x * 4; i0 < ds; i0 += gridDim.x * 4) {
-    const int i = i0 + wave;
-    const bool live = i < ds;
-    // W_hh rows (r, z, n) of index i stay in registers across the batch loop
-    u32x4 w[3][4];
-#pragma unroll
-    for (int q = 0; q < 3; ++q)
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int ch = lane + 64 * c;
-        w[q][c] = (live && ch < nchunk && j > 1)
-                      ? *(const u32x4 *)(whh + ((size_t)(q * ds + i)) * ds + (size_t)ch * EPL)
-                      : u32x4{0u, 0u, 0u, 0u};
-      }
-    for (int b = 0; b < bs; ++b) {
-      float acc[3] = {0.f, 0.f, 0.f};
-      if (j > 1 && live) {
-        const float *hp = hprev + (size_t)b * ds;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const int ch = lane + 64 * c;
-          if (ch < nchunk) {
-            float hv[EPL];
-#pragma unroll
-            for (int e = 0; e < EPL; e += 4) {
-              const float4 t = *(const float4 *)(hp + (size_t)ch * EPL + e);
-              hv[e] = t.x;
-              hv[e + 1] = t.y;
-              hv[e + 2] = t.z;
-              hv[e + 3] = t.w;
-            }
-#pragma unroll
-            for (int q = 0; q < 3; ++q) {
-              float wf[EPL];
-              unpack16<WT>(w[q][c], wf);
-#pragma unroll
-              for (int e = 0; e < EPL; ++e) acc[q] = fmaf(wf[e], hv[e], acc[q]);
-            }
-          }
-        }
-#pragma unroll
-        for (int q = 0; q < 3; ++q) acc[q] = wave_sum(acc[q]);
-      }
-      if (lane == 0) {
-        float hn = 0.f;
-        if (live) {
-          const float *gy = h.gtab + (size_t)ys[b] * 3 * ds;
-          const float gir = gy[i], giz = gy[ds + i], gin = gy[2 * ds + i];  // b_ih is in G
-          const float ghr = acc[0] + h.bhh[i], ghz = acc[1] + h.bhh[ds + i], ghn = acc[2] + h.bhh[2 * ds + i];
-          const float rg = sigm(gir + ghr), zg = sigm(giz + ghz);
-          const float ng = tanhf(gin + rg * ghn);
-          const float hold = j > 1 ? hprev[(size_t)b * ds + i] : 0.f;
-          hn = (1.f - zg) * ng + zg * hold;
-          hnext[(size_t)b * ds + i] = hn;
-          if (h.states) h.states[((size_t)b * depth + (j - 1)) * ds + i] = hn;
-        }
-      }
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// u: one wave per (k) output, all batch rows
-// ---------------------------------------------------------------------------
-template <typename WT>
-__global__ __launch_bounds__(256) void head_u_kernel(HeadArgs h, int j) {
-  constexpr int EPL = 16 / sizeof(WT);
-  const Dims &D = h.D;
-  const int bs = D.bs, d = D.d, ds = D.ds, r = D.r, depth = D.B - 1;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int k = blockIdx.x * 4 + wave;
-  if (k >= r) return;
-  const float *hn = h.hbuf + (size_t)(j & 1) * bs * ds;
-  const WT *wr = (const WT *)h.w1 + (size_t)k * (d + ds) + d;
-  const int nchunk = ds / EPL;
-  u32x4 w[4];
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const int ch = lane + 64 * c;
-    w[c] = ch < nchunk ? *(const u32x4 *)(wr + (size_t)ch * EPL) : u32x4{0u, 0u, 0u, 0u};
-  }
-  for (int b = 0; b < bs; ++b) {
-    const float *hb = hn + (size_t)b * ds;
-    float acc = 0.f;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int ch = lane + 64 * c;
-      if (ch < nchunk) {
-        float wf[EPL];
-        unpack16<WT>(w[c], wf);
-#pragma unroll
-        for (int e = 0; e < EPL; e += 4) {
-          const float4 t = *(const float4 *)(hb + (size_t)ch * EPL + e);
-          acc = fmaf(wf[e], t.x, acc);
-          acc = fmaf(wf[e + 1], t.y, acc);
-          acc = fmaf(wf[e + 2], t.z, acc);
-          acc = fmaf(wf[e + 3], t.w, acc);
-        }
-      }
-    }
-    acc = wave_sum(acc);
-    if (lane == 0) {
-      const float x = h.P[((size_t)b * depth + (j - 1)) * h.ldp + k] + acc;
-      h.ubuf[(size_t)b * h.u_ld + (size_t)(j - 1) * h.u_pos + k] = x / (1.f + expf(-x));
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
 // state (batches up to kFusedBatch; replaces gru + u): every workgroup forms
 // the whole S_{j-1} itself from the gathered input gates G[y_{j-1}], the
 // hidden gates W_hh S_{j-2} that the previous position left in ghbuf, and
@@ -1346,28 +1206,19 @@ template <typename WT, int KS, int MT>
 static void launch_loop(const HeadArgs &h, hipStream_t st) {
   const Dims &D = h.D;
   const int depth = D.B - 1;
-  const int ga = min((D.ds + 3) / 4, 256);
   constexpr int XF = XStage<WT>::XF;
   const size_t lds = sizeof(u32x4) * KS * MT * 64 * XF + sizeof(float) * (size_t)D.bs * logit_rows(D);
   (void)hipFuncSetAttribute((const void *)head_logits_kernel<WT, KS, MT>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  const int gb = (D.r + 3) / 4;
   const bool fused = D.bs <= kFusedBatch;
   const size_t slds = sizeof(float) * (size_t)D.bs * D.ds;
   const int gs = min((D.r + 3 * D.ds + 2 * kStateWaves - 1) / (2 * kStateWaves), kStateMaxGrid);
   if (fused)
     (void)hipFuncSetAttribute((const void *)head_state_kernel<WT>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)slds);
-  const bool by_gemm = !fused && states_by_gemm(h);
   for (int j = 1; j <= depth; ++j) {
-    if (fused) {
-      hipLaunchKernelGGL(head_state_kernel<WT>, dim3(gs), dim3(kStateWaves * 64), slds, st, h, j);
-    } else if (by_gemm) {
-      states_gemm_step(h, j, true, st);
-    } else {
-      hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(ga), dim3(256), 0, st, h, j);
-      hipLaunchKernelGGL(head_u_kernel<WT>, dim3(gb), dim3(256), 0, st, h, j);
-    }
+    if (fused) hipLaunchKernelGGL(head_state_kernel<WT>, dim3(gs), dim3(kStateWaves * 64), slds, st, h, j);
+    else states_gemm_step(h, j, true, st);
     hipLaunchKernelGGL((head_logits_kernel<WT, KS, MT>), dim3(h.GC), dim3(kLogitWaves * 64), lds, st, h, j);
   }
   hipLaunchKernelGGL(head_merge_kernel, dim3(depth, D.bs), dim3(64), 0, st, h);
@@ -1376,7 +1227,6 @@ static void launch_loop(const HeadArgs &h, hipStream_t st) {
 template <typename WT>
 static void launch_states_t(const HeadArgs &h, hipStream_t st) {
   const Dims &D = h.D;
-  const int ga = min((D.ds + 3) / 4, 256), gb = (D.r + 3) / 4;
   const bool fused = D.bs <= kFusedBatch;
   const size_t slds = sizeof(float) * (size_t)D.bs * D.ds;
   const int rows = (h.skip_u ? 0 : D.r) + 3 * D.ds;
@@ -1384,21 +1234,15 @@ static void launch_states_t(const HeadArgs &h, hipStream_t st) {
   if (fused)
     (void)hipFuncSetAttribute((const void *)head_state_kernel<WT>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)slds);
-  const bool by_gemm = !fused && states_by_gemm(h);
   for (int j = 1; j <= D.B - 1; ++j) {
-    if (fused) {
-      hipLaunchKernelGGL(head_state_kernel<WT>, dim3(gs), dim3(kStateWaves * 64), slds, st, h, j);
-    } else if (by_gemm) {
-      states_gemm_step(h, j, !h.skip_u, st);
-    } else {
-      hipLaunchKernelGGL(head_gru_kernel<WT>, dim3(ga), dim3(256), 0, st, h, j);
-      if (!h.skip_u) hipLaunchKernelGGL(head_u_kernel<WT>, dim3(gb), dim3(256), 0, st, h, j);
-    }
+    if (fused) hipLaunchKernelGGL(head_state_kernel<WT>, dim3(gs), dim3(kStateWaves * 64), slds, st, h, j);
+    else states_gemm_step(h, j, !h.skip_u, st);
   }
 }
 
 hipError_t launch_head_states(const HeadArgs &h, hipStream_t st) {
   if (!h.forced) return hipErrorInvalidValue;
+  if (h.D.bs > kFusedBatch && !states_by_gemm(h)) return hipErrorInvalidValue;
   if (h.D.bf16) launch_states_t<bf16_t>(h, st);
   else launch_states_t<float>(h, st);
   return hipGetLastError();
@@ -1412,6 +1256,7 @@ static void launch_mt(const HeadArgs &h, hipStream_t st) {
 }
 
 hipError_t launch_head(const HeadArgs &h, hipStream_t st) {
+  if (h.D.bs > kFusedBatch && !states_by_gemm(h)) return hipErrorInvalidValue;
   const bool bf = h.D.bf16;
   const int KS = h.D.r / (bf ? 32 : 16);
   if (bf) {
