@@ -380,7 +380,7 @@ constexpr int kLogitWaves = 8;
 // W2 tiles per wave: as many as fit the registers (all of a wave's loads are
 // issued at once, and the grid then fits the GPU in one round)
 constexpr int kTpwSmall = 5;
-constexpr int logit_tpw(int KS, int MT) { return KS * MT <= 8 ? kTpwSmall : (KS * MT <= 16 ? 2 : 1); }
+constexpr int logit_tpw(int KS, int MT) { return KS * MT <= 8 ? kTpwSmall : (KS * MT <= 16 ? 3 : 1); }
 
 template <typename WT, int KS, int MT>
 __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs h, int j) {
