@@ -84,14 +84,16 @@ __global__ __launch_bounds__(kWideThreads) void gemm_wide_kernel(GemmArgs a) {
     for (int h = 0; h < 2; ++h) load_row8(a.X, a.ldx, a.M, mbase + rr + 128 * h, sc * 32 + g * 8, xr[d][h]);
   };
   auto stage = [&](int d, int buf, bool live) {
-    // a k-step past the split's end is staged as zero weights (a select on
-    // loaded data, not a skipped load), so it adds nothing to the products
+    // a k-step past the split's end is staged as zeros (a select on loaded
+    // data, not a skipped load), so it adds nothing to the products
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
     wsm[buf][wave][lane] = live ? wr[d] : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int r = rr + 128 * h;
       u32x4 hl[2];
-      XStage<bf16_t>::put(hl, xr[d][h]);
+      const float4 xv[2] = {live ? xr[d][h][0] : z, live ? xr[d][h][1] : z};
+      XStage<bf16_t>::put(hl, xv);
       const int l = (r & 15) + 16 * g;
       xsm[buf][r >> 4][0][l] = hl[0];
       xsm[buf][r >> 4][1][l] = hl[1];
