@@ -169,3 +169,21 @@ def test_target_entry_points_validation():
     assert st == bd.DOMINO_ERR_INVALID_ARG and "model" in bd.last_error()
     st = lib.domino_target_commit(None, 1, 16, 15, p, p, p, p, p, 1024, p, p, None)
     assert st == bd.DOMINO_ERR_INVALID_ARG
+
+
+def test_appended_rows_must_match_the_context_width():
+    # host-side check before any launch: fused configs take k*d-wide fp32 rows
+    import types
+    import torch
+    cfg = types.SimpleNamespace(hidden=64, ctx_fuse_layers=3)
+    model = types.SimpleNamespace(cfg=cfg)
+    ok = torch.zeros(2, 5, 192, dtype=torch.float32)
+    bd._check_ctx_hidden(model, 2, ok, 5)
+    bd._check_ctx_hidden(model, 2, None, 0)
+    for bad in (torch.zeros(2, 5, 64, dtype=torch.float32),      # d-wide rows for a fused config
+                torch.zeros(2, 5, 192, dtype=torch.float64),     # wrong dtype
+                torch.zeros(2, 192, 5, dtype=torch.float32).transpose(1, 2)):  # not contiguous
+        with pytest.raises(bd.DominoError):
+            bd._check_ctx_hidden(model, 2, bad, 5)
+    cfg0 = types.SimpleNamespace(hidden=64, ctx_fuse_layers=0)
+    bd._check_ctx_hidden(types.SimpleNamespace(cfg=cfg0), 2, torch.zeros(2, 5, 64), 5)
