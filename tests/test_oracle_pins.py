@@ -465,3 +465,64 @@ def test_context_fusion_equal_weights_is_the_mean_of_layers():
     r, r2 = _fused_vs_plain(3, [np.eye(d) / 3] * 3, lambda b: (b[0] + b[1] + b[2]) / 3)
     np.testing.assert_allclose(r["base_logits"], r2["base_logits"], rtol=1e-11, atol=1e-12)
     np.testing.assert_allclose(r["final_logits"], r2["final_logits"], rtol=1e-11, atol=1e-12)
+
+
+# ---------------------------------------------------------------- SiLU, the correction and SwiGLU
+# Logistic values written out to 16 digits: sigma(1) = 1 / (1 + e^-1),
+# sigma(2) = 1 / (1 + e^-2), sigma(-1) = 1 - sigma(1).
+SIGMA_1 = 0.7310585786300049
+SIGMA_2 = 0.8807970779778823
+SIGMA_M1 = 0.2689414213699951
+
+
+def test_silu_matches_torch_and_closed_forms():
+    # SiLU(x) = x * sigma(x) (the correction equation of Sec. 4.1.2 and the FFN's gate)
+    x = np.linspace(-30.0, 30.0, 241)
+    want = torch.nn.functional.silu(torch.from_numpy(x)).numpy()
+    np.testing.assert_allclose(O.silu(x), want, rtol=1e-14, atol=1e-300)
+    assert O.silu(np.array([0.0]))[0] == 0.0
+    np.testing.assert_allclose(O.silu(np.array([1.0, 2.0, -1.0])), [SIGMA_1, 2 * SIGMA_2, -SIGMA_M1], rtol=1e-15)
+    # SiLU(x) -> x for large x, -> 0 from below for very negative x
+    np.testing.assert_allclose(O.silu(np.array([40.0]))[0], 40.0, rtol=1e-15)
+    v = O.silu(np.array([-40.0]))[0]
+    assert v < 0 and abs(v) < 1e-15
+
+
+def test_correction_closed_form_with_selector_rows():
+    # W1 rows pick single entries of [H; S], W2 mixes the two rank rows, so
+    # dL = W2 SiLU(W1 [H; S]) is known by hand: pre-activations (1, -1) give
+    # u = (sigma(1), -sigma(-1)).  Sigmoid in place of SiLU, or no activation,
+    # gives other values.
+    d, ds = 2, 2
+    w1 = np.zeros((2, d + ds))
+    w1[0, 0] = 1.0          # u_0 from H_0
+    w1[1, d + 1] = 2.0      # u_1 from 2 * S_1
+    w2 = np.array([[1.0, 0.0], [0.0, 1.0], [1.0, 1.0]])
+    h = np.array([1.0, 5.0])
+    s = np.array([7.0, -0.5])
+    got = O.correction({"w1": w1, "w2": w2}, h, s)
+    np.testing.assert_allclose(got, [SIGMA_1, -SIGMA_M1, SIGMA_1 - SIGMA_M1], rtol=1e-15)
+
+
+def test_swiglu_ffn_closed_form():
+    # One layer with W_o = 0 (attention adds nothing) and a hand-built FFN:
+    # x = (1, -1, 1, -1) has unit RMS, so with eps 0 and unit gains the FFN
+    # input is x itself.  Unit 0: gate 2*y_0 = 2, up y_1 = -1 -> SiLU(2) * -1;
+    # unit 1: gate y_1 = -1, up 3*y_2 = 3 -> SiLU(-1) * 3.  W_down sends unit 0
+    # to column 0 and unit 1 to column 3.  Swapping gate and up, or sigmoid in
+    # place of SiLU, changes both columns.
+    from types import SimpleNamespace
+    cfg = SimpleNamespace(n_q_heads=1, n_kv_heads=1, head_dim=4, rms_eps=0.0, rope_theta=1e6)
+    rng = np.random.default_rng(21)
+    d, ffn = 4, 2
+    wg = np.zeros((ffn, d)); wg[0, 0] = 2.0; wg[1, 1] = 1.0
+    wu = np.zeros((ffn, d)); wu[0, 1] = 1.0; wu[1, 2] = 3.0
+    wd = np.zeros((d, ffn)); wd[0, 0] = 1.0; wd[3, 1] = 1.0
+    lw = {"attn_norm": np.ones(d), "wq": rng.standard_normal((4, d)), "wk": rng.standard_normal((4, d)),
+          "wv": rng.standard_normal((4, d)), "q_norm": np.ones(4), "k_norm": np.ones(4), "wo": np.zeros((d, 4)),
+          "ffn_norm": np.ones(d), "w_gate": wg, "w_up": wu, "w_down": wd}
+    x = np.array([[1.0, -1.0, 1.0, -1.0]])
+    empty = np.zeros((0, 1, 4))
+    got = O.backbone_layer(cfg, lw, x, np.array([0.0]), empty, empty)
+    want = [1.0 - 2 * SIGMA_2, -1.0, 1.0, -1.0 - 3 * SIGMA_M1]
+    np.testing.assert_allclose(got[0], want, rtol=1e-15, atol=1e-15)
