@@ -287,7 +287,12 @@ domino_status domino_target_commit(domino_model_t target, int32_t batch, int32_t
 
 /*
  * Draft tree from the per-position top-beta tokens (spine-and-leaves, BFS
- * order).  Node 0 is the anchor (parent -1, depth 0, position n_b); node
+ * order).  The paper names tree construction as one cost of a draft step (the
+ * caption of Fig. 1, beside Draft, LM Head and DHead) without defining the
+ * tree, and runs Domino itself as a single block (Table 1), which is the
+ * branch = 1 chain below.  The shape for branch > 1 is this library's reading:
+ * the branch top-ranked tokens of every depth, only the rank-0 token having
+ * children.  Node 0 is the anchor (parent -1, depth 0, position n_b); node
  * 1 + (d-1)*branch + rho holds topk_ids[b][d-1][rho] at depth d, position
  * n_b + d, with parent 0 for d = 1 and 1 + (d-2)*branch (the rank-0 node one
  * level up) otherwise.  ancestor_mask[b][i][k] = 1 iff k is i or an ancestor
@@ -399,6 +404,18 @@ domino_status domino_profile_reset(domino_model_t m);
  * to the model's later draft steps.
  */
 domino_status domino_debug_set_poll_limit(domino_model_t m, int32_t polls);
+
+/*
+ * Which execution paths the model's last draft step (greedy, sampled or
+ * training forward) launched, as DOMINO_PATH_* bits, so that tests can check
+ * that a shape took the path they mean to cover.  Recorded on the host at
+ * launch time; 0 before the first step.
+ */
+enum {
+  DOMINO_PATH_PERSISTENT_ROLLOUT = 1,  /* the whole rollout as one persistent launch */
+  DOMINO_PATH_PERSISTENT_BACKBONE = 2  /* the whole backbone as one persistent launch */
+};
+domino_status domino_debug_last_paths(domino_model_t m, uint32_t *paths);
 
 #ifdef __cplusplus
 }

@@ -86,6 +86,7 @@ def load() -> C.CDLL:
         "domino_profile_read": (i32, [P, i32, C.POINTER(C.c_double), C.POINTER(i32)]),
         "domino_profile_reset": (i32, [P]),
         "domino_debug_set_poll_limit": (i32, [P, i32]),
+        "domino_debug_last_paths": (i32, [P, C.POINTER(u32)]),
         "domino_draft_step_sampled": (i32, [P, i32, P, P, P, P, i32, P, i32, C.c_float, C.c_uint64, P, P, P, P,
                                             C.POINTER(domino_debug), P, sz, P]),
         "domino_verify_sample_workspace_bytes": (sz, [i32, i32, i32]),
@@ -116,7 +117,7 @@ def exported_symbols():
             "domino_draft_step_sampled", "domino_verify_sample_workspace_bytes", "domino_verify_sample",
             "domino_philox4x32_10", "domino_train_workspace_bytes", "domino_train_forward",
             "domino_target_create", "domino_target_workspace_bytes", "domino_target_verify", "domino_target_commit",
-            "domino_debug_set_poll_limit"]
+            "domino_debug_set_poll_limit", "domino_debug_last_paths"]
 
 
 def last_error() -> str:
@@ -363,6 +364,17 @@ def domino_debug_set_poll_limit(model: DominoModel, polls: int):
     """Test hook: polls a persistent-rollout wait makes before it gives up (0:
     every wait gives up at once; negative: the default)."""
     _check(load().domino_debug_set_poll_limit(model.handle, int(polls)))
+
+
+PATH_PERSISTENT_ROLLOUT = 1
+PATH_PERSISTENT_BACKBONE = 2
+
+
+def domino_debug_last_paths(model: DominoModel) -> int:
+    """DOMINO_PATH_* bits of the execution paths the model's last draft step launched."""
+    v = C.c_uint32(0)
+    _check(load().domino_debug_last_paths(model.handle, C.byref(v)))
+    return int(v.value)
 
 
 def domino_profile_read(model: DominoModel, cls: str):

@@ -62,6 +62,7 @@ struct domino_model {
   bool has_head = true;  // false: a target decoder (layers, embedding, LM head only)
   bool persistent = true;  // DOMINO_ROLLOUT=loop selects the launch-pair rollout everywhere
   uint32_t poll_limit = kDefaultPollLimit;  // persistent rollout: polls a wait makes before it gives up
+  uint32_t last_paths = 0;  // DOMINO_PATH_* bits of the last draft step
   Packed lm, w2, w1s;
   int fuse_k = 0;  // context fusion: appended rows are fuse_k*d wide, fused by fc
   Packed fc;
@@ -783,6 +784,7 @@ domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *an
 
   hipStream_t st = (hipStream_t)stream;
   char *ws = (char *)workspace;
+  m->last_paths = 0;
   s = run_backbone(m, batch, anchor_ids, ctx_lens, ctx_k, ctx_v, max_ctx, ctx_hidden_new, n_new, debug, ws, w, st);
   if (s != DOMINO_OK) return s;
 
@@ -797,7 +799,8 @@ domino_status draft_step_impl(domino_model_t m, int32_t batch, const int32_t *an
   hipError_t he = hipSuccess;
   // one persistent launch for the whole rollout where it applies, else a
   // launch pair per position
-  if (!m->persistent || !launch_head_persistent(h, m->n_cu, st)) he = launch_head(h, st);
+  if (m->persistent && launch_head_persistent(h, m->n_cu, st)) m->last_paths |= DOMINO_PATH_PERSISTENT_ROLLOUT;
+  else he = launch_head(h, st);
   prof_end(m, DOMINO_KC_HEADLOOP, st);
   if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "head loop launch: %s", hipGetErrorString(he));
   he = hipGetLastError();
@@ -889,6 +892,7 @@ domino_status domino_train_forward(domino_model_t m, int32_t batch, const int32_
   const WsLayout &w = tl.w;
   const Dims D = make_dims(m, batch);
   const int depth = D.B - 1, Mr = batch * depth;
+  m->last_paths = 0;
   if (!m->side) {
     HIP_TRY(hipStreamCreateWithFlags(&m->side, hipStreamNonBlocking));
     HIP_TRY(hipEventCreateWithFlags(&m->fork, hipEventDisableTiming));
@@ -1149,6 +1153,12 @@ domino_status domino_profile_enable(domino_model_t m, uint32_t class_mask) {
 domino_status domino_profile_reset(domino_model_t m) {
   if (!m) return fail(DOMINO_ERR_INVALID_ARG, "model is NULL");
   for (auto &e : m->ev) e.used = 0;
+  return DOMINO_OK;
+}
+
+domino_status domino_debug_last_paths(domino_model_t m, uint32_t *paths) {
+  if (!m || !paths) return fail(DOMINO_ERR_INVALID_ARG, "NULL argument");
+  *paths = m->last_paths;
   return DOMINO_OK;
 }
 

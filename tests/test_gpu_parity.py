@@ -371,21 +371,30 @@ def persistent_config(batch):
 @pytest.mark.parametrize("batch", [1, 2])
 def test_persistent_rollout_matches_launch_pair_rollout(batch, monkeypatch):
     """bf16, r = 256, one or two batch rows, greedy: the rollout runs as one
-    cooperative launch with the W2 slice held on chip.  It must agree with the
-    launch-pair rollout (DOMINO_ROLLOUT=loop at model creation): the backbone
-    outputs bit for bit, states and logits to fp32 summation order, the drafted
-    tokens exactly away from near-ties; free-running and teacher-forced."""
+    persistent launch (an ordinary launch after an occupancy check) with the W2
+    slice held on chip.  It must agree with the launch-pair rollout
+    (DOMINO_ROLLOUT=loop at model creation): the backbone outputs bit for bit,
+    states and logits to fp32 summation order, the drafted tokens exactly away
+    from near-ties; free-running and teacher-forced.  Each run checks which
+    rollout path its steps took, so neither side can silently be the other."""
+    from paper_2605_29707_amd import binding as bd
     cfg = persistent_config(batch)
     w = synth.make_weights(cfg, seed=21, gain_std=0.1)
     inp = synth.make_inputs(cfg, seed=21)
     f = synth.make_forced_tokens(cfg, seed=21)
     monkeypatch.delenv("DOMINO_ROLLOUT", raising=False)
     run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
-    a, af = run.step(inp), run.step(inp, forced=f)
+    a = run.step(inp)
+    assert bd.domino_debug_last_paths(run.model) & bd.PATH_PERSISTENT_ROLLOUT
+    af = run.step(inp, forced=f)
+    assert bd.domino_debug_last_paths(run.model) & bd.PATH_PERSISTENT_ROLLOUT
     run.close()
     monkeypatch.setenv("DOMINO_ROLLOUT", "loop")
     run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
-    b, bf = run.step(inp), run.step(inp, forced=f)
+    b = run.step(inp)
+    assert not bd.domino_debug_last_paths(run.model) & bd.PATH_PERSISTENT_ROLLOUT
+    bf = run.step(inp, forced=f)
+    assert not bd.domino_debug_last_paths(run.model) & bd.PATH_PERSISTENT_ROLLOUT
     run.close()
     for x, y, forced in ((a, b, False), (af, bf, True)):
         assert x["err"] == 0 and y["err"] == 0
@@ -427,6 +436,7 @@ def test_persistent_rollout_wait_gives_up_then_recovers():
     run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
     good = run.step(inp)
     assert good["err"] == 0
+    assert bd.domino_debug_last_paths(run.model) & bd.PATH_PERSISTENT_ROLLOUT
     bd.domino_debug_set_poll_limit(run.model, 0)
     bad = run.step(inp)
     log(f"forced timeout: error word {bad['err']:#x}")
