@@ -330,6 +330,28 @@ domino_status domino_verify_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                                    int32_t *out_tokens, void *workspace, size_t workspace_bytes,
                                    void *stream);
 
+/*
+ * Greedy acceptance exactly as domino_verify_accept, for callers that cannot
+ * allocate or hand over a workspace (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation).  It calls no allocating
+ * routine: its argmax partials live in a fixed device array of
+ * DOMINO_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends.  batch * n_nodes * ceil(vocab / 4096) * 8 bytes must
+ * fit in it (e.g. batch 32 x 61 nodes at vocab 151936: 593 KB), else
+ * DOMINO_ERR_UNSUPPORTED before any launch.  Every call on a GPU shares that
+ * GPU's array, so calls that overlap on one GPU (other streams, other threads)
+ * race and must be serialised by the caller.
+ *  error_word  device int32 [1]: cleared by the call's first kernel, then
+ *              DOMINO_DEV_BAD_TREE if a node_parent entry is not an earlier node
+ *  other arguments as domino_verify_accept
+ */
+#define DOMINO_NOALLOC_SCRATCH_BYTES (4u << 20)
+domino_status domino_verify_accept_noalloc(int32_t batch, int32_t n_nodes, int32_t vocab, int32_t block,
+                                           const int32_t *node_token, const int32_t *node_parent,
+                                           const void *target_logits, domino_dtype logits_dtype,
+                                           int32_t *accept_len, int32_t *accepted_nodes, int32_t *out_tokens,
+                                           int32_t *error_word, void *stream);
+
 /* Workspace bytes for domino_verify_sample. */
 size_t domino_verify_sample_workspace_bytes(int32_t batch, int32_t block, int32_t vocab);
 

@@ -87,6 +87,7 @@ def load() -> C.CDLL:
         "domino_profile_reset": (i32, [P]),
         "domino_debug_set_poll_limit": (i32, [P, i32]),
         "domino_debug_last_paths": (i32, [P, C.POINTER(u32)]),
+        "domino_verify_accept_noalloc": (i32, [i32, i32, i32, i32, P, P, P, C.c_int, P, P, P, P, P]),
         "domino_draft_step_sampled": (i32, [P, i32, P, P, P, P, i32, P, i32, C.c_float, C.c_uint64, P, P, P, P,
                                             C.POINTER(domino_debug), P, sz, P]),
         "domino_verify_sample_workspace_bytes": (sz, [i32, i32, i32]),
@@ -117,7 +118,7 @@ def exported_symbols():
             "domino_draft_step_sampled", "domino_verify_sample_workspace_bytes", "domino_verify_sample",
             "domino_philox4x32_10", "domino_train_workspace_bytes", "domino_train_forward",
             "domino_target_create", "domino_target_workspace_bytes", "domino_target_verify", "domino_target_commit",
-            "domino_debug_set_poll_limit", "domino_debug_last_paths"]
+            "domino_debug_set_poll_limit", "domino_debug_last_paths", "domino_verify_accept_noalloc"]
 
 
 def last_error() -> str:
@@ -339,6 +340,21 @@ def domino_verify_accept(node_token, node_parent, target_logits, block, accept_l
                                        _ptr(target_logits), dt, _ptr(accept_len), _ptr(accepted_nodes),
                                        _ptr(out_tokens), _ptr(workspace),
                                        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 4 << 20
+
+
+def domino_verify_accept_noalloc(node_token, node_parent, target_logits, block, accept_len, accepted_nodes,
+                                 out_tokens, error_word, stream=None):
+    """Greedy acceptance without a workspace (the library's fixed per-GPU scratch);
+    error_word is a device int32 [1] output."""
+    import torch
+    bs, nn, V = target_logits.shape
+    dt = DOMINO_BF16 if target_logits.dtype == torch.bfloat16 else DOMINO_F32
+    _check(load().domino_verify_accept_noalloc(bs, nn, V, int(block), _ptr(node_token), _ptr(node_parent),
+                                               _ptr(target_logits), dt, _ptr(accept_len), _ptr(accepted_nodes),
+                                               _ptr(out_tokens), _ptr(error_word), _stream(stream)))
 
 
 def domino_workspace_error(workspace, stream=None) -> int:

@@ -9,6 +9,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1075,6 +1076,66 @@ domino_status domino_verify_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                 accept_len, accepted_nodes, out_tokens, workspace, st);
   hipError_t he = hipGetLastError();
   if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "verify_accept launch: %s", hipGetErrorString(he));
+  return DOMINO_OK;
+}
+
+// ---- acceptance without a workspace: the argmax partials live in a fixed
+// device array, one copy per GPU, held until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it is only a stand-in for the
+// symbol); it uses the address hipGetSymbolAddress returns for the current
+// device, looked up once per device.
+namespace {
+constexpr size_t kNoAllocScratchBytes = (size_t)DOMINO_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+domino_status scratch_for_current_device(void **out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(DOMINO_ERR_UNSUPPORTED, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(DOMINO_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DOMINO_OK;
+}
+}  // namespace
+
+domino_status domino_verify_accept_noalloc(int32_t batch, int32_t n_nodes, int32_t vocab, int32_t block,
+                                           const int32_t *node_token, const int32_t *node_parent,
+                                           const void *target_logits, domino_dtype logits_dtype,
+                                           int32_t *accept_len, int32_t *accepted_nodes, int32_t *out_tokens,
+                                           int32_t *error_word, void *stream) {
+  if (batch < 1) return fail(DOMINO_ERR_INVALID_ARG, "batch must be >= 1");
+  if (n_nodes < 1 || n_nodes > 1024) return fail(DOMINO_ERR_INVALID_ARG, "n_nodes must be in [1, 1024]");
+  if (vocab < 1) return fail(DOMINO_ERR_INVALID_ARG, "vocab must be >= 1");
+  if (block < 2 || block > 64) return fail(DOMINO_ERR_INVALID_ARG, "block must be in [2, 64]");
+  if (logits_dtype != DOMINO_F32 && logits_dtype != DOMINO_BF16) return fail(DOMINO_ERR_INVALID_ARG, "bad logits dtype");
+  if (!node_token || !node_parent || !target_logits || !accept_len || !accepted_nodes || !out_tokens || !error_word)
+    return fail(DOMINO_ERR_INVALID_ARG, "a required pointer is NULL");
+  const size_t ent = accept_part_entries(batch, n_nodes, vocab);
+  if (ent * 8 > kNoAllocScratchBytes)
+    return fail(DOMINO_ERR_UNSUPPORTED,
+                "batch %d x %d nodes x vocab %d needs %zu bytes of argmax partials; the fixed scratch holds %zu "
+                "(use domino_verify_accept with a workspace)",
+                batch, n_nodes, vocab, ent * 8, kNoAllocScratchBytes);
+  void *sp = nullptr;
+  domino_status s = scratch_for_current_device(&sp);
+  if (s != DOMINO_OK) return s;
+  float *pv = (float *)sp;
+  launch_accept_parts(batch, n_nodes, vocab, block, node_token, node_parent, target_logits,
+                      logits_dtype == DOMINO_BF16, accept_len, accepted_nodes, out_tokens, pv,
+                      (int32_t *)(pv + ent), error_word, (hipStream_t)stream);
+  hipError_t he = hipGetLastError();
+  if (he != hipSuccess) return fail(DOMINO_ERR_HIP, "verify_accept_noalloc launch: %s", hipGetErrorString(he));
   return DOMINO_OK;
 }
 

@@ -193,6 +193,12 @@ size_t accept_ws_bytes(int bs, int nn, int V);
 void launch_accept(int bs, int nn, int V, int B, const int32_t *tok, const int32_t *par,
                    const void *logits, bool bf16, int32_t *acc_len, int32_t *acc_nodes,
                    int32_t *out_tok, void *ws, hipStream_t st);
+// the same launches with the argmax partials (accept_part_entries values pv and
+// as many ids pi) and the error word (cleared by the first launch) given apart
+size_t accept_part_entries(int bs, int nn, int V);
+void launch_accept_parts(int bs, int nn, int V, int B, const int32_t *tok, const int32_t *par,
+                         const void *logits, bool bf16, int32_t *acc_len, int32_t *acc_nodes,
+                         int32_t *out_tok, float *pv, int32_t *pi, int32_t *err, hipStream_t st);
 
 // ---- temperature sampling: speculative-sampling verification (sample.hip)
 size_t vs_ws_bytes(int bs, int B, int V);

@@ -197,14 +197,21 @@ __global__ __launch_bounds__(256) void accept_walk_kernel(int nn, int V, int B, 
   for (int q = a + threadIdx.x; q < B - 1; q += blockDim.x) acc_nodes[(size_t)b * (B - 1) + q] = -1;
 }
 
+size_t accept_part_entries(int bs, int nn, int V) { return (size_t)bs * nn * ((V + ACH - 1) / ACH); }
+
 void launch_accept(int bs, int nn, int V, int B, const int32_t *tok, const int32_t *par,
                    const void *logits, bool bf16, int32_t *acc_len, int32_t *acc_nodes,
                    int32_t *out_tok, void *ws, hipStream_t st) {
   unsigned char *w = (unsigned char *)ws;
-  int32_t *err = (int32_t *)w;
-  const int nch = (V + ACH - 1) / ACH;
   float *pv = (float *)(w + acc_part_off());
-  int32_t *pi = (int32_t *)(pv + (size_t)bs * nn * nch);
+  launch_accept_parts(bs, nn, V, B, tok, par, logits, bf16, acc_len, acc_nodes, out_tok, pv,
+                      (int32_t *)(pv + accept_part_entries(bs, nn, V)), (int32_t *)w, st);
+}
+
+void launch_accept_parts(int bs, int nn, int V, int B, const int32_t *tok, const int32_t *par,
+                         const void *logits, bool bf16, int32_t *acc_len, int32_t *acc_nodes,
+                         int32_t *out_tok, float *pv, int32_t *pi, int32_t *err, hipStream_t st) {
+  const int nch = (V + ACH - 1) / ACH;
   dim3 grid(nch, nn, bs);
   if (bf16)
     hipLaunchKernelGGL(argmax_partial_kernel<bf16_t>, grid, dim3(256), 0, st, nn, V, (const bf16_t *)logits, pv, pi,

@@ -187,3 +187,16 @@ def test_appended_rows_must_match_the_context_width():
             bd._check_ctx_hidden(model, 2, bad, 5)
     cfg0 = types.SimpleNamespace(hidden=64, ctx_fuse_layers=0)
     bd._check_ctx_hidden(types.SimpleNamespace(cfg=cfg0), 2, torch.zeros(2, 5, 64), 5)
+
+
+def test_noalloc_accept_rejects_sizes_beyond_its_scratch():
+    """domino_verify_accept_noalloc checks the argmax partials against its fixed
+    scratch before any HIP call: 64 rows x 1024 nodes x 38 vocabulary chunks x 8
+    bytes (19.9 MB) exceed DOMINO_NOALLOC_SCRATCH_BYTES."""
+    lib = bd.load()
+    p = 16  # never dereferenced: the size check comes first
+    st = lib.domino_verify_accept_noalloc(64, 1024, 151936, 16, p, p, p, bd.DOMINO_BF16, p, p, p, p, None)
+    assert st == bd.DOMINO_ERR_UNSUPPORTED
+    assert "scratch" in bd.last_error()
+    assert lib.domino_verify_accept_noalloc(1, 16, 100, 16, p, p, p, bd.DOMINO_F32, p, p, p, None, None) == \
+        bd.DOMINO_ERR_INVALID_ARG
