@@ -434,8 +434,7 @@ domino_status domino_debug_set_poll_limit(domino_model_t m, int32_t polls);
  * launch time; 0 before the first step.
  */
 enum {
-  DOMINO_PATH_PERSISTENT_ROLLOUT = 1,  /* the whole rollout as one persistent launch */
-  DOMINO_PATH_PERSISTENT_BACKBONE = 2  /* the whole backbone as one persistent launch */
+  DOMINO_PATH_PERSISTENT_ROLLOUT = 1  /* the whole rollout as one persistent launch */
 };
 domino_status domino_debug_last_paths(domino_model_t m, uint32_t *paths);
 

@@ -383,7 +383,6 @@ def domino_debug_set_poll_limit(model: DominoModel, polls: int):
 
 
 PATH_PERSISTENT_ROLLOUT = 1
-PATH_PERSISTENT_BACKBONE = 2
 
 
 def domino_debug_last_paths(model: DominoModel) -> int:

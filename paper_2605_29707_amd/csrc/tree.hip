@@ -59,10 +59,12 @@ void launch_build_tree(int bs, int depth, int beta, const int32_t *topk, const i
 }
 
 // ---------------------------------------------------------------------------
-// acceptance: two launches.  (1) the argmax of every node row, split into
-// vocabulary chunks (all rows, so the walk never scans a row itself; a leaf
-// row costs one more pass over V values, read once); (2) one workgroup per
-// batch row checks the tree and walks it from the root.
+// acceptance: two launches.  (1) the argmax of the rows of nodes that have
+// children (the walk can only continue from those), split into vocabulary
+// chunks; (2) one workgroup per batch row checks the tree and walks it from
+// the root.  When the walk stops on a node without children (a leaf of a
+// tree, or the end of a fully accepted chain) the bonus token is that row's
+// argmax, which the walk's workgroup scans itself: one row, and only then.
 // workspace: [err:int32][pad to 256 B][partials: (float,int) bs*nn*nchunk]
 // ---------------------------------------------------------------------------
 constexpr int ACH = 4096;  // vocabulary elements per argmax chunk
@@ -88,10 +90,15 @@ DEVI float ld_logit<bf16_t>(const bf16_t *p) {
 // also clears the error word (only the walk, a later launch, raises errors).
 template <typename LT>
 __global__ __launch_bounds__(256) void argmax_partial_kernel(int nn, int V, const LT *__restrict__ logits,
-                                                             float *part_v, int32_t *part_i, int32_t *err) {
+                                                             const int32_t *__restrict__ par, float *part_v,
+                                                             int32_t *part_i, int32_t *err) {
   const int ch = blockIdx.x, m = blockIdx.y, b = blockIdx.z;
   const int nch = gridDim.x;
   if ((ch | m | b) == 0 && threadIdx.x == 0) *err = 0;
+  // rows of nodes without children are left to the walk (children come after their parent)
+  bool has_child = false;
+  for (int c = m + 1 + (int)threadIdx.x; c < nn; c += blockDim.x) has_child |= par[(size_t)b * nn + c] == m;
+  if (!__syncthreads_or(has_child)) return;
   const LT *row = logits + ((size_t)b * nn + m) * V;
   const int v0 = ch * ACH, v1 = min(V, v0 + ACH);
   // ACH / 256 = 16 values per thread, loaded together at clamped addresses
@@ -130,10 +137,12 @@ __global__ __launch_bounds__(256) void argmax_partial_kernel(int nn, int V, cons
   }
 }
 
+template <typename LT>
 __global__ __launch_bounds__(256) void accept_walk_kernel(int nn, int V, int B, const int32_t *__restrict__ tok,
                                                           const int32_t *__restrict__ par,
                                                           const float *__restrict__ part_v,
                                                           const int32_t *__restrict__ part_i,
+                                                          const LT *__restrict__ logits,
                                                           int32_t *acc_len, int32_t *acc_nodes,
                                                           int32_t *out_tok, int32_t *err) {
   const int b = blockIdx.x;
@@ -149,15 +158,39 @@ __global__ __launch_bounds__(256) void accept_walk_kernel(int nn, int V, int B, 
   int cur = 0, a = 0;
   int R = 0;
   while (true) {
-    // R = argmax of row cur, from its chunk partials
+    // R = argmax of row cur: from its chunk partials when cur has children
+    // (the partial launch took exactly those rows), else by a scan of the row
+    bool has_child = false;
+    for (int c = cur + 1 + (int)threadIdx.x; c < nn; c += blockDim.x) has_child |= par[(size_t)b * nn + c] == cur;
+    has_child = __syncthreads_or(has_child);
     float bv = -INFINITY;
     int bi = INT_MAX;
-    const size_t o = ((size_t)b * nn + cur) * nch;
-    for (int c = threadIdx.x; c < nch; c += blockDim.x)
-      if (better(part_v[o + c], part_i[o + c], bv, bi)) {
-        bv = part_v[o + c];
-        bi = part_i[o + c];
+    if (has_child) {
+      const size_t o = ((size_t)b * nn + cur) * nch;
+      for (int c = threadIdx.x; c < nch; c += blockDim.x)
+        if (better(part_v[o + c], part_i[o + c], bv, bi)) {
+          bv = part_v[o + c];
+          bi = part_i[o + c];
+        }
+    } else {
+      // ids visited in increasing order per thread: a strict > keeps the smallest id
+      const LT *row = logits + ((size_t)b * nn + cur) * V;
+      constexpr int PER = 16;
+      for (int v0 = threadIdx.x; v0 < V; v0 += 256 * PER) {
+        float x[PER];
+#pragma unroll
+        for (int q = 0; q < PER; ++q) x[q] = ld_logit<LT>(row + min(v0 + q * 256, V - 1));
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+          const int v = v0 + q * 256;
+          const float ov = order_val(x[q]);
+          if (v < V && (ov > bv || bi == INT_MAX)) {
+            bv = ov;
+            bi = v;
+          }
+        }
       }
+    }
     wave_best(bv, bi);
     if ((threadIdx.x & 63) == 0) {
       sv[threadIdx.x >> 6] = bv;
@@ -213,14 +246,17 @@ void launch_accept_parts(int bs, int nn, int V, int B, const int32_t *tok, const
                          int32_t *out_tok, float *pv, int32_t *pi, int32_t *err, hipStream_t st) {
   const int nch = (V + ACH - 1) / ACH;
   dim3 grid(nch, nn, bs);
-  if (bf16)
-    hipLaunchKernelGGL(argmax_partial_kernel<bf16_t>, grid, dim3(256), 0, st, nn, V, (const bf16_t *)logits, pv, pi,
-                       err);
-  else
-    hipLaunchKernelGGL(argmax_partial_kernel<float>, grid, dim3(256), 0, st, nn, V, (const float *)logits, pv, pi,
-                       err);
-  hipLaunchKernelGGL(accept_walk_kernel, dim3(bs), dim3(256), 0, st, nn, V, B, tok, par, pv, pi, acc_len, acc_nodes,
-                     out_tok, err);
+  if (bf16) {
+    hipLaunchKernelGGL(argmax_partial_kernel<bf16_t>, grid, dim3(256), 0, st, nn, V, (const bf16_t *)logits, par, pv,
+                       pi, err);
+    hipLaunchKernelGGL(accept_walk_kernel<bf16_t>, dim3(bs), dim3(256), 0, st, nn, V, B, tok, par, pv, pi,
+                       (const bf16_t *)logits, acc_len, acc_nodes, out_tok, err);
+  } else {
+    hipLaunchKernelGGL(argmax_partial_kernel<float>, grid, dim3(256), 0, st, nn, V, (const float *)logits, par, pv,
+                       pi, err);
+    hipLaunchKernelGGL(accept_walk_kernel<float>, dim3(bs), dim3(256), 0, st, nn, V, B, tok, par, pv, pi,
+                       (const float *)logits, acc_len, acc_nodes, out_tok, err);
+  }
 }
 
 }  // namespace dk

@@ -20,8 +20,10 @@ if not torch.cuda.is_available():
     pytest.skip("no GPU", allow_module_level=True)
 
 
-def oracle_for(cfg, w64, inp, gpu, beta, lens=None):
-    drafted = gpu["topk_ids"][:, :, 0]
+def oracle_for(cfg, w64, inp, gpu, beta, lens=None, forced=None):
+    """The oracle teacher-forced on the tokens the GPU step fed back: its own
+    top-1 tokens, or `forced` when the GPU step was forced."""
+    drafted = gpu["topk_ids"][:, :, 0] if forced is None else forced
     return oracle.draft_step(cfg, w64, inp["anchor"], inp["ctx_lens"] if lens is None else lens,
                              inp["ctx_k"], inp["ctx_v"], beta, forced=drafted,
                              ctx_hidden=inp.get("ctx_hidden"))
@@ -271,6 +273,12 @@ def test_verify_accept_bit_exact(beta, dtype, kind):
                 row[m] = mx
                 row[(m + 17) % V] = mx
                 row[5] = np.nan
+                # every other row (leaves included, whose argmax the walk scans itself) gets a
+                # second copy of its maximum
+                for node in range(1, lg.shape[1]):
+                    r2 = lg[b, node]
+                    k = int(np.nanargmax(r2))
+                    r2[(k + 17) % V] = r2[k]
         t_dt = torch.bfloat16 if dtype == "bf16" else torch.float32
         lt = torch.from_numpy(lg).to("cuda:0").to(t_dt)
         got = _accept_gpu(tree["node_token"], tree["node_parent"], lt, cfg.block)
@@ -338,9 +346,11 @@ def test_qwen3_8b_bs1_full_size_parity():
     w = synth.make_weights(cfg, seed=0)
     inp = synth.make_inputs(cfg, seed=0)
     log("uploading + packing")
+    from paper_2605_29707_amd import binding as bd
     run = GpuRun(cfg, w, inp["max_ctx"], beta=1)
     plain = run.step(inp, debug=False)
     log("gpu step done")
+    assert bd.domino_debug_last_paths(run.model) & bd.PATH_PERSISTENT_ROLLOUT
     gpu = run.step(inp, debug=True)
     np.testing.assert_array_equal(plain["topk_ids"], gpu["topk_ids"])
     np.testing.assert_array_equal(plain["topk_vals"], gpu["topk_vals"])
@@ -447,3 +457,4 @@ def test_persistent_rollout_wait_gives_up_then_recovers():
     assert again["err"] == 0
     for k in ("topk_ids", "topk_vals", "final_logits", "states"):
         np.testing.assert_array_equal(again[k], good[k], err_msg=k)
+
