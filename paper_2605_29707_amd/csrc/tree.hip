@@ -86,54 +86,137 @@ DEVI float ld_logit<bf16_t>(const bf16_t *p) {
   return to_f32(*p);
 }
 
-// Partial argmax of row (b, m) over one vocabulary chunk.  The first workgroup
-// also clears the error word (only the walk, a later launch, raises errors).
+// 16 bytes of logits as values: 8 bf16 or 4 fp32
 template <typename LT>
-__global__ __launch_bounds__(256) void argmax_partial_kernel(int nn, int V, const LT *__restrict__ logits,
-                                                             const int32_t *__restrict__ par, float *part_v,
-                                                             int32_t *part_i, int32_t *err) {
-  const int ch = blockIdx.x, m = blockIdx.y, b = blockIdx.z;
-  const int nch = gridDim.x;
-  if ((ch | m | b) == 0 && threadIdx.x == 0) *err = 0;
-  // rows of nodes without children are left to the walk (children come after their parent)
-  bool has_child = false;
-  for (int c = m + 1 + (int)threadIdx.x; c < nn; c += blockDim.x) has_child |= par[(size_t)b * nn + c] == m;
-  if (!__syncthreads_or(has_child)) return;
-  const LT *row = logits + ((size_t)b * nn + m) * V;
-  const int v0 = ch * ACH, v1 = min(V, v0 + ACH);
-  // ACH / 256 = 16 values per thread, loaded together at clamped addresses
-  constexpr int PER = ACH / 256;
-  float x[PER];
+struct LVec;
+template <>
+struct LVec<bf16_t> {
+  static constexpr int N = 8;
+  DEVI static float get(const u32x4 &x, int e) {
+    const uint32_t w = x[e >> 1];
+    return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+};
+template <>
+struct LVec<float> {
+  static constexpr int N = 4;
+  DEVI static float get(const u32x4 &x, int e) { return __uint_as_float(x[e]); }
+};
+
+// Fold the values of one 16-byte load (ids id0 .. id0 + N - 1, those below v1)
+// into a running best; ids grow within a thread, so a strict comparison keeps
+// the smallest id of equal values.
+template <typename LT>
+DEVI void fold_vec(const u32x4 &x, int id0, int v1, float &bv, int &bi) {
 #pragma unroll
-  for (int q = 0; q < PER; ++q) x[q] = ld_logit<LT>(row + min(v0 + (int)threadIdx.x + q * 256, v1 - 1));
-  float bv = -INFINITY;
-  int bi = INT_MAX;
-#pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    const int v = v0 + (int)threadIdx.x + q * 256;  // increasing in q: a strict > keeps the smallest id
-    const float o = v < v1 ? order_val(x[q]) : -INFINITY;
+  for (int e = 0; e < LVec<LT>::N; ++e) {
+    const int v = id0 + e;
+    const float o = order_val(LVec<LT>::get(x, e));
     if (v < v1 && (o > bv || bi == INT_MAX)) {
       bv = o;
       bi = v;
     }
   }
+}
+
+// (bv, bi) of the 256-thread workgroup: every thread gets the best
+DEVI void block_best(float &bv, int &bi, float (&sv)[4], int (&si)[4]) {
   wave_best(bv, bi);
-  __shared__ float sv[4];
-  __shared__ int si[4];
+  __syncthreads();  // the arrays may hold the previous reduction
   if ((threadIdx.x & 63) == 0) {
     sv[threadIdx.x >> 6] = bv;
     si[threadIdx.x >> 6] = bi;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int w = 1; w < 4; ++w)
-      if (better(sv[w], si[w], bv, bi)) {
-        bv = sv[w];
-        bi = si[w];
+  bv = sv[0];
+  bi = si[0];
+  for (int w = 1; w < 4; ++w)
+    if (better(sv[w], si[w], bv, bi)) {
+      bv = sv[w];
+      bi = si[w];
+    }
+}
+
+// Partial argmax of rows m0 .. m0 + kArgRows - 1 of batch row b over one
+// vocabulary chunk (one row per workgroup for small grids, several when there
+// are many node rows), for the rows of nodes that have children (the walk scans
+// another row itself if it ends there).  Rows are 16-byte aligned when V is a
+// multiple of 8 (bf16) or 4 (fp32); then every value comes from 16-byte loads,
+// all of the workgroup's rows in flight together; otherwise one value per
+// load.  The first workgroup also clears the error word (only the walk, a
+// later launch, raises errors).
+template <typename LT, int kArgRows>
+__global__ __launch_bounds__(256) void argmax_partial_kernel(int nn, int V, const LT *__restrict__ logits,
+                                                             const int32_t *__restrict__ par, float *part_v,
+                                                             int32_t *part_i, int32_t *err) {
+  constexpr int EV = LVec<LT>::N, VPT = ACH / EV / 256;  // 16-byte loads per thread and row
+  const int ch = blockIdx.x, m0 = blockIdx.y * kArgRows, b = blockIdx.z;
+  const int nch = gridDim.x, tid = threadIdx.x;
+  if ((ch | blockIdx.y | b) == 0 && tid == 0) *err = 0;
+  __shared__ int s_has[kArgRows];
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  if (tid < kArgRows) s_has[tid] = 0;
+  __syncthreads();
+  // children come after their parent
+  for (int c = m0 + 1 + tid; c < nn; c += blockDim.x) {
+    const int p = par[(size_t)b * nn + c];
+    if (p >= m0 && p < m0 + kArgRows && p < c) s_has[p - m0] = 1;
+  }
+  __syncthreads();
+  const int v0 = ch * ACH, v1 = min(V, v0 + ACH);
+  if (V % EV == 0) {
+    u32x4 x[kArgRows][VPT];
+#pragma unroll
+    for (int r = 0; r < kArgRows; ++r) {
+      if (!s_has[r] || m0 + r >= nn) continue;  // uniform: a leaf's row is not read
+      const LT *row = logits + ((size_t)b * nn + m0 + r) * V;
+#pragma unroll
+      for (int q = 0; q < VPT; ++q) {  // clamped within the row: every lane's load valid
+        const int id0 = min(v0 + (q * 256 + tid) * EV, V - EV);
+        x[r][q] = *(const u32x4 *)(row + id0);
       }
-    const size_t o = ((size_t)b * nn + m) * nch + ch;
-    part_v[o] = bv;
-    part_i[o] = bi;
+    }
+#pragma unroll
+    for (int r = 0; r < kArgRows; ++r) {
+      if (!s_has[r] || m0 + r >= nn) continue;  // uniform over the workgroup
+      float bv = -INFINITY;
+      int bi = INT_MAX;
+#pragma unroll
+      for (int q = 0; q < VPT; ++q) fold_vec<LT>(x[r][q], v0 + (q * 256 + tid) * EV, v1, bv, bi);
+      block_best(bv, bi, sv, si);
+      if (tid == 0) {
+        const size_t o = ((size_t)b * nn + m0 + r) * nch + ch;
+        part_v[o] = bv;
+        part_i[o] = bi;
+      }
+    }
+    return;
+  }
+  for (int r = 0; r < kArgRows; ++r) {
+    if (!s_has[r] || m0 + r >= nn) continue;  // uniform over the workgroup
+    const LT *row = logits + ((size_t)b * nn + m0 + r) * V;
+    constexpr int PER = ACH / 256;
+    float x[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) x[q] = ld_logit<LT>(row + min(v0 + tid + q * 256, v1 - 1));
+    float bv = -INFINITY;
+    int bi = INT_MAX;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int v = v0 + tid + q * 256;  // increasing in q: a strict > keeps the smallest id
+      const float o = v < v1 ? order_val(x[q]) : -INFINITY;
+      if (v < v1 && (o > bv || bi == INT_MAX)) {
+        bv = o;
+        bi = v;
+      }
+    }
+    block_best(bv, bi, sv, si);
+    if (tid == 0) {
+      const size_t o = ((size_t)b * nn + m0 + r) * nch + ch;
+      part_v[o] = bv;
+      part_i[o] = bi;
+    }
   }
 }
 
@@ -175,18 +258,32 @@ __global__ __launch_bounds__(256) void accept_walk_kernel(int nn, int V, int B, 
     } else {
       // ids visited in increasing order per thread: a strict > keeps the smallest id
       const LT *row = logits + ((size_t)b * nn + cur) * V;
-      constexpr int PER = 16;
-      for (int v0 = threadIdx.x; v0 < V; v0 += 256 * PER) {
-        float x[PER];
+      constexpr int EV = LVec<LT>::N, U = 16;
+      if (V % EV == 0) {  // 16-byte rows: U loads of EV values per thread in flight
+        const int nv = V / EV;
+        for (int g0 = 0; g0 < nv; g0 += 256 * U) {
+          u32x4 x[U];
 #pragma unroll
-        for (int q = 0; q < PER; ++q) x[q] = ld_logit<LT>(row + min(v0 + q * 256, V - 1));
+          for (int q = 0; q < U; ++q) x[q] = *(const u32x4 *)(row + (size_t)min(g0 + q * 256 + (int)threadIdx.x, nv - 1) * EV);
 #pragma unroll
-        for (int q = 0; q < PER; ++q) {
-          const int v = v0 + q * 256;
-          const float ov = order_val(x[q]);
-          if (v < V && (ov > bv || bi == INT_MAX)) {
-            bv = ov;
-            bi = v;
+          for (int q = 0; q < U; ++q) {
+            const int gi = g0 + q * 256 + (int)threadIdx.x;
+            fold_vec<LT>(x[q], gi * EV, gi < nv ? V : 0, bv, bi);
+          }
+        }
+      } else {
+        for (int v0 = threadIdx.x; v0 < V; v0 += 256 * U) {
+          float x[U];
+#pragma unroll
+          for (int q = 0; q < U; ++q) x[q] = ld_logit<LT>(row + min(v0 + q * 256, V - 1));
+#pragma unroll
+          for (int q = 0; q < U; ++q) {
+            const int v = v0 + q * 256;
+            const float ov = order_val(x[q]);
+            if (v < V && (ov > bv || bi == INT_MAX)) {
+              bv = ov;
+              bi = v;
+            }
           }
         }
       }
@@ -245,15 +342,28 @@ void launch_accept_parts(int bs, int nn, int V, int B, const int32_t *tok, const
                          const void *logits, bool bf16, int32_t *acc_len, int32_t *acc_nodes,
                          int32_t *out_tok, float *pv, int32_t *pi, int32_t *err, hipStream_t st) {
   const int nch = (V + ACH - 1) / ACH;
-  dim3 grid(nch, nn, bs);
+  // a workgroup per row while the grid is small; eight rows per workgroup for
+  // many rows (most of them leaves of a tree), which keeps the grid of
+  // workgroups that only find no children from dominating
+  const bool many = (long)nch * nn * bs > 4096;
+  const int rpw = many ? 8 : 1;
+  dim3 grid(nch, (nn + rpw - 1) / rpw, bs);
   if (bf16) {
-    hipLaunchKernelGGL(argmax_partial_kernel<bf16_t>, grid, dim3(256), 0, st, nn, V, (const bf16_t *)logits, par, pv,
-                       pi, err);
+    if (many)
+      hipLaunchKernelGGL((argmax_partial_kernel<bf16_t, 8>), grid, dim3(256), 0, st, nn, V, (const bf16_t *)logits,
+                         par, pv, pi, err);
+    else
+      hipLaunchKernelGGL((argmax_partial_kernel<bf16_t, 1>), grid, dim3(256), 0, st, nn, V, (const bf16_t *)logits,
+                         par, pv, pi, err);
     hipLaunchKernelGGL(accept_walk_kernel<bf16_t>, dim3(bs), dim3(256), 0, st, nn, V, B, tok, par, pv, pi,
                        (const bf16_t *)logits, acc_len, acc_nodes, out_tok, err);
   } else {
-    hipLaunchKernelGGL(argmax_partial_kernel<float>, grid, dim3(256), 0, st, nn, V, (const float *)logits, par, pv,
-                       pi, err);
+    if (many)
+      hipLaunchKernelGGL((argmax_partial_kernel<float, 8>), grid, dim3(256), 0, st, nn, V, (const float *)logits, par,
+                         pv, pi, err);
+    else
+      hipLaunchKernelGGL((argmax_partial_kernel<float, 1>), grid, dim3(256), 0, st, nn, V, (const float *)logits, par,
+                         pv, pi, err);
     hipLaunchKernelGGL(accept_walk_kernel<float>, dim3(bs), dim3(256), 0, st, nn, V, B, tok, par, pv, pi,
                        (const float *)logits, acc_len, acc_nodes, out_tok, err);
   }
