@@ -140,7 +140,7 @@ Dims make_dims(const domino_model *m, int bs) {
 // ---- workspace layout of the draft step
 struct WsLayout {
   size_t err, best, slots, hdr_words, X, X2, A, FC, HP, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
-      praw, total;
+      praw, XF, total;
   int GC, ldl;
 };
 
@@ -158,9 +158,23 @@ GemmPlan plan_proj(const domino_model *m, const Packed &pk, int M, int epi, int 
   if (m->bf16 && M > kSkinnyMaxRows) return plan_gemm_wide(pk.NT, pk.KS, M, epi, m->n_cu, max_split);
   return plan_gemm(pk.NT, pk.KS, M, epi, m->n_cu, max_split);
 }
-void launch_proj(const domino_model *m, int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
-  if (p.wide) launch_gemm_wide(epi, a, p, st);  // a.K == a.KS * 32
-  else launch_gemm(m->bf16, epi, a, p, st);
+// false when a wide plan's arguments were refused (nothing launched)
+bool launch_proj(const domino_model *m, int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
+  if (p.wide) return launch_gemm_wide(epi, a, p, st);  // a.K == a.KS * 32, a.xf set
+  launch_gemm(m->bf16, epi, a, p, st);
+  return true;
+}
+
+// Fragment scratch of the wide projections of a layout: the most rows any of
+// them has times the widest K among them (0 when every plan is skinny)
+size_t wide_scratch(const domino_model *m, const Plans &p, int rows, int train_rows) {
+  const Dims &D = m->D;
+  const bool wide = p.qkv.wide || p.wo.wide || p.gateup.wide || p.down.wide || p.lm.wide || p.fc.wide;
+  const int kmax = std::max({D.d, D.nq * D.dh, D.ffn, std::max(m->fuse_k, 1) * D.d, D.ds});
+  size_t b = wide ? gemm_wide_scratch_bytes(rows, kmax) : 0;
+  if (train_rows > 0 && m->bf16 && train_rows > kSkinnyMaxRows)
+    b = std::max(b, gemm_wide_scratch_bytes(train_rows, D.ds));
+  return b;
 }
 
 // Plans for M block rows, Mlm LM-head rows and Ma QKV rows (block rows, then
@@ -227,6 +241,7 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.pval = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
   w.pid = take((size_t)(D.B - 1) * bs * w.GC * beta * 4);
   w.praw = take((size_t)(D.B - 1) * bs * w.GC * 4);
+  w.XF = take(wide_scratch(m, p, Ma, bs * (D.B - 1)));  // also the training forward's W1 S-half rows
   w.total = o;
   return true;
 }
@@ -283,6 +298,7 @@ bool target_layout(const domino_model *m, int bs, int nn, int max_ctx, TargetLay
   w.H = take((size_t)M * D.d * 4);
   w.ldl = m->lm.NT * 16;
   w.LP = take((size_t)M * w.ldl * 4);
+  w.XF = take(wide_scratch(m, p, M, 0));
   t.tok = take((size_t)M * 4);
   t.pos = take((size_t)M * 4);
   t.mask = take((size_t)bs * t.Bp * t.Bp);
@@ -325,13 +341,15 @@ hipError_t build_gtab(domino_model *m, const void *w_ih, const void *b_ih) {
   pk.KS = (K + KSTEP - 1) / KSTEP;
   pk.off = 0;
   const int CH = 8192;
-  void *P = nullptr;
+  void *P = nullptr, *XF = nullptr;
   float *X = nullptr;
   hipError_t e = hipMalloc(&P, (size_t)pk.NT * pk.KS * 1024);
   if (e != hipSuccess) return e;
   e = hipMalloc(&X, (size_t)CH * K * 4);
+  if (e == hipSuccess && m->bf16) e = hipMalloc(&XF, gemm_wide_scratch_bytes(CH, K));
   if (e != hipSuccess) {
     (void)hipFree(P);
+    if (X) (void)hipFree(X);
     return e;
   }
   launch_pack(m->bf16, w_ih, N, K, K, P, pk.NT, pk.KS, 1, 0, nullptr);
@@ -340,14 +358,21 @@ hipError_t build_gtab(domino_model *m, const void *w_ih, const void *b_ih) {
     const int rows = std::min(CH, D.V - r0);
     launch_to_f32((const char *)m->embed + (size_t)r0 * K * m->esz, m->bf16, X, (size_t)rows * K, nullptr);
     const GemmPlan pl = plan_proj(m, pk, rows, EPI_STORE, 1);
-    const GemmArgs a = gemm_args(P, pk, 0, pk.NT, N, X, K, rows, K, G + (size_t)r0 * N, N, pl);
-    launch_proj(m, EPI_STORE, a, pl, nullptr);
+    GemmArgs a = gemm_args(P, pk, 0, pk.NT, N, X, K, rows, K, G + (size_t)r0 * N, N, pl);
+    a.xf = XF;
+    if (!launch_proj(m, EPI_STORE, a, pl, nullptr)) {
+      e = hipErrorInvalidValue;
+      break;
+    }
     launch_add_row_bias(G + (size_t)r0 * N, rows, N, b_ih, m->bf16, nullptr);
   }
-  e = hipGetLastError();
-  if (e == hipSuccess) e = hipDeviceSynchronize();
+  // finish what was launched before anything is freed, whatever stopped the loop
+  const hipError_t le = hipGetLastError(), se = hipDeviceSynchronize();
+  if (e == hipSuccess) e = le;
+  if (e == hipSuccess) e = se;
   (void)hipFree(P);
   (void)hipFree(X);
+  if (XF) (void)hipFree(XF);
   return e;
 }
 
@@ -618,7 +643,8 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
     prof_begin(m, DOMINO_KC_CTXPROJ, st);
     GemmArgs a = gemm_args(base + m->fc.off, m->fc, 0, m->fc.NT, D.d, (const float *)ctx_hidden_new, kf, rows, kf,
                            F(w.FC), D.d, p.fc);
-    launch_proj(m, EPI_STORE, a, p.fc, st);
+    a.xf = ws + w.XF;
+    if (!launch_proj(m, EPI_STORE, a, p.fc, st)) return fail(DOMINO_ERR_UNSUPPORTED, "context fusion projection refused");
     launch_sum_parts(F(w.FC), p.fc.ksplit, (size_t)rows * D.d, rows, D.d, F(w.A) + (size_t)M * D.d, D.d, st);
     prof_end(m, DOMINO_KC_CTXPROJ, st);
   } else if (n_new > 0) {
@@ -628,6 +654,11 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
   }
 
   const size_t rstride = (size_t)M * D.d;  // partial-output stride of the residual projections
+  // every projection of the step: wide plans split their activations into the workspace's fragment planes
+  auto proj = [&](int epi, GemmArgs a, const GemmPlan &pl) {
+    a.xf = ws + w.XF;
+    return launch_proj(m, epi, a, pl, st);
+  };
   // the residual stream ping-pongs between two buffers: every RMSNorm launch
   // reads one and writes the updated residual to the other
   float *xc = F(w.X), *xn = F(w.X2);
@@ -646,7 +677,7 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
     prof_begin(m, DOMINO_KC_QKV, st);
     GemmArgs a = gemm_args(base + m->qkv[l].off, m->qkv[l], 0, m->qkv[l].NT, qkvw, F(w.A), D.d, Ma, D.d, F(w.QKV),
                            qkvw, p.qkv);
-    launch_proj(m, EPI_STORE, a, p.qkv, st);
+    if (!proj(EPI_STORE, a, p.qkv)) return fail(DOMINO_ERR_UNSUPPORTED, "qkv projection refused");
     prof_end(m, DOMINO_KC_QKV, st);
 
     prof_begin(m, DOMINO_KC_ROPE, st);
@@ -660,7 +691,7 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
 
     prof_begin(m, DOMINO_KC_WO, st);
     a = gemm_args(base + m->wo[l].off, m->wo[l], 0, m->wo[l].NT, D.d, F(w.O), qd, M, qd, F(w.WOp), D.d, p.wo);
-    launch_proj(m, EPI_STORE, a, p.wo, st);
+    if (!proj(EPI_STORE, a, p.wo)) return fail(DOMINO_ERR_UNSUPPORTED, "wo projection refused");
     prof_end(m, DOMINO_KC_WO, st);
 
     // residual += attention output, then the FFN RMSNorm
@@ -673,13 +704,13 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
     prof_begin(m, DOMINO_KC_GATEUP, st);
     a = gemm_args(base + m->gateup[l].off, m->gateup[l], 0, m->gateup[l].NT, D.ffn, F(w.A), D.d, M, D.d, F(w.F),
                   D.ffn, p.gateup);
-    launch_proj(m, EPI_SWIGLU, a, p.gateup, st);
+    if (!proj(EPI_SWIGLU, a, p.gateup)) return fail(DOMINO_ERR_UNSUPPORTED, "gateup projection refused");
     prof_end(m, DOMINO_KC_GATEUP, st);
 
     prof_begin(m, DOMINO_KC_DOWN, st);
     a = gemm_args(base + m->down[l].off, m->down[l], 0, m->down[l].NT, D.d, F(w.F), D.ffn, M, D.ffn, F(w.DNp), D.d,
                   p.down);
-    launch_proj(m, EPI_STORE, a, p.down, st);
+    if (!proj(EPI_STORE, a, p.down)) return fail(DOMINO_ERR_UNSUPPORTED, "down projection refused");
     prof_end(m, DOMINO_KC_DOWN, st);
   }
 
@@ -694,7 +725,7 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
   float *LP = F(w.LP);
   prof_begin(m, DOMINO_KC_LMHEAD, st);
   GemmArgs a = gemm_args(base + m->lm.off, m->lm, 0, m->lm.NT, w.ldl, H, D.d, Mh, D.d, LP, w.ldl, p.lm);
-  launch_proj(m, EPI_STORE, a, p.lm, st);
+  if (!proj(EPI_STORE, a, p.lm)) return fail(DOMINO_ERR_UNSUPPORTED, "lm projection refused");
   prof_end(m, DOMINO_KC_LMHEAD, st);
   if (!spec.all_rows && debug && debug->base_logits) {
     hipError_t ce = hipMemcpy2DAsync(debug->base_logits, (size_t)D.V * 4, LP, (size_t)w.ldl * 4, (size_t)D.V * 4, Mh,
@@ -929,7 +960,9 @@ domino_status domino_train_forward(domino_model_t m, int32_t batch, const int32_
   const GemmPlan py = plan_proj(m, m->w1s, Mr, EPI_STORE, 1);
   const GemmArgs ga = gemm_args((const char *)m->mem + m->w1s.off, m->w1s, 0, m->w1s.NT, D.r, h.states, D.ds, Mr,
                                 D.ds, (float *)(ws + tl.Y), D.r, py);
-  launch_proj(m, EPI_STORE, ga, py, st);
+  GemmArgs gx = ga;
+  gx.xf = ws + w.XF;
+  if (!launch_proj(m, EPI_STORE, gx, py, st)) return fail(DOMINO_ERR_UNSUPPORTED, "W1 state projection refused");
 
   TrainArgs t;
   t.V = D.V;

@@ -4,20 +4,23 @@
 // with the packed weight tiles of the skinny kernel and the same hi + lo bf16
 // split of the activations, so both kernels compute to the same precision.
 //
-// The skinny kernel gives each wave one 16-column weight tile against all rows
-// of its m-group (at most 64), so above 64 rows it re-reads every weight tile
-// once per m-group and feeds each staged activation fragment to a single
-// tile.  Here a workgroup of 8 waves owns 8 weight tiles (128 output columns)
-// and 256 rows: waves form a 2 (columns) x 4 (rows) grid, each wave multiplies
-// 4 weight tiles by 4 row blocks (16 accumulators), so a weight byte leaves
-// HBM once per 256 rows and every fragment read from LDS feeds 4 products.
+// The activations are split once per projection (split_frag_kernel) into two
+// bf16 planes, hi and lo, stored in MFMA fragment order: fragment (row block
+// rb, k-step s) is 1 KB, lane l = 16 g + r holding the 8 k values
+// 32 s + 8 g .. + 7 of row 16 rb + r.  A fragment is then one coalesced 1 KB
+// wave load, exactly like a packed weight fragment, and no arithmetic is left
+// between the loads and the products.
 //
-// Per k-step the workgroup stages 8 KB of weights and 32 KB of activations
-// (256 rows x 32 k, split into hi/lo fragments) into one of two LDS buffers;
-// each thread keeps kWideDepth k-steps of loads in flight in registers, so
-// the loads of later k-steps overlap the products of the current one.  A K
-// split (grid.y) writes partial outputs that the consumer adds in split
-// order, as in the skinny kernel.
+// A workgroup of 4 waves owns 8 weight tiles (128 output columns) and 16 row
+// blocks (256 rows); wave w multiplies all 8 tiles by row blocks 4w .. 4w + 3,
+// hi and lo: 64 products of 16x16x32 per k-step.  The weight fragments, used
+// by all four waves, go through LDS (two 8 KB buffers, one barrier per
+// k-step); the activation fragments, used by one wave only, are loaded
+// straight into that wave's registers one k-step ahead.  Registers are capped
+// at 256 per lane so that two workgroups share a CU: while one waits at its
+// barrier, the other's products keep the matrix cores busy.  A K split
+// (grid.y) writes partial outputs that the consumer adds in split order, as
+// in the skinny kernel.
 #include "common.h"
 #include "kernels.h"
 #include "mfma.h"
@@ -28,138 +31,184 @@ namespace dk {
 
 namespace {
 
-constexpr int kWideTN = 4, kWideTM = 4;          // tiles and row blocks per wave
-constexpr int kWideWN = 2, kWideWM = 4;          // wave grid
-constexpr int kWideTiles = kWideTN * kWideWN;    // 8 weight tiles per workgroup
-constexpr int kWideBlocks = kWideTM * kWideWM;   // 16 row blocks of 16
-constexpr int kWideRows = kWideBlocks * 16;      // 256 rows per workgroup
-constexpr int kWideDepth = 4;                    // k-steps of loads in flight per thread
-constexpr int kWideThreads = 512;
+constexpr int kWideTiles = 8;                    // weight tiles per workgroup (128 columns)
+constexpr int kWideBlocks = 16;                  // row blocks per workgroup (256 rows)
+constexpr int kWideRows = kWideBlocks * 16;
+constexpr int kWideWaves = 4;                    // wave w: row blocks kWideTM * w ..
+constexpr int kWideTM = kWideBlocks / kWideWaves;
+constexpr int kWideThreads = kWideWaves * 64;
+constexpr int kWideWPW = kWideTiles / kWideWaves;  // weight fragments each wave stages: 2
+static_assert(kWideTiles % kWideWaves == 0, "weight fragments must divide over the waves");
 
 DEVI float silu_w(float x) { return x / (1.f + expf(-x)); }
 
-// 8 consecutive k of row m from k0 (K is a multiple of 32, so k0 + 8 <= K).
-// Rows past M read row M - 1 instead: they only feed output rows that are
-// never stored, and the load stays unconditional, so the compiler can count
-// the loads in flight instead of waiting for all of them.
-DEVI void load_row8(const float *__restrict__ X, int ldx, int M, int m, int k0, float4 (&v)[2]) {
-  const int mc = m < M ? m : M - 1;
-  const float4 *p = (const float4 *)(X + (size_t)mc * ldx + k0);
-  v[0] = p[0];
-  v[1] = p[1];
+// One thread per (row block, k-step, lane): 8 values of one row, split.
+__global__ __launch_bounds__(256) void split_frag_kernel(const float *__restrict__ X, int ldx, int M, int KS,
+                                                         u32x4 *__restrict__ Xf, int nrb) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (size_t)nrb * KS * 64) return;
+  const int lane = (int)(idx & 63);
+  const size_t rs = idx >> 6;
+  const int s = (int)(rs % KS), rb = (int)(rs / KS);
+  const int m = rb * 16 + (lane & 15), k0 = s * 32 + (lane >> 4) * 8;
+  float f[8];
+  if (m < M) {
+    const float4 *p = (const float4 *)(X + (size_t)m * ldx + k0);
+    const float4 a = p[0], b = p[1];
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+    f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] = 0.f;
+  }
+  bf16x8 hi, lo;
+  split8(f, hi, lo);
+  Xf[((size_t)rb * KS + s) * 64 + lane] = __builtin_bit_cast(u32x4, hi);
+  Xf[(((size_t)nrb + rb) * KS + s) * 64 + lane] = __builtin_bit_cast(u32x4, lo);
+}
+
+// two workgroups per CU (80 KB of LDS and at most 256 registers each), so one
+// workgroup's products run while the other waits at its barrier
+// Workgroup order (a 1-D grid, workgroup L on XCD L % 8): the workgroups of
+// one (column group, K split) pair u, one per row group, are L = (8 c + mz) *
+// ... such that they share L % 8 and are dispatched 8 apart, so the second row
+// group finds the weight tiles in its XCD's L2 instead of reading them again.
+struct WideMap {
+  int groups, ksplit, mgroups;
+};
+DEVI bool wide_coords(const WideMap &mp, int L, int &grp, int &ky, int &mz) {
+  const int x = L & 7, r = L >> 3;
+  const int c = r / mp.mgroups;
+  mz = r % mp.mgroups;
+  const int u = c * 8 + x;
+  grp = u % mp.groups;
+  ky = u / mp.groups;
+  return ky < mp.ksplit;
 }
 
 template <int EPI>
-__global__ __launch_bounds__(kWideThreads) void gemm_wide_kernel(GemmArgs a) {
-  __shared__ u32x4 wsm[2][kWideTiles][64];
-  __shared__ u32x4 xsm[2][kWideBlocks][2][64];
+__global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2))) void gemm_wide_kernel(GemmArgs a,
+                                                                                                       int nrb,
+                                                                                                       WideMap mp) {
+  __shared__ u32x4 lw[2][kWideTiles][64];  // [buffer][weight tile][lane]
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn = wave % kWideWN, wm = wave / kWideWN;
-  const int grp = blockIdx.x, ky = blockIdx.y, mz = blockIdx.z;
+  int grp, ky, mz;
+  if (!wide_coords(mp, (int)blockIdx.x, grp, ky, mz)) return;  // past the last pair (workgroup-uniform)
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int KS = a.KS;
   const int spw = (KS + a.ksplit - 1) / a.ksplit;
   const int s0 = min(KS, ky * spw), s1 = min(KS, s0 + spw);
-  const int mbase = mz * kWideRows;
 
-  // this thread's loads of a k-step: 16 bytes of weight tile `wave`, and 8 k
-  // (k-group g) of rows rr and rr + 128
-  const int wt = grp * kWideTiles + wave;
-  const u32x4 *__restrict__ Pw =
-      (const u32x4 *)a.P + (size_t)(a.tile0 + min(wt, a.ntiles - 1)) * KS * 64 + lane;
-  const int g = tid & 3, rr = tid >> 2;
-
-  floatx4 acc[kWideTN][kWideTM];
+  // weight tiles grp * 8 + 2 * wave + q staged by this wave; this wave's row
+  // blocks in the two planes.  Tiles and blocks past the end are clamped: they
+  // only feed outputs that are never stored.
+  const u32x4 *wsrc[kWideWPW];
 #pragma unroll
-  for (int i = 0; i < kWideTN; ++i)
+  for (int q = 0; q < kWideWPW; ++q) {
+    const int t = min(grp * kWideTiles + kWideWPW * wave + q, a.ntiles - 1);
+    wsrc[q] = (const u32x4 *)a.P + (size_t)(a.tile0 + t) * KS * 64;
+  }
+  const u32x4 *xsrc[2 * kWideTM];
+#pragma unroll
+  for (int f = 0; f < 2 * kWideTM; ++f) {
+    const int rb = min(mz * kWideBlocks + kWideTM * wave + f % kWideTM, nrb - 1);
+    xsrc[f] = (const u32x4 *)a.xf + ((size_t)(f / kWideTM) * nrb + rb) * KS * 64;
+  }
+
+  floatx4 acc[kWideTiles][kWideTM];
+#pragma unroll
+  for (int i = 0; i < kWideTiles; ++i)
 #pragma unroll
     for (int j = 0; j < kWideTM; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 wr[kWideDepth];
-  float4 xr[kWideDepth][2][2];
-  auto issue = [&](int d, int s) {
+  // weight fragments on their way to LDS, two k-steps ahead (slot = k-step
+  // parity); activation fragments of even / odd k-steps, one k-step ahead
+  u32x4 wr[2][kWideWPW];
+  u32x4 xa[2 * kWideTM], xb[2 * kWideTM];
+  auto issue_w = [&](int d, int s) {
     const int sc = min(s, s1 - 1);  // clamped: every load stays valid and unconditional
-    wr[d] = __builtin_nontemporal_load(Pw + (size_t)sc * 64);
 #pragma unroll
-    for (int h = 0; h < 2; ++h) load_row8(a.X, a.ldx, a.M, mbase + rr + 128 * h, sc * 32 + g * 8, xr[d][h]);
+    for (int q = 0; q < kWideWPW; ++q) wr[d][q] = __builtin_nontemporal_load(wsrc[q] + (size_t)sc * 64 + lane);
   };
-  auto stage = [&](int d, int buf, bool live) {
-    // a k-step past the split's end is staged as zeros (a select on loaded
-    // data, not a skipped load), so it adds nothing to the products
-    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-    wsm[buf][wave][lane] = live ? wr[d] : u32x4{0u, 0u, 0u, 0u};
+  auto issue_x = [&](int s, u32x4 (&x)[2 * kWideTM]) {
+    const int sc = min(s, s1 - 1);
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int r = rr + 128 * h;
-      u32x4 hl[2];
-      const float4 xv[2] = {live ? xr[d][h][0] : z, live ? xr[d][h][1] : z};
-      XStage<bf16_t>::put(hl, xv);
-      const int l = (r & 15) + 16 * g;
-      xsm[buf][r >> 4][0][l] = hl[0];
-      xsm[buf][r >> 4][1][l] = hl[1];
-    }
+    for (int f = 0; f < 2 * kWideTM; ++f) x[f] = xsrc[f][(size_t)sc * 64 + lane];
   };
-  auto compute = [&](int buf) {
-    bf16x8 xb[kWideTM][2];
+  auto stage = [&](int d) {
 #pragma unroll
-    for (int j = 0; j < kWideTM; ++j) {
-      xb[j][0] = __builtin_bit_cast(bf16x8, xsm[buf][wm * kWideTM + j][0][lane]);
-      xb[j][1] = __builtin_bit_cast(bf16x8, xsm[buf][wm * kWideTM + j][1][lane]);
-    }
+    for (int q = 0; q < kWideWPW; ++q) lw[d][kWideWPW * wave + q][lane] = wr[d][q];
+  };
+  auto compute = [&](int buf, const u32x4 (&x)[2 * kWideTM]) {
 #pragma unroll
-    for (int i = 0; i < kWideTN; ++i) {
-      const bf16x8 w = __builtin_bit_cast(bf16x8, wsm[buf][wn * kWideTN + i][lane]);
+    for (int i = 0; i < kWideTiles; ++i) {
+      const bf16x8 w = __builtin_bit_cast(bf16x8, lw[buf][i][lane]);
 #pragma unroll
-      for (int j = 0; j < kWideTM; ++j) {
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, xb[j][0], acc[i][j], 0, 0, 0);
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, xb[j][1], acc[i][j], 0, 0, 0);
-      }
+      for (int j = 0; j < kWideTM; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, __builtin_bit_cast(bf16x8, x[j]), acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < kWideTM; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, __builtin_bit_cast(bf16x8, x[kWideTM + j]), acc[i][j],
+                                                            0, 0, 0);
     }
   };
 
   if (s0 < s1) {
-#pragma unroll
-    for (int d = 0; d < kWideDepth; ++d) issue(d, s0 + d);
-    // k-step s0 + i sits in ring slot i % depth and LDS buffer i & 1 (the
-    // depth is even); the ring index is a compile-time constant inside the
-    // unrolled body.  The loop runs whole rounds of the ring with no branch
-    // inside (k-steps past the end are staged as zeros), so the compiler can
-    // keep the later rounds' loads in flight across the loop's back edge.
+    // k-step s0 + i: weights in slot and LDS buffer i & 1, activations in xa
+    // (even i) or xb (odd i).  Each step stages its weights, issues the
+    // weights of step i + 2 and the activations of step i + 1, passes the
+    // barrier and multiplies.  A buffer is rewritten only after the barrier
+    // that every wave passes once it has finished its products on it.  An odd
+    // step past the end (odd count) stages a copy of the last step and skips
+    // its products (a workgroup-uniform branch).  The prologue's loads go out
+    // in order (no reordering across the scheduling barriers), so the waits
+    // in the loop leave the later loads in flight.
+    issue_w(0, s0);
+    __builtin_amdgcn_sched_barrier(0);
+    issue_x(s0, xa);
+    __builtin_amdgcn_sched_barrier(0);
+    issue_w(1, s0 + 1);
+    __builtin_amdgcn_sched_barrier(0);
     const int nsteps = s1 - s0;
-    for (int i0 = 0; i0 < nsteps; i0 += kWideDepth) {
-#pragma unroll
-      for (int d = 0; d < kWideDepth; ++d) {
-        stage(d, d & 1, i0 + d < nsteps);
-        issue(d, s0 + i0 + d + kWideDepth);
-        __syncthreads();
-        compute(d & 1);
-      }
+    for (int i0 = 0; i0 < nsteps; i0 += 2) {
+      stage(0);
+      issue_w(0, s0 + i0 + 2);
+      issue_x(s0 + i0 + 1, xb);
+      __syncthreads();
+      compute(0, xa);
+      stage(1);
+      issue_w(1, s0 + i0 + 3);
+      issue_x(s0 + i0 + 2, xa);
+      __syncthreads();
+      if (i0 + 1 < nsteps) compute(1, xb);
     }
   }
 
   float *Y = a.Y + (size_t)ky * a.ysplit;
+  const int mbase = mz * kWideRows;
 #pragma unroll
-  for (int i = 0; i < kWideTN; ++i) {
-    const int tile = grp * kWideTiles + wn * kWideTN + i;
+  for (int i = 0; i < kWideTiles; ++i) {
+    const int tile = grp * kWideTiles + i;
     if (EPI == EPI_SWIGLU) {
       // packed tiles come in (gate, up) pairs; tile parity equals i's parity
       if ((i & 1) || tile + 1 >= a.ntiles) continue;
       const int col = (tile / 2) * 16 + 4 * (lane >> 4);
 #pragma unroll
       for (int j = 0; j < kWideTM; ++j) {
-        const int m = mbase + (wm * kWideTM + j) * 16 + (lane & 15);
+        const int m = mbase + (wave * kWideTM + j) * 16 + (lane & 15);
         if (m >= a.M) continue;
         float *y = Y + (size_t)m * a.ldy + col;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          if (col + e < a.N) y[e] = silu_w(acc[i][j][e]) * acc[i + (i + 1 < kWideTN ? 1 : 0)][j][e];
+          if (col + e < a.N) y[e] = silu_w(acc[i][j][e]) * acc[i + (i + 1 < kWideTiles ? 1 : 0)][j][e];
       }
     } else {
       if (tile >= a.ntiles) continue;
       const int n = tile * 16 + 4 * (lane >> 4);
 #pragma unroll
       for (int j = 0; j < kWideTM; ++j) {
-        const int m = mbase + (wm * kWideTM + j) * 16 + (lane & 15);
+        const int m = mbase + (wave * kWideTM + j) * 16 + (lane & 15);
         if (m >= a.M) continue;
         float *y = Y + (size_t)m * a.ldy + n;
         if (n + 4 <= a.N && (a.ldy & 3) == 0) {
@@ -187,7 +236,7 @@ GemmPlan plan_gemm_wide(int ntiles, int KS, int M, int epi, int n_cu, int max_sp
   p.groups = (ntiles + kWideTiles - 1) / kWideTiles;
   p.mgroups = (M + kWideRows - 1) / kWideRows;
   // K split (power of two, at least 8 k-steps per split) by a cost model in
-  // k-step units of the busiest CU: rounds of workgroups times (k-steps per
+  // k-step units of the busiest CU: rounds of workgroup pairs times (k-steps per
   // split + ~8 of pipeline fill and epilogue), plus the partial outputs
   // written and read back (a k-step moves ~40 KB per workgroup).  SwiGLU,
   // nonlinear in the sum, is never split.
@@ -196,7 +245,7 @@ GemmPlan plan_gemm_wide(int ntiles, int KS, int M, int epi, int n_cu, int max_sp
     const long wgs = (long)p.groups * p.mgroups;
     double best = 1e300;
     for (int ks = 1; ks <= max_split && KS / ks >= 8; ks *= 2) {
-      const double rounds = (double)((wgs * ks + n_cu - 1) / n_cu);
+      const double rounds = (double)((wgs * ks + 2 * n_cu - 1) / (2 * n_cu));  // two workgroups per CU
       const double part = ks > 1 ? 2.0 * ks * (double)M * ntiles * 16 * 4 / n_cu / 40960.0 : 0.0;
       const double cost = rounds * ((KS + ks - 1) / ks + 8) + part;
       if (cost < best * 0.999) {
@@ -208,13 +257,25 @@ GemmPlan plan_gemm_wide(int ntiles, int KS, int M, int epi, int n_cu, int max_sp
   return p;
 }
 
-void launch_gemm_wide(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
+size_t gemm_wide_scratch_bytes(int M, int K) {
+  const size_t nrb = (size_t)(M + 15) / 16, KS = (size_t)(K + 31) / 32;
+  return 2 * nrb * KS * 1024;
+}
+
+bool launch_gemm_wide(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
   // the activation loads assume whole k-steps (K = 32 KS) and at least one row;
   // the model's config checks guarantee both for every projection
-  if (a.K != a.KS * 32 || a.M <= 0 || a.ldx < a.K) return;
-  const dim3 grid(p.groups, p.ksplit, p.mgroups);
-  if (epi == EPI_SWIGLU) hipLaunchKernelGGL(gemm_wide_kernel<EPI_SWIGLU>, grid, dim3(kWideThreads), 0, st, a);
-  else hipLaunchKernelGGL(gemm_wide_kernel<EPI_STORE>, grid, dim3(kWideThreads), 0, st, a);
+  if (a.K != a.KS * 32 || a.M <= 0 || a.ldx < a.K || !a.xf) return false;
+  const int nrb = (a.M + 15) / 16;
+  const size_t items = (size_t)nrb * a.KS * 64;
+  hipLaunchKernelGGL(split_frag_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, a.X, a.ldx, a.M, a.KS,
+                     (u32x4 *)a.xf, nrb);
+  const WideMap mp{p.groups, p.ksplit, p.mgroups};
+  const long pairs = (long)p.groups * p.ksplit;
+  const dim3 grid((unsigned)((pairs + 7) / 8 * 8 * p.mgroups));
+  if (epi == EPI_SWIGLU) hipLaunchKernelGGL(gemm_wide_kernel<EPI_SWIGLU>, grid, dim3(kWideThreads), 0, st, a, nrb, mp);
+  else hipLaunchKernelGGL(gemm_wide_kernel<EPI_STORE>, grid, dim3(kWideThreads), 0, st, a, nrb, mp);
+  return true;
 }
 
 }  // namespace dk

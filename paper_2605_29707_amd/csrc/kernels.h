@@ -20,6 +20,8 @@ struct GemmArgs {
   int ldy;
   size_t ysplit;
   int ksplit;
+  void *xf = nullptr;  // wide kernel: scratch for the activations' hi/lo fragment planes
+                       // (gemm_wide_scratch_bytes(M, K) bytes)
 };
 
 struct GemmPlan {
@@ -35,10 +37,14 @@ struct GemmPlan {
 GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu, int max_split);
 void launch_gemm(bool bf16, int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st);
 // Wide activations (bf16 weights; more rows than the skinny kernel's 64 per
-// m-group): workgroup tiles of 128 columns x 256 rows, same packed weights,
-// same hi/lo activation split, K-split partials as above.
+// m-group): the activations are first split into hi/lo bf16 fragment planes
+// (in a.xf), then workgroup tiles of 256 columns x 256 rows multiply them with
+// the same packed weights; K-split partials as above.
 GemmPlan plan_gemm_wide(int ntiles, int KS, int M, int epi, int n_cu, int max_split);
-void launch_gemm_wide(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st);
+// false (nothing launched) when the arguments break the kernel's assumptions
+// (K not 32 KS, no rows, no fragment scratch)
+bool launch_gemm_wide(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t st);
+size_t gemm_wide_scratch_bytes(int M, int K);
 // above this many rows a bf16 GEMM whose K is a multiple of 32 runs the wide kernel
 constexpr int kSkinnyMaxRows = 64;
 void launch_pack(bool bf16, const void *W, int N, int K, int ldw, void *P, int NT, int KS,
