@@ -665,13 +665,245 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Context attention over a bf16 cache, one online-softmax pass per workgroup
+// (batched steps): workgroup (c, kv head, batch row) takes keys
+// [c * kpw, (c + 1) * kpw) of the sequence context[0, n) + block[0, B) and
+// writes the same partial (unnormalised output, row max, row sum) as
+// attn_partial_kernel, for the same merge.
+//
+// Wave w owns query rows 16 w .. 16 w + 15 of the group (R = G * B = 16 NW
+// rows) and keeps their Q fragments (hi and lo) in registers.  Context keys
+// go in blocks of 64 through two LDS buffers (K row-major, V transposed),
+// staged from registers loaded one block ahead.  Per block a wave forms
+// S^T = K Q^T (exact bf16 keys: two products per tile), updates its rows'
+// running max and sum, and adds P V.  S^T leaves lane (g, cc) holding row
+// cc's scores of keys 16 t + 4 g + e, which is already the A fragment of P V
+// when the 32 keys of a product step are ordered (4 g .. 4 g + 3,
+// 16 + 4 g .. 16 + 4 g + 3); V's B fragment is read in that order from the
+// transposed copy.  The block's own keys (fp32) come last, in one more block
+// with hi and lo parts in the two buffers and three products per tile.
+// ---------------------------------------------------------------------------
+constexpr int kFlashKB = 64;                 // keys per block
+constexpr int kFlashKP = 128 + 8;            // K row stride (bf16): conflict-free 16-byte fragment reads
+constexpr int kFlashVP = kFlashKB + 4;       // transposed V row stride (bf16): conflict-free 8-byte reads
+constexpr size_t kFlashK = (size_t)kFlashKB * kFlashKP, kFlashV = (size_t)128 * kFlashVP;  // bf16 per buffer part
+constexpr size_t kFlashLds = 2 * (kFlashK + kFlashV) * sizeof(uint16_t);
+
+DEVI uint32_t pack_lo16(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
+DEVI uint32_t pack_hi16(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
+
+template <int NW>
+__global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__restrict__ Q, const float *__restrict__ Kb,
+                                                             const float *__restrict__ Vb, const bf16_t *__restrict__ ck,
+                                                             const bf16_t *__restrict__ cv,
+                                                             const int32_t *__restrict__ ctx_lens, int max_ctx,
+                                                             float *__restrict__ part, int B, int nq, int nkv, int nch,
+                                                             float scale, int kpw) {
+  constexpr int DH = 128, T = NW * 64, KCH = kFlashKB * DH / 8 / T;  // 16-byte K chunks per thread per block
+  extern __shared__ __align__(16) uint16_t fsm[];
+  auto Kbuf = [&](int bb) { return fsm + bb * (kFlashK + kFlashV); };  // buffer bb: K, then transposed V
+  auto Vbuf = [&](int bb) { return fsm + bb * (kFlashK + kFlashV) + kFlashK; };
+
+  const int c = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int G = nq / nkv;
+  int n = ctx_lens[b];
+  n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
+  const int total = n + B;
+  const int k0 = c * kpw, k1 = min(total, k0 + kpw);
+  if (k0 >= total) return;  // workgroup-uniform
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, cc = lane & 15;
+
+  // this wave's query rows: Q^T fragments (dims 32 s + 8 g .. of row 16 wave + cc)
+  bf16x8 qhf[DH / 32], qlf[DH / 32];
+  {
+    const int qi = 16 * wave + cc, qh = kvh * G + qi / B, j = qi % B;
+    const float *qrow = Q + (((size_t)b * B + j) * nq + qh) * DH;
+#pragma unroll
+    for (int s = 0; s < DH / 32; ++s) {
+      const float4 a = *(const float4 *)(qrow + 32 * s + 8 * g), d = *(const float4 *)(qrow + 32 * s + 8 * g + 4);
+      const float f[8] = {a.x, a.y, a.z, a.w, d.x, d.y, d.z, d.w};
+      split8(f, qhf[s], qlf[s]);
+    }
+  }
+  floatx4 oacc[DH / 16];
+#pragma unroll
+  for (int x = 0; x < DH / 16; ++x) oacc[x] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;  // of query row cc (the same in every g)
+
+  // scores of one block against this wave's rows -> online softmax -> P V.
+  // HILO: the block's keys are fp32 (hi parts in buffer 0, lo parts in buffer 1).
+  auto fold = [&](int nvalid, bool hilo, int bb) {
+    const uint16_t *Kh = Kbuf(bb), *Vh = Vbuf(bb), *Kl = Kbuf(1), *Vl = Vbuf(1);
+    floatx4 sacc[kFlashKB / 16];
+#pragma unroll
+    for (int t = 0; t < kFlashKB / 16; ++t) {
+      sacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < DH / 32; ++s) {
+        const bf16x8 kh = ld_frag(Kh + (16 * t + cc) * kFlashKP + 32 * s + 8 * g);
+        if (hilo) {
+          const bf16x8 kl = ld_frag(Kl + (16 * t + cc) * kFlashKP + 32 * s + 8 * g);
+          sacc[t] = mfma3(kh, kl, qhf[s], qlf[s], sacc[t]);
+        } else {
+          sacc[t] = mfma2(kh, qhf[s], qlf[s], sacc[t]);
+        }
+      }
+    }
+    float mb = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < kFlashKB / 16; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float v = 16 * t + 4 * g + e < nvalid ? sacc[t][e] * scale : -INFINITY;
+        sacc[t][e] = v;
+        mb = fmaxf(mb, v);
+      }
+    mb = fmaxf(mb, __shfl_xor(mb, 16, 64));
+    mb = fmaxf(mb, __shfl_xor(mb, 32, 64));
+    const float mn = fmaxf(m_run, mb);  // finite: every block has a valid key
+    const float alpha = m_run == -INFINITY ? 0.f : expf(m_run - mn);
+    m_run = mn;
+    float p[kFlashKB / 16][4], lb = 0.f;
+#pragma unroll
+    for (int t = 0; t < kFlashKB / 16; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        p[t][e] = sacc[t][e] == -INFINITY ? 0.f : expf(sacc[t][e] - mn);
+        lb += p[t][e];
+      }
+    lb += __shfl_xor(lb, 16, 64);
+    lb += __shfl_xor(lb, 32, 64);
+    l_run = alpha * l_run + lb;
+    // output rows are 4 g + e: their factors come from lanes 4 g + e
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float ae = __shfl(alpha, 4 * g + e, 64);
+#pragma unroll
+      for (int x = 0; x < DH / 16; ++x) oacc[x][e] *= ae;
+    }
+#pragma unroll
+    for (int u = 0; u < kFlashKB / 32; ++u) {
+      const float f[8] = {p[2 * u][0], p[2 * u][1], p[2 * u][2], p[2 * u][3],
+                          p[2 * u + 1][0], p[2 * u + 1][1], p[2 * u + 1][2], p[2 * u + 1][3]};
+      bf16x8 ph, pl;
+      split8(f, ph, pl);
+#pragma unroll
+      for (int x = 0; x < DH / 16; ++x) {
+        const uint16_t *vr = Vh + (16 * x + cc) * kFlashVP + 32 * u + 4 * g;
+        const uint2 v0 = *(const uint2 *)vr, v1 = *(const uint2 *)(vr + 16);
+        const bf16x8 vh = __builtin_bit_cast(bf16x8, u32x4{v0.x, v0.y, v1.x, v1.y});
+        if (hilo) {
+          const uint16_t *vq = Vl + (16 * x + cc) * kFlashVP + 32 * u + 4 * g;
+          const uint2 w0 = *(const uint2 *)vq, w1 = *(const uint2 *)(vq + 16);
+          const bf16x8 vl = __builtin_bit_cast(bf16x8, u32x4{w0.x, w0.y, w1.x, w1.y});
+          oacc[x] = mfma3(ph, pl, vh, vl, oacc[x]);
+        } else {
+          oacc[x] = mfma2b(ph, pl, vh, oacc[x]);
+        }
+      }
+    }
+  };
+
+  // ---- context keys [k0, c1) from the cache, 64 per block
+  const int c1 = min(k1, n);
+  const int nblk = c1 > k0 ? (c1 - k0 + kFlashKB - 1) / kFlashKB : 0;
+  u32x4 kr[KCH], vr[4];
+  auto load_blk = [&](int i) {  // rows clamped into [k0, c1): every load valid and unconditional
+    const int base = k0 + i * kFlashKB;
+#pragma unroll
+    for (int q = 0; q < KCH; ++q) {
+      const int e = tid + q * T, key = min(base + e / (DH / 8), c1 - 1);
+      kr[q] = *(const u32x4 *)(ck + (((size_t)b * max_ctx + key) * nkv + kvh) * DH + 8 * (e % (DH / 8)));
+    }
+    const int u = min(tid, 255), dof = u % 16, kq = u / 16;  // V: 4 keys x 8 dims per thread (threads < 256)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int key = min(base + 4 * kq + r, c1 - 1);
+      vr[r] = *(const u32x4 *)(cv + (((size_t)b * max_ctx + key) * nkv + kvh) * DH + 8 * dof);
+    }
+  };
+  auto store_blk = [&](int i, int bb) {  // keys past c1 get zero values (their scores are masked)
+    const int base = k0 + i * kFlashKB;
+#pragma unroll
+    for (int q = 0; q < KCH; ++q) {
+      const int e = tid + q * T;
+      *(u32x4 *)(Kbuf(bb) + (e / (DH / 8)) * kFlashKP + 8 * (e % (DH / 8))) = kr[q];
+    }
+    if (tid < 256) {
+      const int dof = tid % 16, kq = tid / 16;
+      u32x4 v[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] = base + 4 * kq + r < c1 ? vr[r] : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {  // dims 8 dof + 2 w (low halves) and + 1 (high halves)
+        uint16_t *row = Vbuf(bb) + (8 * dof + 2 * w) * kFlashVP + 4 * kq;
+        *(uint2 *)row = make_uint2(pack_lo16(v[0][w], v[1][w]), pack_lo16(v[2][w], v[3][w]));
+        *(uint2 *)(row + kFlashVP) = make_uint2(pack_hi16(v[0][w], v[1][w]), pack_hi16(v[2][w], v[3][w]));
+      }
+    }
+  };
+  if (nblk > 0) load_blk(0);
+  for (int i = 0; i < nblk; ++i) {
+    // buffer i & 1 was last read by block i - 2, which every wave finished
+    // before the barrier of block i - 1
+    store_blk(i, i & 1);
+    if (i + 1 < nblk) load_blk(i + 1);
+    __syncthreads();
+    fold(min(kFlashKB, c1 - (k0 + i * kFlashKB)), false, i & 1);
+  }
+
+  // ---- block keys [max(k0, n), k1): fp32, hi parts in buffer 0, lo in buffer 1
+  const int b0 = max(k0, n) - n, nb = k1 - n - b0;
+  if (nb > 0) {
+    __syncthreads();  // both buffers free
+    for (int e = tid; e < kFlashKB * DH / 4; e += T) {
+      const int kk = e / (DH / 4), d4 = e % (DH / 4);
+      const size_t row = (((size_t)b * B + b0 + min(kk, nb - 1)) * nkv + kvh) * DH;
+      const float4 kv = kk < nb ? *(const float4 *)(Kb + row + 4 * d4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 vv = kk < nb ? *(const float4 *)(Vb + row + 4 * d4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      uint2 hi, lo;
+      split4(kv, hi, lo);
+      *(uint2 *)(Kbuf(0) + kk * kFlashKP + 4 * d4) = hi;
+      *(uint2 *)(Kbuf(1) + kk * kFlashKP + 4 * d4) = lo;
+      split4(vv, hi, lo);
+      const uint32_t hv[4] = {hi.x & 0xffffu, hi.x >> 16, hi.y & 0xffffu, hi.y >> 16};
+      const uint32_t lv[4] = {lo.x & 0xffffu, lo.x >> 16, lo.y & 0xffffu, lo.y >> 16};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        Vbuf(0)[(4 * d4 + q) * kFlashVP + kk] = (uint16_t)hv[q];
+        Vbuf(1)[(4 * d4 + q) * kFlashVP + kk] = (uint16_t)lv[q];
+      }
+    }
+    __syncthreads();
+    fold(nb, true, 0);
+  }
+
+  // ---- partial: unnormalised rows 4 g + e of this wave, and row cc's statistics
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int qi = 16 * wave + 4 * g + e, qh = kvh * G + qi / B, j = qi % B;
+    float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2);
+#pragma unroll
+    for (int x = 0; x < DH / 16; ++x) dst[16 * x + cc] = oacc[x][e];
+  }
+  if (g == 0) {
+    const int qi = 16 * wave + cc, qh = kvh * G + qi / B, j = qi % B;
+    float *dst = part + ((((size_t)b * nq + qh) * B + j) * nch + c) * (DH + 2);
+    dst[DH] = m_run;
+    dst[DH + 1] = l_run;
+  }
+}
+
 // Merge the chunks of one (batch, query head, block row) with log-sum-exp
 // weights; one wave per row.  The first CB chunks' output rows and maxima are
-// loaded together with the statistics pass, so a context of up to CB chunks
-// costs one memory round trip: lane c folds chunks c, c + 64, ... into a
+// loaded together with the statistics pass (at clamped chunk indices, so
+// CB sized to the usual chunk count: 40 for the chunked kernel at one batch
+// row, 8 after the one-pass kernel), so a context of up to CB chunks costs
+// one memory round trip: lane c folds chunks c, c + 64, ... into a
 // running (max, sum) pair, the wave combines the pairs, then the rows are
 // weighted and summed in chunk order.
-template <int DH>
+template <int DH, int CB = 40>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float *__restrict__ part,
                                                            const int32_t *__restrict__ ctx_lens,
                                                            int max_ctx, float *__restrict__ O, int bs,
@@ -684,7 +916,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float *__restri
   n = n < 0 ? 0 : (n > max_ctx ? max_ctx : n);
   const int nc = (n + B + CH - 1) / CH;
   const float *base = part + (((size_t)b * nq + qh) * B + j) * nch * (DH + 2);
-  constexpr int PER = DH / 64, CB = 40;
+  constexpr int PER = DH / 64;
   float w[CB], v[CB][PER];
 #pragma unroll
   for (int u = 0; u < CB; ++u) {  // chunk u's max and this lane's output values (clamped, in flight together)
@@ -856,7 +1088,7 @@ static bool attn_dispatch_m(const Dims &D, const float *Q, const float *Kb, cons
 // unless the grid has enough (batch row, kv head) pairs that, doubling the
 // chunks per workgroup, it still holds at least four workgroups per CU; then
 // the partial outputs and the merge shrink by that factor.
-static int attn_chunks_per_wg(const Dims &D, int nc) {
+static int attn_cu_count() {
   static int n_cu = 0;
   if (n_cu == 0) {
     int dev = 0, v = 0;
@@ -866,6 +1098,10 @@ static int attn_chunks_per_wg(const Dims &D, int nc) {
     else
       n_cu = 256;
   }
+  return n_cu;
+}
+static int attn_chunks_per_wg(const Dims &D, int nc) {
+  const int n_cu = attn_cu_count();
   const long pairs = (long)D.bs * D.nkv;
   int cpw = 1;
   while (cpw < 64 && pairs * ((nc + 2 * cpw - 1) / (2 * cpw)) >= 4L * n_cu) cpw *= 2;
@@ -881,6 +1117,37 @@ void launch_attention(const Dims &D, const float *Q, const float *Kb, const floa
                       const void *ck, const void *cv, const int32_t *ctx_lens, int max_ctx,
                       float *part, float *O, int32_t *err, hipStream_t st, const uint8_t *amask) {
   (void)err;
+  // batched steps over a bf16 cache: the one-pass kernel, about two
+  // workgroups per CU, each over a contiguous run of keys
+  {
+    const int G = D.nq / D.nkv, R = G * D.B;
+    const long pairs = (long)D.bs * D.nkv;
+    if (D.bf16 && D.dh == 128 && !amask && (R == 64 || R == 128) && pairs >= 32) {
+      const int n_cu = attn_cu_count();
+      const int nkeys = max_ctx + D.B;
+      const long target = std::max(1L, 2L * n_cu / pairs);
+      const int kpw = (int)(((nkeys + target - 1) / target + kFlashKB - 1) / kFlashKB * kFlashKB);
+      const int ngrp = (nkeys + kpw - 1) / kpw;
+      const int nch = attn_nchunks(max_ctx, D.B);
+      const float scale = 1.0f / sqrtf(128.f);
+      const dim3 grid(ngrp, D.nkv, D.bs);
+      if (R == 64) {
+        (void)hipFuncSetAttribute((const void *)attn_flash_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)kFlashLds);
+        hipLaunchKernelGGL(attn_flash_kernel<4>, grid, dim3(256), kFlashLds, st, Q, Kb, Vb, (const bf16_t *)ck,
+                           (const bf16_t *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv, nch, scale, kpw);
+      } else {
+        (void)hipFuncSetAttribute((const void *)attn_flash_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)kFlashLds);
+        hipLaunchKernelGGL(attn_flash_kernel<8>, grid, dim3(512), kFlashLds, st, Q, Kb, Vb, (const bf16_t *)ck,
+                           (const bf16_t *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv, nch, scale, kpw);
+      }
+      const int items = D.bs * D.nq * D.B;
+      hipLaunchKernelGGL((attn_combine_kernel<128, 8>), dim3((items + 3) / 4), dim3(256), 0, st, part, ctx_lens,
+                         max_ctx, O, D.bs, D.B, D.nq, nch, kpw);
+      return;
+    }
+  }
   const int nch = attn_nchunks(max_ctx, D.B);
   const int CH0 = attn_ch((D.nq / D.nkv) * D.B);
   const int cpw = attn_chunks_per_wg(D, (max_ctx + D.B + CH0 - 1) / CH0);

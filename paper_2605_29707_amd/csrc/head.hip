@@ -382,20 +382,151 @@ constexpr int kLogitWaves = 8;
 constexpr int kTpwSmall = 5;
 constexpr int logit_tpw(int KS, int MT) { return KS * MT <= 8 ? kTpwSmall : (KS * MT <= 16 ? 3 : 1); }
 
+// Compare-exchange under the selection order: (a, b) -> (better, worse).
+DEVI void sel_ce(float &va, int &ia, float &vb, int &ib) {
+  const bool t = better(vb, ib, va, ia);
+  const float v0 = t ? vb : va, v1 = t ? va : vb;
+  const int i0 = t ? ib : ia, i1 = t ? ia : ib;
+  va = v0;
+  ia = i0;
+  vb = v1;
+  ib = i1;
+}
+// a (sorted best first) <- the best L of a and b (both sorted): the pairwise
+// better of a[i] and b[L-1-i] is a bitonic sequence holding exactly those L,
+// which a bitonic merge network sorts.
+template <int L>
+DEVI void sel_merge(float (&av)[L], int (&ai)[L], const float (&bv)[L], const int (&bi)[L]) {
+#pragma unroll
+  for (int i = 0; i < L; ++i) {
+    const bool t = better(bv[L - 1 - i], bi[L - 1 - i], av[i], ai[i]);
+    av[i] = t ? bv[L - 1 - i] : av[i];
+    ai[i] = t ? bi[L - 1 - i] : ai[i];
+  }
+#pragma unroll
+  for (int st = L / 2; st >= 1; st >>= 1)
+#pragma unroll
+    for (int i = 0; i < L; ++i)
+      if ((i & st) == 0) sel_ce(av[i], ai[i], av[i + st], ai[i + st]);
+}
+
+// Top-beta (beta <= L) of a logits workgroup's rows for every batch row, in
+// registers: each lane sorts its own candidates of a batch row into an
+// L-entry list; within a wave the four lanes of a row (g) hand their lists to
+// lane g = 0 through LDS, which merges them; the waves' lists meet in LDS,
+// where one thread per batch row merges them and emits the first beta
+// entries (and the top-1 into the position's key).  (Merging by cross-lane
+// shuffles instead made the compiler take minutes per instantiation.)
+// LDS the lists need (after the u fragments): a wave's lane lists of one
+// m-tile, and each wave's list per batch row
+constexpr size_t topl_lds_bytes(int L, int MT) {
+  return (size_t)kLogitWaves * (4 * 16 + MT * 16) * L * (sizeof(float) + sizeof(int));
+}
+template <int L, int kTPW, int MT>
+DEVI void logits_topl(const HeadArgs &h, int j, const int (&tiles)[kTPW], const float4 (&lb)[kTPW][MT],
+                      const floatx4 (&acc)[kTPW][MT], unsigned char *sbuf) {
+  const Dims &D = h.D;
+  const int bs = D.bs, V = D.V, beta = h.beta;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, cc = lane & 15;
+  auto xg_v = (float(*)[4][16][L])sbuf;  // [kLogitWaves][4][16][L]
+  auto xg_i = (int(*)[4][16][L])(sbuf + sizeof(float) * kLogitWaves * 4 * 16 * L);
+  auto cand_v = (float(*)[MT * 16][L])(sbuf + (sizeof(float) + sizeof(int)) * kLogitWaves * 4 * 16 * L);
+  auto cand_i = (int(*)[MT * 16][L])(sbuf + (sizeof(float) + sizeof(int)) * kLogitWaves * 4 * 16 * L +
+                                     sizeof(float) * kLogitWaves * MT * 16 * L);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    float lv[L];
+    int li[L];
+#pragma unroll
+    for (int k = 0; k < L; ++k) {
+      lv[k] = -INFINITY;
+      li[k] = INT_MAX;
+    }
+#pragma unroll
+    for (int q = 0; q < kTPW; ++q)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int n = tiles[q] * 16 + 4 * g + e;
+        const float lbe = e == 0 ? lb[q][mt].x : (e == 1 ? lb[q][mt].y : (e == 2 ? lb[q][mt].z : lb[q][mt].w));
+        float v = n < V ? order_val(lbe + acc[q][mt][e]) : -INFINITY;
+        int id = n < V ? n : INT_MAX;
+#pragma unroll
+        for (int k = 0; k < L; ++k) sel_ce(lv[k], li[k], v, id);  // bubble (v, id) into place
+      }
+    // a wave's LDS accesses complete in order, so lane g = 0 reads the lists
+    // the other lanes of its wave wrote just before (and the next m-tile's
+    // writes follow its reads)
+    if (g > 0) {
+#pragma unroll
+      for (int k = 0; k < L; ++k) {
+        xg_v[wave][g][cc][k] = lv[k];
+        xg_i[wave][g][cc][k] = li[k];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (g == 0) {
+#pragma unroll
+      for (int o = 1; o < 4; ++o) {
+        float ov[L];
+        int oi[L];
+#pragma unroll
+        for (int k = 0; k < L; ++k) {
+          ov[k] = xg_v[wave][o][cc][k];
+          oi[k] = xg_i[wave][o][cc][k];
+        }
+        sel_merge<L>(lv, li, ov, oi);
+      }
+#pragma unroll
+      for (int k = 0; k < L; ++k) {
+        cand_v[wave][mt * 16 + cc][k] = lv[k];
+        cand_i[wave][mt * 16 + cc][k] = li[k];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  __syncthreads();
+  for (int bb = tid; bb < bs; bb += kLogitWaves * 64) {
+    float lv[L];
+    int li[L];
+#pragma unroll
+    for (int k = 0; k < L; ++k) {
+      lv[k] = cand_v[0][bb][k];
+      li[k] = cand_i[0][bb][k];
+    }
+    for (int w = 1; w < kLogitWaves; ++w) {
+      float ov[L];
+      int oi[L];
+#pragma unroll
+      for (int k = 0; k < L; ++k) {
+        ov[k] = cand_v[w][bb][k];
+        oi[k] = cand_i[w][bb][k];
+      }
+      sel_merge<L>(lv, li, ov, oi);
+    }
+    const size_t o = (((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x) * beta;
+#pragma unroll
+    for (int k = 0; k < L; ++k)
+      if (k < beta) {
+        h.pval[o + k] = lv[k];
+        h.pid[o + k] = li[k];
+      }
+    // top-1 of this workgroup into the position's best key (order-independent max)
+    if (li[0] != INT_MAX)
+      atomicMax(&h.best[((size_t)(j - 1) * bs + bb) * kBestSlots + (blockIdx.x % kBestSlots)], encode_best(lv[0], li[0]));
+  }
+}
+
 template <typename WT, int KS, int MT>
 __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs h, int j) {
   constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP, XF = XStage<WT>::XF;
   constexpr int kTPW = logit_tpw(KS, MT);
-  constexpr int kLogitRows = kLogitWaves * kTPW * 16;
   const Dims &D = h.D;
   const int bs = D.bs, r = D.r, V = D.V, depth = D.B - 1, beta = h.beta;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, cc = lane & 15;
   const int NT = (V + 15) / 16;
-  const int row0 = blockIdx.x * kLogitRows;
   extern __shared__ __align__(16) unsigned char smem[];
   u32x4 *us = (u32x4 *)smem;                                      // [KS][MT][64][XF]
-  float *lv = (float *)(smem + sizeof(u32x4) * KS * MT * 64 * XF);  // [bs][kLogitRows]
 
   // u_j first (a few L2-resident values), so the matrix-core work can follow
   // the W2 stream as its fragments arrive
@@ -538,63 +669,23 @@ __global__ __launch_bounds__(kLogitWaves * 64) void head_logits_kernel(HeadArgs 
     }
     return;
   }
+  if (h.final_logits) {
 #pragma unroll
-  for (int q = 0; q < kTPW; ++q)
+    for (int q = 0; q < kTPW; ++q)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int bb = mt * 16 + cc;
-      if (bb >= bs) continue;
+      for (int mt = 0; mt < MT; ++mt) {
+        const int bb = mt * 16 + cc;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int n = tiles[q] * 16 + 4 * g + e;
-        const float lbe = e == 0 ? lb[q][mt].x : (e == 1 ? lb[q][mt].y : (e == 2 ? lb[q][mt].z : lb[q][mt].w));
-        const float val = lbe + acc[q][mt][e];
-        lv[(size_t)bb * kLogitRows + (n - row0)] = n < V ? val : -INFINITY;
-        if (n < V && h.final_logits) h.final_logits[((size_t)bb * depth + (j - 1)) * V + n] = val;
+        for (int e = 0; e < 4; ++e) {
+          const int n = tiles[q] * 16 + 4 * g + e;
+          const float lbe = e == 0 ? lb[q][mt].x : (e == 1 ? lb[q][mt].y : (e == 2 ? lb[q][mt].z : lb[q][mt].w));
+          if (bb < bs && n < V) h.final_logits[((size_t)bb * depth + (j - 1)) * V + n] = lbe + acc[q][mt][e];
+        }
       }
-    }
-  __syncthreads();
-  const int nrows = min(kLogitRows, V - row0);
-  // this workgroup's top-beta per batch row; with fewer rows than waves, each
-  // row's candidates are split over P waves and the P lists merged after
-  const int P = bs >= kLogitWaves ? 1 : kLogitWaves / bs;
-  __shared__ float cand_v[kLogitWaves][8];
-  __shared__ int cand_i[kLogitWaves][8];
-  auto emit = [&](int bb, float mv, int mi) __attribute__((always_inline)) {
-    if (lane < beta) {
-      const size_t o = (((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x) * beta + lane;
-      h.pval[o] = mv;
-      h.pid[o] = mi;
-    }
-    // top-1 of this workgroup into the position's best key (order-independent max)
-    if (lane == 0 && mi != INT_MAX)
-      atomicMax(&h.best[((size_t)(j - 1) * bs + bb) * kBestSlots + (blockIdx.x % kBestSlots)], encode_best(mv, mi));
-  };
-  for (int t = wave; t < bs * P; t += kLogitWaves) {
-    const int bb = t / P, part = t % P;
-    float mv;
-    int mi;
-    const float *lr = lv + (size_t)bb * kLogitRows;
-    wave_select([&](int c, float &v, int &id) { v = lr[c]; id = row0 + c; }, part * nrows / P,
-                (part + 1) * nrows / P, beta, mv, mi);
-    if (P == 1) {
-      emit(bb, mv, mi);
-    } else if (lane < 8) {
-      cand_v[t][lane] = mv;
-      cand_i[t][lane] = mi;
-    }
   }
-  if (P > 1) {
-    __syncthreads();
-    if (wave < bs) {
-      float mv;
-      int mi;
-      const int t0 = wave * P;
-      wave_select([&](int c, float &v, int &id) { v = cand_v[t0 + c / beta][c % beta]; id = cand_i[t0 + c / beta][c % beta]; },
-                  0, P * beta, beta, mv, mi);
-      emit(wave, mv, mi);
-    }
-  }
+  unsigned char *sbuf = smem + sizeof(u32x4) * KS * MT * 64 * XF;
+  if (beta <= 4) logits_topl<4, kTPW, MT>(h, j, tiles, lb, acc, sbuf);
+  else logits_topl<8, kTPW, MT>(h, j, tiles, lb, acc, sbuf);
 }
 
 // Merge every workgroup's top-beta list of one (position, batch row) after the
@@ -1207,7 +1298,9 @@ static void launch_loop(const HeadArgs &h, hipStream_t st) {
   const Dims &D = h.D;
   const int depth = D.B - 1;
   constexpr int XF = XStage<WT>::XF;
-  const size_t lds = sizeof(u32x4) * KS * MT * 64 * XF + sizeof(float) * (size_t)D.bs * logit_rows(D);
+  // the largest request (beta 8) plus the kernel's 6 KB of static LDS fits a CU's 160 KB
+  static_assert(sizeof(u32x4) * KS * MT * 64 * XF + topl_lds_bytes(8, MT) + 8192 <= 160 * 1024, "logits LDS");
+  const size_t lds = sizeof(u32x4) * KS * MT * 64 * XF + (h.beta == 1 ? 0 : topl_lds_bytes(h.beta <= 4 ? 4 : 8, MT));
   (void)hipFuncSetAttribute((const void *)head_logits_kernel<WT, KS, MT>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   const bool fused = D.bs <= kFusedBatch;

@@ -130,6 +130,29 @@ def test_long_context_folded_chunks(dtype, nq):
     run.close()
 
 
+@pytest.mark.parametrize("nq", [8, 16])
+def test_bf16_batched_context_one_pass(nq):
+    """bf16 cache, head dim 128 and 16 batch rows over 2 kv heads (32 pairs):
+    the one-pass context attention (64-key blocks, a run of 128 keys per
+    workgroup here).  The ragged lengths give an empty context, partial
+    blocks, block keys split between two workgroups (n = 120, 1016), and
+    contexts ending on a workgroup boundary (n = 128, 1024); nq = 8 and 16
+    over 2 kv heads: 64 and 128 query rows per workgroup."""
+    lens = [1024, 0, 1, 63, 64, 65, 120, 127, 128, 129, 500, 777, 1000, 1008, 1016, 255]
+    cfg = synth.get_config("tiny").with_(dtype="bf16", n_q_heads=nq, head_dim=128, batch=len(lens), ctx=1024,
+                                         ctx_from_hidden=False)
+    w = synth.make_weights(cfg, seed=17, gain_std=0.1)
+    inp = synth.make_inputs(cfg, seed=17, ctx_lens=np.array(lens, np.int32), max_ctx=1024)
+    log(f"one-pass context attention: nq={nq} bs={len(lens)}")
+    run = GpuRun(cfg, w, 1024, beta=1)
+    gpu = run.step(inp)
+    assert gpu["err"] == 0
+    ref = oracle_for(cfg, oracle.as_f64_weights(w), inp, gpu, 1)
+    n = check_against_oracle(cfg, gpu, ref, 2e-2, 1)
+    assert n >= 10 * len(lens)
+    run.close()
+
+
 @pytest.mark.parametrize("nq,block", [(8, 32), (4, 64)])
 def test_tiny_large_blocks(nq, block):
     """(n_q / n_kv) * block = 128 query rows per workgroup: the attention uses
