@@ -714,18 +714,7 @@ __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__rest
   if (k0 >= total) return;  // workgroup-uniform
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, cc = lane & 15;
 
-  // this wave's query rows: Q^T fragments (dims 32 s + 8 g .. of row 16 wave + cc)
-  bf16x8 qhf[DH / 32], qlf[DH / 32];
-  {
-    const int qi = 16 * wave + cc, qh = kvh * G + qi / B, j = qi % B;
-    const float *qrow = Q + (((size_t)b * B + j) * nq + qh) * DH;
-#pragma unroll
-    for (int s = 0; s < DH / 32; ++s) {
-      const float4 a = *(const float4 *)(qrow + 32 * s + 8 * g), d = *(const float4 *)(qrow + 32 * s + 8 * g + 4);
-      const float f[8] = {a.x, a.y, a.z, a.w, d.x, d.y, d.z, d.w};
-      split8(f, qhf[s], qlf[s]);
-    }
-  }
+  bf16x8 qhf[DH / 32], qlf[DH / 32];  // this wave's query rows as Q^T fragments (loaded below)
   floatx4 oacc[DH / 16];
 #pragma unroll
   for (int x = 0; x < DH / 16; ++x) oacc[x] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -844,6 +833,18 @@ __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__rest
     }
   };
   if (nblk > 0) load_blk(0);
+  // this wave's query rows: Q^T fragments (dims 32 s + 8 g .. of row 16 wave + cc),
+  // loaded after the first block's keys so the two memory round trips overlap
+  {
+    const int qi = 16 * wave + cc, qh = kvh * G + qi / B, j = qi % B;
+    const float *qrow = Q + (((size_t)b * B + j) * nq + qh) * DH;
+#pragma unroll
+    for (int s = 0; s < DH / 32; ++s) {
+      const float4 a = *(const float4 *)(qrow + 32 * s + 8 * g), d = *(const float4 *)(qrow + 32 * s + 8 * g + 4);
+      const float f[8] = {a.x, a.y, a.z, a.w, d.x, d.y, d.z, d.w};
+      split8(f, qhf[s], qlf[s]);
+    }
+  }
   for (int i = 0; i < nblk; ++i) {
     // buffer i & 1 was last read by block i - 2, which every wave finished
     // before the barrier of block i - 1
@@ -1122,7 +1123,7 @@ void launch_attention(const Dims &D, const float *Q, const float *Kb, const floa
   {
     const int G = D.nq / D.nkv, R = G * D.B;
     const long pairs = (long)D.bs * D.nkv;
-    if (D.bf16 && D.dh == 128 && !amask && (R == 64 || R == 128) && pairs >= 32) {
+    if (D.bf16 && D.dh == 128 && !amask && (R == 64 || R == 128) && pairs >= 8) {
       const int n_cu = attn_cu_count();
       const int nkeys = max_ctx + D.B;
       const long target = std::max(1L, 2L * n_cu / pairs);
@@ -1143,8 +1144,12 @@ void launch_attention(const Dims &D, const float *Q, const float *Kb, const floa
                            (const bf16_t *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv, nch, scale, kpw);
       }
       const int items = D.bs * D.nq * D.B;
-      hipLaunchKernelGGL((attn_combine_kernel<128, 8>), dim3((items + 3) / 4), dim3(256), 0, st, part, ctx_lens,
-                         max_ctx, O, D.bs, D.B, D.nq, nch, kpw);
+      if (ngrp <= 8)
+        hipLaunchKernelGGL((attn_combine_kernel<128, 8>), dim3((items + 3) / 4), dim3(256), 0, st, part, ctx_lens,
+                           max_ctx, O, D.bs, D.B, D.nq, nch, kpw);
+      else
+        hipLaunchKernelGGL((attn_combine_kernel<128, 40>), dim3((items + 3) / 4), dim3(256), 0, st, part, ctx_lens,
+                           max_ctx, O, D.bs, D.B, D.nq, nch, kpw);
       return;
     }
   }
