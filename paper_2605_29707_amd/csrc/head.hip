@@ -811,7 +811,10 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
   constexpr int EPL = 8, KSTEP = 32;
   const Dims &D = h.D;
   const int bs = D.bs, ds = D.ds, r = D.r, d = D.d, depth = D.B - 1, V = D.V;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform in a wave: held in a scalar register, so the
+  // per-wave offsets below cost no vector registers (the resident W2 tiles
+  // take 128 of the 256)
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, cc = lane & 15;
   const int G = gridDim.x, NT = (V + 15) / 16;
   const int nchunk = ds / EPL;  // 16-byte chunks of a row (<= 256 by the config check)
@@ -864,6 +867,13 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
 
   const int nit = bs * ds / 4;  // state items: four indices of one batch row
   for (int j = 1; j <= depth; ++j) {
+    // the thread index, opaque to the compiler once per position: addresses
+    // derived from it are recomputed here (a few instructions) instead of being
+    // hoisted out of the loop, where they would not fit the registers the
+    // resident W2 tiles leave and would be reloaded from scratch every position
+    int tj = threadIdx.x;
+    __asm__ volatile("" : "+v"(tj));
+    const int lane_j = tj & 63, cc_j = lane_j & 15;
     // L_base of this lane's row and tiles, straight from memory into LDS (no
     // registers held; complete by the wait before the u slots are published)
     {
@@ -877,12 +887,12 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
       }
     }
     // ---- y_{j-1}: anchor, forced token, or the argmax the previous wait delivered
-    if (tid < bs) {
+    if (tj < bs) {
       int y;
-      if (j == 1) y = clamp_token(h.anchor[tid], V, h.err);
-      else if (h.forced) y = clamp_token(h.forced[(size_t)tid * depth + (j - 2)], V, h.err);
-      else y = ys[tid];
-      ys[tid] = y;
+      if (j == 1) y = clamp_token(h.anchor[tj], V, h.err);
+      else if (h.forced) y = clamp_token(h.forced[(size_t)tj * depth + (j - 2)], V, h.err);
+      else y = ys[tj];
+      ys[tj] = y;
     }
     __syncthreads();
     // ---- S_{j-1} = GRU(E[y_{j-1}], S_{j-2}) in place; items beyond one per thread
@@ -997,8 +1007,8 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
       const bool ok = poll_tagged<4 * BS>(h.uslot, bs * r, (unsigned long long)j, 32, h.abort_flag, h.err, h.poll_limit, w);
 #pragma unroll
       for (int q = 0; q < 4 * BS; ++q) {
-        const int e = lane + 64 * q;
-        if (e < bs * r) u_s[e] = __uint_as_float((uint32_t)(w[q] & 0xffffffffu));
+        const int e = lane_j + 64 * q;
+        if (BS == 1 || e < bs * r) u_s[e] = __uint_as_float((uint32_t)(w[q] & 0xffffffffu));  // bs * r = 256 q-words at BS 1
       }
       if (lane == 0) s_ok = ok;
     }
@@ -1035,55 +1045,51 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
           __builtin_bit_cast(bf16x8, w2s[((size_t)wave * kPersKS + s) * 64 + lane]), xb, acc[kPersRegTiles], 0, 0, 0);
     }
     // lane (g, cc) holds vocabulary ids 16 (tile0 + q) + 4 g + e: column cc < bs
-    // adds the low-part column of lane cc + bs (a row shift within 16 lanes)
-    float val[kPersTiles][4];
-#pragma unroll
-    for (int q = 0; q < kPersTiles; ++q) {
-      const float4 l4 = lbs[((size_t)wave * kPersTiles + q) * 64 + lane];
-      const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int a = __float_as_int(acc[q][e]);
-        const int lo1 = __builtin_amdgcn_update_dpp(0, a, 0x101, 0xf, 0xf, false);  // lane + 1
-        const int lo2 = __builtin_amdgcn_update_dpp(0, a, 0x102, 0xf, 0xf, false);  // lane + 2
-        val[q][e] = lv[e] + (acc[q][e] + __int_as_float(BS == 1 || bs == 1 ? lo1 : lo2));
-      }
-    }
+    // adds the low-part column of lane cc + bs (a row shift within 16 lanes).
+    // Each tile's four corrected logits are formed, written (DBG) and folded
+    // into the running best before the next tile's, so only one tile's values
+    // are live at a time.
     const bool rowok = cc < bs;
-    if (DBG && rowok) {  // the final logits (output of sampled drafting, debug output otherwise)
-      float *fl = h.final_logits + ((size_t)cc * depth + (j - 1)) * V;
-      const bool vec = (V & 3) == 0;  // rows start 16-byte aligned: four ids per store
-#pragma unroll
-      for (int q = 0; q < kPersTiles; ++q) {
-        const int n = (tile0 + q) * 16 + 4 * g;
-        if (vec && n + 4 <= V) {
-          *(float4 *)(fl + n) = make_float4(val[q][0], val[q][1], val[q][2], val[q][3]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (n + e < V) fl[n + e] = val[q][e];
-        }
-      }
-    }
     {
       // ids grow along (q, e) within a lane, so a strict comparison keeps the
       // smallest id of equal keys; ids past V occur only in the last workgroup
       float bv = -INFINITY, br = 0.f;
       int bi = (tile0 * 16 + 4 * g) < V ? tile0 * 16 + 4 * g : INT_MAX;
       const bool full = (tile0 + kPersTiles) * 16 <= V;
+      float *fl = DBG ? h.final_logits + ((size_t)min(cc, bs - 1) * depth + (j - 1)) * V : nullptr;
 #pragma unroll
       for (int q = 0; q < kPersTiles; ++q) {
+        const float4 l4 = lbs[((size_t)wave * kPersTiles + q) * 64 + lane];
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        float val[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int a = __float_as_int(acc[q][e]);
+          const int lo1 = __builtin_amdgcn_update_dpp(0, a, 0x101, 0xf, 0xf, false);  // lane + 1
+          const int lo2 = __builtin_amdgcn_update_dpp(0, a, 0x102, 0xf, 0xf, false);  // lane + 2
+          val[e] = lv[e] + (acc[q][e] + __int_as_float(BS == 1 || bs == 1 ? lo1 : lo2));
+        }
+        if (DBG && rowok) {  // the final logits (output of sampled drafting, debug output otherwise)
+          const int n = (tile0 + q) * 16 + 4 * g;
+          if ((V & 3) == 0 && n + 4 <= V) {  // rows start 16-byte aligned: four ids per store
+            *(float4 *)(fl + n) = make_float4(val[0], val[1], val[2], val[3]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (n + e < V) fl[n + e] = val[e];
+          }
+        }
         Philox4 noise = {{0u, 0u, 0u, 0u}};
         if (SAMPLE) noise = rng_block(h.seed_lo, h.seed_hi, RNG_DRAFT, cc, j, (tile0 + q) * 4 + g);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int n = (tile0 + q) * 16 + 4 * g + e;
-          const float key = SAMPLE ? val[q][e] * h.inv_temp + rng_gumbel(noise.x[e]) : val[q][e];
+          const float key = SAMPLE ? val[e] * h.inv_temp + rng_gumbel(noise.x[e]) : val[e];
           const float ov = (full || n < V) ? order_val(key) : -INFINITY;
           const bool take = ov > bv;
           bv = take ? ov : bv;
           bi = take ? n : bi;
-          if (SAMPLE) br = take ? val[q][e] : br;
+          if (SAMPLE) br = take ? val[e] : br;
         }
       }
       if (!rowok) {
@@ -1101,15 +1107,15 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
         if (SAMPLE) br = take ? orw : br;
       }
       if (g == 0) {
-        best_v[wave][cc] = bv;
-        best_i[wave][cc] = bi;
-        if (SAMPLE) best_r[SAMPLE ? wave : 0][cc] = br;
+        best_v[wave][cc_j] = bv;
+        best_i[wave][cc_j] = bi;
+        if (SAMPLE) best_r[SAMPLE ? wave : 0][cc_j] = br;
       }
     }
     __builtin_amdgcn_s_waitcnt(0);  // this thread's gate stores are done
     __syncthreads();                // ... and every thread's
-    if (tid < bs) {
-      const int bb = tid;
+    if (tj < bs) {
+      const int bb = tj;
       float v = best_v[0][bb], raw = SAMPLE ? best_r[0][bb] : 0.f;
       int id = best_i[0][bb];
 #pragma unroll
