@@ -79,14 +79,21 @@ DEVI void load_xfrag(const float *__restrict__ X, int ldx, int M, int K, int m, 
   const int mc = m < M ? m : M - 1;
   const int kc = k0 + EPL <= K ? k0 : K - EPL;
   const float4 *p = (const float4 *)(X + (size_t)mc * ldx + kc);
+  // `ok` enters as an opaque all-ones / zero mask ANDed into the loaded bits:
+  // every lane then needs its load, so the compiler cannot sink the load into
+  // a branch on `ok` (a branch whose join drains every load in flight), and
+  // masked lanes get exact zeros whatever the clamped row holds
+  uint32_t mask = ok ? 0xffffffffu : 0u;
+  __asm__ volatile("" : "+v"(mask));
 #pragma unroll
   for (int q = 0; q < EPL / 4; ++q) {
     const float4 t = p[q];
-    v[q] = ok ? t : make_float4(0.f, 0.f, 0.f, 0.f);
+    v[q] = make_float4(__uint_as_float(__float_as_uint(t.x) & mask), __uint_as_float(__float_as_uint(t.y) & mask),
+                       __uint_as_float(__float_as_uint(t.z) & mask), __uint_as_float(__float_as_uint(t.w) & mask));
   }
 }
 
-template <typename WT, int MT, int WPT, int EPI, int KCM, int kWaves>
+template <typename WT, int MT, int WPT, int EPI, int KCM, int kWaves, int XA>
 __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
   constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP;
   constexpr int XF = XStage<WT>::XF;
@@ -155,7 +162,42 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
     }
   };
 
-  if (c0 < c1) {
+  if (XA == 2 && c0 < c1) {
+    // weights one chunk ahead, activations two (an activation chunk then has a
+    // whole chunk's products to arrive from L2 before it is staged).  Loads
+    // past the range are issued anyway (clamped inside load_w / load_xfrag to
+    // valid addresses) and never used, so no branch holds them: the compiler
+    // counts them and its waits leave the younger loads in flight.  Pays on
+    // long ranges only; a short one waits for the deeper fill instead.
+    u32x4 wa[KW], wb[KW];
+    float4 xa[IPT][EPL / 4], xb[IPT][EPL / 4];
+    // in flight at the loop head: chunk c's activations (xb) older than its
+    // weights (wa), the order the loop body issues them in
+    load_x(xa, c0);
+    __builtin_amdgcn_sched_barrier(0);
+    load_x(xb, c0 + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    load_w(wa, c0);
+    __builtin_amdgcn_sched_barrier(0);
+    store_x(xa, 0);
+    __syncthreads();
+    for (int c = c0; c < c1; c += 2) {
+      // chunk c: weights in wa, activations in LDS buffer 0 (xb holds chunk c + 1)
+      load_x(xa, c + 2);
+      load_w(wb, c + 1);
+      compute(wa, c, 0);
+      store_x(xb, 1);
+      __syncthreads();
+      if (c + 1 >= c1) break;
+      // chunk c + 1: weights in wb, activations in LDS buffer 1 (xa holds chunk c + 2)
+      load_x(xb, c + 3);
+      load_w(wa, c + 2);
+      compute(wb, c + 1, 1);
+      store_x(xa, 0);
+      __syncthreads();
+    }
+  } else if (c0 < c1) {
+    // weights and activations one chunk ahead
     u32x4 wa[KW], wb[KW];
     float4 xr[IPT][EPL / 4];
     load_x(xr, c0);
@@ -432,10 +474,17 @@ static void launch_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
     return;
   }
   dim3 grid(p.groups, p.ksplit, p.mgroups);
-  if (p.nw == 6)
-    hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 6>), grid, dim3(6 * 64), 0, st, a);
-  else
-    hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 8>), grid, dim3(8 * 64), 0, st, a);
+  // activations two chunks ahead once a workgroup's range is long enough to
+  // repay the deeper fill
+  const int nch = (a.KS + KCM - 1) / KCM, cpw = (nch + p.ksplit - 1) / p.ksplit;
+  const bool far = cpw >= 4;
+  if (p.nw == 6) {
+    if (far) hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 6, 2>), grid, dim3(6 * 64), 0, st, a);
+    else hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 6, 1>), grid, dim3(6 * 64), 0, st, a);
+  } else {
+    if (far) hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 8, 2>), grid, dim3(8 * 64), 0, st, a);
+    else hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 8, 1>), grid, dim3(8 * 64), 0, st, a);
+  }
 }
 
 template <typename WT, int MT>
