@@ -66,6 +66,38 @@ DEVI float wave_sum_dpp(float v) {
   const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
   return (r0 + r1) + (r2 + r3);
 }
+// Lane move within each 16-lane row: lane i reads lane (i + N) mod 16 of its row
+// (DPP row_ror), an ALU-latency exchange.
+template <int N>
+DEVI int row_ror(int v) {
+  static_assert(N >= 1 && N <= 15, "row_ror takes 1..15");
+  return __builtin_amdgcn_update_dpp(0, v, 0x120 + N, 0xf, 0xf, false);
+}
+template <int N>
+DEVI float row_ror(float v) { return __int_as_float(row_ror<N>(__float_as_int(v))); }
+template <int N>
+DEVI unsigned long long row_ror(unsigned long long v) {
+  const int lo = row_ror<N>((int)(uint32_t)v), hi = row_ror<N>((int)(uint32_t)(v >> 32));
+  return ((unsigned long long)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+// Maximum of a 64-bit key over the whole wave: within rows by rotations, then
+// the four row maxima read out.  Every lane gets the result.
+DEVI unsigned long long wave_max_u64(unsigned long long k) {
+  unsigned long long o;
+  o = row_ror<8>(k); k = o > k ? o : k;
+  o = row_ror<4>(k); k = o > k ? o : k;
+  o = row_ror<2>(k); k = o > k ? o : k;
+  o = row_ror<1>(k); k = o > k ? o : k;
+  unsigned long long best = 0;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)k, 16 * r);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(k >> 32), 16 * r);
+    const unsigned long long v = ((unsigned long long)hi << 32) | lo;
+    best = v > best ? v : best;
+  }
+  return best;
+}
 DEVI float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

@@ -136,6 +136,11 @@ DEVI void wave_select_mem(const float *__restrict__ pv, const int32_t *__restric
 }
 
 DEVI float sigm(float x) { return 1.f / (1.f + expf(-x)); }
+// The GRU's new state (1 - z) n + z h, written as n + z (h - n) with one
+// explicit fused multiply-add: left to the compiler, the two products of the
+// plain form get contracted differently from one kernel instantiation to the
+// next, and the instantiations would disagree in the last bit.
+DEVI float gru_mix(float z, float n, float h) { return fmaf(z, h - n, n); }
 
 constexpr int kBestSlots = 8;  // atomic targets per (position, row), spread to cut contention
 
@@ -255,8 +260,8 @@ __global__ __launch_bounds__(kStateWaves * 64) void head_state_kernel(HeadArgs h
     for (int e = 0; e < 4; ++e) {
       const float rg = sigm(gi[0][e] + gh[0][e]);
       const float zg = sigm(gi[1][e] + gh[1][e]);
-      const float ng = tanhf(gi[2][e] + rg * gh[2][e]);
-      out[e] = (1.f - zg) * ng + zg * hold[e];
+      const float ng = tanhf(fmaf(rg, gh[2][e], gi[2][e]));
+      out[e] = gru_mix(zg, ng, hold[e]);
     }
     const float4 o = make_float4(out[0], out[1], out[2], out[3]);
     *(float4 *)(sl + (size_t)b * ds + i) = o;
@@ -349,9 +354,9 @@ __global__ __launch_bounds__(256) void head_gru_elem_kernel(HeadArgs h, int j, c
   }
   const float *gy = h.gtab + (size_t)ysh * 3 * ds;  // b_ih is in G
   const float rg = sigm(gy[i] + gh[0]), zg = sigm(gy[ds + i] + gh[1]);
-  const float ng = tanhf(gy[2 * ds + i] + rg * gh[2]);
+  const float ng = tanhf(fmaf(rg, gh[2], gy[2 * ds + i]));
   const float hold = j > 1 ? hprev[(size_t)b * ds + i] : 0.f;
-  const float hn = (1.f - zg) * ng + zg * hold;
+  const float hn = gru_mix(zg, ng, hold);
   hnext[(size_t)b * ds + i] = hn;
   if (h.states) h.states[((size_t)b * depth + (j - 1)) * ds + i] = hn;
 }
@@ -825,9 +830,8 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
   u32x4 *us = (u32x4 *)(S + (size_t)bs * ds);           // [KS][64] u as B fragments
   u32x4 *w2s = us + kPersKS * 64;                       // [waves][KS][64] each wave's last W2 tile
   float4 *lbs = (float4 *)(w2s + kPersWaves * kPersKS * 64);  // [waves][tiles][64] this lane's L_base values
-  float *u_s = (float *)(lbs + kPersWaves * kPersTiles * 64);  // [bs][r] u of the position
   const int nu = (r + G - 1) / G;                              // u rows per workgroup: k < nu (R < r)
-  float *P_s = u_s + (size_t)bs * r;                           // [depth][bs][nu] W1[:, :d] H at the u rows
+  float *P_s = (float *)(lbs + kPersWaves * kPersTiles * 64);  // [depth][bs][nu] W1[:, :d] H at the u rows
   __shared__ float best_v[kPersWaves][16], best_r[SAMPLE ? kPersWaves : 1][16];
   __shared__ int best_i[kPersWaves][16];
   __shared__ int win_id[SAMPLE ? 64 : 1][BS];  // workgroup 0: each position's drafted token
@@ -858,6 +862,8 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
     rows[e] = *(const u32x4 *)(src + (size_t)ch * EPL);
   }
   for (int e = tid; e < bs * ds; e += kPersWaves * 64) S[e] = 0.f;
+  // the u fragments' unused columns (2 bs and up) stay zero for the whole launch
+  for (int e = tid; e < kPersKS * 64; e += kPersWaves * 64) us[e] = u32x4{0u, 0u, 0u, 0u};
   for (int e = tid; e < depth * bs * nu; e += kPersWaves * 64) {
     const int k = e % nu, b = (e / nu) % bs, jj = e / (nu * bs);
     const int R = min(blockIdx.x + k * G, r - 1);
@@ -874,8 +880,19 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
     int tj = threadIdx.x;
     __asm__ volatile("" : "+v"(tj));
     const int lane_j = tj & 63, cc_j = lane_j & 15;
+    // ---- y_{j-1}: anchor, forced token, or the argmax the previous wait delivered
+    if (tj < bs) {
+      int y;
+      if (j == 1) y = clamp_token(h.anchor[tj], V, h.err);
+      else if (h.forced) y = clamp_token(h.forced[(size_t)tj * depth + (j - 2)], V, h.err);
+      else y = ys[tj];
+      ys[tj] = y;
+    }
+    __syncthreads();
     // L_base of this lane's row and tiles, straight from memory into LDS (no
-    // registers held; complete by the wait before the u slots are published)
+    // registers held).  Issued after the barrier above, whose wait would
+    // otherwise take in its whole latency, and alongside the GRU's loads: the
+    // barrier after the GRU finds both complete.
     {
       const int bb = min(cc, bs - 1);
 #pragma unroll
@@ -886,15 +903,6 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
             (void __attribute__((address_space(3))) *)(lbs + ((size_t)wave * kPersTiles + q) * 64), 16, 0, 0);
       }
     }
-    // ---- y_{j-1}: anchor, forced token, or the argmax the previous wait delivered
-    if (tj < bs) {
-      int y;
-      if (j == 1) y = clamp_token(h.anchor[tj], V, h.err);
-      else if (h.forced) y = clamp_token(h.forced[(size_t)tj * depth + (j - 2)], V, h.err);
-      else y = ys[tj];
-      ys[tj] = y;
-    }
-    __syncthreads();
     // ---- S_{j-1} = GRU(E[y_{j-1}], S_{j-2}) in place; items beyond one per thread
     // (batches above 2 at d_s = 1024) load their gates here
     for (int it = tid; it < nit; it += kPersWaves * 64) {
@@ -923,8 +931,8 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float rg = sigm(gi[0][e] + ghv[0][e]), zg = sigm(gi[1][e] + ghv[1][e]);
-        const float ng = tanhf(gi[2][e] + rg * ghv[2][e]);
-        out[e] = (1.f - zg) * ng + zg * hold[e];
+        const float ng = tanhf(fmaf(rg, ghv[2][e], gi[2][e]));
+        out[e] = gru_mix(zg, ng, hold[e]);
       }
       s4 = make_float4(out[0], out[1], out[2], out[3]);
       *(float4 *)(S + (size_t)b * ds + i) = s4;
@@ -1005,33 +1013,29 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
     if (wave == 0) {
       unsigned long long w[4 * BS];
       const bool ok = poll_tagged<4 * BS>(h.uslot, bs * r, (unsigned long long)j, 32, h.abort_flag, h.err, h.poll_limit, w);
+      // u goes straight into the B fragments of the logits product: element
+      // (b, k) sits at k-step k / 32, lane 16 ((k / 8) mod 4) + column, slot k mod 8,
+      // where column b holds the bf16 high part of batch row b's u and column
+      // bs + b its low part (u - hi).  One product per tile and k-step then
+      // carries both; the two columns are summed after the k loop.
+      unsigned short *us16 = (unsigned short *)us;
 #pragma unroll
       for (int q = 0; q < 4 * BS; ++q) {
-        const int e = lane_j + 64 * q;
-        if (BS == 1 || e < bs * r) u_s[e] = __uint_as_float((uint32_t)(w[q] & 0xffffffffu));  // bs * r = 256 q-words at BS 1
+        const int e = lane_j + 64 * q;  // slot b * r + k (r = 256)
+        if (BS == 1 || e < bs * r) {
+          const float u = __uint_as_float((uint32_t)(w[q] & 0xffffffffu));
+          const __bf16 hi = (__bf16)u, lo = (__bf16)(u - (float)hi);
+          const int b = e >> 8, k = e & 255;
+          const int at = ((k >> 5) * 64 + ((k >> 3) & 3) * 16 + b) * 8 + (k & 7);
+          us16[at] = __builtin_bit_cast(unsigned short, hi);
+          us16[at + bs * 8] = __builtin_bit_cast(unsigned short, lo);
+        }
       }
       if (lane == 0) s_ok = ok;
     }
     __syncthreads();
     if (!s_ok) return;
-    // ---- logits: u as B fragments against the resident W2.  Column b holds the
-    // bf16 high part of batch row b's u, column bs + b its low part (u - hi), so
-    // one product per tile and k-step carries both; the two columns are summed
-    // after the k loop.
-    {
-      const int l = tid & 63, s = tid >> 6;  // kPersKS * 64 == kPersWaves * 64 items, one per thread
-      const int n = l & 15;
-      const int bb = n < bs ? n : min(n - bs, bs - 1);
-      const float *src = u_s + (size_t)bb * r + s * KSTEP + (l >> 4) * EPL;
-      const float4 v0 = *(const float4 *)src, v1 = *(const float4 *)(src + 4);
-      const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-      bf16x8 hi, lo;
-      split8(f, hi, lo);
-      u32x4 frag = n < bs ? __builtin_bit_cast(u32x4, hi) : __builtin_bit_cast(u32x4, lo);
-      if (n >= 2 * bs) frag = u32x4{0u, 0u, 0u, 0u};
-      us[tid] = frag;
-    }
-    __syncthreads();
+    // ---- logits: u as B fragments against the resident W2
     floatx4 acc[kPersTiles];
 #pragma unroll
     for (int q = 0; q < kPersTiles; ++q) acc[q] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -1114,24 +1118,32 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
     }
     __builtin_amdgcn_s_waitcnt(0);  // this thread's gate stores are done
     __syncthreads();                // ... and every thread's
-    if (tj < bs) {
-      const int bb = tj;
-      float v = best_v[0][bb], raw = SAMPLE ? best_r[0][bb] : 0.f;
-      int id = best_i[0][bb];
-#pragma unroll
-      for (int w = 1; w < kPersWaves; ++w)
-        if (better(best_v[w][bb], best_i[w][bb], v, id)) {
-          v = best_v[w][bb];
-          id = best_i[w][bb];
-          if (SAMPLE) raw = best_r[SAMPLE ? w : 0][bb];
+    if (wave == 0) {
+      // row b of wave 0 (lanes 16 b ..) merges the eight waves' bests of batch
+      // row b by rotations within the row
+      const int bb = lane_j >> 4, w = lane_j & 15;
+      const bool have = bb < bs && w < kPersWaves;
+      float v = have ? best_v[w][bb] : -INFINITY, raw = (SAMPLE && have) ? best_r[SAMPLE ? w : 0][bb] : 0.f;
+      int id = have ? best_i[w][bb] : INT_MAX;
+      auto step = [&](float ov, int oi, float orw) {
+        const bool take = better(ov, oi, v, id);
+        v = take ? ov : v;
+        id = take ? oi : id;
+        if (SAMPLE) raw = take ? orw : raw;
+      };
+      step(row_ror<8>(v), row_ror<8>(id), SAMPLE ? row_ror<8>(raw) : 0.f);
+      step(row_ror<4>(v), row_ror<4>(id), SAMPLE ? row_ror<4>(raw) : 0.f);
+      step(row_ror<2>(v), row_ror<2>(id), SAMPLE ? row_ror<2>(raw) : 0.f);
+      step(row_ror<1>(v), row_ror<1>(id), SAMPLE ? row_ror<1>(raw) : 0.f);
+      if (w == 0 && bb < bs) {
+        if (SAMPLE) {  // the raw logit goes out before the key that announces it
+          st_coherent(h.praw + ((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x, raw);
+          __builtin_amdgcn_s_waitcnt(0);
         }
-      if (SAMPLE) {  // the raw logit goes out before the key that announces it
-        st_coherent(h.praw + ((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x, raw);
-        __builtin_amdgcn_s_waitcnt(0);
+        // an empty slice (no valid id) publishes the smallest key
+        const unsigned long long key = id == INT_MAX ? 0ull : pack_key50(v, id);
+        st_slot(h.kslot + (size_t)bb * G + blockIdx.x, ((unsigned long long)j << 50) | key);
       }
-      // an empty slice (no valid id) publishes the smallest key
-      const unsigned long long key = id == INT_MAX ? 0ull : pack_key50(v, id);
-      st_slot(h.kslot + (size_t)bb * G + blockIdx.x, ((unsigned long long)j << 50) | key);
     }
     // ---- wait for every workgroup's top-1: the maximum key is y_j.  Also the
     // guard that no workgroup writes the next position's slots while another
@@ -1150,11 +1162,7 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
             const unsigned long long k = w[q] & ((1ull << 50) - 1);
             if (e >= b * G && e < (b + 1) * G && e < bs * G) best = k > best ? k : best;
           }
-#pragma unroll
-          for (int o = 32; o >= 1; o >>= 1) {
-            const unsigned long long other = __shfl_xor(best, o, 64);
-            best = other > best ? other : best;
-          }
+          best = wave_max_u64(best);
           if (lane == 0) {
             const int id = key50_id(best);
             ys[b] = min(max(id, 0), V - 1);
@@ -1198,7 +1206,7 @@ bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st) {
   const int nr = (D.r + 3 * D.ds + G - 1) / G;
   const size_t lds = (size_t)nr * (D.ds / 8) * 16 + sizeof(float) * (size_t)D.bs * D.ds +
                      sizeof(u32x4) * kPersKS * 64 + sizeof(u32x4) * kPersWaves * kPersKS * 64 +
-                     sizeof(float4) * kPersWaves * kPersTiles * 64 + sizeof(float) * (size_t)D.bs * D.r +
+                     sizeof(float4) * kPersWaves * kPersTiles * 64 +
                      sizeof(float) * (size_t)(D.B - 1) * D.bs * ((D.r + G - 1) / G);
   if (lds > 160 * 1024) return false;
   const bool dbg = h.final_logits != nullptr, smp = h.sample != 0;
