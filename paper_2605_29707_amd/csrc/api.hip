@@ -214,7 +214,7 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   };
   w.err = take(256);
   w.best = take((size_t)(D.B - 1) * bs * head_best_slots() * 8);
-  w.slots = take((size_t)bs * (D.r + w.GC) * 8);  // persistent rollout: u and key slots
+  w.slots = take((size_t)bs * (D.r + w.GC) * 8 * kSlotStride);  // persistent rollout: u and key slots
   w.hdr_words = o / 4;  // error word (+ rollout abort flag), best keys, slots: cleared at every step
   const int qkvw = (D.nq + 2 * D.nkv) * D.dh;
   w.X = take((size_t)M * D.d * 4);
@@ -785,7 +785,7 @@ HeadArgs head_args(domino_model_t m, int32_t batch, int32_t branch, char *ws, co
   h.seed_hi = 0u;
   h.praw = F(w.praw);
   h.uslot = (unsigned long long *)(ws + w.slots);
-  h.kslot = h.uslot + (size_t)batch * D.r;
+  h.kslot = h.uslot + (size_t)batch * D.r * kSlotStride;
   h.abort_flag = (unsigned *)(ws + w.err + 128);
   h.poll_limit = m->poll_limit;
   h.whh_p = base + m->whh.off;

@@ -779,9 +779,10 @@ DEVI unsigned long long pack_key50(float v, int id) {
 }
 DEVI int key50_id(unsigned long long k) { return (1 << kKeyIdBits) - 1 - (int)(k & ((1ull << kKeyIdBits) - 1)); }
 
-// Wave 0 polls `n` slots until each carries `tag` (top bits from `shift`);
-// lane l holds slots l, l+64, ... in w[].  Returns false on timeout (`limit`
-// polls made, none complete) or when another workgroup has aborted.
+// Wave 0 polls `n` slots (kSlotStride words apart) until each carries `tag`
+// (top bits from `shift`); lane l holds slots l, l+64, ... in w[].  Returns
+// false on timeout (`limit` polls made, none complete) or when another
+// workgroup has aborted.
 template <int MAXQ>
 DEVI bool poll_tagged(const unsigned long long *slots, int n, unsigned long long tag, int shift,
                       unsigned *abort_flag, int32_t *err, unsigned limit, unsigned long long (&w)[MAXQ]) {
@@ -796,7 +797,7 @@ DEVI bool poll_tagged(const unsigned long long *slots, int n, unsigned long long
       return false;
     }
 #pragma unroll
-    for (int q = 0; q < MAXQ; ++q) w[q] = ld_slot(slots + min(lane + 64 * q, n - 1));
+    for (int q = 0; q < MAXQ; ++q) w[q] = ld_slot(slots + (size_t)min(lane + 64 * q, n - 1) * kSlotStride);
     bool ready = true;
 #pragma unroll
     for (int q = 0; q < MAXQ; ++q) ready = ready && (w[q] >> shift) == tag;
@@ -965,7 +966,7 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
       if (lane == 0) {
         const float x = P_s[((size_t)(j - 1) * bs + b) * nu + k] + acc;
         const float u = x / (1.f + expf(-x));
-        st_slot(h.uslot + (size_t)b * r + R, ((unsigned long long)j << 32) | __float_as_uint(u));
+        st_slot(h.uslot + ((size_t)b * r + R) * kSlotStride, ((unsigned long long)j << 32) | __float_as_uint(u));
       }
     }
     // ---- gates of the next position, W_hh S_{j-1} + b_hh (plain device-scope
@@ -1142,7 +1143,7 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
         }
         // an empty slice (no valid id) publishes the smallest key
         const unsigned long long key = id == INT_MAX ? 0ull : pack_key50(v, id);
-        st_slot(h.kslot + (size_t)bb * G + blockIdx.x, ((unsigned long long)j << 50) | key);
+        st_slot(h.kslot + ((size_t)bb * G + blockIdx.x) * kSlotStride, ((unsigned long long)j << 50) | key);
       }
     }
     // ---- wait for every workgroup's top-1: the maximum key is y_j.  Also the
