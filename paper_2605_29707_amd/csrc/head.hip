@@ -833,8 +833,9 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
   float4 *lbs = (float4 *)(w2s + kPersWaves * kPersKS * 64);  // [waves][tiles][64] this lane's L_base values
   const int nu = (r + G - 1) / G;                              // u rows per workgroup: k < nu (R < r)
   float *P_s = (float *)(lbs + kPersWaves * kPersTiles * 64);  // [depth][bs][nu] W1[:, :d] H at the u rows
-  __shared__ float best_v[kPersWaves][16], best_r[SAMPLE ? kPersWaves : 1][16];
-  __shared__ int best_i[kPersWaves][16];
+  // each lane's best of its tiles: [wave][row group g][column]
+  __shared__ float best_v[kPersWaves][4][16], best_r[SAMPLE ? kPersWaves : 1][4][16];
+  __shared__ int best_i[kPersWaves][4][16];
   __shared__ int win_id[SAMPLE ? 64 : 1][BS];  // workgroup 0: each position's drafted token
   __shared__ int ys[kFusedBatch];
   __shared__ int s_ok;
@@ -872,7 +873,11 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
   }
   __syncthreads();
 
-  const int nit = bs * ds / 4;  // state items: four indices of one batch row
+  // state items: two indices of one batch row each, so that all eight waves
+  // share the GRU's transcendental arithmetic (one item per thread at one
+  // batch row and d_s = 1024)
+  constexpr int GE = 2;
+  const int nit = bs * ds / GE;
   for (int j = 1; j <= depth; ++j) {
     // the thread index, opaque to the compiler once per position: addresses
     // derived from it are recomputed here (a few instructions) instead of being
@@ -904,40 +909,36 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
             (void __attribute__((address_space(3))) *)(lbs + ((size_t)wave * kPersTiles + q) * 64), 16, 0, 0);
       }
     }
-    // ---- S_{j-1} = GRU(E[y_{j-1}], S_{j-2}) in place; items beyond one per thread
-    // (batches above 2 at d_s = 1024) load their gates here
+    // ---- S_{j-1} = GRU(E[y_{j-1}], S_{j-2}) in place
     for (int it = tid; it < nit; it += kPersWaves * 64) {
-      const int b = it / (ds / 4), i = (it % (ds / 4)) * 4;
+      const int b = it / (ds / GE), i = (it % (ds / GE)) * GE;
       // W_hh S_{j-2} + b_hh (stored by the previous position's row owners) and the G row, loaded together
-      float ghv[3][4];
+      float ghv[3][GE];
       {
         const float *gb = h.ghbuf + (size_t)((j - 1) & 1) * bs * 3 * ds + (size_t)b * 3 * ds + i;
 #pragma unroll
         for (int q = 0; q < 3; ++q) {
-          const float4 c0 = *(const float4 *)(h.bhh + q * ds + i);  // the gates at j = 1 (S = 0)
+          const float2 c0 = *(const float2 *)(h.bhh + q * ds + i);  // the gates at j = 1 (S = 0)
           const float v0 = ld_coherent(gb + q * ds), v1 = ld_coherent(gb + q * ds + 1);
-          const float v2 = ld_coherent(gb + q * ds + 2), v3 = ld_coherent(gb + q * ds + 3);
           ghv[q][0] = j > 1 ? v0 : c0.x;
           ghv[q][1] = j > 1 ? v1 : c0.y;
-          ghv[q][2] = j > 1 ? v2 : c0.z;
-          ghv[q][3] = j > 1 ? v3 : c0.w;
         }
       }
       const float *gy = h.gtab + (size_t)ys[b] * 3 * ds + i;
-      const float4 g0 = *(const float4 *)gy, g1 = *(const float4 *)(gy + ds), g2 = *(const float4 *)(gy + 2 * ds);
-      const float gi[3][4] = {{g0.x, g0.y, g0.z, g0.w}, {g1.x, g1.y, g1.z, g1.w}, {g2.x, g2.y, g2.z, g2.w}};
-      float4 s4 = *(const float4 *)(S + (size_t)b * ds + i);
-      const float hold[4] = {s4.x, s4.y, s4.z, s4.w};
-      float out[4];
+      const float2 g0 = *(const float2 *)gy, g1 = *(const float2 *)(gy + ds), g2 = *(const float2 *)(gy + 2 * ds);
+      const float gi[3][GE] = {{g0.x, g0.y}, {g1.x, g1.y}, {g2.x, g2.y}};
+      float2 s2 = *(const float2 *)(S + (size_t)b * ds + i);
+      const float hold[GE] = {s2.x, s2.y};
+      float out[GE];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
+      for (int e = 0; e < GE; ++e) {
         const float rg = sigm(gi[0][e] + ghv[0][e]), zg = sigm(gi[1][e] + ghv[1][e]);
         const float ng = tanhf(fmaf(rg, ghv[2][e], gi[2][e]));
         out[e] = gru_mix(zg, ng, hold[e]);
       }
-      s4 = make_float4(out[0], out[1], out[2], out[3]);
-      *(float4 *)(S + (size_t)b * ds + i) = s4;
-      if (blockIdx.x == 0 && h.states) *(float4 *)(h.states + ((size_t)b * depth + (j - 1)) * ds + i) = s4;
+      s2 = make_float2(out[0], out[1]);
+      *(float2 *)(S + (size_t)b * ds + i) = s2;
+      if (blockIdx.x == 0 && h.states) *(float2 *)(h.states + ((size_t)b * depth + (j - 1)) * ds + i) = s2;
     }
     __syncthreads();
     // ---- this workgroup's u rows against S_{j-1} into the tagged u slots
@@ -1097,35 +1098,24 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
           if (SAMPLE) br = take ? val[e] : br;
         }
       }
-      if (!rowok) {
-        bv = -INFINITY;
-        bi = INT_MAX;
-      }
-#pragma unroll
-      for (int o = 16; o <= 32; o <<= 1) {
-        const float ov = __shfl_xor(bv, o, 64);
-        const int oi = __shfl_xor(bi, o, 64);
-        const float orw = SAMPLE ? __shfl_xor(br, o, 64) : 0.f;
-        const bool take = better(ov, oi, bv, bi);
-        bv = take ? ov : bv;
-        bi = take ? oi : bi;
-        if (SAMPLE) br = take ? orw : br;
-      }
-      if (g == 0) {
-        best_v[wave][cc_j] = bv;
-        best_i[wave][cc_j] = bi;
-        if (SAMPLE) best_r[SAMPLE ? wave : 0][cc_j] = br;
-      }
+      // every lane's best goes to LDS as it is (no cross-row exchange here):
+      // the merge below takes 32 candidates per batch row
+      // (lanes of columns past the batch are written too and never read)
+      (&best_v[wave][0][0])[lane_j] = bv;
+      (&best_i[wave][0][0])[lane_j] = bi;
+      if (SAMPLE) (&best_r[SAMPLE ? wave : 0][0][0])[lane_j] = br;
     }
     __builtin_amdgcn_s_waitcnt(0);  // this thread's gate stores are done
     __syncthreads();                // ... and every thread's
     if (wave == 0) {
-      // row b of wave 0 (lanes 16 b ..) merges the eight waves' bests of batch
-      // row b by rotations within the row
-      const int bb = lane_j >> 4, w = lane_j & 15;
-      const bool have = bb < bs && w < kPersWaves;
-      float v = have ? best_v[w][bb] : -INFINITY, raw = (SAMPLE && have) ? best_r[SAMPLE ? w : 0][bb] : 0.f;
-      int id = have ? best_i[w][bb] : INT_MAX;
+      // wave 0 merges the 32 candidates (8 waves x 4 row groups) of batch row b
+      // in lanes 32 b ..: rotations within each 16-lane row, then across the
+      // two rows of a batch row
+      const int bb = lane_j >> 5, c = lane_j & 31;
+      const bool have = bb < bs;
+      float v = have ? best_v[c >> 2][c & 3][bb] : -INFINITY;
+      float raw = (SAMPLE && have) ? best_r[SAMPLE ? c >> 2 : 0][c & 3][bb] : 0.f;
+      int id = have ? best_i[c >> 2][c & 3][bb] : INT_MAX;
       auto step = [&](float ov, int oi, float orw) {
         const bool take = better(ov, oi, v, id);
         v = take ? ov : v;
@@ -1136,7 +1126,14 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
       step(row_ror<4>(v), row_ror<4>(id), SAMPLE ? row_ror<4>(raw) : 0.f);
       step(row_ror<2>(v), row_ror<2>(id), SAMPLE ? row_ror<2>(raw) : 0.f);
       step(row_ror<1>(v), row_ror<1>(id), SAMPLE ? row_ror<1>(raw) : 0.f);
-      if (w == 0 && bb < bs) {
+      // the odd rows take the best of the row before them (DPP row_bcast:15:
+      // lane 15 of rows 0 and 2 to every lane of rows 1 and 3), so lanes 16 and
+      // 48 hold the workgroup's best of batch rows 0 and 1
+      step(__int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x142, 0xa, 0xf, false)),
+           __builtin_amdgcn_update_dpp(id, id, 0x142, 0xa, 0xf, false),
+           SAMPLE ? __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(raw), __float_as_int(raw), 0x142, 0xa, 0xf, false))
+                  : 0.f);
+      if (c == 16 && have) {
         if (SAMPLE) {  // the raw logit goes out before the key that announces it
           st_coherent(h.praw + ((size_t)(j - 1) * bs + bb) * h.GC + blockIdx.x, raw);
           __builtin_amdgcn_s_waitcnt(0);
