@@ -141,8 +141,12 @@ Dims make_dims(const domino_model *m, int bs) {
 struct WsLayout {
   size_t err, best, slots, hdr_words, X, X2, A, FC, HP, QKV, Q, Kb, Vb, attn, O, WOp, F, DNp, H, LP, hbuf, ghbuf, ubuf, pval, pid,
       praw, XF, total;
+  // residual-epilogue tickets (in the cleared header) and row sums of squares
+  // of the deferred RMSNorms; 0: this layout has none
+  size_t tickets = 0, SSQ = 0;
   int GC, ldl;
 };
+
 
 struct Plans {
   GemmPlan qkv, wo, gateup, down, lm;
@@ -215,7 +219,8 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.err = take(256);
   w.best = take((size_t)(D.B - 1) * bs * head_best_slots() * 8);
   w.slots = take((size_t)bs * (D.r + w.GC) * 8 * kSlotStride);  // persistent rollout: u and key slots
-  w.hdr_words = o / 4;  // error word (+ rollout abort flag), best keys, slots: cleared at every step
+  w.tickets = take((size_t)2 * m->cfg.n_layers * kNormGroups * 4);
+  w.hdr_words = o / 4;  // error word (+ rollout abort flag), best keys, slots, tickets: cleared at every step
   const int qkvw = (D.nq + 2 * D.nkv) * D.dh;
   w.X = take((size_t)M * D.d * 4);
   w.X2 = take((size_t)M * D.d * 4);
@@ -232,6 +237,7 @@ bool layout(const domino_model *m, int bs, int max_ctx, int max_new, int beta, W
   w.WOp = take((size_t)p.wo.ksplit * M * D.d * 4);
   w.F = take((size_t)M * D.ffn * 4);
   w.DNp = take((size_t)p.down.ksplit * M * D.d * 4);
+  w.SSQ = take((size_t)kNormGroups * M * 4);
   w.H = take((size_t)Mh * D.d * 4);
   w.ldl = m->lm.NT * 16;
   w.LP = take((size_t)Mh * w.ldl * 4);  // [L_base | pad | P] per draft row
@@ -662,21 +668,53 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
   // the residual stream ping-pongs between two buffers: every RMSNorm launch
   // reads one and writes the updated residual to the other
   float *xc = F(w.X), *xn = F(w.X2);
+  // Fused norms (one batch row's block on the skinny kernel): the O and down
+  // projections end with the residual update (EPI_RESID), which also leaves the
+  // next RMSNorm's input times its gain in A and the row sums of squares in SSQ;
+  // the gate/up and next QKV projections then scale their output rows by the
+  // norm factor.  Only layer 0's RMSNorm (of the embedding rows) and the final
+  // one remain launches of their own.  The tickets start at zero: layer 0's
+  // RMSNorm clears the header (clear_header), or the caller cleared it before
+  // (the training forward); a layout without tickets never fuses.
+  auto fusable = [](const GemmPlan &pl) { return !pl.wide && pl.pgrid == 0 && pl.WPT == 1 && pl.mgroups == 1; };
+  const bool fuse = w.tickets && w.SSQ && n_new == 0 && m->bf16 && fusable(p.qkv) && fusable(p.wo) &&
+                    fusable(p.gateup) && fusable(p.down) && p.wo.groups <= kNormGroups &&
+                    p.down.groups <= kNormGroups && D.d % 4 == 0;
+  unsigned *tickets = fuse ? (unsigned *)(ws + w.tickets) : nullptr;
+  float *SSQ = fuse ? F(w.SSQ) : nullptr;
+  auto resid = [&](GemmArgs &a, const void *gain, int slot) {
+    a.res_in = xc;
+    a.res_out = xn;
+    a.res_xg = F(w.A);
+    a.res_ssq = SSQ;
+    a.res_gain = gain;
+    a.res_tickets = tickets + (size_t)slot * kNormGroups;
+  };
+  auto deferred = [&](GemmArgs &a, int ng) {
+    a.rs_ssq = SSQ;
+    a.rs_ng = ng;
+    a.rs_d = D.d;
+    a.rs_eps = m->cfg.rms_eps;
+  };
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const char *ck = (const char *)ctx_k + l * layer_elems * m->esz;
     const char *cv = (const char *)ctx_v + l * layer_elems * m->esz;
     // residual += previous layer's down projection, then the attention RMSNorm
-    prof_begin(m, DOMINO_KC_NORM, st);
-    // (layer 0: the residual starts as the embedding of [anchor, MASK, ...])
-    launch_add_norm(D, xc, xn, D.d, F(w.DNp), l > 0 ? p.down.ksplit : 0, rstride, m->attn_norm[l], F(w.A), D.d,
-                    M, D.d, false, l == 0 ? m->embed : nullptr, anchor_ids, err, st, spec.tokens,
-                    l == 0 && clear_header ? (uint32_t *)ws : nullptr, (int)w.hdr_words);
-    std::swap(xc, xn);
-    prof_end(m, DOMINO_KC_NORM, st);
+    // (fused: done by that down projection, except at layer 0)
+    if (l == 0 || !fuse) {
+      prof_begin(m, DOMINO_KC_NORM, st);
+      // (layer 0: the residual starts as the embedding of [anchor, MASK, ...])
+      launch_add_norm(D, xc, xn, D.d, F(w.DNp), l > 0 ? p.down.ksplit : 0, rstride, m->attn_norm[l], F(w.A), D.d,
+                      M, D.d, false, l == 0 ? m->embed : nullptr, anchor_ids, err, st, spec.tokens,
+                      l == 0 && clear_header ? (uint32_t *)ws : nullptr, (int)w.hdr_words);
+      std::swap(xc, xn);
+      prof_end(m, DOMINO_KC_NORM, st);
+    }
 
     prof_begin(m, DOMINO_KC_QKV, st);
     GemmArgs a = gemm_args(base + m->qkv[l].off, m->qkv[l], 0, m->qkv[l].NT, qkvw, F(w.A), D.d, Ma, D.d, F(w.QKV),
                            qkvw, p.qkv);
+    if (fuse && l > 0) deferred(a, p.down.groups);
     if (!proj(EPI_STORE, a, p.qkv)) return fail(DOMINO_ERR_UNSUPPORTED, "qkv projection refused");
     prof_end(m, DOMINO_KC_QKV, st);
 
@@ -691,26 +729,40 @@ domino_status run_layers(domino_model_t m, const Dims &D, const Plans &p, const 
 
     prof_begin(m, DOMINO_KC_WO, st);
     a = gemm_args(base + m->wo[l].off, m->wo[l], 0, m->wo[l].NT, D.d, F(w.O), qd, M, qd, F(w.WOp), D.d, p.wo);
-    if (!proj(EPI_STORE, a, p.wo)) return fail(DOMINO_ERR_UNSUPPORTED, "wo projection refused");
+    if (fuse) {  // residual += attention output, and the FFN RMSNorm's statistics
+      resid(a, m->ffn_norm[l], 2 * l);
+      if (!proj(EPI_RESID, a, p.wo)) return fail(DOMINO_ERR_UNSUPPORTED, "wo projection refused");
+      std::swap(xc, xn);
+    } else if (!proj(EPI_STORE, a, p.wo)) {
+      return fail(DOMINO_ERR_UNSUPPORTED, "wo projection refused");
+    }
     prof_end(m, DOMINO_KC_WO, st);
 
-    // residual += attention output, then the FFN RMSNorm
-    prof_begin(m, DOMINO_KC_NORM, st);
-    launch_add_norm(D, xc, xn, D.d, F(w.WOp), p.wo.ksplit, rstride, m->ffn_norm[l], F(w.A), D.d, M, D.d, false,
-                    nullptr, nullptr, err, st);
-    std::swap(xc, xn);
-    prof_end(m, DOMINO_KC_NORM, st);
+    if (!fuse) {  // residual += attention output, then the FFN RMSNorm
+      prof_begin(m, DOMINO_KC_NORM, st);
+      launch_add_norm(D, xc, xn, D.d, F(w.WOp), p.wo.ksplit, rstride, m->ffn_norm[l], F(w.A), D.d, M, D.d, false,
+                      nullptr, nullptr, err, st);
+      std::swap(xc, xn);
+      prof_end(m, DOMINO_KC_NORM, st);
+    }
 
     prof_begin(m, DOMINO_KC_GATEUP, st);
     a = gemm_args(base + m->gateup[l].off, m->gateup[l], 0, m->gateup[l].NT, D.ffn, F(w.A), D.d, M, D.d, F(w.F),
                   D.ffn, p.gateup);
+    if (fuse) deferred(a, p.wo.groups);
     if (!proj(EPI_SWIGLU, a, p.gateup)) return fail(DOMINO_ERR_UNSUPPORTED, "gateup projection refused");
     prof_end(m, DOMINO_KC_GATEUP, st);
 
     prof_begin(m, DOMINO_KC_DOWN, st);
     a = gemm_args(base + m->down[l].off, m->down[l], 0, m->down[l].NT, D.d, F(w.F), D.ffn, M, D.ffn, F(w.DNp), D.d,
                   p.down);
-    if (!proj(EPI_STORE, a, p.down)) return fail(DOMINO_ERR_UNSUPPORTED, "down projection refused");
+    if (fuse && l + 1 < m->cfg.n_layers) {  // residual += FFN output, and the next attention RMSNorm's statistics
+      resid(a, m->attn_norm[l + 1], 2 * l + 1);
+      if (!proj(EPI_RESID, a, p.down)) return fail(DOMINO_ERR_UNSUPPORTED, "down projection refused");
+      std::swap(xc, xn);
+    } else if (!proj(EPI_STORE, a, p.down)) {
+      return fail(DOMINO_ERR_UNSUPPORTED, "down projection refused");
+    }
     prof_end(m, DOMINO_KC_DOWN, st);
   }
 

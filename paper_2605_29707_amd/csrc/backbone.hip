@@ -900,7 +900,7 @@ __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__rest
 // weights; one wave per row.  The first CB chunks' output rows and maxima are
 // loaded together with the statistics pass (at clamped chunk indices, so
 // CB sized to the usual chunk count: 40 for the chunked kernel at one batch
-// row, 8 after the one-pass kernel), so a context of up to CB chunks costs
+// row, 8 or 24 after the one-pass kernel), so a context of up to CB chunks costs
 // one memory round trip: lane c folds chunks c, c + 64, ... into a
 // running (max, sum) pair, the wave combines the pairs, then the rows are
 // weighted and summed in chunk order.
@@ -1146,6 +1146,9 @@ void launch_attention(const Dims &D, const float *Q, const float *Kb, const floa
       const int items = D.bs * D.nq * D.B;
       if (ngrp <= 8)
         hipLaunchKernelGGL((attn_combine_kernel<128, 8>), dim3((items + 3) / 4), dim3(256), 0, st, part, ctx_lens,
+                           max_ctx, O, D.bs, D.B, D.nq, nch, kpw);
+      else if (ngrp <= 24)  // one batch row at a 1024-key context: 17 runs
+        hipLaunchKernelGGL((attn_combine_kernel<128, 24>), dim3((items + 3) / 4), dim3(256), 0, st, part, ctx_lens,
                            max_ctx, O, D.bs, D.B, D.nq, nch, kpw);
       else
         hipLaunchKernelGGL((attn_combine_kernel<128, 40>), dim3((items + 3) / 4), dim3(256), 0, st, part, ctx_lens,

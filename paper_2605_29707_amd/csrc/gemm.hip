@@ -93,6 +93,58 @@ DEVI void load_xfrag(const float *__restrict__ X, int ldx, int M, int K, int m, 
   }
 }
 
+// EPI_RESID, after this workgroup's partial went out (device-scope stores):
+// wait for the stores, take a ticket of the column group, and if it is the
+// group's last split, form res_in + partial_0 + ... + partial_{ksplit-1} (split
+// order: the result does not depend on which split came last) over the group's
+// TW * 16 columns and every row, write it and its gain-scaled copy, and the
+// row sums of its squares.  `sq` is LDS scratch of `nsq` floats.
+template <typename WT, int TW>
+DEVI void resid_epilogue(const GemmArgs &a, int grp, float *sq, int nsq) {
+  __shared__ int s_last;
+  __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores are complete
+  __syncthreads();                // ... and every thread's
+  if (threadIdx.x == 0)
+    s_last = __hip_atomic_fetch_add(a.res_tickets + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+             (unsigned)(a.ksplit - 1);
+  __syncthreads();
+  if (!s_last) return;
+  const int c0 = grp * TW * 16;
+  constexpr int PR = TW * 4;  // float4 items per row of the group
+  const WT *gain = (const WT *)a.res_gain;
+  for (int it = threadIdx.x; it < a.M * PR; it += blockDim.x) {
+    const int m = it / PR, n = c0 + 4 * (it % PR);
+    float ss = 0.f;
+    if (n < a.N) {  // N is a multiple of 4
+      const size_t at = (size_t)m * a.ldy + n;
+      float4 v = *(const float4 *)(a.res_in + at);
+      for (int sp = 0; sp < a.ksplit; ++sp) {
+        const unsigned long long *p = (const unsigned long long *)(a.Y + sp * a.ysplit + at);
+        const unsigned long long p0 = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned long long p1 = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        v.x += __uint_as_float((uint32_t)p0);
+        v.y += __uint_as_float((uint32_t)(p0 >> 32));
+        v.z += __uint_as_float((uint32_t)p1);
+        v.w += __uint_as_float((uint32_t)(p1 >> 32));
+      }
+      *(float4 *)(a.res_out + at) = v;
+      *(float4 *)(a.res_xg + at) = make_float4(v.x * to_f32(gain[n]), v.y * to_f32(gain[n + 1]),
+                                               v.z * to_f32(gain[n + 2]), v.w * to_f32(gain[n + 3]));
+      ss = fmaf(v.x, v.x, ss);
+      ss = fmaf(v.y, v.y, ss);
+      ss = fmaf(v.z, v.z, ss);
+      ss = fmaf(v.w, v.w, ss);
+    }
+    if (it < nsq) sq[it] = ss;
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < a.M) {  // row sums in column order
+    float t = 0.f;
+    for (int i = 0; i < PR; ++i) t += sq[threadIdx.x * PR + i];
+    a.res_ssq[(size_t)grp * a.M + threadIdx.x] = t;
+  }
+}
+
 template <typename WT, int MT, int WPT, int EPI, int KCM, int kWaves, int XA>
 __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
   constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP;
@@ -121,6 +173,17 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
   floatx4 acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  // deferred RMSNorm: the producer's per-group sums of squares of this
+  // workgroup's rows, one load per thread into LDS now (in flight with the
+  // first chunks), summed by the epilogue (after the loop's barriers)
+  __shared__ float rs_part[kNormGroups * MT * 16];
+  const int rs_ng = min(a.rs_ng, kNormGroups);  // (the host keeps rs_ng within kNormGroups)
+  const int rs_n = a.rs_ssq ? rs_ng * MT * 16 : 0;  // [group][row of the m-group]
+  for (int e = tid; e < rs_n; e += kWaves * 64) {
+    const int g = e / (MT * 16), m = min(mbase + e % (MT * 16), a.M - 1);
+    rs_part[e] = a.rs_ssq[(size_t)g * a.M + m];
+  }
 
   auto load_w = [&](u32x4 (&w)[KW], int c) {
 #pragma unroll
@@ -226,6 +289,17 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
     }
   }
 
+  if (a.rs_ssq) {  // (the loop's barriers have made rs_part visible)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      float t = 0.f;
+      for (int g = 0; g < rs_ng; ++g) t += rs_part[g * MT * 16 + mt * 16 + (lane & 15)];
+      const float rs = 1.0f / sqrtf(t / (float)a.rs_d + a.rs_eps);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[mt][e] *= rs;
+    }
+  }
+
   // waves sharing a tile: fold into the first one
   if (WPT > 1) {
     if (wave % WPT) {
@@ -264,6 +338,24 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
       for (int e = 0; e < 4; ++e)
         if (col + e < a.N) y[e] = silu_f(acc[mt][e]) * uv[e];
     }
+    return;
+  }
+  if (EPI == EPI_RESID) {
+    // this split's partial, written through to the device coherence point
+    if (wave % WPT == 0 && tvalid) {
+      const int n = tile * 16 + 4 * (lane >> 4);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = mbase + mt * 16 + (lane & 15);
+        if (m >= a.M) continue;
+        unsigned long long *y = (unsigned long long *)(Y + (size_t)m * a.ldy + n);  // n + 4 <= N, ldy % 4 == 0
+        __hip_atomic_store(y, ((unsigned long long)__float_as_uint(acc[mt][1]) << 32) | __float_as_uint(acc[mt][0]),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(y + 1, ((unsigned long long)__float_as_uint(acc[mt][3]) << 32) | __float_as_uint(acc[mt][2]),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    resid_epilogue<WT, kWaves / WPT>(a, grp, (float *)&xch[0][0][0], sizeof(xch) / sizeof(float));
     return;
   }
   if (wave % WPT || !tvalid) return;
@@ -492,9 +584,11 @@ static void launch_m(int epi, const GemmArgs &a, const GemmPlan &p, hipStream_t 
   constexpr int K1 = 16 / MT, K2 = 8 / MT;
   if (p.kcm == K2) {
     if (epi == EPI_SWIGLU) launch_t<WT, MT, EPI_SWIGLU, K2>(a, p, st);
+    else if (epi == EPI_RESID) launch_t<WT, MT, EPI_RESID, K2>(a, p, st);
     else launch_t<WT, MT, EPI_STORE, K2>(a, p, st);
   } else {
     if (epi == EPI_SWIGLU) launch_t<WT, MT, EPI_SWIGLU, K1>(a, p, st);
+    else if (epi == EPI_RESID) launch_t<WT, MT, EPI_RESID, K1>(a, p, st);
     else launch_t<WT, MT, EPI_STORE, K1>(a, p, st);
   }
 }

@@ -6,7 +6,13 @@
 
 namespace dk {
 
-enum { EPI_STORE = 0, EPI_SWIGLU = 2 };
+// Most column groups a residual epilogue (and so a deferred RMSNorm) covers.
+constexpr int kNormGroups = 64;
+
+// EPI_STORE: outputs (or K-split partials) stored; EPI_SWIGLU: silu(gate) * up
+// of interleaved (gate, up) tile pairs; EPI_RESID: K-split partials, then the
+// residual update with the next RMSNorm's statistics (GemmArgs res_*)
+enum { EPI_STORE = 0, EPI_SWIGLU = 2, EPI_RESID = 3 };
 
 struct GemmArgs {
   const void *P;   // packed weights
@@ -22,6 +28,21 @@ struct GemmArgs {
   int ksplit;
   void *xf = nullptr;  // wide kernel: scratch for the activations' hi/lo fragment planes
                        // (gemm_wide_scratch_bytes(M, K) bytes)
+  // Deferred RMSNorm of the activations (skinny kernel): X holds x * gain and
+  // every output row m is scaled by rsqrt(sum_g rs_ssq[g][m] / rs_d + rs_eps),
+  // the per-row sums of squares left by the producing projection's EPI_RESID.
+  const float *rs_ssq = nullptr;
+  int rs_ng = 0, rs_d = 0;
+  float rs_eps = 0.f;
+  // EPI_RESID (skinny kernel, K split over workgroups): each split's partial
+  // goes out to the device coherence point and the last split of a column group
+  // to arrive (res_tickets[group], zero at launch) adds the partials in split
+  // order to res_in, writes the sum to res_out and, times res_gain, to res_xg,
+  // and the sum's squares over the group's columns to res_ssq[group][m].
+  const float *res_in = nullptr;
+  float *res_out = nullptr, *res_xg = nullptr, *res_ssq = nullptr;
+  const void *res_gain = nullptr;
+  unsigned *res_tickets = nullptr;
 };
 
 struct GemmPlan {
