@@ -24,7 +24,7 @@ HBM_PEAK = 8.0e12  # B/s, MI355X HBM3E
 
 # HBM bytes per LM-head launch from rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by a 1 GiB copy),
 # valid for the GEMM source with this sha1 (see profiles/lm_head_gemm_qwen3_8b_bs1.md)
-LMHEAD_TRAFFIC = {"gemm_sha1": "4f3faa3f3efb9853984243d62c1cb39e84e9966a", "bytes": 1257955487,
+LMHEAD_TRAFFIC = {"gemm_sha1": "006a7f4d6799993e62c02698dee41828284515b3", "bytes": 1257953704,
                   "config": "qwen3_8b"}
 
 
