@@ -722,12 +722,17 @@ __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__rest
 
   // scores of one block against this wave's rows -> online softmax -> P V.
   // HILO: the block's keys are fp32 (hi parts in buffer 0, lo parts in buffer 1).
+  // Only the 16-key tiles holding valid keys are multiplied (and only the
+  // 32-key steps of P V that cover them): a short run, such as the block's own
+  // 16 keys, skips three quarters of the products.
   auto fold = [&](int nvalid, bool hilo, int bb) {
     const uint16_t *Kh = Kbuf(bb), *Vh = Vbuf(bb), *Kl = Kbuf(1), *Vl = Vbuf(1);
+    const int nkt = (nvalid + 15) / 16;  // workgroup-uniform
     floatx4 sacc[kFlashKB / 16];
 #pragma unroll
     for (int t = 0; t < kFlashKB / 16; ++t) {
       sacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+      if (t >= nkt) continue;
 #pragma unroll
       for (int s = 0; s < DH / 32; ++s) {
         const bf16x8 kh = ld_frag(Kh + (16 * t + cc) * kFlashKP + 32 * s + 8 * g);
@@ -773,6 +778,7 @@ __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__rest
     }
 #pragma unroll
     for (int u = 0; u < kFlashKB / 32; ++u) {
+      if (2 * u >= nkt) break;  // (keys past the valid tiles have p = 0)
       const float f[8] = {p[2 * u][0], p[2 * u][1], p[2 * u][2], p[2 * u][3],
                           p[2 * u + 1][0], p[2 * u + 1][1], p[2 * u + 1][2], p[2 * u + 1][3]};
       bf16x8 ph, pl;
@@ -833,6 +839,22 @@ __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__rest
     }
   };
   if (nblk > 0) load_blk(0);
+  // the block's own keys [max(k0, n), k1): this thread's first PB items (rows
+  // kk = e / 32 of e = tid + T q, 4 dims each; every row of a 16-row block at
+  // 256 threads) are loaded now, in flight with the context keys and Q, not
+  // after the context blocks
+  const int b0 = max(k0, n) - n, nb = k1 - n - b0;
+  constexpr int PB = 2;
+  float4 pk[PB], pv[PB];
+  if (nb > 0) {
+#pragma unroll
+    for (int q = 0; q < PB; ++q) {
+      const int e = tid + T * q, kk = e / (DH / 4), d4 = e % (DH / 4);
+      const size_t row = (((size_t)b * B + b0 + min(kk, nb - 1)) * nkv + kvh) * DH;
+      pk[q] = *(const float4 *)(Kb + row + 4 * d4);
+      pv[q] = *(const float4 *)(Vb + row + 4 * d4);
+    }
+  }
   // this wave's query rows: Q^T fragments (dims 32 s + 8 g .. of row 16 wave + cc),
   // loaded after the first block's keys so the two memory round trips overlap
   {
@@ -855,14 +877,19 @@ __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__rest
   }
 
   // ---- block keys [max(k0, n), k1): fp32, hi parts in buffer 0, lo in buffer 1
-  const int b0 = max(k0, n) - n, nb = k1 - n - b0;
   if (nb > 0) {
     __syncthreads();  // both buffers free
-    for (int e = tid; e < kFlashKB * DH / 4; e += T) {
-      const int kk = e / (DH / 4), d4 = e % (DH / 4);
+    // rows the fold reads: the 32-key steps covering the nb keys (the rest stay unwritten)
+    const int nrow = (nb + 31) / 32 * 32;
+#pragma unroll
+    for (int qi = 0; qi < kFlashKB * DH / 4 / T; ++qi) {
+      const int e = tid + T * qi, kk = e / (DH / 4), d4 = e % (DH / 4);
+      if (T * qi >= nrow * (DH / 4)) break;  // workgroup-uniform
       const size_t row = (((size_t)b * B + b0 + min(kk, nb - 1)) * nkv + kvh) * DH;
-      const float4 kv = kk < nb ? *(const float4 *)(Kb + row + 4 * d4) : make_float4(0.f, 0.f, 0.f, 0.f);
-      const float4 vv = kk < nb ? *(const float4 *)(Vb + row + 4 * d4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 kv = kk >= nb ? make_float4(0.f, 0.f, 0.f, 0.f) : qi < PB ? pk[qi < PB ? qi : 0]
+                                                                             : *(const float4 *)(Kb + row + 4 * d4);
+      const float4 vv = kk >= nb ? make_float4(0.f, 0.f, 0.f, 0.f) : qi < PB ? pv[qi < PB ? qi : 0]
+                                                                             : *(const float4 *)(Vb + row + 4 * d4);
       uint2 hi, lo;
       split4(kv, hi, lo);
       *(uint2 *)(Kbuf(0) + kk * kFlashKP + 4 * d4) = hi;
