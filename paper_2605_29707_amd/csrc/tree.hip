@@ -220,6 +220,16 @@ __global__ __launch_bounds__(256) void argmax_partial_kernel(int nn, int V, cons
   }
 }
 
+// The walk of one batch row.  Every table the walk needs is formed in
+// parallel first, with all of its memory reads in flight together: which nodes
+// have children (the rows argmax_partial_kernel took), each such node's argmax
+// R from its chunk partials (a wave per node, four nodes per pass), and the
+// first child of each node whose token is that R.  The walk from the root is
+// then a chase through LDS.  Only if it stops on a node without children (a
+// leaf of a tree, or the end of a fully accepted chain) is that row's argmax
+// needed, which the workgroup scans itself.
+constexpr int kWalkMaxNodes = 1024;
+
 template <typename LT>
 __global__ __launch_bounds__(256) void accept_walk_kernel(int nn, int V, int B, const int32_t *__restrict__ tok,
                                                           const int32_t *__restrict__ par,
@@ -228,103 +238,130 @@ __global__ __launch_bounds__(256) void accept_walk_kernel(int nn, int V, int B, 
                                                           const LT *__restrict__ logits,
                                                           int32_t *acc_len, int32_t *acc_nodes,
                                                           int32_t *out_tok, int32_t *err) {
-  const int b = blockIdx.x;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nch = (V + ACH - 1) / ACH;
   __shared__ float sv[4];
   __shared__ int si[4];
-  __shared__ int s_next;
-  // the tree: node 0 is the root, every other node's parent comes before it
-  for (int c = threadIdx.x; c < nn; c += blockDim.x) {
-    const int p = par[(size_t)b * nn + c];
-    if (!((c == 0) ? (p == -1) : (p >= 0 && p < c))) raise_error(err, DEV_BAD_TREE);
+  __shared__ int s_R[kWalkMaxNodes], s_next[kWalkMaxNodes];
+  __shared__ unsigned char s_kid[kWalkMaxNodes];
+  const int32_t *pr = par + (size_t)b * nn, *tk = tok + (size_t)b * nn;
+  for (int c = tid; c < nn; c += blockDim.x) {
+    s_kid[c] = 0;
+    s_next[c] = INT_MAX;
   }
-  int cur = 0, a = 0;
-  int R = 0;
+  __syncthreads();
+  // the tree: node 0 is the root, every other node's parent comes before it
+  for (int c = tid; c < nn; c += blockDim.x) {
+    const int p = pr[c];
+    if (!((c == 0) ? (p == -1) : (p >= 0 && p < c))) raise_error(err, DEV_BAD_TREE);
+    if (c > 0 && p >= 0 && p < c) s_kid[p] = 1;
+  }
+  __syncthreads();
+  // R of every node with children: wave w takes nodes w + 4 q (+ 16 per pass),
+  // lanes over the vocabulary chunks
+  for (int c0 = wave; c0 < nn; c0 += 16) {
+    float bv[4];
+    int bi[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      bv[q] = -INFINITY;
+      bi[q] = INT_MAX;
+    }
+    for (int k0 = 0; k0 < nch; k0 += 64) {
+      float lv[4];
+      int li[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {  // clamped: every load valid, all in flight together
+        const int c = min(c0 + 4 * q, nn - 1), k = min(k0 + lane, nch - 1);
+        const size_t o = ((size_t)b * nn + c) * nch + k;
+        lv[q] = part_v[o];
+        li[q] = part_i[o];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = c0 + 4 * q;
+        if (c < nn && s_kid[c] && k0 + lane < nch && better(lv[q], li[q], bv[q], bi[q])) {
+          bv[q] = lv[q];
+          bi[q] = li[q];
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      wave_best(bv[q], bi[q]);
+      const int c = c0 + 4 * q;
+      if (lane == 0 && c < nn) s_R[c] = bi[q];
+    }
+  }
+  __syncthreads();
+  // each node's child carrying R (children have distinct tokens; the first one)
+  for (int c = 1 + tid; c < nn; c += blockDim.x) {
+    const int p = pr[c];
+    if (p >= 0 && p < c && tk[c] == s_R[p]) atomicMin(&s_next[p], c);
+  }
+  __syncthreads();
+  // the walk (every thread follows it)
+  int cur = 0, a = 0, R = 0;
+  bool leaf = false;
   while (true) {
-    // R = argmax of row cur: from its chunk partials when cur has children
-    // (the partial launch took exactly those rows), else by a scan of the row
-    bool has_child = false;
-    for (int c = cur + 1 + (int)threadIdx.x; c < nn; c += blockDim.x) has_child |= par[(size_t)b * nn + c] == cur;
-    has_child = __syncthreads_or(has_child);
-    float bv = -INFINITY;
-    int bi = INT_MAX;
-    if (has_child) {
-      const size_t o = ((size_t)b * nn + cur) * nch;
-      for (int c = threadIdx.x; c < nch; c += blockDim.x)
-        if (better(part_v[o + c], part_i[o + c], bv, bi)) {
-          bv = part_v[o + c];
-          bi = part_i[o + c];
-        }
-    } else {
-      // ids visited in increasing order per thread: a strict > keeps the smallest id
-      const LT *row = logits + ((size_t)b * nn + cur) * V;
-      constexpr int EV = LVec<LT>::N, U = 16;
-      if (V % EV == 0) {  // 16-byte rows: U loads of EV values per thread in flight
-        const int nv = V / EV;
-        for (int g0 = 0; g0 < nv; g0 += 256 * U) {
-          u32x4 x[U];
-#pragma unroll
-          for (int q = 0; q < U; ++q) x[q] = *(const u32x4 *)(row + (size_t)min(g0 + q * 256 + (int)threadIdx.x, nv - 1) * EV);
-#pragma unroll
-          for (int q = 0; q < U; ++q) {
-            const int gi = g0 + q * 256 + (int)threadIdx.x;
-            fold_vec<LT>(x[q], gi * EV, gi < nv ? V : 0, bv, bi);
-          }
-        }
-      } else {
-        for (int v0 = threadIdx.x; v0 < V; v0 += 256 * U) {
-          float x[U];
-#pragma unroll
-          for (int q = 0; q < U; ++q) x[q] = ld_logit<LT>(row + min(v0 + q * 256, V - 1));
-#pragma unroll
-          for (int q = 0; q < U; ++q) {
-            const int v = v0 + q * 256;
-            const float ov = order_val(x[q]);
-            if (v < V && (ov > bv || bi == INT_MAX)) {
-              bv = ov;
-              bi = v;
-            }
-          }
-        }
-      }
+    if (!s_kid[cur]) {
+      leaf = true;
+      break;
     }
-    wave_best(bv, bi);
-    if ((threadIdx.x & 63) == 0) {
-      sv[threadIdx.x >> 6] = bv;
-      si[threadIdx.x >> 6] = bi;
-    }
-    __syncthreads();
-    bv = sv[0];
-    bi = si[0];
-    for (int w = 1; w < 4; ++w)
-      if (better(sv[w], si[w], bv, bi)) {
-        bv = sv[w];
-        bi = si[w];
-      }
-    R = bi;
+    R = s_R[cur];
     if (a >= B - 1) break;  // walk bound
-    // the child of cur whose token is R (children have distinct tokens; take the first)
-    if (threadIdx.x == 0) s_next = INT_MAX;
-    __syncthreads();
-    for (int c = threadIdx.x; c < nn; c += blockDim.x)
-      if (c > 0 && par[(size_t)b * nn + c] == cur && tok[(size_t)b * nn + c] == R) atomicMin(&s_next, c);
-    __syncthreads();
-    const int nx = s_next;
-    __syncthreads();
+    const int nx = s_next[cur];
     if (nx == INT_MAX || nx <= cur) break;
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
       acc_nodes[(size_t)b * (B - 1) + a] = nx;
       out_tok[(size_t)b * B + a] = R;
     }
     ++a;
     cur = nx;
   }
-  if (threadIdx.x == 0) {
+  if (leaf) {  // the bonus token: the argmax of this row, scanned here
+    float bv = -INFINITY;
+    int bi = INT_MAX;
+    // ids visited in increasing order per thread: a strict > keeps the smallest id
+    const LT *row = logits + ((size_t)b * nn + cur) * V;
+    constexpr int EV = LVec<LT>::N, U = 16;
+    if (V % EV == 0) {  // 16-byte rows: U loads of EV values per thread in flight
+      const int nv = V / EV;
+      for (int g0 = 0; g0 < nv; g0 += 256 * U) {
+        u32x4 x[U];
+#pragma unroll
+        for (int q = 0; q < U; ++q) x[q] = *(const u32x4 *)(row + (size_t)min(g0 + q * 256 + tid, nv - 1) * EV);
+#pragma unroll
+        for (int q = 0; q < U; ++q) {
+          const int gi = g0 + q * 256 + tid;
+          fold_vec<LT>(x[q], gi * EV, gi < nv ? V : 0, bv, bi);
+        }
+      }
+    } else {
+      for (int v0 = tid; v0 < V; v0 += 256 * U) {
+        float x[U];
+#pragma unroll
+        for (int q = 0; q < U; ++q) x[q] = ld_logit<LT>(row + min(v0 + q * 256, V - 1));
+#pragma unroll
+        for (int q = 0; q < U; ++q) {
+          const int v = v0 + q * 256;
+          const float ov = order_val(x[q]);
+          if (v < V && (ov > bv || bi == INT_MAX)) {
+            bv = ov;
+            bi = v;
+          }
+        }
+      }
+    }
+    block_best(bv, bi, sv, si);
+    R = bi;
+  }
+  if (tid == 0) {
     acc_len[b] = a;
     out_tok[(size_t)b * B + a] = R;
   }
-  for (int q = a + 1 + threadIdx.x; q < B; q += blockDim.x) out_tok[(size_t)b * B + q] = -1;
-  for (int q = a + threadIdx.x; q < B - 1; q += blockDim.x) acc_nodes[(size_t)b * (B - 1) + q] = -1;
+  for (int q = a + 1 + tid; q < B; q += blockDim.x) out_tok[(size_t)b * B + q] = -1;
+  for (int q = a + tid; q < B - 1; q += blockDim.x) acc_nodes[(size_t)b * (B - 1) + q] = -1;
 }
 
 size_t accept_part_entries(int bs, int nn, int V) { return (size_t)bs * nn * ((V + ACH - 1) / ACH); }
