@@ -26,8 +26,10 @@
 // split writes its own partial output and the consuming kernel adds the
 // partials in split order: no workgroup ever waits on another, and the sums
 // are bitwise reproducible.  Grids larger than the device (the LM head: 1189
-// groups of 8 tiles) run as one workgroup per CU looping over its groups with a
-// single pipeline, which saves the pipeline fill of every further workgroup.
+// groups of 8 tiles) run as one workgroup per CU that owns several groups and
+// multiplies each staged activation chunk into all of them, with a single
+// pipeline, which saves the pipeline fill of every further workgroup and all
+// but one staging of each chunk.
 #include "common.h"
 #include "kernels.h"
 #include "mfma.h"
@@ -93,6 +95,30 @@ DEVI void load_xfrag(const float *__restrict__ X, int ldx, int M, int K, int m, 
   }
 }
 
+// load_xfrag in two parts: the load (clamped address) and the lane's mask,
+// applied later by mask_xfrag (so that nothing needs the loaded values before
+// the caller wants them)
+template <int EPL>
+DEVI uint32_t load_xfrag_raw(const float *__restrict__ X, int ldx, int M, int K, int m, int k0,
+                             float4 (&v)[EPL / 4]) {
+  const bool ok = m < M && k0 + EPL <= K;
+  const int mc = m < M ? m : M - 1;
+  const int kc = k0 + EPL <= K ? k0 : K - EPL;
+  const float4 *p = (const float4 *)(X + (size_t)mc * ldx + kc);
+#pragma unroll
+  for (int q = 0; q < EPL / 4; ++q) v[q] = p[q];
+  uint32_t mask = ok ? 0xffffffffu : 0u;
+  __asm__ volatile("" : "+v"(mask));
+  return mask;
+}
+template <int EPL>
+DEVI void mask_xfrag(float4 (&v)[EPL / 4], uint32_t mask) {
+#pragma unroll
+  for (int q = 0; q < EPL / 4; ++q)
+    v[q] = make_float4(__uint_as_float(__float_as_uint(v[q].x) & mask), __uint_as_float(__float_as_uint(v[q].y) & mask),
+                       __uint_as_float(__float_as_uint(v[q].z) & mask), __uint_as_float(__float_as_uint(v[q].w) & mask));
+}
+
 // EPI_RESID, after this workgroup's partial went out (device-scope stores):
 // wait for the stores, take a ticket of the column group, and if it is the
 // group's last split, form res_in + partial_0 + ... + partial_{ksplit-1} (split
@@ -145,7 +171,7 @@ DEVI void resid_epilogue(const GemmArgs &a, int grp, float *sq, int nsq) {
   }
 }
 
-template <typename WT, int MT, int WPT, int EPI, int KCM, int kWaves, int XA>
+template <typename WT, int MT, int WPT, int EPI, int KCM, int kWaves>
 __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
   constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP;
   constexpr int XF = XStage<WT>::XF;
@@ -211,81 +237,61 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
       XStage<WT>::put(&xs[buf][s][mt][l][0], v[q]);
     }
   };
+  auto mac = [&](const u32x4 &w, int buf, int u) {
+    u32x4 xf[MT * XF];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int f = 0; f < XF; ++f) xf[mt * XF + f] = xs[buf][ksub + u][mt][lane][f];
+    Mac2<WT, MT>::step(w, xf, acc);
+  };
   auto compute = [&](const u32x4 (&w)[KW], int c, int buf) {
+    if (c * KCM + ksub + KW <= KS) {  // every step of the chunk is in range: no per-step test
 #pragma unroll
-    for (int u = 0; u < KW; ++u) {
-      if (c * KCM + ksub + u < KS) {
-        u32x4 xf[MT * XF];
+      for (int u = 0; u < KW; ++u) mac(w[u], buf, u);
+    } else {
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int f = 0; f < XF; ++f) xf[mt * XF + f] = xs[buf][ksub + u][mt][lane][f];
-        Mac2<WT, MT>::step(w[u], xf, acc);
-      }
+      for (int u = 0; u < KW; ++u)
+        if (c * KCM + ksub + u < KS) mac(w[u], buf, u);
+      consume(w);
     }
   };
 
-  if (XA == 2 && c0 < c1) {
-    // weights one chunk ahead, activations two (an activation chunk then has a
-    // whole chunk's products to arrive from L2 before it is staged).  Loads
-    // past the range are issued anyway (clamped inside load_w / load_xfrag to
-    // valid addresses) and never used, so no branch holds them: the compiler
-    // counts them and its waits leave the younger loads in flight.  Pays on
-    // long ranges only; a short one waits for the deeper fill instead.
-    u32x4 wa[KW], wb[KW];
-    float4 xa[IPT][EPL / 4], xb[IPT][EPL / 4];
-    // in flight at the loop head: chunk c's activations (xb) older than its
-    // weights (wa), the order the loop body issues them in
-    load_x(xa, c0);
-    __builtin_amdgcn_sched_barrier(0);
-    load_x(xb, c0 + 1);
-    __builtin_amdgcn_sched_barrier(0);
-    load_w(wa, c0);
-    __builtin_amdgcn_sched_barrier(0);
-    store_x(xa, 0);
-    __syncthreads();
-    for (int c = c0; c < c1; c += 2) {
-      // chunk c: weights in wa, activations in LDS buffer 0 (xb holds chunk c + 1)
-      load_x(xa, c + 2);
-      load_w(wb, c + 1);
-      compute(wa, c, 0);
-      store_x(xb, 1);
-      __syncthreads();
-      if (c + 1 >= c1) break;
-      // chunk c + 1: weights in wb, activations in LDS buffer 1 (xa holds chunk c + 2)
-      load_x(xb, c + 3);
-      load_w(wa, c + 2);
-      compute(wb, c + 1, 1);
-      store_x(xa, 0);
-      __syncthreads();
-    }
-  } else if (c0 < c1) {
-    // weights and activations one chunk ahead
+  // Weights and activations one chunk ahead, in straight-line code over three
+  // chunks at a time (a fresh pipeline fill per three chunks).  Measured
+  // against loops that keep one or two chunks in flight throughout, on the
+  // gate/up shape, this is the fastest: the compiler's waits in straight-line
+  // code are exact, while a loop's are taken over every path it cannot rule
+  // out (a path that leaves a load unconsumed makes it drain the prefetch).
+  if (c0 < c1) {
     u32x4 wa[KW], wb[KW];
     float4 xr[IPT][EPL / 4];
-    load_x(xr, c0);
-    load_w(wa, c0);
-    store_x(xr, 0);
-    __syncthreads();
-    for (int c = c0; c < c1; c += 2) {
-      // chunk c in (wa, buf 0); prefetch c+1 into (xr, wb)
-      const bool n1 = c + 1 < c1;
-      if (n1) {
-        load_x(xr, c + 1);
-        load_w(wb, c + 1);
-      }
-      compute(wa, c, 0);
-      if (n1) store_x(xr, 1);
+    for (int cb = c0; cb < c1; cb += 3) {
+      const int n = min(3, c1 - cb);
+      if (cb > c0) __syncthreads();  // every wave is done reading the previous three's buffers
+      load_x(xr, cb);
+      load_w(wa, cb);
+      store_x(xr, 0);
       __syncthreads();
-      if (!n1) break;
-      const bool n2 = c + 2 < c1;
-      if (n2) {
-        load_x(xr, c + 2);
-        load_w(wa, c + 2);
+      if (n == 1) {
+        compute(wa, cb, 0);
+      } else {
+        load_x(xr, cb + 1);
+        load_w(wb, cb + 1);
+        compute(wa, cb, 0);
+        store_x(xr, 1);
+        __syncthreads();
+        if (n == 2) {
+          compute(wb, cb + 1, 1);
+        } else {
+          load_x(xr, cb + 2);
+          load_w(wa, cb + 2);
+          compute(wb, cb + 1, 1);
+          store_x(xr, 0);
+          __syncthreads();
+          compute(wa, cb + 2, 0);
+        }
       }
-      compute(wb, c + 1, 1);
-      if (n2) store_x(xr, 0);
-      __syncthreads();
     }
   }
 
@@ -375,11 +381,22 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_kernel(GemmArgs a) {
   }
 }
 
-// Stored-output variant for grids larger than the device: pgrid workgroups
-// each take groups blockIdx.x, blockIdx.x + pgrid, ... one after another with a
-// single double-buffered pipeline over (group, chunk), so a workgroup never
-// restarts it (the fill of a fresh workgroup costs a memory round trip).
-template <typename WT, int MT, int KCM, int kWaves>
+// Most column groups one workgroup of the persistent variant below owns.
+constexpr int kStreamMaxGroups = 8;
+
+// Stored-output variant for grids larger than the device (the LM head: 1189
+// groups of 8 tiles): pgrid workgroups, workgroup b owning groups b, b + pgrid,
+// ... (at most GR of them).  The loop runs chunk-outer: a chunk of activations
+// is staged once and multiplied into the tiles of every owned group (GR sets of
+// sums), so the staging and its barrier come once per chunk instead of once per
+// group and chunk.  One pipeline covers every item (chunk, group), weights one
+// item ahead, so a workgroup never refills it.  Each tile still sums its
+// k-steps in ascending order: its results equal the other kernels'.
+// The host launches it for whole chunks only, an even number of them and no K
+// split, so the loop body has no branch at all: a workgroup owning fewer than
+// GR groups multiplies its last group's weights again (loaded from L2) into
+// sums it never stores.
+template <typename WT, int MT, int KCM, int kWaves, int GR>
 __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(GemmArgs a, int ngroups) {
   constexpr int EPL = Frag<WT>::EPL, KSTEP = Frag<WT>::KSTEP;
   constexpr int XF = XStage<WT>::XF;
@@ -388,116 +405,123 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(GemmArgs a, in
   constexpr int IPT = (ITEMS + kWaves * 64 - 1) / (kWaves * 64);
   __shared__ u32x4 xs[2][KCM][MT][64][XF];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int ky = blockIdx.y, mz = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int mz = blockIdx.z;
   const int KS = a.KS;
-  const int nch = (KS + KCM - 1) / KCM;
-  const int cpw = (nch + a.ksplit - 1) / a.ksplit;
-  const int c0 = min(nch, ky * cpw), c1 = min(nch, c0 + cpw);
-  const int nck = c1 - c0;
-  const int mine = (int)blockIdx.x < ngroups ? (ngroups - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
-  const int total = mine * nck;
-  if (total <= 0) return;
+  const int nch = KS / KCM;  // whole chunks, an even number of them
+  // owned groups (the host keeps every workgroup's count within GR)
+  const int mine = (int)blockIdx.x < ngroups ? min(GR, (ngroups - 1 - (int)blockIdx.x) / (int)gridDim.x + 1) : 0;
+  if (mine <= 0 || nch <= 0) return;
   const int mbase = mz * MT * 16;
-  float *Y = a.Y + (size_t)ky * a.ysplit;
 
-  auto tile_of = [&](int it) { return ((int)blockIdx.x + (it / nck) * (int)gridDim.x) * kWaves + wave; };
-  auto load_w = [&](u32x4 (&w)[KW], int it) {
-    const int t = min(tile_of(it), a.ntiles - 1);
-    const u32x4 *Pv = (const u32x4 *)a.P + ((size_t)(a.tile0 + t) * KS) * 64 + lane;
-    const int c = c0 + it % nck;
+  auto tile_of = [&](int j) { return ((int)blockIdx.x + j * (int)gridDim.x) * kWaves + wave; };
+  // item (c, j): chunk c of owned group j (groups past the owned ones: the last
+  // owned group again; the item after the last: the last item again)
+  auto load_w = [&](u32x4 (&w)[KW], int c, int j) {
+    const bool past = c >= nch;
+    c = past ? nch - 1 : c;
+    j = past ? mine - 1 : min(j, mine - 1);
+    const int t = min(tile_of(j), a.ntiles - 1);
+    const u32x4 *Pv = (const u32x4 *)a.P + ((size_t)(a.tile0 + t) * KS + (size_t)c * KCM) * 64 + lane;
 #pragma unroll
-    for (int u = 0; u < KW; ++u) {
-      const int s = min(c * KCM + u, KS - 1);
-      w[u] = __builtin_nontemporal_load(Pv + (size_t)s * 64);
-    }
+    for (int u = 0; u < KW; ++u) w[u] = __builtin_nontemporal_load(Pv + u * 64);
   };
-  auto load_x = [&](float4 (&v)[IPT][EPL / 4], int it) {
-    const int c = c0 + it % nck;
+  uint32_t xm[IPT];  // the staged fragments' lane masks (zero outside [0, M) x [0, K))
+  auto load_x = [&](float4 (&v)[IPT][EPL / 4], int c) {
+    c = min(c, nch - 1);
 #pragma unroll
     for (int q = 0; q < IPT; ++q) {
       const int i2 = min(tid + q * kWaves * 64, ITEMS - 1);
       const int l = i2 & 63, mt = (i2 >> 6) % MT, s = (i2 >> 6) / MT;
       const int m = mbase + mt * 16 + (l & 15);
       const int k0 = (c * KCM + s) * KSTEP + (l >> 4) * EPL;
-      load_xfrag<EPL>(a.X, a.ldx, a.M, a.K, m, k0, v[q]);
+      xm[q] = load_xfrag_raw<EPL>(a.X, a.ldx, a.M, a.K, m, k0, v[q]);
     }
   };
-  auto store_x = [&](const float4 (&v)[IPT][EPL / 4], int buf) {
+  auto store_x = [&](float4 (&v)[IPT][EPL / 4], int buf) {
 #pragma unroll
     for (int q = 0; q < IPT; ++q) {
       const int i2 = tid + q * kWaves * 64;
       if (ITEMS % (kWaves * 64) != 0 && i2 >= ITEMS) continue;
       const int l = i2 & 63, mt = (i2 >> 6) % MT, s = (i2 >> 6) / MT;
+      mask_xfrag<EPL>(v[q], xm[q]);
       XStage<WT>::put(&xs[buf][s][mt][l][0], v[q]);
     }
   };
-  floatx4 acc[MT];
+  floatx4 acc[GR][MT];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-  auto compute = [&](const u32x4 (&w)[KW], int it, int buf) {
-    const int c = c0 + it % nck;
+  for (int j = 0; j < GR; ++j)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[j][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](floatx4 (&ac)[MT], const u32x4 (&w)[KW], int buf) {
 #pragma unroll
     for (int u = 0; u < KW; ++u) {
-      if (c * KCM + u < KS) {
-        u32x4 xf[MT * XF];
+      u32x4 xf[MT * XF];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int f = 0; f < XF; ++f) xf[mt * XF + f] = xs[buf][u][mt][lane][f];
-        Mac2<WT, MT>::step(w[u], xf, acc);
-      }
+        for (int f = 0; f < XF; ++f) xf[mt * XF + f] = xs[buf][u][mt][lane][f];
+      Mac2<WT, MT>::step(w[u], xf, ac);
     }
-  };
-  auto finish = [&](int it) {  // after the last chunk of an item: store and restart the sums
-    if (it % nck != nck - 1) return;
-    const int tile = tile_of(it);
-    if (tile < a.ntiles) {
-      const int n = tile * 16 + 4 * (lane >> 4);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = mbase + mt * 16 + (lane & 15);
-        if (m >= a.M) continue;
-        float *y = Y + (size_t)m * a.ldy + n;
-        if (n + 4 <= a.N && ((a.ldy & 3) == 0)) {
-          *(floatx4 *)y = acc[mt];
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (n + e < a.N) y[e] = acc[mt][e];
-        }
-      }
-    }
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
   };
 
   u32x4 wa[KW], wb[KW];
   float4 xr[IPT][EPL / 4];
   load_x(xr, 0);
-  load_w(wa, 0);
+  load_w(wa, 0, 0);
   store_x(xr, 0);
   __syncthreads();
-  for (int it = 0; it < total; it += 2) {
-    const bool n1 = it + 1 < total;
-    if (n1) {
-      load_x(xr, it + 1);
-      load_w(wb, it + 1);
+  // chunks in pairs, c in LDS buffer 0 and c + 1 in buffer 1; the 2 GR items
+  // of a pair are unrolled, even ones holding their weights in wa and odd ones
+  // in wb.  The next chunk's activations load with a chunk's first item and
+  // are staged after its last.
+  for (int c = 0; c < nch; c += 2) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int cc = c + h;
+#pragma unroll
+      for (int j = 0; j < GR; ++j) {
+        // each item issues the next item's loads, then multiplies: the
+        // scheduler keeps that order (sunk into the products, the prefetch
+        // would be waited for by the very next item)
+        __builtin_amdgcn_sched_barrier(0);
+        if (j == 0) load_x(xr, cc + 1);
+        const int nc = j + 1 < GR ? cc : cc + 1, nj = j + 1 < GR ? j + 1 : 0;
+        const bool even = ((h * GR + j) & 1) == 0;
+        if (even) load_w(wb, nc, nj);
+        else load_w(wa, nc, nj);
+        __builtin_amdgcn_sched_barrier(0);
+        if (even) compute(acc[j], wa, h);
+        else compute(acc[j], wb, h);
+        if (j == GR - 1) {
+          __builtin_amdgcn_sched_barrier(0);
+          pin(xr);
+          store_x(xr, h ^ 1);
+          __syncthreads();
+        }
+      }
     }
-    compute(wa, it, 0);
-    finish(it);
-    if (n1) store_x(xr, 1);
-    __syncthreads();
-    if (!n1) break;
-    const bool n2 = it + 2 < total;
-    if (n2) {
-      load_x(xr, it + 2);
-      load_w(wa, it + 2);
+  }
+
+#pragma unroll
+  for (int j = 0; j < GR; ++j) {
+    const int tile = tile_of(j);
+    if (j >= mine || tile >= a.ntiles) continue;
+    const int n = tile * 16 + 4 * (lane >> 4);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = mbase + mt * 16 + (lane & 15);
+      if (m >= a.M) continue;
+      float *y = a.Y + (size_t)m * a.ldy + n;
+      if (n + 4 <= a.N && ((a.ldy & 3) == 0)) {
+        *(floatx4 *)y = acc[j][mt];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n + e < a.N) y[e] = acc[j][mt][e];
+      }
     }
-    compute(wb, it + 1, 1);
-    finish(it + 1);
-    if (n2) store_x(xr, 0);
-    __syncthreads();
   }
 }
 
@@ -553,30 +577,38 @@ GemmPlan plan_gemm(int ntiles, int KS, int M, int epi, int n_cu, int max_split) 
     const int per = std::max(1, n_cu / (p.ksplit * p.mgroups));  // CUs per (split, m-group)
     const int rounds = (p.groups + per - 1) / per;
     const int pg = std::min(per, ((p.groups + rounds - 1) / rounds + 7) / 8 * 8);
-    if (pg < p.groups) p.pgrid = pg;
+    // (the persistent kernel takes whole chunks, an even number of them, and no K split)
+    const bool shape_ok = p.ksplit == 1 && KS % p.kcm == 0 && (KS / p.kcm) % 2 == 0;
+    if (shape_ok && pg < p.groups && (p.groups + pg - 1) / pg <= kStreamMaxGroups) p.pgrid = pg;
   }
   return p;
 }
 
+// the persistent kernel for a plan with pgrid > 0
+template <typename WT, int MT, int KCM>
+static void launch_stream(const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
+  // groups per workgroup: 2..6 or 8 (7 runs the 8 instance, its last group idle)
+  const int gr = (p.groups + p.pgrid - 1) / p.pgrid;
+  const dim3 grid(p.pgrid, p.ksplit, p.mgroups), block(8 * 64);
+  if (gr <= 2) hipLaunchKernelGGL((gemm_stream_kernel<WT, MT, KCM, 8, 2>), grid, block, 0, st, a, p.groups);
+  else if (gr == 3) hipLaunchKernelGGL((gemm_stream_kernel<WT, MT, KCM, 8, 3>), grid, block, 0, st, a, p.groups);
+  else if (gr == 4) hipLaunchKernelGGL((gemm_stream_kernel<WT, MT, KCM, 8, 4>), grid, block, 0, st, a, p.groups);
+  else if (gr == 5) hipLaunchKernelGGL((gemm_stream_kernel<WT, MT, KCM, 8, 5>), grid, block, 0, st, a, p.groups);
+  else if (gr == 6) hipLaunchKernelGGL((gemm_stream_kernel<WT, MT, KCM, 8, 6>), grid, block, 0, st, a, p.groups);
+  else hipLaunchKernelGGL((gemm_stream_kernel<WT, MT, KCM, 8, kStreamMaxGroups>), grid, block, 0, st, a, p.groups);
+}
+
 template <typename WT, int MT, int EPI, int KCM>
 static void launch_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
-  if (EPI == EPI_STORE && p.pgrid > 0 && p.nw == 8) {
-    hipLaunchKernelGGL((gemm_stream_kernel<WT, MT, KCM, 8>), dim3(p.pgrid, p.ksplit, p.mgroups), dim3(8 * 64), 0, st,
-                       a, p.groups);
-    return;
+  if constexpr (EPI == EPI_STORE && KCM == 16 / MT) {  // (the only shapes the planner makes persistent)
+    if (p.pgrid > 0 && p.nw == 8) {
+      launch_stream<WT, MT, KCM>(a, p, st);
+      return;
+    }
   }
   dim3 grid(p.groups, p.ksplit, p.mgroups);
-  // activations two chunks ahead once a workgroup's range is long enough to
-  // repay the deeper fill
-  const int nch = (a.KS + KCM - 1) / KCM, cpw = (nch + p.ksplit - 1) / p.ksplit;
-  const bool far = cpw >= 4;
-  if (p.nw == 6) {
-    if (far) hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 6, 2>), grid, dim3(6 * 64), 0, st, a);
-    else hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 6, 1>), grid, dim3(6 * 64), 0, st, a);
-  } else {
-    if (far) hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 8, 2>), grid, dim3(8 * 64), 0, st, a);
-    else hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 8, 1>), grid, dim3(8 * 64), 0, st, a);
-  }
+  if (p.nw == 6) hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 6>), grid, dim3(6 * 64), 0, st, a);
+  else hipLaunchKernelGGL((gemm_kernel<WT, MT, 1, EPI, KCM, 8>), grid, dim3(8 * 64), 0, st, a);
 }
 
 template <typename WT, int MT>

@@ -35,6 +35,28 @@ template <> struct XStage<float> {
   DEVI static void put(u32x4 *dst, const float4 (&v)[1]) { dst[0] = __builtin_bit_cast(u32x4, v[0]); }
 };
 
+// Marks loaded registers as used on a path that does not multiply them, so
+// that the compiler waits for their loads there.  The compiler's wait
+// insertion assumes the worst over all paths: a load left unconsumed on one
+// path makes it drain every younger load (the next chunk's prefetch included)
+// before the register is next written.
+template <int N>
+DEVI void consume(const u32x4 (&w)[N]) {
+#pragma unroll
+  for (int u = 0; u < N; ++u) __asm__ volatile("" ::"v"(w[u]));
+}
+
+// Passes loaded values through an empty asm that the compiler keeps in order
+// with the scheduling barriers around it, so that work on them (and the wait
+// for their loads) cannot move up to where they were loaded.
+template <int N, int E>
+DEVI void pin(float4 (&v)[N][E]) {
+#pragma unroll
+  for (int q = 0; q < N; ++q)
+#pragma unroll
+    for (int e = 0; e < E; ++e) __asm__ volatile("" : "+v"(v[q][e].x), "+v"(v[q][e].y), "+v"(v[q][e].z), "+v"(v[q][e].w));
+}
+
 template <typename WT, int MT>
 struct Mac2 {
   // xf points at fragments [mt][XF] of one k-step
