@@ -24,7 +24,7 @@ HBM_PEAK = 8.0e12  # B/s, MI355X HBM3E
 
 # HBM bytes per LM-head launch from rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by a 1 GiB copy),
 # valid for the GEMM source with this sha1 (see profiles/lm_head_gemm_qwen3_8b_bs1.md)
-LMHEAD_TRAFFIC = {"gemm_sha1": "006a7f4d6799993e62c02698dee41828284515b3", "bytes": 1257953704,
+LMHEAD_TRAFFIC = {"gemm_sha1": "e8987b5a6e4f8d3b83754dc3ef0aea363b0efc04", "bytes": 1259095722,
                   "config": "qwen3_8b"}
 
 
@@ -413,7 +413,7 @@ def run_gpu(args, cfg, w, inp):
                    "batch": bs, "ctx": cfg.ctx, "block": cfg.block, "branch": beta,
                    "hidden": cfg.hidden, "layers": cfg.n_layers, "vocab": V,
                    "storage": cfg.dtype},
-        "roofline": {"kernel": "LM-head GEMM (gemm_stream_kernel<bf16_t, 1, 16, 8>, W1 H-half fused)", "bound": "hbm",
+        "roofline": {"kernel": "LM-head GEMM (gemm_stream_kernel<bf16_t, 1, 16, 8, 5>, W1 H-half fused)", "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                      "frac": round(achieved * 1e9 / HBM_PEAK, 4), "traffic": lmhead_traffic(cfg.name),
                      "launch_us": round(dom_launch_s * 1e6, 2), "launches": dom_n,

@@ -35,6 +35,7 @@
 #include "mfma.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace dk {
 
@@ -416,14 +417,15 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(GemmArgs a, in
   const int mbase = mz * MT * 16;
 
   auto tile_of = [&](int j) { return ((int)blockIdx.x + j * (int)gridDim.x) * kWaves + wave; };
-  // item (c, j): chunk c of owned group j (groups past the owned ones: the last
-  // owned group again; the item after the last: the last item again)
+  // item (c, j): chunk c of owned group j.  A group past the owned ones loads
+  // the first KW KB of the activations instead (in L2: every chunk's staging
+  // reads them), never multiplied; a streamed weight chunk loaded again would
+  // come from HBM, its lines being the first the cache gives up.
   auto load_w = [&](u32x4 (&w)[KW], int c, int j) {
-    const bool past = c >= nch;
-    c = past ? nch - 1 : c;
-    j = past ? mine - 1 : min(j, mine - 1);
-    const int t = min(tile_of(j), a.ntiles - 1);
-    const u32x4 *Pv = (const u32x4 *)a.P + ((size_t)(a.tile0 + t) * KS + (size_t)c * KCM) * 64 + lane;
+    c = min(c, nch - 1);
+    const int t = min(tile_of(min(j, mine - 1)), a.ntiles - 1);
+    const u32x4 *Pv = j < mine ? (const u32x4 *)a.P + ((size_t)(a.tile0 + t) * KS + (size_t)c * KCM) * 64 + lane
+                               : (const u32x4 *)a.X + lane;
 #pragma unroll
     for (int u = 0; u < KW; ++u) w[u] = __builtin_nontemporal_load(Pv + u * 64);
   };
@@ -475,26 +477,31 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(GemmArgs a, in
   // chunks in pairs, c in LDS buffer 0 and c + 1 in buffer 1; the 2 GR items
   // of a pair are unrolled, even ones holding their weights in wa and odd ones
   // in wb.  The next chunk's activations load with a chunk's first item and
-  // are staged after its last.
-  for (int c = 0; c < nch; c += 2) {
+  // are staged after its last.  The last pair is a copy that loads nothing past
+  // the range (a load of the last item again would come from HBM).
+  auto pair = [&](int c, auto last) {
+    constexpr bool kLast = decltype(last)::value;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int cc = c + h;
+      const bool final_chunk = kLast && h == 1;
 #pragma unroll
       for (int j = 0; j < GR; ++j) {
         // each item issues the next item's loads, then multiplies: the
         // scheduler keeps that order (sunk into the products, the prefetch
         // would be waited for by the very next item)
         __builtin_amdgcn_sched_barrier(0);
-        if (j == 0) load_x(xr, cc + 1);
+        if (j == 0 && !final_chunk) load_x(xr, cc + 1);
         const int nc = j + 1 < GR ? cc : cc + 1, nj = j + 1 < GR ? j + 1 : 0;
         const bool even = ((h * GR + j) & 1) == 0;
-        if (even) load_w(wb, nc, nj);
-        else load_w(wa, nc, nj);
+        if (!(final_chunk && j == GR - 1)) {
+          if (even) load_w(wb, nc, nj);
+          else load_w(wa, nc, nj);
+        }
         __builtin_amdgcn_sched_barrier(0);
         if (even) compute(acc[j], wa, h);
         else compute(acc[j], wb, h);
-        if (j == GR - 1) {
+        if (j == GR - 1 && !final_chunk) {
           __builtin_amdgcn_sched_barrier(0);
           pin(xr);
           store_x(xr, h ^ 1);
@@ -502,7 +509,9 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(GemmArgs a, in
         }
       }
     }
-  }
+  };
+  for (int c = 0; c + 2 < nch; c += 2) pair(c, std::false_type{});
+  pair(nch - 2, std::true_type{});
 
 #pragma unroll
   for (int j = 0; j < GR; ++j) {
@@ -601,7 +610,9 @@ static void launch_stream(const GemmArgs &a, const GemmPlan &p, hipStream_t st) 
 template <typename WT, int MT, int EPI, int KCM>
 static void launch_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st) {
   if constexpr (EPI == EPI_STORE && KCM == 16 / MT) {  // (the only shapes the planner makes persistent)
-    if (p.pgrid > 0 && p.nw == 8) {
+    // (the persistent kernel's idle groups read the first KCM KB of X)
+    const bool x_covers = (size_t)(a.M - 1) * a.ldx + a.K >= (size_t)KCM * 256;
+    if (p.pgrid > 0 && p.nw == 8 && x_covers) {
       launch_stream<WT, MT, KCM>(a, p, st);
       return;
     }
