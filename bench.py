@@ -24,7 +24,7 @@ HBM_PEAK = 8.0e12  # B/s, MI355X HBM3E
 
 # HBM bytes per LM-head launch from rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by a 1 GiB copy),
 # valid for the GEMM source with this sha1 (see profiles/lm_head_gemm_qwen3_8b_bs1.md)
-LMHEAD_TRAFFIC = {"gemm_sha1": "e8987b5a6e4f8d3b83754dc3ef0aea363b0efc04", "bytes": 1259095722,
+LMHEAD_TRAFFIC = {"gemm_sha1": "d9fa868d45f2fb76ea5d40388e30935f5d80b17d", "bytes": 1259095722,
                   "config": "qwen3_8b"}
 
 

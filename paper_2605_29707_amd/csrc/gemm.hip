@@ -14,15 +14,14 @@
 // bf16 weights meet fp32 activations split into hi + lo bf16 parts (two MFMAs
 // per fragment; products are exact in fp32), so the GEMM keeps fp32 accuracy.
 //
-// Work split: a workgroup of 8 waves owns 8/WPT consecutive tiles (WPT waves
-// per tile) and a range of K chunks of KCM k-steps (16/MT, or 8/MT: half the
-// registers, two workgroups per CU, finer K splits).  The activations of a
-// chunk are staged once per workgroup into LDS, already split into hi/lo
-// fragments, and shared by all its waves; weight fragments of the next chunk
-// are in flight while the current chunk is multiplied.  Loads are issued
-// unconditionally (addresses clamped) and activations before weights, so the
-// in-order vector-memory counter never makes a wave wait for the weights it
-// just prefetched.  When K is split across workgroups (ksplit > 1) each
+// Work split: a workgroup of 8 (or 6) waves owns one tile per wave and a
+// range of K chunks of KCM k-steps (16/MT, or 8/MT: half the registers, two
+// workgroups per CU, finer K splits).  The activations of a chunk are staged
+// once per workgroup into LDS, already split into hi/lo fragments, and shared
+// by all its waves; weight fragments of the next chunk are in flight while the
+// current chunk is multiplied.  Activations load before weights, at clamped
+// addresses, so the in-order vector-memory counter never makes a wave wait for
+// the weights it just prefetched.  When K is split across workgroups (ksplit > 1) each
 // split writes its own partial output and the consuming kernel adds the
 // partials in split order: no workgroup ever waits on another, and the sums
 // are bitwise reproducible.  Grids larger than the device (the LM head: 1189
