@@ -141,9 +141,16 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
     for (int q = 0; q < kWideWPW; ++q) lw[d][kWideWPW * wave + q][lane] = wr[d][q];
   };
   auto compute = [&](int buf, const u32x4 (&x)[2 * kWideTM]) {
+    // tile i + 1's weight fragment is read from LDS before tile i's products
+    // (scheduling barriers keep that order), so the read's latency hides
+    // behind them; left to itself the compiler read each pair of tiles just
+    // before their products (the registers allow two fragments)
+    u32x4 wn = lw[buf][0][lane];
 #pragma unroll
     for (int i = 0; i < kWideTiles; ++i) {
-      const bf16x8 w = __builtin_bit_cast(bf16x8, lw[buf][i][lane]);
+      const bf16x8 w = __builtin_bit_cast(bf16x8, wn);
+      if (i + 1 < kWideTiles) wn = lw[buf][i + 1][lane];
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int j = 0; j < kWideTM; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, __builtin_bit_cast(bf16x8, x[j]), acc[i][j], 0, 0, 0);
@@ -151,6 +158,7 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
       for (int j = 0; j < kWideTM; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, __builtin_bit_cast(bf16x8, x[kWideTM + j]), acc[i][j],
                                                             0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
