@@ -740,7 +740,8 @@ __global__ __launch_bounds__(64) void head_merge_kernel(HeadArgs h) {
 }
 
 // ---------------------------------------------------------------------------
-// Persistent rollout (bf16 weights, r = 256, one or two batch rows, greedy): one
+// Persistent rollout (bf16 weights, r = 256, one or two batch rows, greedy or
+// sampled; three or four rows as one launch per pair): one
 // launch of at most one workgroup per CU runs all B-1 positions.  Each workgroup keeps its slice
 // of W2 resident for the whole rollout (kPersTiles tiles per wave, the last
 // one in LDS, the rest in registers: 77.8 MB over 238 workgroups at the Qwen3
@@ -764,6 +765,7 @@ __global__ __launch_bounds__(64) void head_merge_kernel(HeadArgs h) {
 // drafted token and its value of every position (no merge kernel).
 // ---------------------------------------------------------------------------
 constexpr int kPersWaves = 8, kPersTiles = 5, kPersKS = 8, kPersRegTiles = kPersTiles - 1;
+constexpr int kPersMaxBatch = 4;  // batch rows the persistent rollout takes (in launches of two)
 constexpr int kKeyIdBits = 18;
 
 DEVI unsigned long long ld_slot(const unsigned long long *p) {
@@ -1086,7 +1088,7 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
           }
         }
         Philox4 noise = {{0u, 0u, 0u, 0u}};
-        if (SAMPLE) noise = rng_block(h.seed_lo, h.seed_hi, RNG_DRAFT, cc, j, (tile0 + q) * 4 + g);
+        if (SAMPLE) noise = rng_block(h.seed_lo, h.seed_hi, RNG_DRAFT, h.row0 + cc, j, (tile0 + q) * 4 + g);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int n = (tile0 + q) * 16 + 4 * g + e;
@@ -1189,11 +1191,11 @@ __global__ __launch_bounds__(kPersWaves * 64) void head_persist_kernel(HeadArgs 
   }
 }
 
-bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st) {
+// The persistent kernel for one or two batch rows of `h` (D.bs <= 2): checks
+// the shapes and the device, and picks the instantiation and its LDS size.
+static bool persist_plan(const HeadArgs &h, int n_cu, const void **fn, size_t *lds_out, int *nr_out) {
   const Dims &D = h.D;
-  // one or two batch rows, branch 1 (larger batches run the launch-pair
-  // rollout: their register demand would spill here)
-  if (!D.bf16 || D.r != kPersKS * 32 || D.bs > 2 || h.beta != 1 || D.ds % 32 || D.ds > 256 * 8 ||
+  if (!D.bf16 || D.r != kPersKS * 32 || D.bs < 1 || D.bs > 2 || h.beta != 1 || D.ds % 32 || D.ds > 256 * 8 ||
       D.V >= (1 << kKeyIdBits) || D.B > 64 || !h.uslot || !h.kslot || !h.abort_flag || (h.sample && !h.praw))
     return false;
   const int NT = (D.V + 15) / 16;
@@ -1208,18 +1210,17 @@ bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st) {
                      sizeof(float) * (size_t)(D.B - 1) * D.bs * ((D.r + G - 1) / G);
   if (lds > 160 * 1024) return false;
   const bool dbg = h.final_logits != nullptr, smp = h.sample != 0;
-  const void *fn;
   switch ((D.bs == 1 ? 0 : 4) + (dbg ? 2 : 0) + (smp ? 1 : 0)) {
-    case 0: fn = (const void *)head_persist_kernel<1, false, false>; break;
-    case 1: fn = (const void *)head_persist_kernel<1, false, true>; break;
-    case 2: fn = (const void *)head_persist_kernel<1, true, false>; break;
-    case 3: fn = (const void *)head_persist_kernel<1, true, true>; break;
-    case 4: fn = (const void *)head_persist_kernel<2, false, false>; break;
-    case 5: fn = (const void *)head_persist_kernel<2, false, true>; break;
-    case 6: fn = (const void *)head_persist_kernel<2, true, false>; break;
-    default: fn = (const void *)head_persist_kernel<2, true, true>; break;
+    case 0: *fn = (const void *)head_persist_kernel<1, false, false>; break;
+    case 1: *fn = (const void *)head_persist_kernel<1, false, true>; break;
+    case 2: *fn = (const void *)head_persist_kernel<1, true, false>; break;
+    case 3: *fn = (const void *)head_persist_kernel<1, true, true>; break;
+    case 4: *fn = (const void *)head_persist_kernel<2, false, false>; break;
+    case 5: *fn = (const void *)head_persist_kernel<2, false, true>; break;
+    case 6: *fn = (const void *)head_persist_kernel<2, true, false>; break;
+    default: *fn = (const void *)head_persist_kernel<2, true, true>; break;
   }
-  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
+  if (hipFuncSetAttribute(*fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
     (void)hipGetLastError();
     return false;
   }
@@ -1230,16 +1231,63 @@ bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st) {
   // on the stream has drained.  Should other work hold CUs, the waits are
   // bounded and end in DEV_BARRIER_TIMEOUT rather than a hang.
   int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kPersWaves * 64, lds) != hipSuccess || per_cu < 1) {
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, *fn, kPersWaves * 64, lds) != hipSuccess || per_cu < 1) {
     (void)hipGetLastError();
     return false;
   }
+  *lds_out = lds;
+  *nr_out = nr;
+  return true;
+}
+
+// The rollout of `h` with the batch rows [b0, b0 + nb) only: every per-row
+// pointer moves to row b0 (the exchange slots too, so each launch has slots
+// of its own, zeroed with the step's header), the batch becomes nb.
+static HeadArgs rows_of(const HeadArgs &h, int b0, int nb) {
   HeadArgs a = h;
-  int nrv = nr;
-  void *args[] = {&a, &nrv};
-  if (hipLaunchKernel(fn, dim3(G), dim3(kPersWaves * 64), args, lds, st) != hipSuccess) {
-    (void)hipGetLastError();
-    return false;
+  const int depth = h.D.B - 1;
+  a.D.bs = nb;
+  a.row0 = h.row0 + b0;
+  a.anchor = h.anchor + b0;
+  if (h.forced) a.forced = h.forced + (size_t)b0 * depth;
+  a.topk_ids = h.topk_ids + (size_t)b0 * depth * h.beta;
+  a.topk_vals = h.topk_vals + (size_t)b0 * depth * h.beta;
+  if (h.final_logits) a.final_logits = h.final_logits + (size_t)b0 * depth * h.D.V;
+  if (h.states) a.states = h.states + (size_t)b0 * depth * h.D.ds;
+  a.P = h.P + (size_t)b0 * depth * h.ldp;
+  a.Lbase = h.Lbase + (size_t)b0 * depth * h.ldl;
+  a.uslot = h.uslot + (size_t)b0 * h.D.r * kSlotStride;
+  a.kslot = h.kslot + (size_t)b0 * h.GC * kSlotStride;
+  return a;
+}
+
+bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st) {
+  const Dims &D = h.D;
+  // one or two batch rows per launch (more would spill the per-lane state);
+  // three or four rows run as one launch per pair of rows, one after the
+  // other (each re-reads W2: 2 x ~140 us against ~480 us for the launch-pair
+  // rollout of four rows, measured at the Qwen3-4B shape); larger batches
+  // run the launch-pair rollout
+  if (D.bs < 1 || D.bs > kPersMaxBatch) return false;
+  const int npair = (D.bs + 1) / 2;
+  const void *fn[2];
+  size_t lds[2];
+  int nr[2];
+  for (int p = 0; p < npair; ++p) {  // every launch's plan first: all or nothing
+    const int nb = std::min(2, D.bs - 2 * p);
+    if (!persist_plan(rows_of(h, 2 * p, nb), n_cu, &fn[nb - 1], &lds[nb - 1], &nr[nb - 1])) return false;
+  }
+  for (int p = 0; p < npair; ++p) {
+    const int nb = std::min(2, D.bs - 2 * p);
+    HeadArgs a = rows_of(h, 2 * p, nb);
+    int nrv = nr[nb - 1];
+    void *args[] = {&a, &nrv};
+    if (hipLaunchKernel(fn[nb - 1], dim3(a.GC), dim3(kPersWaves * 64), args, lds[nb - 1], st) != hipSuccess) {
+      // (a failure after the first pair leaves nothing wrong behind: the
+      // launch-pair rollout that follows rewrites every row's outputs)
+      (void)hipGetLastError();
+      return false;
+    }
   }
   return true;
 }

@@ -172,6 +172,7 @@ struct HeadArgs {
   int whh_NT, whh_KS, w1s_NT, w1s_KS;
   float *hpart;
   int n_cu;
+  int row0 = 0;  // batch row of this launch's first row (the Philox stream's row index)
 };
 constexpr int kHeadFusedBatch = 8;  // batches up to this run the fused state kernel
 constexpr int kHeadMaxSplit = 16;
@@ -181,9 +182,10 @@ inline size_t head_part_floats(const Dims &D) {
 int head_logits_grid(const Dims &D);
 int head_best_slots();
 hipError_t launch_head(const HeadArgs &h, hipStream_t st);
-// One persistent launch for the whole rollout where the shapes allow it (bf16,
-// r = 256, batch <= 2, greedy branch 1, a grid that fits the device at one
-// workgroup per CU, vocabulary < 2^18); returns false (nothing launched) otherwise.
+// The persistent rollout where the shapes allow it (bf16, r = 256, batch <= 4,
+// branch 1, a grid that fits the device at one workgroup per CU, vocabulary
+// < 2^18): one launch per pair of batch rows; returns false (nothing launched)
+// otherwise.
 bool launch_head_persistent(const HeadArgs &h, int n_cu, hipStream_t st);
 // the state recurrence of every position, teacher-forced (no logits): u into
 // ubuf as above, or with skip_u only the states into `states`

@@ -401,11 +401,11 @@ def persistent_config(batch):
                                           ctx_from_hidden=False)
 
 
-@pytest.mark.parametrize("batch", [1, 2])
+@pytest.mark.parametrize("batch", [1, 2, 3, 4])
 def test_persistent_rollout_matches_launch_pair_rollout(batch, monkeypatch):
-    """bf16, r = 256, one or two batch rows, greedy: the rollout runs as one
-    persistent launch (an ordinary launch after an occupancy check) with the W2
-    slice held on chip.  It must agree with the launch-pair rollout
+    """bf16, r = 256, one to four batch rows, greedy: the rollout runs as one
+    persistent launch per pair of rows (an ordinary launch after an occupancy
+    check) with the W2 slice held on chip.  It must agree with the launch-pair rollout
     (DOMINO_ROLLOUT=loop at model creation): the backbone outputs bit for bit,
     states and logits to fp32 summation order, the drafted tokens exactly away
     from near-ties; free-running and teacher-forced.  Each run checks which

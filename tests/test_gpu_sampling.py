@@ -93,11 +93,13 @@ def _check_sampled(cfg, gpu, inp, w64, T, seed, tol):
 
 @pytest.mark.parametrize("dtype,batch,T,wide", [("f32", 3, 1.0, False), ("f32", 1, 0.6, False),
                                                 ("bf16", 5, 1.0, False), ("bf16", 12, 1.3, False),
-                                                ("bf16", 1, 1.0, True), ("bf16", 2, 0.7, True)])
+                                                ("bf16", 1, 1.0, True), ("bf16", 2, 0.7, True),
+                                                ("bf16", 3, 0.9, True)])
 def test_sampled_drafting_tiny(dtype, batch, T, wide):
-    """wide: d_s = 256 and 8192 tokens, where bf16 with one or two batch rows
-    runs the persistent rollout (its sampled variant); the other cases run the
-    launch-pair rollout."""
+    """wide: d_s = 256 and 8192 tokens, where bf16 with up to four batch rows
+    runs the persistent rollout (its sampled variant; three rows as a launch
+    for rows 0-1 and one for row 2, whose Philox words must still be row 2's);
+    the other cases run the launch-pair rollout."""
     cfg = synth.get_config("tiny").with_(dtype=dtype, batch=batch, branch=1, ctx_from_hidden=False)
     if wide:
         cfg = cfg.with_(gru_hidden=256, vocab=8192)
