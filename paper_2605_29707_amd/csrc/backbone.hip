@@ -693,7 +693,7 @@ constexpr size_t kFlashLds = 2 * (kFlashK + kFlashV) * sizeof(uint16_t);
 DEVI uint32_t pack_lo16(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
 DEVI uint32_t pack_hi16(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
 
-template <int NW>
+template <int NW, int PD>
 __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__restrict__ Q, const float *__restrict__ Kb,
                                                              const float *__restrict__ Vb, const bf16_t *__restrict__ ck,
                                                              const bf16_t *__restrict__ cv,
@@ -803,33 +803,34 @@ __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__rest
   // ---- context keys [k0, c1) from the cache, 64 per block
   const int c1 = min(k1, n);
   const int nblk = c1 > k0 ? (c1 - k0 + kFlashKB - 1) / kFlashKB : 0;
-  u32x4 kr[KCH], vr[4];
-  auto load_blk = [&](int i) {  // rows clamped into [k0, c1): every load valid and unconditional
+  // PD register stages: block i's loads land in stage i % PD
+  u32x4 kr[PD][KCH], vr[PD][4];
+  auto load_blk = [&](int i, int sg) {  // rows clamped into [k0, c1): every load valid and unconditional
     const int base = k0 + i * kFlashKB;
 #pragma unroll
     for (int q = 0; q < KCH; ++q) {
       const int e = tid + q * T, key = min(base + e / (DH / 8), c1 - 1);
-      kr[q] = *(const u32x4 *)(ck + (((size_t)b * max_ctx + key) * nkv + kvh) * DH + 8 * (e % (DH / 8)));
+      kr[sg][q] = *(const u32x4 *)(ck + (((size_t)b * max_ctx + key) * nkv + kvh) * DH + 8 * (e % (DH / 8)));
     }
     const int u = min(tid, 255), dof = u % 16, kq = u / 16;  // V: 4 keys x 8 dims per thread (threads < 256)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int key = min(base + 4 * kq + r, c1 - 1);
-      vr[r] = *(const u32x4 *)(cv + (((size_t)b * max_ctx + key) * nkv + kvh) * DH + 8 * dof);
+      vr[sg][r] = *(const u32x4 *)(cv + (((size_t)b * max_ctx + key) * nkv + kvh) * DH + 8 * dof);
     }
   };
-  auto store_blk = [&](int i, int bb) {  // keys past c1 get zero values (their scores are masked)
+  auto store_blk = [&](int i, int bb, int sg) {  // keys past c1 get zero values (their scores are masked)
     const int base = k0 + i * kFlashKB;
 #pragma unroll
     for (int q = 0; q < KCH; ++q) {
       const int e = tid + q * T;
-      *(u32x4 *)(Kbuf(bb) + (e / (DH / 8)) * kFlashKP + 8 * (e % (DH / 8))) = kr[q];
+      *(u32x4 *)(Kbuf(bb) + (e / (DH / 8)) * kFlashKP + 8 * (e % (DH / 8))) = kr[sg][q];
     }
     if (tid < 256) {
       const int dof = tid % 16, kq = tid / 16;
       u32x4 v[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = base + 4 * kq + r < c1 ? vr[r] : u32x4{0u, 0u, 0u, 0u};
+      for (int r = 0; r < 4; ++r) v[r] = base + 4 * kq + r < c1 ? vr[sg][r] : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
       for (int w = 0; w < 4; ++w) {  // dims 8 dof + 2 w (low halves) and + 1 (high halves)
         uint16_t *row = Vbuf(bb) + (8 * dof + 2 * w) * kFlashVP + 4 * kq;
@@ -838,7 +839,12 @@ __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__rest
       }
     }
   };
-  if (nblk > 0) load_blk(0);
+  if constexpr (PD == 1) {
+    if (nblk > 0) load_blk(0, 0);
+  } else if (nblk > 0) {  // (no context keys here: c1 - 1 may be no row at all)
+#pragma unroll
+    for (int sg = 0; sg < PD; ++sg) load_blk(sg, sg);  // clamped: issued even past the last block
+  }
   // the block's own keys [max(k0, n), k1): this thread's first PB items (rows
   // kk = e / 32 of e = tid + T q, 4 dims each; every row of a 16-row block at
   // 256 threads) are loaded now, in flight with the context keys and Q, not
@@ -867,13 +873,30 @@ __global__ __launch_bounds__(NW * 64) void attn_flash_kernel(const float *__rest
       split8(f, qhf[s], qlf[s]);
     }
   }
-  for (int i = 0; i < nblk; ++i) {
-    // buffer i & 1 was last read by block i - 2, which every wave finished
-    // before the barrier of block i - 1
-    store_blk(i, i & 1);
-    if (i + 1 < nblk) load_blk(i + 1);
-    __syncthreads();
-    fold(min(kFlashKB, c1 - (k0 + i * kFlashKB)), false, i & 1);
+  if constexpr (PD == 1) {
+    for (int i = 0; i < nblk; ++i) {
+      // buffer i & 1 was last read by block i - 2, which every wave finished
+      // before the barrier of block i - 1
+      store_blk(i, i & 1, 0);
+      if (i + 1 < nblk) load_blk(i + 1, 0);
+      __syncthreads();
+      fold(min(kFlashKB, c1 - (k0 + i * kFlashKB)), false, i & 1);
+    }
+  } else {
+    // PD blocks in flight while one is multiplied.  The loads are
+    // unconditional (clamped rows past the last block), so every path through
+    // the loop leaves the same loads outstanding and the compiler's waits for
+    // a stage cover only that stage's loads, not the younger ones.
+    for (int i = 0; i < nblk; i += PD) {
+#pragma unroll
+      for (int sg = 0; sg < PD; ++sg) {
+        const int ii = i + sg;
+        store_blk(ii, ii & 1, sg);
+        load_blk(ii + PD, sg);
+        __syncthreads();
+        if (ii < nblk) fold(min(kFlashKB, c1 - (k0 + ii * kFlashKB)), false, ii & 1);  // workgroup-uniform
+      }
+    }
   }
 
   // ---- block keys [max(k0, n), k1): fp32, hi parts in buffer 0, lo in buffer 1
@@ -1153,21 +1176,22 @@ void launch_attention(const Dims &D, const float *Q, const float *Kb, const floa
     if (D.bf16 && D.dh == 128 && !amask && (R == 64 || R == 128) && pairs >= 8) {
       const int n_cu = attn_cu_count();
       const int nkeys = max_ctx + D.B;
-      const long target = std::max(1L, 2L * n_cu / pairs);
+      // workgroups resident per CU: two of 4 waves (LDS), one of 8 (registers)
+      const long target = std::max(1L, (R == 64 ? 2L : 1L) * n_cu / pairs);
       const int kpw = (int)(((nkeys + target - 1) / target + kFlashKB - 1) / kFlashKB * kFlashKB);
       const int ngrp = (nkeys + kpw - 1) / kpw;
       const int nch = attn_nchunks(max_ctx, D.B);
       const float scale = 1.0f / sqrtf(128.f);
       const dim3 grid(ngrp, D.nkv, D.bs);
       if (R == 64) {
-        (void)hipFuncSetAttribute((const void *)attn_flash_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize,
+        (void)hipFuncSetAttribute((const void *)attn_flash_kernel<4, 1>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                   (int)kFlashLds);
-        hipLaunchKernelGGL(attn_flash_kernel<4>, grid, dim3(256), kFlashLds, st, Q, Kb, Vb, (const bf16_t *)ck,
+        hipLaunchKernelGGL((attn_flash_kernel<4, 1>), grid, dim3(256), kFlashLds, st, Q, Kb, Vb, (const bf16_t *)ck,
                            (const bf16_t *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv, nch, scale, kpw);
       } else {
-        (void)hipFuncSetAttribute((const void *)attn_flash_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
+        (void)hipFuncSetAttribute((const void *)attn_flash_kernel<8, 2>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                   (int)kFlashLds);
-        hipLaunchKernelGGL(attn_flash_kernel<8>, grid, dim3(512), kFlashLds, st, Q, Kb, Vb, (const bf16_t *)ck,
+        hipLaunchKernelGGL((attn_flash_kernel<8, 2>), grid, dim3(512), kFlashLds, st, Q, Kb, Vb, (const bf16_t *)ck,
                            (const bf16_t *)cv, ctx_lens, max_ctx, part, D.B, D.nq, D.nkv, nch, scale, kpw);
       }
       const int items = D.bs * D.nq * D.B;

@@ -133,8 +133,9 @@ def test_long_context_folded_chunks(dtype, nq):
 @pytest.mark.parametrize("nq", [8, 16])
 def test_bf16_batched_context_one_pass(nq):
     """bf16 cache, head dim 128 and 16 batch rows over 2 kv heads (32 pairs):
-    the one-pass context attention (64-key blocks, a run of 128 keys per
-    workgroup here).  The ragged lengths give an empty context, partial
+    the one-pass context attention (64-key blocks; a run of 128 keys per
+    workgroup at nq = 8, and of 192 at nq = 16, whose 8-wave workgroups keep two
+    blocks in flight).  The ragged lengths give an empty context, partial
     blocks, block keys split between two workgroups (n = 120, 1016), and
     contexts ending on a workgroup boundary (n = 128, 1024); nq = 8 and 16
     over 2 kv heads: 64 and 128 query rows per workgroup."""
