@@ -154,6 +154,27 @@ def test_bf16_batched_context_one_pass(nq):
     run.close()
 
 
+def test_bf16_batched_context_one_pass_long_runs():
+    """The one-pass attention over long runs: 64 query rows per workgroup
+    (nq = 8 over 2 kv heads), 16 batch rows at a 4096-key context, 320 keys
+    (5 blocks) per workgroup.  Ragged lengths: empty, one key, partial blocks,
+    contexts ending on a block or a run boundary (64, 320) and one key either
+    side of them, block keys split between two runs (n = 310, 3832)."""
+    lens = [4096, 0, 1, 63, 64, 65, 319, 320, 321, 310, 2047, 2048, 3000, 4000, 3832, 255]
+    cfg = synth.get_config("tiny").with_(dtype="bf16", n_q_heads=8, head_dim=128, batch=len(lens), ctx=4096,
+                                         ctx_from_hidden=False)
+    w = synth.make_weights(cfg, seed=18, gain_std=0.1)
+    inp = synth.make_inputs(cfg, seed=18, ctx_lens=np.array(lens, np.int32), max_ctx=4096)
+    log(f"one-pass context attention, long runs: bs={len(lens)} ctx 4096")
+    run = GpuRun(cfg, w, 4096, beta=1)
+    gpu = run.step(inp)
+    assert gpu["err"] == 0
+    ref = oracle_for(cfg, oracle.as_f64_weights(w), inp, gpu, 1)
+    n = check_against_oracle(cfg, gpu, ref, 2e-2, 1)
+    assert n >= 10 * len(lens)
+    run.close()
+
+
 @pytest.mark.parametrize("nq,block", [(8, 32), (4, 64)])
 def test_tiny_large_blocks(nq, block):
     """(n_q / n_kv) * block = 128 query rows per workgroup: the attention uses
