@@ -418,7 +418,8 @@ domino_status domino_profile_reset(domino_model_t m);
 
 /*
  * Test hook for the failure path of the persistent rollout (greedy or sampled
- * drafting with bf16 weights, rank 256 and one or two batch rows): the number
+ * drafting with bf16 weights, rank 256 and up to four batch rows, one launch
+ * per pair of rows): the number
  * of polls a cross-workgroup wait may make before it gives up, raising
  * DOMINO_DEV_BARRIER_TIMEOUT in the error word and letting every workgroup
  * leave (the step's outputs are then undefined); 0 makes every wait give up at
